@@ -1,0 +1,298 @@
+"""Benchmark of the shared-stage hot path on one MI355X.
+
+Headline: prefill tokens/s of the 4-layer thinker stack (hidden 3584, 28/4
+heads, head_dim 128, FFN 18944) over the seeded ragged batch of 8 requests
+(T = 10,515 rows), at the full 256-CU budget.  Also reported: the same stack
+at CU budgets 64/128/192 (fraction of the CU-scaled bf16 MFMA peak) and the
+spatial co-run of that prefill on a 128-CU mask with a 16-layer talker decode
+step (batch 32) looping on the complementary 128 CUs.
+
+Prints one JSON line.  The CPU reference is timed on a bounded sample of the
+same workload (rank 0, N = 1 only).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15       # MI355X dense bf16 MFMA, FLOP/s, 256 CUs
+PEAK_HBM = 8.0e12        # bytes/s
+N_CUS = 256
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def thinker_flops(shape, lengths, ctx=None):
+    """Algorithmic FLOPs of one layer: 2 * params per row + 4 * Hq * dh per visible (query, key) pair."""
+    L = np.asarray(lengths, np.int64)
+    c = np.zeros_like(L) if ctx is None else np.asarray(ctx, np.int64)
+    params = shape.params_per_layer
+    pairs = int(np.sum(L * c + L * (L + 1) // 2))
+    return 2.0 * params * int(L.sum()), 4.0 * shape.n_q_heads * shape.head_dim * pairs
+
+
+def talker_bytes(shape, n_layers, kv_lens):
+    """HBM bytes of one decode step: weights once + cached K/V read + new K/V written."""
+    per_tok = 2 * shape.n_kv_heads * shape.head_dim * 2  # K and V, bf16, per layer
+    kv = np.asarray(kv_lens, np.int64)
+    return n_layers * (shape.params_per_layer * 2 + per_tok * int(kv.sum()) + per_tok * len(kv))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--budgets", type=str, default="64,128,192")
+    ap.add_argument("--no-corun", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=24, help="rows per sequence in the CPU-reference sample")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build measures one GPU only; the hot path is a single-GPU "
+                                   "spatial-sharing design (run with --gpus 1)"}))
+        sys.exit(2)
+
+    import torch
+    from paper_2608_01785_amd import binding, workloads as W
+    from paper_2608_01785_amd.device_data import DeviceCache, to_device, upload_weights
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = "cuda:0"
+    budgets = [int(b) for b in args.budgets.split(",") if b]
+    ctx = binding.Context(0, budgets=sorted(set(budgets + [128, 256])))
+
+    # ---------------------------------------------------------------- thinker stack
+    shape, n_layers = W.THINKER, 4
+    t0 = time.time()
+    layers = W.make_weights(shape, n_layers, W.SEEDS["thinker"]["weights"])
+    batch = W.thinker_batch()
+    log(f"[bench] generated thinker weights/batch in {time.time() - t0:.1f}s, T={batch.n_tokens}")
+    wdev = upload_weights(layers, dev)
+    x = to_device(batch.x, dev)
+    y = torch.empty_like(x)
+    T, B = batch.n_tokens, batch.n_seqs
+    max_pos = int(batch.lengths.max())
+    ws = torch.empty(binding.hs_workspace_size(shape, T, B, max_pos), dtype=torch.uint8, device=dev)
+    lin, att = thinker_flops(shape, batch.lengths)
+    flops_step = n_layers * (lin + att)
+    torch.cuda.synchronize()
+
+    def run(budget, k):
+        s = binding.hs_context_stream(ctx, budget, binding.HS_ROLE_SHARED)
+        ts = torch.cuda.ExternalStream(s)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(ts)
+        for _ in range(k):
+            binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, None, None, budget, None, ws)
+        e1.record(ts)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / k
+
+    for _ in range(args.warmup):
+        run(256, 1)
+    binding.hs_timing_enable(ctx, True)
+    ms = run(256, args.steps)
+    kern = {k: binding.hs_timing_read(ctx, k) for k in binding.KERNEL_KINDS}
+    binding.hs_timing_enable(ctx, False)
+    tok_s = T / (ms / 1e3)
+    log(f"[bench] thinker stack @256 CUs: {ms:.3f} ms/step, {tok_s:,.0f} tok/s, "
+        f"{flops_step / (ms / 1e3) / 1e12:.1f} TFLOP/s")
+    kernel_ms = {k: (v[0] / v[1] if v[1] else 0.0) for k, v in kern.items()}
+    for k, v in kern.items():
+        if v[1]:
+            log(f"    {k:12s} {v[0] / v[1]:8.3f} ms avg over {v[1]} launches")
+
+    # Dominant kernel: the gate/up projection (SwiGLU epilogue), ~58 % of the FLOPs.
+    gu_flops = 2.0 * T * shape.hidden * 2 * shape.ffn
+    gu_ms = kernel_ms["gate_up"]
+    achieved = gu_flops / (gu_ms / 1e3) / 1e12
+    roofline = {"bound": "mfma", "kernel": "gate_up_swiglu_gemm", "achieved": round(achieved, 1),
+                "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s", "frac": round(achieved / (PEAK_BF16 / 1e12), 4),
+                "traffic": None, "avg_launch_ms": round(gu_ms, 4)}
+
+    per_budget = {}
+    for b in budgets:
+        if b == 256:
+            continue
+        run(b, 1)
+        mb = run(b, max(2, args.steps // 2))
+        per_budget[str(b)] = {"ms_per_step": round(mb, 3), "tok_s": round(T / (mb / 1e3)),
+                              "mfma_frac_cu_scaled": round(flops_step / (mb / 1e3) / (PEAK_BF16 * b / N_CUS), 4)}
+        log(f"[bench] thinker stack @{b} CUs: {mb:.3f} ms/step, {T / (mb / 1e3):,.0f} tok/s")
+    per_budget["256"] = {"ms_per_step": round(ms, 3), "tok_s": round(tok_s),
+                         "mfma_frac_cu_scaled": round(flops_step / (ms / 1e3) / PEAK_BF16, 4)}
+
+    # ---------------------------------------------------------------- co-run
+    corun = None
+    if not args.no_corun:
+        corun = corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flops_step)
+
+    # ---------------------------------------------------------------- CPU reference sample
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(W, layers, batch, shape, args.cpu_rows)
+
+    out = {
+        "metric": "shared-stage prefill tok/s vs CU budget (% MFMA roofline); co-run decode tok/s",
+        "value": round(tok_s, 1),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) token rows)",
+        "config": {"workload": "thinker 4-layer stack prefill, hidden 3584, 28/4 heads, dh 128, ffn 18944, "
+                               "8 ragged requests T=10515, 256 CUs",
+                   "global_batch": B, "seq_len": int(batch.lengths.max()), "tokens": T,
+                   "parallelism": "single GPU, CU-masked streams"},
+        "tflops": round(flops_step / (ms / 1e3) / 1e12, 1),
+        "mfma_frac": round(flops_step / (ms / 1e3) / PEAK_BF16, 4),
+        "roofline": roofline,
+        "kernel_ms": {k: round(v, 4) for k, v in kernel_ms.items() if v},
+        "budgets": per_budget,
+        "corun": corun,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    torch.cuda.synchronize()
+    ctx.close()
+
+
+def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flops_step):
+    """Prefill on a 128-CU mask while talker decode steps loop on the other 128 CUs."""
+    from paper_2608_01785_amd.device_data import DeviceCache, to_device, upload_weights
+    ts_shape, ts_layers, bt = W.TALKER, 16, 32
+    seeds = W.SEEDS["talker"]
+    kv_lens = W.talker_kv_lens(bt, seeds["cache"])
+    tl = upload_weights(W.make_weights(ts_shape, ts_layers, seeds["weights"]), dev)
+    max_ctx = int(np.ceil((kv_lens.max() + 1) / 64) * 64)
+    cache = DeviceCache(ts_layers, bt, max_ctx, ts_shape.n_kv_heads, ts_shape.head_dim, dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seeds["cache"])
+    for l in range(ts_layers):
+        for b in range(bt):
+            cache.fill_random(l, b, int(kv_lens[b]), gen)
+    xt = to_device(W.talker_batch(ts_shape, ts_layers, bt, seeds, with_cache=False).x, dev)
+    yt = torch.empty_like(xt)
+    wst = torch.empty(binding.hs_workspace_size(ts_shape, bt, bt, int(kv_lens.max()) + 1), dtype=torch.uint8, device=dev)
+    step_bytes = talker_bytes(ts_shape, ts_layers, kv_lens)
+    s_sh = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_SHARED))
+    s_dn = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_DOWN))
+
+    def decode(n):
+        ev = []
+        for _ in range(n):
+            binding.hs_downstream_decode_step(ctx, ts_shape, tl, xt, yt, cache.as_arg(), kv_lens, 128, None, wst)
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(s_dn)
+            ev.append(e)
+        return ev
+
+    # Solo decode on its 128 CUs.
+    torch.cuda.synchronize()
+    decode(3)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e0.record(s_dn)
+    ev = decode(20)
+    torch.cuda.synchronize()
+    solo_ms = e0.elapsed_time(ev[-1]) / 20
+
+    # Solo prefill on its 128 CUs.
+    p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    p0.record(s_sh)
+    binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, None, None, 128, None, ws)
+    p1.record(s_sh)
+    torch.cuda.synchronize()
+    prefill_solo = p0.elapsed_time(p1)
+
+    # Co-run: both streams start after a common point.
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    start.record(s_sh)
+    s_dn.wait_event(start)
+    binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, None, None, 128, None, ws)
+    p_end = torch.cuda.Event(enable_timing=True)
+    p_end.record(s_sh)
+    dec_ev = []
+    while True:
+        dec_ev += decode(1)
+        if p_end.query():
+            break
+        if len(dec_ev) > 4:
+            dec_ev[-4].synchronize()
+        if len(dec_ev) > 2000:
+            break
+    torch.cuda.synchronize()
+    window = start.elapsed_time(p_end)
+    done = [start.elapsed_time(e) for e in dec_ev]
+    n_in = sum(1 for t in done if t <= window)
+    t_last = max([t for t in done if t <= window], default=0.0)
+    dec_ms = t_last / n_in if n_in else float("nan")
+    T = batch.n_tokens
+    res = {
+        "shared_cus": 128, "down_cus": 128,
+        "prefill_ms": round(window, 3), "prefill_tok_s": round(T / (window / 1e3)),
+        "prefill_solo_ms": round(prefill_solo, 3),
+        "prefill_mfma_frac_cu_scaled": round(flops_step / (window / 1e3) / (PEAK_BF16 * 128 / N_CUS), 4),
+        "decode_steps_in_window": n_in,
+        "decode_ms_per_step": round(dec_ms, 4),
+        "decode_tok_s": round(32 / (dec_ms / 1e3)) if n_in else None,
+        "decode_hbm_frac_cu_scaled": round(step_bytes / (dec_ms / 1e3) / (PEAK_HBM * 128 / N_CUS), 4) if n_in else None,
+        "decode_solo_ms_per_step": round(solo_ms, 4),
+        "decode_solo_tok_s": round(32 / (solo_ms / 1e3)),
+        "decode_solo_hbm_frac_cu_scaled": round(step_bytes / (solo_ms / 1e3) / (PEAK_HBM * 128 / N_CUS), 4),
+        "decode_bytes_per_step": int(step_bytes),
+        "talker": "16 layers, hidden 1024, 16/16 heads, dh 64, ffn 4096, batch 32, kv_len U[128,1024] (sum 17437)",
+    }
+    log(f"[bench] co-run: prefill {window:.2f} ms (solo {prefill_solo:.2f}), decode {dec_ms:.3f} ms/step "
+        f"(solo {solo_ms:.3f}), {n_in} steps in window")
+    return res
+
+
+def cpu_baseline(W, layers, batch, shape, rows_per_seq):
+    """The float64 reference on the host: first rows of every request through all layers.
+
+    By causality the first r rows of a request depend only on themselves, so the
+    sample is a faithful slice of the same workload.
+    """
+    from oracle import layer as ref
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count()])
+    except Exception:
+        cores = os.cpu_count()
+    r = rows_per_seq
+    xs = np.concatenate([batch.x[o:o + r] for o in batch.seq_offsets[:-1]])
+    off = np.arange(batch.n_seqs + 1) * r
+    w64 = [{k: W.bf16_to_f32(v).astype(np.float64) for k, v in lw.items()} for lw in layers]
+    x64 = W.bf16_to_f32(xs).astype(np.float64)
+    t0 = time.time()
+    ref.stack_forward(x64, w64, shape, off)
+    dt = time.time() - t0
+    rows = int(off[-1])
+    log(f"[bench] CPU reference: {rows} rows x {len(layers)} layers in {dt:.1f}s")
+    return {"value": round(rows / dt, 2), "unit": "tok/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {r} rows of each of the {batch.n_seqs} requests through all {len(layers)} layers "
+                      f"({rows} rows), float64 NumPy", "seconds": round(dt, 2)}
+
+
+if __name__ == "__main__":
+    main()

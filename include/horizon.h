@@ -1,0 +1,232 @@
+/*
+ * horizon.h - C ABI of the MI355X (gfx950) shared-stage hot path.
+ *
+ * The library runs the shared multimodal stage ("thinker") of an omni model:
+ * a stack of pre-norm decoder layers over a packed ragged batch of prefill
+ * rows, on an explicit budget of compute units, while a downstream decode
+ * stage ("talker") runs on the complementary compute units of the same GPU.
+ *
+ * Paper passages this interface follows (HorizonServe):
+ *   - §2.1 "Autoregressive transformers": prefill processes the context and
+ *     builds the key/value cache; decode re-reads the weights and the cache.
+ *   - §4.4 "Complementary downstream headroom" and Algorithm 1, step 3: the
+ *     downstream stage gets s_down = S_tot - s_shared.
+ *   - §4.5 Algorithm 1, step 4: the selected batch runs with cap s_shared.
+ *   - §5: one pre-built allocation per ladder level, selected (not created)
+ *     before each forward pass; the two stages' ladders are complementary.
+ *
+ * Conventions for every entry point:
+ *   - Device pointers are HIP device addresses; "host" arrays are ordinary
+ *     host memory that the call reads before it returns (the caller may
+ *     reuse them at once).  Streams are hipStream_t passed as void*.
+ *   - bf16 means IEEE bfloat16 stored as 16-bit words.
+ *   - Weight matrices are [out, in] row-major, so y = x * W^T.
+ *   - Every function returns an hs_status.  No C++ exception crosses the
+ *     ABI.  On any error other than HS_ERR_HIP nothing has been enqueued.
+ *     hs_last_error() returns a thread-local message for the last failure.
+ *   - Compute calls are asynchronous with respect to their stream; device
+ *     faults surface at the caller's next synchronisation.
+ *   - A context is not thread-safe; use one per host thread.
+ */
+#ifndef HORIZON_H_
+#define HORIZON_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum hs_status {
+  HS_OK = 0,
+  HS_ERR_INVALID_ARG = 1, /* null pointer, bad shape, bad offsets, aliasing */
+  HS_ERR_UNSUPPORTED = 2, /* valid request outside what the kernels implement */
+  HS_ERR_BUDGET = 3,      /* CU budget outside [1, n_cus] or not matching the stream */
+  HS_ERR_WORKSPACE = 4,   /* workspace missing or smaller than hs_workspace_size() */
+  HS_ERR_HIP = 5,         /* a HIP runtime call failed; see hs_last_error() */
+  HS_ERR_INTERNAL = 6
+} hs_status;
+
+/* Shape of one decoder layer (all layers of a stack share it).
+ * Requirements: hidden % 256 == 0, head_dim in {64, 128},
+ * n_q_heads % n_kv_heads == 0, (n_q_heads + 2 n_kv_heads) * head_dim % 256 == 0,
+ * n_q_heads * head_dim % 64 == 0, ffn % 128 == 0. */
+typedef struct hs_layer_cfg {
+  int32_t hidden;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t ffn;
+  float rms_eps;   /* RMSNorm epsilon, inside the square root */
+  float rope_base; /* RoPE base; pair (j, j + dh/2) turns by pos * base^(-2j/dh) */
+} hs_layer_cfg;
+
+/* Device pointers to one layer's bf16 weights.
+ *   ln1, ln2   [hidden]                              RMSNorm gains
+ *   w_qkv      [(Hq + 2 Hkv) * dh, hidden]           rows: Q heads | K heads | V heads
+ *   w_o        [hidden, Hq * dh]
+ *   w_gate_up  [2 * ffn, hidden]                      rows: gate | up
+ *   w_down     [hidden, ffn]                                                    */
+typedef struct hs_layer_weights {
+  const void* ln1;
+  const void* w_qkv;
+  const void* w_o;
+  const void* ln2;
+  const void* w_gate_up;
+  const void* w_down;
+} hs_layer_weights;
+
+/* Key/value cache.  k[l] and v[l] are device pointers for layer l (host
+ * arrays of n_layers pointers, owned by the caller).  Per layer:
+ *   K: bf16 [n_slots, max_ctx, Hkv, dh]   (row-major, token-major)
+ *   V: bf16 [n_slots, Hkv, dh, max_ctx]   (dimension-major: the P.V
+ *      contraction reads keys contiguously)
+ * Sequence b of a call uses slot b.  max_ctx % 64 == 0. */
+typedef struct hs_kv_cache {
+  void* const* k;
+  void* const* v;
+  int32_t n_slots;
+  int32_t max_ctx;
+} hs_kv_cache;
+
+/* Per mask bit i (bit i%32 of word i/32): hardware XCD, shader engine and CU
+ * index inside that shader engine. */
+typedef struct hs_topology {
+  int32_t n_cus;
+  int32_t n_xcc;
+  uint8_t xcc[256];
+  uint8_t se[256];
+  uint8_t cu[256];
+} hs_topology;
+
+typedef struct hs_context hs_context;
+
+enum { HS_ROLE_SHARED = 0, HS_ROLE_DOWN = 1 };
+
+/* Human-readable name of a status code (static storage). */
+const char* hs_status_string(hs_status s);
+
+/* Message of the last failing call on this host thread ("" if none). */
+const char* hs_last_error(void);
+
+/* Default topology of an n_cus / n_xcc part with 4 shader engines per XCD:
+ * bit i -> XCD i % n_xcc, slot j = i / n_xcc -> (se j % 4, cu j / 4).
+ * Host only. */
+hs_status hs_default_topology(int32_t n_cus, int32_t n_xcc, hs_topology* out);
+
+/* Complementary CU partition (§4.4 complementary headroom; §5 complementary
+ * ladders).  Pure host function of (topology, budget):
+ *   XCD x receives floor(c / n_xcc) + (x < c % n_xcc) shared CUs, taken from
+ *   that XCD's mask bits ordered by (cu, se, bit); every other bit is down.
+ * shared_mask and down_mask are 8 words each (256 bits), written by the call.
+ * Errors: HS_ERR_BUDGET for c outside [1, n_cus]; HS_ERR_INVALID_ARG for null
+ * pointers or a topology with more than 256 CUs or an XCD too small. */
+hs_status hs_cu_partition(const hs_topology* topo, int32_t shared_cus, uint32_t shared_mask[8],
+                          uint32_t down_mask[8]);
+
+/* Packed-batch metadata (Algorithm 1, step 4: batch B).  Host only.
+ * seq_offsets[n_seqs + 1] (host) must start at 0 and be non-decreasing;
+ * ctx_lens[n_seqs] (host, may be NULL = all 0) must be >= 0.  Writes
+ * pos_out[T] = ctx_lens[b] + (t - seq_offsets[b]) and seq_id_out[T] = b for
+ * every packed row t, T = seq_offsets[n_seqs]. */
+hs_status hs_plan_metadata(const int32_t* seq_offsets, const int32_t* ctx_lens, int32_t n_seqs,
+                           int32_t* pos_out, int32_t* seq_id_out);
+
+/* Create a context on HIP device `device` with a ladder of CU-masked stream
+ * pairs, one pair per budget in budgets[n_budgets] (each in [1, n_cus]).
+ * Budget n_cus has a SHARED stream only.  topo may be NULL (default
+ * topology); the masks are hs_cu_partition(topo, budget).  The context owns
+ * its streams and a small pinned staging ring. */
+hs_status hs_context_create(int32_t device, const int32_t* budgets, int32_t n_budgets,
+                            const hs_topology* topo, hs_context** out);
+
+/* Topology the context's masks were built from. */
+hs_status hs_context_topology(const hs_context* ctx, hs_topology* out);
+
+/* Pre-built stream of the ladder for (budget, role).  HS_ERR_BUDGET if the
+ * budget is not on the ladder or role is DOWN at the full budget. */
+hs_status hs_context_stream(hs_context* ctx, int32_t cu_budget, int32_t role, void** stream_out);
+
+/* Masks of the ladder level (8 words each; either pointer may be NULL). */
+hs_status hs_context_masks(const hs_context* ctx, int32_t cu_budget, uint32_t shared_mask[8],
+                           uint32_t down_mask[8]);
+
+hs_status hs_context_destroy(hs_context* ctx);
+
+/* Workspace bytes needed by the calls below for up to max_tokens packed rows,
+ * max_seqs sequences and positions up to max_pos (exclusive). */
+hs_status hs_workspace_size(const hs_layer_cfg* cfg, int32_t max_tokens, int32_t max_seqs,
+                            int32_t max_pos, size_t* bytes);
+
+/* Shared-stage forward: n_layers decoder layers over a packed ragged batch.
+ *   x_in, x_out  bf16 [T, hidden] device, T = seq_offsets[n_seqs]; must not alias.
+ *   w            host array of n_layers weight sets.
+ *   seq_offsets  host [n_seqs + 1];  ctx_lens host [n_seqs] or NULL.
+ *   kv           NULL: keys/values live in the workspace only (plain prefill).
+ *                non-NULL: row i of sequence b is written to slot b at
+ *                position ctx_lens[b] + i of every layer's cache, and the
+ *                sequence attends to cache positions 0 .. ctx_lens[b] + i
+ *                (§2.1: prefill builds the cache).  Requires ctx_lens.
+ *   cu_budget    CU cap s_shared (§4.5, Algorithm 1, step 4).  stream NULL
+ *                selects the context's SHARED stream of that budget; a
+ *                non-NULL stream must carry exactly cu_budget CUs.
+ *   workspace    device buffer of ws_bytes >= hs_workspace_size(cfg, T,
+ *                n_seqs, max position + 1), owned by the caller; must not
+ *                overlap the inputs or outputs.  It may be reused as soon as
+ *                the stream has passed this call.
+ * The output is the residual stream after the last layer (no final norm). */
+hs_status hs_shared_stage_forward(hs_context* ctx, const hs_layer_cfg* cfg,
+                                  const hs_layer_weights* w, int32_t n_layers, const void* x_in,
+                                  void* x_out, const int32_t* seq_offsets,
+                                  const int32_t* ctx_lens, int32_t n_seqs, const hs_kv_cache* kv,
+                                  int32_t cu_budget, void* stream, void* workspace,
+                                  size_t ws_bytes);
+
+/* Downstream decode step (§2.1: decode re-reads weights and the cache):
+ * one new row per sequence through n_layers layers.
+ *   x_in, x_out  bf16 [batch, hidden] device; must not alias.
+ *   kv_lens      host [batch]: cached rows before the step.  The new row is at
+ *                position kv_lens[b], its K/V are written there in slot b, and
+ *                it attends to kv_lens[b] + 1 keys.  kv_lens[b] < max_ctx.
+ *   cu_budget, stream, workspace as for hs_shared_stage_forward, with the
+ *   DOWN role: stream NULL selects the context's DOWN stream for the ladder
+ *   level whose SHARED budget is n_cus - cu_budget.
+ * The library never changes kv_lens; the caller advances them. */
+hs_status hs_downstream_decode_step(hs_context* ctx, const hs_layer_cfg* cfg,
+                                    const hs_layer_weights* w, int32_t n_layers,
+                                    const void* x_in, void* x_out, const hs_kv_cache* kv,
+                                    const int32_t* kv_lens, int32_t batch, int32_t cu_budget,
+                                    void* stream, void* workspace, size_t ws_bytes);
+
+/* Topology probe: launches n_groups work-groups on `stream` (NULL = the
+ * context's full-budget stream); each writes, into out_ids (device, uint32
+ * [n_groups * 4]): XCC id, shader engine, CU id, and the low 32 bits of the
+ * constant-rate clock at its start.  Used to check that masks hold. */
+hs_status hs_probe_hw_ids(hs_context* ctx, void* stream, int32_t n_groups, void* out_ids);
+
+/* Per-kernel timing with HIP events on the launch stream.  While enabled,
+ * every launch of the compute calls is bracketed by a pair of events (a pool
+ * of 8192 pairs; launches beyond it are not recorded).  hs_timing_enable(ctx,
+ * 1) clears earlier records; hs_timing_read waits for the recorded events of
+ * one kernel kind and returns their summed duration and count. */
+enum {
+  HS_KERNEL_RMSNORM = 0,
+  HS_KERNEL_QKV = 1,          /* QKV projection with RoPE and key/value store */
+  HS_KERNEL_ATTENTION = 2,    /* multi-row causal attention */
+  HS_KERNEL_DECODE_ATTN = 3,  /* single-row attention (split keys + merge) */
+  HS_KERNEL_O_PROJ = 4,       /* output projection + residual */
+  HS_KERNEL_GATE_UP = 5,      /* gate/up projection + SwiGLU */
+  HS_KERNEL_DOWN = 6,         /* down projection + residual */
+  HS_KERNEL_ROPE_TABLE = 7,
+  HS_KERNEL_KINDS = 8
+};
+
+hs_status hs_timing_enable(hs_context* ctx, int32_t enable);
+hs_status hs_timing_read(hs_context* ctx, int32_t kernel_kind, double* total_ms, int32_t* n_launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HORIZON_H_ */

@@ -1,0 +1,287 @@
+"""ctypes binding of ``libhorizon.so``: argument marshalling only.
+
+Every function here has the name of the C entry point it calls and only
+converts arguments (torch tensors -> device pointers, Python sequences ->
+host arrays, status codes -> exceptions).  All computation happens in the
+library's HIP kernels.  Importing this module fails loudly when the library
+has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhorizon.so")
+
+HS_OK, HS_ERR_INVALID_ARG, HS_ERR_UNSUPPORTED, HS_ERR_BUDGET, HS_ERR_WORKSPACE, HS_ERR_HIP, HS_ERR_INTERNAL = range(7)
+HS_ROLE_SHARED, HS_ROLE_DOWN = 0, 1
+
+SYMBOLS = (
+    "hs_status_string", "hs_last_error", "hs_default_topology", "hs_cu_partition", "hs_plan_metadata",
+    "hs_context_create", "hs_context_topology", "hs_context_stream", "hs_context_masks",
+    "hs_context_destroy", "hs_workspace_size", "hs_shared_stage_forward", "hs_downstream_decode_step",
+    "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read",
+)
+
+KERNEL_KINDS = {"rmsnorm": 0, "qkv": 1, "attention": 2, "decode_attn": 3, "o_proj": 4, "gate_up": 5,
+                "down": 6, "rope_table": 7}
+
+
+class LayerCfg(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("rope_base", ctypes.c_float)]
+
+    @classmethod
+    def of(cls, s) -> "LayerCfg":
+        return cls(s.hidden, s.n_q_heads, s.n_kv_heads, s.head_dim, s.ffn, s.rms_eps, s.rope_base)
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("ln1", "w_qkv", "w_o", "ln2", "w_gate_up", "w_down")]
+
+
+class KvCache(ctypes.Structure):
+    _fields_ = [("k", ctypes.POINTER(ctypes.c_void_p)), ("v", ctypes.POINTER(ctypes.c_void_p)),
+                ("n_slots", ctypes.c_int32), ("max_ctx", ctypes.c_int32)]
+
+
+class Topology(ctypes.Structure):
+    _fields_ = [("n_cus", ctypes.c_int32), ("n_xcc", ctypes.c_int32), ("xcc", ctypes.c_uint8 * 256),
+                ("se", ctypes.c_uint8 * 256), ("cu", ctypes.c_uint8 * 256)]
+
+
+class HorizonError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_status_name(status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise ImportError(f"{_LIB_PATH} is missing: build it with python -m paper_2608_01785_amd.build")
+        L = ctypes.CDLL(_LIB_PATH)
+        vp, i32, u32p, i32p = ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_uint32), ctypes.POINTER(ctypes.c_int32)
+        L.hs_status_string.restype = ctypes.c_char_p
+        L.hs_status_string.argtypes = [ctypes.c_int]
+        L.hs_last_error.restype = ctypes.c_char_p
+        L.hs_last_error.argtypes = []
+        sigs = {
+            "hs_default_topology": [i32, i32, ctypes.POINTER(Topology)],
+            "hs_cu_partition": [ctypes.POINTER(Topology), i32, u32p, u32p],
+            "hs_plan_metadata": [i32p, i32p, i32, i32p, i32p],
+            "hs_context_create": [i32, i32p, i32, ctypes.POINTER(Topology), ctypes.POINTER(vp)],
+            "hs_context_topology": [vp, ctypes.POINTER(Topology)],
+            "hs_context_stream": [vp, i32, i32, ctypes.POINTER(vp)],
+            "hs_context_masks": [vp, i32, u32p, u32p],
+            "hs_context_destroy": [vp],
+            "hs_workspace_size": [ctypes.POINTER(LayerCfg), i32, i32, i32, ctypes.POINTER(ctypes.c_size_t)],
+            "hs_shared_stage_forward": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp, vp,
+                                        i32p, i32p, i32, ctypes.POINTER(KvCache), i32, vp, vp, ctypes.c_size_t],
+            "hs_downstream_decode_step": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp, vp,
+                                          ctypes.POINTER(KvCache), i32p, i32, i32, vp, vp, ctypes.c_size_t],
+            "hs_probe_hw_ids": [vp, vp, i32, vp],
+            "hs_timing_enable": [vp, i32],
+            "hs_timing_read": [vp, i32, ctypes.POINTER(ctypes.c_double), i32p],
+        }
+        for name, args in sigs.items():
+            fn = getattr(L, name)
+            fn.restype = ctypes.c_int
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _status_name(s: int) -> str:
+    try:
+        return lib().hs_status_string(s).decode()
+    except Exception:  # pragma: no cover - library missing
+        return str(s)
+
+
+def _check(status: int) -> None:
+    if status != HS_OK:
+        raise HorizonError(status, lib().hs_last_error().decode())
+
+
+def hs_last_error() -> str:
+    return lib().hs_last_error().decode()
+
+
+def _i32_array(values) -> Optional[ctypes.Array]:
+    if values is None:
+        return None
+    a = np.ascontiguousarray(np.asarray(values, dtype=np.int32))
+    return (ctypes.c_int32 * len(a))(*a.tolist())
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+# --------------------------------------------------------------------------- host-only calls
+
+def hs_default_topology(n_cus: int = 256, n_xcc: int = 8) -> Topology:
+    t = Topology()
+    _check(lib().hs_default_topology(n_cus, n_xcc, ctypes.byref(t)))
+    return t
+
+
+def topology_from_lists(xcc, se, cu, n_xcc: int) -> Topology:
+    t = Topology()
+    t.n_cus, t.n_xcc = len(xcc), n_xcc
+    for i in range(len(xcc)):
+        t.xcc[i], t.se[i], t.cu[i] = int(xcc[i]), int(se[i]), int(cu[i])
+    return t
+
+
+def hs_cu_partition(topo: Topology, shared_cus: int) -> Tuple[List[int], List[int]]:
+    sh = (ctypes.c_uint32 * 8)()
+    dn = (ctypes.c_uint32 * 8)()
+    _check(lib().hs_cu_partition(ctypes.byref(topo), shared_cus, sh, dn))
+    return list(sh), list(dn)
+
+
+def hs_plan_metadata(seq_offsets, ctx_lens=None) -> Tuple[np.ndarray, np.ndarray]:
+    off = _i32_array(seq_offsets)
+    T = int(off[len(off) - 1]) if len(off) else 0
+    pos = (ctypes.c_int32 * max(T, 1))()
+    sid = (ctypes.c_int32 * max(T, 1))()
+    _check(lib().hs_plan_metadata(off, _i32_array(ctx_lens), len(off) - 1, pos, sid))
+    return np.frombuffer(pos, dtype=np.int32)[:T].copy(), np.frombuffer(sid, dtype=np.int32)[:T].copy()
+
+
+def hs_workspace_size(cfg, max_tokens: int, max_seqs: int, max_pos: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().hs_workspace_size(ctypes.byref(LayerCfg.of(cfg)), max_tokens, max_seqs, max_pos, ctypes.byref(n)))
+    return int(n.value)
+
+
+# --------------------------------------------------------------------------- context
+
+class Context:
+    """Owns an ``hs_context`` (CU-masked stream ladder)."""
+
+    def __init__(self, device: int = 0, budgets: Sequence[int] = (64, 128, 192, 256),
+                 topo: Optional[Topology] = None):
+        h = ctypes.c_void_p()
+        b = _i32_array(list(budgets))
+        _check(lib().hs_context_create(device, b, len(budgets), ctypes.byref(topo) if topo else None,
+                                       ctypes.byref(h)))
+        self.handle = h
+        self.device = device
+
+    def close(self):
+        if self.handle:
+            lib().hs_context_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):  # pragma: no cover
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def hs_context_create(device: int = 0, budgets=(64, 128, 192, 256), topo=None) -> Context:
+    return Context(device, budgets, topo)
+
+
+def hs_context_stream(ctx: Context, cu_budget: int, role: int = HS_ROLE_SHARED) -> int:
+    s = ctypes.c_void_p()
+    _check(lib().hs_context_stream(ctx.handle, cu_budget, role, ctypes.byref(s)))
+    return int(s.value)
+
+
+def hs_context_masks(ctx: Context, cu_budget: int) -> Tuple[List[int], List[int]]:
+    sh = (ctypes.c_uint32 * 8)()
+    dn = (ctypes.c_uint32 * 8)()
+    _check(lib().hs_context_masks(ctx.handle, cu_budget, sh, dn))
+    return list(sh), list(dn)
+
+
+def hs_context_topology(ctx: Context) -> Topology:
+    t = Topology()
+    _check(lib().hs_context_topology(ctx.handle, ctypes.byref(t)))
+    return t
+
+
+def hs_context_destroy(ctx: Context) -> None:
+    ctx.close()
+
+
+# --------------------------------------------------------------------------- compute calls
+
+def _weights_array(weights: List[Dict[str, object]]):
+    arr = (LayerWeights * len(weights))()
+    for i, w in enumerate(weights):
+        for name in ("ln1", "w_qkv", "w_o", "ln2", "w_gate_up", "w_down"):
+            setattr(arr[i], name, _ptr(w[name]))
+    return arr
+
+
+def _kv_struct(kv) -> Optional[KvCache]:
+    """kv: None or (k_list, v_list, n_slots, max_ctx) of device tensors / pointers."""
+    if kv is None:
+        return None
+    k_list, v_list, n_slots, max_ctx = kv
+    kp = (ctypes.c_void_p * len(k_list))(*[_ptr(t) for t in k_list])
+    vp = (ctypes.c_void_p * len(v_list))(*[_ptr(t) for t in v_list])
+    s = KvCache(ctypes.cast(kp, ctypes.POINTER(ctypes.c_void_p)), ctypes.cast(vp, ctypes.POINTER(ctypes.c_void_p)),
+                n_slots, max_ctx)
+    s._keep = (kp, vp)
+    return s
+
+
+def hs_shared_stage_forward(ctx: Context, cfg, weights, x_in, x_out, seq_offsets, ctx_lens=None, kv=None,
+                            cu_budget: int = 256, stream=None, workspace=None, ws_bytes: Optional[int] = None) -> None:
+    warr = _weights_array(weights)
+    off = _i32_array(seq_offsets)
+    kvs = _kv_struct(kv)
+    if ws_bytes is None:
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().hs_shared_stage_forward(
+        ctx.handle, ctypes.byref(LayerCfg.of(cfg)), warr, len(weights), _ptr(x_in), _ptr(x_out), off,
+        _i32_array(ctx_lens), len(off) - 1, ctypes.byref(kvs) if kvs is not None else None, cu_budget,
+        _ptr(stream), _ptr(workspace), ws_bytes))
+
+
+def hs_downstream_decode_step(ctx: Context, cfg, weights, x_in, x_out, kv, kv_lens, cu_budget: int,
+                              stream=None, workspace=None, ws_bytes: Optional[int] = None) -> None:
+    warr = _weights_array(weights)
+    kvs = _kv_struct(kv)
+    lens = _i32_array(kv_lens)
+    if ws_bytes is None:
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().hs_downstream_decode_step(
+        ctx.handle, ctypes.byref(LayerCfg.of(cfg)), warr, len(weights), _ptr(x_in), _ptr(x_out),
+        ctypes.byref(kvs), lens, len(lens), cu_budget, _ptr(stream), _ptr(workspace), ws_bytes))
+
+
+def hs_probe_hw_ids(ctx: Context, stream, n_groups: int, out_ids) -> None:
+    _check(lib().hs_probe_hw_ids(ctx.handle, _ptr(stream), n_groups, _ptr(out_ids)))
+
+
+def hs_timing_enable(ctx: Context, enable: bool = True) -> None:
+    _check(lib().hs_timing_enable(ctx.handle, 1 if enable else 0))
+
+
+def hs_timing_read(ctx: Context, kind) -> Tuple[float, int]:
+    """(summed milliseconds, launches) of one kernel kind since timing was enabled."""
+    k = KERNEL_KINDS[kind] if isinstance(kind, str) else int(kind)
+    ms = ctypes.c_double(0)
+    n = ctypes.c_int32(0)
+    _check(lib().hs_timing_read(ctx.handle, k, ctypes.byref(ms), ctypes.byref(n)))
+    return float(ms.value), int(n.value)

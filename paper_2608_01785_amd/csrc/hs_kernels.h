@@ -1,0 +1,89 @@
+// Host-visible launch interface of the gfx950 kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hs {
+
+enum Epilogue : int {
+  EPI_STORE = 0,   // out = acc
+  EPI_RESID = 1,   // out = resid + acc
+  EPI_SWIGLU = 2,  // out = silu(gate) * up, gate/up rows gathered from [gate | up]
+  EPI_QKV = 3,     // RoPE on Q and K heads, Q -> q buffer, K/V -> key/value store
+};
+
+struct GemmArgs {
+  const uint16_t* A;  // activations [M, K] bf16 row-major
+  const uint16_t* W;  // weights [N, K] bf16 row-major
+  int M, K;
+  int n_tiles_n;      // output tiles along N (256 weight rows each; 128 outputs for SWIGLU)
+  uint16_t* out;      // STORE / RESID / SWIGLU output, row stride ldo
+  int ldo;
+  const uint16_t* resid;  // RESID: residual input with row stride ldo
+  int ffn;                // SWIGLU: offset of the 'up' rows
+  // QKV epilogue
+  uint16_t* q;            // [M, hq, dh]
+  uint16_t* kstore;       // keys: element k_off[m] + g * dh + d
+  uint16_t* vstore;       // values (dimension-major): v_off[m] + (g * dh + d) * v_stride
+  const int32_t* pos;     // [M] RoPE position of each row
+  const int64_t* k_off;   // [M]
+  const int64_t* v_off;   // [M]
+  int64_t v_stride;
+  const float2* rope;     // [max_pos, dh / 2] (cos, sin)
+  int hq, hkv, dh;
+};
+
+hipError_t launch_gemm(int epi, const GemmArgs& a, int max_blocks, hipStream_t s);
+
+struct AttnArgs {
+  const uint16_t* q;        // [T, hq, dh]
+  const uint16_t* kstore;   // token-major keys
+  const uint16_t* vstore;   // dimension-major values
+  uint16_t* o;              // [T, hq * dh]
+  const int32_t* items;     // [n_items][2] = (sequence, first query row within it)
+  int n_items;
+  const int32_t* seq_start; // [B] first packed row
+  const int32_t* seq_len;   // [B] query rows
+  const int32_t* seq_ctx;   // [B] cached rows before the chunk
+  const int64_t* seq_kbase; // [B] element offset of key position 0 (head 0)
+  const int64_t* seq_vbase; // [B] element offset of value position 0 (head 0, dim 0)
+  int64_t v_stride;
+  int hq, hkv, dh;
+  float scale_log2;         // log2(e) / sqrt(dh)
+};
+
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+
+// Single-row (decode) attention, split over key chunks, then combined.
+struct DecodeAttnArgs {
+  const uint16_t* q;
+  const uint16_t* kstore;
+  const uint16_t* vstore;
+  uint16_t* o;
+  const int4* items;        // [n_items] = (row index r, kv head g, chunk c, 0)
+  int n_items;
+  const int4* rows;         // [R] = (packed row t, sequence b, first item, n_chunks)
+  int n_rows;
+  const int32_t* seq_ctx;   // keys of row r's sequence: seq_ctx[b] + 1
+  const int64_t* seq_kbase;
+  const int64_t* seq_vbase;
+  int64_t v_stride;
+  float* part_o;            // [n_items, group, dh]
+  float* part_ml;           // [n_items, group, 2]
+  int hq, hkv, dh;
+  float scale_log2;
+};
+
+constexpr int kDecodeChunk = 256;
+
+hipError_t launch_decode_attention(const DecodeAttnArgs& a, hipStream_t s);
+
+hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* gamma, uint16_t* y, int rows, int d,
+                          float eps, int max_blocks, hipStream_t s);
+
+hipError_t launch_rope_table(float2* tab, int max_pos, int dh, float base, hipStream_t s);
+
+hipError_t launch_probe(uint32_t* out, int n_groups, hipStream_t s);
+
+}  // namespace hs

@@ -1,0 +1,120 @@
+// RMSNorm, RoPE table and topology-probe kernels for gfx950.
+#include "hs_device.h"
+#include "hs_kernels.h"
+
+namespace hs {
+namespace {
+
+constexpr int kMaxChunksPerLane = 16;  // hidden <= 64 lanes * 16 chunks * 8 = 8192
+
+// One wave per row: y = x / sqrt(mean(x^2) + eps) * gamma, fp32 reduction,
+// bf16 output.  16-byte loads; the row stays in registers between passes.
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x,
+                                                      const uint16_t* __restrict__ gamma,
+                                                      uint16_t* __restrict__ y, int rows, int d,
+                                                      float eps) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int chunks = d >> 3;
+  const float inv_d = 1.0f / float(d);
+  for (int row = blockIdx.x * 4 + wave; row < rows; row += gridDim.x * 4) {
+    const uint16_t* xr = x + int64_t(row) * d;
+    u32x4 v[kMaxChunksPerLane];
+    float ss = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kMaxChunksPerLane; ++i) {
+      const int c = lane + 64 * i;
+      if (c < chunks) {
+        v[i] = *reinterpret_cast<const u32x4*>(xr + c * 8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float lo = __uint_as_float(v[i][e] << 16);
+          const float hi = __uint_as_float(v[i][e] & 0xffff0000u);
+          ss += lo * lo + hi * hi;
+        }
+      }
+    }
+    ss = wave_sum(ss);
+    const float r = rsqrtf(ss * inv_d + eps);
+    uint16_t* yr = y + int64_t(row) * d;
+#pragma unroll
+    for (int i = 0; i < kMaxChunksPerLane; ++i) {
+      const int c = lane + 64 * i;
+      if (c < chunks) {
+        const u32x4 gv = *reinterpret_cast<const u32x4*>(gamma + c * 8);
+        u32x4 out;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float lo = __uint_as_float(v[i][e] << 16) * r * __uint_as_float(gv[e] << 16);
+          const float hi = __uint_as_float(v[i][e] & 0xffff0000u) * r * __uint_as_float(gv[e] & 0xffff0000u);
+          out[e] = pack2bf(lo, hi);
+        }
+        *reinterpret_cast<u32x4*>(yr + c * 8) = out;
+      }
+    }
+  }
+}
+
+// tab[p, j] = (cos, sin)(p * base^(-2j/dh)), angle formed in double precision.
+__global__ void rope_table_kernel(float2* tab, int max_pos, int dh, double base) {
+  const int half = dh / 2;
+  const int64_t n = int64_t(max_pos) * half;
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
+    const int p = int(i / half), j = int(i % half);
+    const double inv = pow(base, -2.0 * double(j) / double(dh));
+    double s, c;
+    sincos(double(p) * inv, &s, &c);
+    tab[i] = make_float2(float(c), float(s));
+  }
+}
+
+// HW_ID (hardware register 4) and XCC_ID (hardware register 20), full 32 bits.
+constexpr int kHwRegHwId = (31 << 11) | 4;
+constexpr int kHwRegXccId = (31 << 11) | 20;
+
+// Each block records where it ran: XCC id, shader engine, CU (shader-array
+// bit and CU id), and the constant 100 MHz clock.  Blocks then wait about
+// 20 microseconds (bounded) so that the dispatcher spreads them over CUs.
+__global__ void probe_kernel(uint32_t* out, int n) {
+  if (threadIdx.x == 0 && blockIdx.x < n) {
+    const uint32_t hw = __builtin_amdgcn_s_getreg(kHwRegHwId);
+    const uint32_t xcc = __builtin_amdgcn_s_getreg(kHwRegXccId);
+    const uint64_t t0 = wall_clock64();
+    u32x4 rec;
+    rec.x = xcc & 0xfu;
+    rec.y = (hw >> 13) & 0x7u;
+    rec.z = (((hw >> 12) & 1u) << 4) | ((hw >> 8) & 0xfu);
+    rec.w = uint32_t(t0);
+    *reinterpret_cast<u32x4*>(out + 4 * int64_t(blockIdx.x)) = rec;
+    while (wall_clock64() - t0 < 2000) {
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* gamma, uint16_t* y, int rows, int d,
+                          float eps, int max_blocks, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  int grid = (rows + 3) / 4;
+  if (grid > max_blocks) grid = max_blocks;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(grid), dim3(256), 0, s, x, gamma, y, rows, d, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_table(float2* tab, int max_pos, int dh, float base, hipStream_t s) {
+  if (max_pos <= 0) return hipSuccess;
+  const int64_t n = int64_t(max_pos) * (dh / 2);
+  int grid = int((n + 255) / 256);
+  if (grid > 4096) grid = 4096;
+  hipLaunchKernelGGL(rope_table_kernel, dim3(grid), dim3(256), 0, s, tab, max_pos, dh, double(base));
+  return hipGetLastError();
+}
+
+hipError_t launch_probe(uint32_t* out, int n_groups, hipStream_t s) {
+  if (n_groups <= 0) return hipSuccess;
+  hipLaunchKernelGGL(probe_kernel, dim3(n_groups), dim3(64), 0, s, out, n_groups);
+  return hipGetLastError();
+}
+
+}  // namespace hs

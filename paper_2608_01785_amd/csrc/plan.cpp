@@ -1,0 +1,342 @@
+// Host-only planner: status strings, thread-local errors, CU partition,
+// batch metadata, attention work lists and the workspace layout.
+#include "plan.h"
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <numeric>
+
+namespace hs {
+
+namespace {
+thread_local std::string g_error;
+}
+
+void set_error(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_error = buf;
+}
+
+hs_status fail(hs_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return s;
+}
+
+void clear_error() { g_error.clear(); }
+
+const char* last_error_cstr() { return g_error.c_str(); }
+
+hs_status validate_cfg(const hs_layer_cfg* c) {
+  if (!c) return fail(HS_ERR_INVALID_ARG, "layer config is null");
+  if (c->hidden <= 0 || c->hidden % 256 != 0 || c->hidden > 8192)
+    return fail(HS_ERR_UNSUPPORTED, "hidden %d must be a positive multiple of 256, at most 8192", c->hidden);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(HS_ERR_UNSUPPORTED, "head_dim %d must be 64 or 128", c->head_dim);
+  if (c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->n_q_heads % c->n_kv_heads != 0)
+    return fail(HS_ERR_INVALID_ARG, "n_q_heads %d must be a positive multiple of n_kv_heads %d",
+                c->n_q_heads, c->n_kv_heads);
+  if (c->n_q_heads / c->n_kv_heads > 8)
+    return fail(HS_ERR_UNSUPPORTED, "query heads per key/value head %d exceeds 8",
+                c->n_q_heads / c->n_kv_heads);
+  if (((c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim) % 256 != 0)
+    return fail(HS_ERR_UNSUPPORTED, "(Hq + 2 Hkv) * head_dim must be a multiple of 256");
+  if ((c->n_q_heads * c->head_dim) % 64 != 0)
+    return fail(HS_ERR_UNSUPPORTED, "Hq * head_dim must be a multiple of 64");
+  if (c->ffn <= 0 || c->ffn % 128 != 0)
+    return fail(HS_ERR_UNSUPPORTED, "ffn %d must be a positive multiple of 128", c->ffn);
+  if (!(c->rms_eps > 0.0f) || !(c->rope_base > 1.0f))
+    return fail(HS_ERR_INVALID_ARG, "rms_eps must be > 0 and rope_base > 1");
+  return HS_OK;
+}
+
+hs_status validate_batch(const int32_t* off, const int32_t* ctx, int32_t B, int32_t* n_tokens,
+                         int32_t* max_pos) {
+  if (!off) return fail(HS_ERR_INVALID_ARG, "seq_offsets is null");
+  if (B < 1) return fail(HS_ERR_INVALID_ARG, "n_seqs %d must be >= 1", B);
+  if (off[0] != 0) return fail(HS_ERR_INVALID_ARG, "seq_offsets[0] = %d, expected 0", off[0]);
+  int64_t mp = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    if (off[b + 1] < off[b])
+      return fail(HS_ERR_INVALID_ARG, "seq_offsets decrease at %d (%d -> %d)", b, off[b], off[b + 1]);
+    const int64_t c = ctx ? ctx[b] : 0;
+    if (c < 0) return fail(HS_ERR_INVALID_ARG, "ctx_lens[%d] = %lld is negative", b, (long long)c);
+    const int64_t end = c + (off[b + 1] - off[b]);
+    if (end > (int64_t(1) << 30)) return fail(HS_ERR_UNSUPPORTED, "position too large in sequence %d", b);
+    mp = std::max(mp, end);
+  }
+  if (off[B] <= 0) return fail(HS_ERR_INVALID_ARG, "batch has no rows");
+  *n_tokens = off[B];
+  *max_pos = int32_t(mp);
+  return HS_OK;
+}
+
+int64_t max_att_items(int32_t T, int32_t B) { return int64_t(T) / kAttnBlockQ + B + 1; }
+
+int64_t max_dec_items(const hs_layer_cfg& c, int32_t B, int32_t max_pos) {
+  return int64_t(B) * c.n_kv_heads * ((max_pos + kDecChunk - 1) / kDecChunk + 1);
+}
+
+static size_t meta_bytes(int32_t T, int32_t B, int64_t att, int64_t dec_items) {
+  size_t s = 0;
+  s += align_up(size_t(T) * 4, 16);       // pos
+  s += align_up(size_t(T) * 8, 16) * 2;   // k_off, v_off
+  s += align_up(size_t(B) * 4, 16) * 3;   // seq_start, seq_len, seq_ctx
+  s += align_up(size_t(B) * 8, 16) * 2;   // seq_kbase, seq_vbase
+  s += align_up(size_t(att) * 8, 16);     // att items
+  s += align_up(size_t(B) * 16, 16);      // dec rows
+  s += align_up(size_t(dec_items) * 16, 16);
+  return align_up(s, kAlign);
+}
+
+WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos) {
+  WsLayout w{};
+  const size_t d = c.hidden, hq = c.n_q_heads, hkv = c.n_kv_heads, dh = c.head_dim, f = c.ffn;
+  const int64_t dec = max_dec_items(c, B, max_pos);
+  size_t p = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = p;
+    p = align_up(p + bytes, kAlign);
+    return at;
+  };
+  w.meta_bytes = meta_bytes(T, B, max_att_items(T, B), dec);
+  w.meta = take(w.meta_bytes);
+  w.n = take(size_t(T) * d * 2);
+  w.q = take(size_t(T) * hq * dh * 2);
+  w.kpack = take(size_t(T + 64) * hkv * dh * 2);
+  w.v_stride = int64_t(align_up(size_t(T), 64)) + 64;
+  w.vpack = take(size_t(hkv) * dh * size_t(w.v_stride) * 2);
+  w.o = take(size_t(T) * hq * dh * 2);
+  w.h = take(size_t(T) * d * 2);
+  w.a = take(size_t(T) * f * 2);
+  w.xtmp = take(size_t(T) * d * 2);
+  w.rope = take(size_t(max_pos) * (dh / 2) * 8);
+  const size_t group = hq / hkv;
+  w.part_o = take(size_t(dec) * group * dh * 4);
+  w.part_ml = take(size_t(dec) * group * 2 * 4);
+  w.total = p;
+  return w;
+}
+
+hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* ctx, int32_t B,
+                     const KvPlacement& kv, Plan* out) {
+  Plan& P = *out;
+  hs_status st = validate_batch(off, ctx, B, &P.T, &P.max_pos);
+  if (st != HS_OK) return st;
+  P.B = B;
+  const int64_t hkv = c.n_kv_heads, dh = c.head_dim;
+  const int64_t T = P.T;
+
+  // Attention work: multi-row sequences in 128-row query blocks, longest
+  // key range first; single-row sequences take the split-key decode path.
+  struct Item { int32_t b, q0, keys; };
+  std::vector<Item> att;
+  std::vector<int32_t> dec_seq;
+  for (int32_t b = 0; b < B; ++b) {
+    const int32_t len = off[b + 1] - off[b];
+    const int32_t cx = ctx ? ctx[b] : 0;
+    if (len == 1) {
+      dec_seq.push_back(b);
+    } else {
+      for (int32_t q0 = 0; q0 < len; q0 += kAttnBlockQ)
+        att.push_back({b, q0, cx + std::min(q0 + kAttnBlockQ, len)});
+    }
+  }
+  std::stable_sort(att.begin(), att.end(), [](const Item& x, const Item& y) { return x.keys > y.keys; });
+  P.n_att_items = int32_t(att.size());
+  P.n_dec_rows = int32_t(dec_seq.size());
+  int64_t n_dec_items = 0;
+  for (int32_t b : dec_seq) {
+    const int32_t keys = (ctx ? ctx[b] : 0) + 1;
+    n_dec_items += hkv * ((keys + kDecChunk - 1) / kDecChunk);
+  }
+  P.n_dec_items = int32_t(n_dec_items);
+
+  // Image layout (must match meta_bytes' order and bounds).
+  size_t p = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = p;
+    p += align_up(bytes, 16);
+    return at;
+  };
+  P.pos = take(size_t(T) * 4);
+  P.k_off = take(size_t(T) * 8);
+  P.v_off = take(size_t(T) * 8);
+  P.seq_start = take(size_t(B) * 4);
+  P.seq_len = take(size_t(B) * 4);
+  P.seq_ctx = take(size_t(B) * 4);
+  P.seq_kbase = take(size_t(B) * 8);
+  P.seq_vbase = take(size_t(B) * 8);
+  P.att_items = take(size_t(P.n_att_items) * 8);
+  P.dec_rows = take(size_t(P.n_dec_rows) * 16);
+  P.dec_items = take(size_t(P.n_dec_items) * 16);
+  P.image.assign(align_up(p, kAlign), 0);
+
+  auto i32 = [&](size_t at) { return reinterpret_cast<int32_t*>(P.image.data() + at); };
+  auto i64 = [&](size_t at) { return reinterpret_cast<int64_t*>(P.image.data() + at); };
+
+  if (kv.cache) {
+    P.v_stride = kv.max_ctx;
+  } else {
+    P.v_stride = kv.packed_v_stride;
+  }
+  const int64_t slot_k = int64_t(kv.max_ctx) * hkv * dh;  // elements per cache slot (K)
+  const int64_t slot_v = hkv * dh * int64_t(kv.max_ctx);  // elements per cache slot (V)
+  for (int32_t b = 0; b < B; ++b) {
+    const int32_t cx = ctx ? ctx[b] : 0;
+    i32(P.seq_start)[b] = off[b];
+    i32(P.seq_len)[b] = off[b + 1] - off[b];
+    i32(P.seq_ctx)[b] = cx;
+    if (kv.cache) {
+      i64(P.seq_kbase)[b] = int64_t(b) * slot_k;
+      i64(P.seq_vbase)[b] = int64_t(b) * slot_v;
+    } else {
+      i64(P.seq_kbase)[b] = int64_t(off[b]) * hkv * dh;
+      i64(P.seq_vbase)[b] = off[b];
+    }
+    for (int32_t t = off[b]; t < off[b + 1]; ++t) {
+      const int32_t pos = cx + (t - off[b]);
+      i32(P.pos)[t] = pos;
+      if (kv.cache) {
+        i64(P.k_off)[t] = (int64_t(b) * kv.max_ctx + pos) * hkv * dh;
+        i64(P.v_off)[t] = int64_t(b) * slot_v + pos;
+      } else {
+        i64(P.k_off)[t] = int64_t(t) * hkv * dh;
+        i64(P.v_off)[t] = t;
+      }
+    }
+  }
+  for (int32_t i = 0; i < P.n_att_items; ++i) {
+    i32(P.att_items)[2 * i] = att[i].b;
+    i32(P.att_items)[2 * i + 1] = att[i].q0;
+  }
+  int32_t item = 0;
+  for (int32_t r = 0; r < P.n_dec_rows; ++r) {
+    const int32_t b = dec_seq[r];
+    const int32_t keys = (ctx ? ctx[b] : 0) + 1;
+    const int32_t nch = (keys + kDecChunk - 1) / kDecChunk;
+    int32_t* row = i32(P.dec_rows) + 4 * r;
+    row[0] = off[b];
+    row[1] = b;
+    row[2] = item;
+    row[3] = nch;
+    for (int32_t g = 0; g < hkv; ++g)
+      for (int32_t ch = 0; ch < nch; ++ch) {
+        int32_t* it = i32(P.dec_items) + 4 * item;
+        it[0] = r;
+        it[1] = g;
+        it[2] = ch;
+        it[3] = 0;
+        ++item;
+      }
+  }
+  return HS_OK;
+}
+
+}  // namespace hs
+
+// ---------------------------------------------------------------------------
+// Host-only C entry points.
+
+extern "C" {
+
+const char* hs_status_string(hs_status s) {
+  switch (s) {
+    case HS_OK: return "HS_OK";
+    case HS_ERR_INVALID_ARG: return "HS_ERR_INVALID_ARG";
+    case HS_ERR_UNSUPPORTED: return "HS_ERR_UNSUPPORTED";
+    case HS_ERR_BUDGET: return "HS_ERR_BUDGET";
+    case HS_ERR_WORKSPACE: return "HS_ERR_WORKSPACE";
+    case HS_ERR_HIP: return "HS_ERR_HIP";
+    case HS_ERR_INTERNAL: return "HS_ERR_INTERNAL";
+  }
+  return "HS_ERR_UNKNOWN";
+}
+
+const char* hs_last_error(void) { return hs::last_error_cstr(); }
+
+hs_status hs_default_topology(int32_t n_cus, int32_t n_xcc, hs_topology* out) {
+  if (!out) return hs::fail(HS_ERR_INVALID_ARG, "topology output is null");
+  if (n_cus < 1 || n_cus > 256 || n_xcc < 1 || n_xcc > hs::kMaxXcc || n_cus % n_xcc != 0)
+    return hs::fail(HS_ERR_INVALID_ARG, "bad topology size %d / %d", n_cus, n_xcc);
+  memset(out, 0, sizeof(*out));
+  out->n_cus = n_cus;
+  out->n_xcc = n_xcc;
+  for (int i = 0; i < n_cus; ++i) {
+    const int slot = i / n_xcc;
+    out->xcc[i] = uint8_t(i % n_xcc);
+    out->se[i] = uint8_t(slot % 4);
+    out->cu[i] = uint8_t(slot / 4);
+  }
+  return HS_OK;
+}
+
+hs_status hs_cu_partition(const hs_topology* t, int32_t c, uint32_t shared[8], uint32_t down[8]) {
+  if (!t || !shared || !down) return hs::fail(HS_ERR_INVALID_ARG, "null argument to hs_cu_partition");
+  if (t->n_cus < 1 || t->n_cus > 256 || t->n_xcc < 1 || t->n_xcc > hs::kMaxXcc)
+    return hs::fail(HS_ERR_INVALID_ARG, "bad topology (%d CUs, %d XCDs)", t->n_cus, t->n_xcc);
+  if (c < 1 || c > t->n_cus) return hs::fail(HS_ERR_BUDGET, "budget %d outside [1, %d]", c, t->n_cus);
+  uint32_t sh[8] = {0}, dn[8] = {0};
+  bool taken[256] = {false};
+  for (int x = 0; x < t->n_xcc; ++x) {
+    const int want = c / t->n_xcc + (x < c % t->n_xcc ? 1 : 0);
+    std::vector<int> bits;
+    for (int i = 0; i < t->n_cus; ++i)
+      if (t->xcc[i] == x) bits.push_back(i);
+    std::sort(bits.begin(), bits.end(), [&](int a, int b) {
+      if (t->cu[a] != t->cu[b]) return t->cu[a] < t->cu[b];
+      if (t->se[a] != t->se[b]) return t->se[a] < t->se[b];
+      return a < b;
+    });
+    if (int(bits.size()) < want)
+      return hs::fail(HS_ERR_INVALID_ARG, "XCD %d has %d CUs, %d requested", x, int(bits.size()), want);
+    for (int k = 0; k < want; ++k) taken[bits[k]] = true;
+  }
+  for (int i = 0; i < t->n_cus; ++i) {
+    if (taken[i])
+      sh[i / 32] |= 1u << (i % 32);
+    else
+      dn[i / 32] |= 1u << (i % 32);
+  }
+  memcpy(shared, sh, sizeof(sh));
+  memcpy(down, dn, sizeof(dn));
+  return HS_OK;
+}
+
+hs_status hs_plan_metadata(const int32_t* off, const int32_t* ctx, int32_t n_seqs, int32_t* pos_out,
+                           int32_t* seq_id_out) {
+  if (!pos_out || !seq_id_out) return hs::fail(HS_ERR_INVALID_ARG, "null output array");
+  int32_t T = 0, mp = 0;
+  hs_status st = hs::validate_batch(off, ctx, n_seqs, &T, &mp);
+  if (st != HS_OK) return st;
+  for (int32_t b = 0; b < n_seqs; ++b)
+    for (int32_t t = off[b]; t < off[b + 1]; ++t) {
+      pos_out[t] = (ctx ? ctx[b] : 0) + (t - off[b]);
+      seq_id_out[t] = b;
+    }
+  return HS_OK;
+}
+
+hs_status hs_workspace_size(const hs_layer_cfg* cfg, int32_t max_tokens, int32_t max_seqs, int32_t max_pos,
+                            size_t* bytes) {
+  hs_status st = hs::validate_cfg(cfg);
+  if (st != HS_OK) return st;
+  if (!bytes) return hs::fail(HS_ERR_INVALID_ARG, "bytes output is null");
+  if (max_tokens < 1 || max_seqs < 1 || max_pos < 1)
+    return hs::fail(HS_ERR_INVALID_ARG, "sizes must be >= 1");
+  *bytes = hs::ws_layout(*cfg, max_tokens, max_seqs, max_pos).total;
+  return HS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,80 @@
+// Host-only planner: validation, batch metadata, work lists and workspace
+// layout.  Pure C++ (no HIP), so it builds with g++ for sanitizer runs.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "horizon.h"
+
+namespace hs {
+
+void set_error(const char* fmt, ...);
+hs_status fail(hs_status s, const char* fmt, ...);
+void clear_error();
+
+constexpr int kMaxXcc = 8;
+constexpr size_t kAlign = 256;
+constexpr int kAttnBlockQ = 128;   // query rows per prefill-attention block
+constexpr int kDecChunk = 256;     // keys per decode-attention block
+
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+hs_status validate_cfg(const hs_layer_cfg* cfg);
+
+// Checks offsets (and optional cached lengths); returns T and the largest
+// position + 1 over all rows.
+hs_status validate_batch(const int32_t* seq_offsets, const int32_t* ctx_lens, int32_t n_seqs,
+                         int32_t* n_tokens, int32_t* max_pos);
+
+// Byte offsets of every buffer inside the caller's workspace.
+struct WsLayout {
+  size_t meta;        // metadata image (copied from the host each call)
+  size_t meta_bytes;
+  size_t n;           // [T, d] normalised rows
+  size_t q;           // [T, hq, dh]
+  size_t kpack;       // [T + 64, hkv, dh]   keys when no cache is given
+  size_t vpack;       // [hkv, dh, v_stride] values when no cache is given
+  int64_t v_stride;   // round_up(T, 64) + 64
+  size_t o;           // [T, hq * dh]
+  size_t h;           // [T, d]
+  size_t a;           // [T, ffn]
+  size_t xtmp;        // [T, d]
+  size_t rope;        // [max_pos, dh / 2] float2
+  size_t part_o;      // decode partials [items, group, dh] f32
+  size_t part_ml;     // [items, group, 2] f32
+  size_t total;
+};
+
+// Upper bounds used for sizing: T rows, B sequences, positions < max_pos.
+int64_t max_att_items(int32_t T, int32_t B);
+int64_t max_dec_items(const hs_layer_cfg& c, int32_t B, int32_t max_pos);
+
+WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos);
+
+// Metadata of one call, laid out as one host image mirrored in the workspace.
+struct Plan {
+  int32_t T = 0, B = 0, max_pos = 0;
+  std::vector<uint8_t> image;
+  // byte offsets inside image
+  size_t pos = 0, k_off = 0, v_off = 0;
+  size_t seq_start = 0, seq_len = 0, seq_ctx = 0, seq_kbase = 0, seq_vbase = 0;
+  size_t att_items = 0, dec_rows = 0, dec_items = 0;
+  int32_t n_att_items = 0, n_dec_rows = 0, n_dec_items = 0;
+  int64_t v_stride = 0;
+};
+
+// Key/value placement: packed (no cache, rows in the workspace) or cache slots.
+struct KvPlacement {
+  bool cache = false;
+  int32_t max_ctx = 0;
+  int64_t packed_v_stride = 0;
+};
+
+hs_status build_plan(const hs_layer_cfg& c, const int32_t* seq_offsets, const int32_t* ctx_lens,
+                     int32_t n_seqs, const KvPlacement& kv, Plan* out);
+
+}  // namespace hs

@@ -1,0 +1,525 @@
+// HIP runtime side of the C ABI: contexts with a ladder of CU-masked stream
+// pairs, argument checks, metadata staging and the per-layer launch sequence.
+#include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
+#include <string.h>
+
+#include <vector>
+
+#include "hs_kernels.h"
+#include "plan.h"
+
+namespace {
+
+constexpr int kStagingSlots = 4;
+
+struct Level {
+  int budget = 0;
+  uint32_t shared[8] = {0};
+  uint32_t down[8] = {0};
+  hipStream_t s_shared = nullptr;
+  hipStream_t s_down = nullptr;
+};
+
+struct Slot {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+
+int popcount8(const uint32_t m[8]) {
+  int n = 0;
+  for (int i = 0; i < 8; ++i) n += __builtin_popcount(m[i]);
+  return n;
+}
+
+#define HIP_TRY(expr)                                                                      \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess) return hs::fail(HS_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+}  // namespace
+
+struct hs_context {
+  int device = 0;
+  int n_cus = 0;
+  hs_topology topo{};
+  std::vector<Level> levels;
+  Slot slots[kStagingSlots];
+  int next_slot = 0;
+  // Optional per-launch event timing.
+  struct TimingRec {
+    int kind;
+    hipEvent_t a, b;
+  };
+  bool timing = false;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_next = 0;
+  std::vector<TimingRec> recs;
+};
+
+namespace {
+
+const Level* find_level(const hs_context* ctx, int budget) {
+  for (const Level& l : ctx->levels)
+    if (l.budget == budget) return &l;
+  return nullptr;
+}
+
+void destroy_context(hs_context* ctx) {
+  if (!ctx) return;
+  hipSetDevice(ctx->device);
+  for (Level& l : ctx->levels) {
+    if (l.s_shared) hipStreamDestroy(l.s_shared);
+    if (l.s_down) hipStreamDestroy(l.s_down);
+  }
+  for (hipEvent_t e : ctx->ev_pool) hipEventDestroy(e);
+  for (Slot& s : ctx->slots) {
+    if (s.ev) {
+      hipEventSynchronize(s.ev);
+      hipEventDestroy(s.ev);
+    }
+    if (s.host) hipHostFree(s.host);
+  }
+  delete ctx;
+}
+
+// Copy the plan's metadata image to the workspace through a pinned slot.
+hs_status stage_metadata(hs_context* ctx, const hs::Plan& plan, void* dst, hipStream_t s) {
+  Slot& slot = ctx->slots[ctx->next_slot];
+  ctx->next_slot = (ctx->next_slot + 1) % kStagingSlots;
+  if (slot.pending) {
+    HIP_TRY(hipEventSynchronize(slot.ev));
+    slot.pending = false;
+  }
+  const size_t bytes = plan.image.size();
+  if (slot.cap < bytes) {
+    if (slot.host) HIP_TRY(hipHostFree(slot.host));
+    slot.host = nullptr;
+    slot.cap = 0;
+    const size_t cap = hs::align_up(bytes, size_t(1) << 20);
+    HIP_TRY(hipHostMalloc(&slot.host, cap, hipHostMallocDefault));
+    slot.cap = cap;
+  }
+  memcpy(slot.host, plan.image.data(), bytes);
+  HIP_TRY(hipMemcpyAsync(dst, slot.host, bytes, hipMemcpyHostToDevice, s));
+  HIP_TRY(hipEventRecord(slot.ev, s));
+  slot.pending = true;
+  return HS_OK;
+}
+
+// Resolve the stream for (budget, role) and check that its mask carries the budget.
+hs_status resolve_stream(hs_context* ctx, int32_t budget, int role, void* stream, hipStream_t* out) {
+  if (budget < 1 || budget > ctx->n_cus)
+    return hs::fail(HS_ERR_BUDGET, "CU budget %d outside [1, %d]", budget, ctx->n_cus);
+  if (!stream) {
+    const int level_budget = role == HS_ROLE_SHARED ? budget : ctx->n_cus - budget;
+    const Level* l = find_level(ctx, level_budget);
+    if (!l) return hs::fail(HS_ERR_BUDGET, "no ladder level for a %s budget of %d CUs",
+                            role == HS_ROLE_SHARED ? "shared" : "downstream", budget);
+    *out = role == HS_ROLE_SHARED ? l->s_shared : l->s_down;
+    if (!*out) return hs::fail(HS_ERR_BUDGET, "ladder level %d has no downstream stream", level_budget);
+    return HS_OK;
+  }
+  uint32_t mask[8] = {0};
+  HIP_TRY(hipExtStreamGetCUMask(reinterpret_cast<hipStream_t>(stream), 8, mask));
+  const int n = popcount8(mask);
+  if (n != budget)
+    return hs::fail(HS_ERR_BUDGET, "stream carries %d CUs, budget is %d", n, budget);
+  *out = reinterpret_cast<hipStream_t>(stream);
+  return HS_OK;
+}
+
+template <typename T>
+T* at(void* base, size_t off) {
+  return reinterpret_cast<T*>(static_cast<uint8_t*>(base) + off);
+}
+
+constexpr size_t kTimingPairs = 8192;
+
+void timing_begin(hs_context* ctx, hipStream_t s, hipEvent_t* a, hipEvent_t* b) {
+  *a = *b = nullptr;
+  if (!ctx->timing || ctx->ev_next + 2 > ctx->ev_pool.size()) return;
+  *a = ctx->ev_pool[ctx->ev_next++];
+  *b = ctx->ev_pool[ctx->ev_next++];
+  hipEventRecord(*a, s);
+}
+
+void timing_end(hs_context* ctx, hipStream_t s, int kind, hipEvent_t a, hipEvent_t b) {
+  if (!a) return;
+  hipEventRecord(b, s);
+  ctx->recs.push_back({kind, a, b});
+}
+
+#define TIMED(kind, expr)                              \
+  do {                                                 \
+    hipEvent_t ta_, tb_;                               \
+    timing_begin(ctx, s, &ta_, &tb_);                  \
+    HIP_TRY(expr);                                     \
+    timing_end(ctx, s, kind, ta_, tb_);                \
+  } while (0)
+
+// Shared body of the prefill forward and the decode step.
+hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w, int32_t n_layers,
+                    const void* x_in, void* x_out, const int32_t* seq_offsets, const int32_t* ctx_lens,
+                    int32_t n_seqs, const hs_kv_cache* kv, int32_t budget, int role, void* stream,
+                    void* ws, size_t ws_bytes) {
+  hs::clear_error();
+  hs_status st = hs::validate_cfg(cfg);
+  if (st != HS_OK) return st;
+  if (!w || n_layers < 1) return hs::fail(HS_ERR_INVALID_ARG, "weights missing or n_layers %d < 1", n_layers);
+  for (int l = 0; l < n_layers; ++l)
+    if (!w[l].ln1 || !w[l].w_qkv || !w[l].w_o || !w[l].ln2 || !w[l].w_gate_up || !w[l].w_down)
+      return hs::fail(HS_ERR_INVALID_ARG, "layer %d has a null weight pointer", l);
+  if (!x_in || !x_out) return hs::fail(HS_ERR_INVALID_ARG, "x_in / x_out is null");
+  if (x_in == x_out) return hs::fail(HS_ERR_INVALID_ARG, "x_in and x_out must not alias");
+  int32_t T = 0, max_pos = 0;
+  st = hs::validate_batch(seq_offsets, ctx_lens, n_seqs, &T, &max_pos);
+  if (st != HS_OK) return st;
+  hs::KvPlacement place;
+  if (kv) {
+    if (!ctx_lens) return hs::fail(HS_ERR_INVALID_ARG, "a key/value cache needs ctx_lens");
+    if (!kv->k || !kv->v) return hs::fail(HS_ERR_INVALID_ARG, "cache pointer arrays are null");
+    for (int l = 0; l < n_layers; ++l)
+      if (!kv->k[l] || !kv->v[l]) return hs::fail(HS_ERR_INVALID_ARG, "cache of layer %d is null", l);
+    if (kv->max_ctx < 64 || kv->max_ctx % 64 != 0)
+      return hs::fail(HS_ERR_INVALID_ARG, "max_ctx %d must be a positive multiple of 64", kv->max_ctx);
+    if (n_seqs > kv->n_slots)
+      return hs::fail(HS_ERR_INVALID_ARG, "%d sequences but only %d cache slots", n_seqs, kv->n_slots);
+    if (max_pos > kv->max_ctx)
+      return hs::fail(HS_ERR_INVALID_ARG, "position %d exceeds max_ctx %d", max_pos - 1, kv->max_ctx);
+    place.cache = true;
+    place.max_ctx = kv->max_ctx;
+  } else if (ctx_lens) {
+    for (int b = 0; b < n_seqs; ++b)
+      if (ctx_lens[b] != 0)
+        return hs::fail(HS_ERR_INVALID_ARG, "ctx_lens[%d] = %d but no cache holds the prefix", b, ctx_lens[b]);
+  }
+  if (!ctx) return hs::fail(HS_ERR_INVALID_ARG, "context is null");
+  hipStream_t s = nullptr;
+  st = resolve_stream(ctx, budget, role, stream, &s);
+  if (st != HS_OK) return st;
+  if (!ws) return hs::fail(HS_ERR_WORKSPACE, "workspace is null");
+  const hs::WsLayout lay = hs::ws_layout(*cfg, T, n_seqs, max_pos);
+  if (ws_bytes < lay.total)
+    return hs::fail(HS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, lay.total);
+  place.packed_v_stride = lay.v_stride;
+  hs::Plan plan;
+  st = hs::build_plan(*cfg, seq_offsets, ctx_lens, n_seqs, place, &plan);
+  if (st != HS_OK) return st;
+  if (plan.image.size() > lay.meta_bytes) return hs::fail(HS_ERR_INTERNAL, "metadata image exceeds its region");
+
+  HIP_TRY(hipSetDevice(ctx->device));
+  st = stage_metadata(ctx, plan, at<void>(ws, lay.meta), s);
+  if (st != HS_OK) return st;
+
+  const int d = cfg->hidden, hq = cfg->n_q_heads, hkv = cfg->n_kv_heads, dh = cfg->head_dim, f = cfg->ffn;
+  uint8_t* meta = at<uint8_t>(ws, lay.meta);
+  const int32_t* d_pos = reinterpret_cast<const int32_t*>(meta + plan.pos);
+  const int64_t* d_koff = reinterpret_cast<const int64_t*>(meta + plan.k_off);
+  const int64_t* d_voff = reinterpret_cast<const int64_t*>(meta + plan.v_off);
+  float2* rope = at<float2>(ws, lay.rope);
+  uint16_t* n_buf = at<uint16_t>(ws, lay.n);
+  uint16_t* q_buf = at<uint16_t>(ws, lay.q);
+  uint16_t* o_buf = at<uint16_t>(ws, lay.o);
+  uint16_t* h_buf = at<uint16_t>(ws, lay.h);
+  uint16_t* a_buf = at<uint16_t>(ws, lay.a);
+  uint16_t* xtmp = at<uint16_t>(ws, lay.xtmp);
+
+  TIMED(HS_KERNEL_ROPE_TABLE, hs::launch_rope_table(rope, max_pos, dh, cfg->rope_base, s));
+
+  const int grid_cap = budget;  // persistent GEMM: one block per CU of the budget
+  const float scale_log2 = 1.4426950408889634f / sqrtf(float(dh));
+  const uint16_t* x_cur = static_cast<const uint16_t*>(x_in);
+  for (int l = 0; l < n_layers; ++l) {
+    // The last layer writes x_out; earlier layers alternate so that no layer
+    // reads and writes the same buffer.
+    const int remaining = n_layers - 1 - l;
+    uint16_t* x_next = (remaining % 2 == 0) ? static_cast<uint16_t*>(x_out) : xtmp;
+    uint16_t* kstore = place.cache ? static_cast<uint16_t*>(kv->k[l]) : at<uint16_t>(ws, lay.kpack);
+    uint16_t* vstore = place.cache ? static_cast<uint16_t*>(kv->v[l]) : at<uint16_t>(ws, lay.vpack);
+
+    TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(x_cur, static_cast<const uint16_t*>(w[l].ln1), n_buf, T, d,
+                                                cfg->rms_eps, 4 * budget, s));
+    hs::GemmArgs g{};
+    g.A = n_buf;
+    g.W = static_cast<const uint16_t*>(w[l].w_qkv);
+    g.M = T;
+    g.K = d;
+    g.n_tiles_n = (hq + 2 * hkv) * dh / 256;
+    g.q = q_buf;
+    g.kstore = kstore;
+    g.vstore = vstore;
+    g.pos = d_pos;
+    g.k_off = d_koff;
+    g.v_off = d_voff;
+    g.v_stride = plan.v_stride;
+    g.rope = rope;
+    g.hq = hq;
+    g.hkv = hkv;
+    g.dh = dh;
+    TIMED(HS_KERNEL_QKV, hs::launch_gemm(hs::EPI_QKV, g, grid_cap, s));
+
+    hs::AttnArgs at_args{};
+    at_args.q = q_buf;
+    at_args.kstore = kstore;
+    at_args.vstore = vstore;
+    at_args.o = o_buf;
+    at_args.items = reinterpret_cast<const int32_t*>(meta + plan.att_items);
+    at_args.n_items = plan.n_att_items;
+    at_args.seq_start = reinterpret_cast<const int32_t*>(meta + plan.seq_start);
+    at_args.seq_len = reinterpret_cast<const int32_t*>(meta + plan.seq_len);
+    at_args.seq_ctx = reinterpret_cast<const int32_t*>(meta + plan.seq_ctx);
+    at_args.seq_kbase = reinterpret_cast<const int64_t*>(meta + plan.seq_kbase);
+    at_args.seq_vbase = reinterpret_cast<const int64_t*>(meta + plan.seq_vbase);
+    at_args.v_stride = plan.v_stride;
+    at_args.hq = hq;
+    at_args.hkv = hkv;
+    at_args.dh = dh;
+    at_args.scale_log2 = scale_log2;
+    if (plan.n_att_items > 0) TIMED(HS_KERNEL_ATTENTION, hs::launch_attention(at_args, s));
+
+    hs::DecodeAttnArgs da{};
+    da.q = q_buf;
+    da.kstore = kstore;
+    da.vstore = vstore;
+    da.o = o_buf;
+    da.items = reinterpret_cast<const int4*>(meta + plan.dec_items);
+    da.n_items = plan.n_dec_items;
+    da.rows = reinterpret_cast<const int4*>(meta + plan.dec_rows);
+    da.n_rows = plan.n_dec_rows;
+    da.seq_ctx = at_args.seq_ctx;
+    da.seq_kbase = at_args.seq_kbase;
+    da.seq_vbase = at_args.seq_vbase;
+    da.v_stride = plan.v_stride;
+    da.part_o = at<float>(ws, lay.part_o);
+    da.part_ml = at<float>(ws, lay.part_ml);
+    da.hq = hq;
+    da.hkv = hkv;
+    da.dh = dh;
+    da.scale_log2 = scale_log2;
+    if (plan.n_dec_items > 0) TIMED(HS_KERNEL_DECODE_ATTN, hs::launch_decode_attention(da, s));
+
+    hs::GemmArgs go{};
+    go.A = o_buf;
+    go.W = static_cast<const uint16_t*>(w[l].w_o);
+    go.M = T;
+    go.K = hq * dh;
+    go.n_tiles_n = d / 256;
+    go.out = h_buf;
+    go.ldo = d;
+    go.resid = x_cur;
+    TIMED(HS_KERNEL_O_PROJ, hs::launch_gemm(hs::EPI_RESID, go, grid_cap, s));
+
+    TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(h_buf, static_cast<const uint16_t*>(w[l].ln2), n_buf, T, d,
+                                                cfg->rms_eps, 4 * budget, s));
+
+    hs::GemmArgs gu{};
+    gu.A = n_buf;
+    gu.W = static_cast<const uint16_t*>(w[l].w_gate_up);
+    gu.M = T;
+    gu.K = d;
+    gu.n_tiles_n = f / 128;
+    gu.out = a_buf;
+    gu.ldo = f;
+    gu.ffn = f;
+    TIMED(HS_KERNEL_GATE_UP, hs::launch_gemm(hs::EPI_SWIGLU, gu, grid_cap, s));
+
+    hs::GemmArgs gd{};
+    gd.A = a_buf;
+    gd.W = static_cast<const uint16_t*>(w[l].w_down);
+    gd.M = T;
+    gd.K = f;
+    gd.n_tiles_n = d / 256;
+    gd.out = x_next;
+    gd.ldo = d;
+    gd.resid = h_buf;
+    TIMED(HS_KERNEL_DOWN, hs::launch_gemm(hs::EPI_RESID, gd, grid_cap, s));
+    x_cur = x_next;
+  }
+  return HS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+hs_status hs_context_create(int32_t device, const int32_t* budgets, int32_t n_budgets, const hs_topology* topo,
+                            hs_context** out) {
+  hs::clear_error();
+  if (!out) return hs::fail(HS_ERR_INVALID_ARG, "output pointer is null");
+  *out = nullptr;
+  if (n_budgets < 0 || (n_budgets > 0 && !budgets))
+    return hs::fail(HS_ERR_INVALID_ARG, "budget list is null");
+  int n_dev = 0;
+  HIP_TRY(hipGetDeviceCount(&n_dev));
+  if (device < 0 || device >= n_dev) return hs::fail(HS_ERR_INVALID_ARG, "device %d of %d", device, n_dev);
+  HIP_TRY(hipSetDevice(device));
+  hipDeviceProp_t prop;
+  HIP_TRY(hipGetDeviceProperties(&prop, device));
+  const int n_cus = prop.multiProcessorCount;
+  if (n_cus < 1 || n_cus > 256) return hs::fail(HS_ERR_UNSUPPORTED, "%d compute units", n_cus);
+
+  hs_context* ctx = new hs_context();
+  ctx->device = device;
+  ctx->n_cus = n_cus;
+  if (topo) {
+    if (topo->n_cus != n_cus) {
+      delete ctx;
+      return hs::fail(HS_ERR_INVALID_ARG, "topology has %d CUs, device has %d", topo->n_cus, n_cus);
+    }
+    ctx->topo = *topo;
+  } else {
+    const int n_xcc = (n_cus % 8 == 0) ? 8 : 1;
+    hs_status st = hs_default_topology(n_cus, n_xcc, &ctx->topo);
+    if (st != HS_OK) {
+      delete ctx;
+      return st;
+    }
+  }
+  std::vector<int32_t> want(budgets, budgets + n_budgets);
+  bool has_full = false;
+  for (int32_t b : want) has_full |= (b == n_cus);
+  if (!has_full) want.push_back(n_cus);
+  for (int32_t b : want) {
+    if (find_level(ctx, b)) continue;
+    Level l;
+    l.budget = b;
+    hs_status st = hs_cu_partition(&ctx->topo, b, l.shared, l.down);
+    if (st != HS_OK) {
+      destroy_context(ctx);
+      return st;
+    }
+    hipError_t e;
+    if (b == n_cus) {
+      e = hipStreamCreateWithFlags(&l.s_shared, hipStreamNonBlocking);
+    } else {
+      e = hipExtStreamCreateWithCUMask(&l.s_shared, 8, l.shared);
+      if (e == hipSuccess) e = hipExtStreamCreateWithCUMask(&l.s_down, 8, l.down);
+    }
+    if (e != hipSuccess) {
+      ctx->levels.push_back(l);
+      destroy_context(ctx);
+      return hs::fail(HS_ERR_HIP, "stream creation for budget %d failed: %s", b, hipGetErrorString(e));
+    }
+    ctx->levels.push_back(l);
+  }
+  for (Slot& s : ctx->slots) {
+    hipError_t e = hipEventCreateWithFlags(&s.ev, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      destroy_context(ctx);
+      return hs::fail(HS_ERR_HIP, "event creation failed: %s", hipGetErrorString(e));
+    }
+  }
+  *out = ctx;
+  return HS_OK;
+}
+
+hs_status hs_context_topology(const hs_context* ctx, hs_topology* out) {
+  if (!ctx || !out) return hs::fail(HS_ERR_INVALID_ARG, "null argument");
+  *out = ctx->topo;
+  return HS_OK;
+}
+
+hs_status hs_context_stream(hs_context* ctx, int32_t cu_budget, int32_t role, void** stream_out) {
+  if (!ctx || !stream_out) return hs::fail(HS_ERR_INVALID_ARG, "null argument");
+  if (role != HS_ROLE_SHARED && role != HS_ROLE_DOWN) return hs::fail(HS_ERR_INVALID_ARG, "role %d", role);
+  const Level* l = find_level(ctx, cu_budget);
+  if (!l) return hs::fail(HS_ERR_BUDGET, "budget %d is not on the ladder", cu_budget);
+  hipStream_t s = role == HS_ROLE_SHARED ? l->s_shared : l->s_down;
+  if (!s) return hs::fail(HS_ERR_BUDGET, "the full budget has no downstream stream");
+  *stream_out = s;
+  return HS_OK;
+}
+
+hs_status hs_context_masks(const hs_context* ctx, int32_t cu_budget, uint32_t shared_mask[8], uint32_t down_mask[8]) {
+  if (!ctx) return hs::fail(HS_ERR_INVALID_ARG, "null context");
+  const Level* l = find_level(ctx, cu_budget);
+  if (!l) return hs::fail(HS_ERR_BUDGET, "budget %d is not on the ladder", cu_budget);
+  if (shared_mask) memcpy(shared_mask, l->shared, sizeof(l->shared));
+  if (down_mask) memcpy(down_mask, l->down, sizeof(l->down));
+  return HS_OK;
+}
+
+hs_status hs_context_destroy(hs_context* ctx) {
+  destroy_context(ctx);
+  return HS_OK;
+}
+
+hs_status hs_shared_stage_forward(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w,
+                                  int32_t n_layers, const void* x_in, void* x_out, const int32_t* seq_offsets,
+                                  const int32_t* ctx_lens, int32_t n_seqs, const hs_kv_cache* kv,
+                                  int32_t cu_budget, void* stream, void* workspace, size_t ws_bytes) {
+  return run_stack(ctx, cfg, w, n_layers, x_in, x_out, seq_offsets, ctx_lens, n_seqs, kv, cu_budget,
+                   HS_ROLE_SHARED, stream, workspace, ws_bytes);
+}
+
+hs_status hs_downstream_decode_step(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w,
+                                    int32_t n_layers, const void* x_in, void* x_out, const hs_kv_cache* kv,
+                                    const int32_t* kv_lens, int32_t batch, int32_t cu_budget, void* stream,
+                                    void* workspace, size_t ws_bytes) {
+  hs::clear_error();
+  if (!kv) return hs::fail(HS_ERR_INVALID_ARG, "decode needs a key/value cache");
+  if (!kv_lens) return hs::fail(HS_ERR_INVALID_ARG, "kv_lens is null");
+  if (batch < 1) return hs::fail(HS_ERR_INVALID_ARG, "batch %d < 1", batch);
+  std::vector<int32_t> off(batch + 1);
+  for (int32_t b = 0; b <= batch; ++b) off[b] = b;
+  return run_stack(ctx, cfg, w, n_layers, x_in, x_out, off.data(), kv_lens, batch, kv, cu_budget,
+                   HS_ROLE_DOWN, stream, workspace, ws_bytes);
+}
+
+hs_status hs_timing_enable(hs_context* ctx, int32_t enable) {
+  hs::clear_error();
+  if (!ctx) return hs::fail(HS_ERR_INVALID_ARG, "null context");
+  HIP_TRY(hipSetDevice(ctx->device));
+  if (enable && ctx->ev_pool.empty()) {
+    ctx->ev_pool.reserve(2 * kTimingPairs);
+    for (size_t i = 0; i < 2 * kTimingPairs; ++i) {
+      hipEvent_t e;
+      HIP_TRY(hipEventCreate(&e));
+      ctx->ev_pool.push_back(e);
+    }
+  }
+  // Finish outstanding records before their events can be recorded again.
+  for (const auto& r : ctx->recs) HIP_TRY(hipEventSynchronize(r.b));
+  ctx->recs.clear();
+  ctx->ev_next = 0;
+  ctx->timing = enable != 0;
+  return HS_OK;
+}
+
+hs_status hs_timing_read(hs_context* ctx, int32_t kind, double* total_ms, int32_t* n_launches) {
+  hs::clear_error();
+  if (!ctx || !total_ms || !n_launches) return hs::fail(HS_ERR_INVALID_ARG, "null argument");
+  if (kind < 0 || kind >= HS_KERNEL_KINDS) return hs::fail(HS_ERR_INVALID_ARG, "kernel kind %d", kind);
+  double total = 0.0;
+  int32_t n = 0;
+  for (const auto& r : ctx->recs) {
+    if (r.kind != kind) continue;
+    HIP_TRY(hipEventSynchronize(r.b));
+    float ms = 0.0f;
+    HIP_TRY(hipEventElapsedTime(&ms, r.a, r.b));
+    total += ms;
+    ++n;
+  }
+  *total_ms = total;
+  *n_launches = n;
+  return HS_OK;
+}
+
+hs_status hs_probe_hw_ids(hs_context* ctx, void* stream, int32_t n_groups, void* out_ids) {
+  hs::clear_error();
+  if (!ctx || !out_ids || n_groups < 1) return hs::fail(HS_ERR_INVALID_ARG, "bad probe arguments");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (!s) {
+    const Level* l = find_level(ctx, ctx->n_cus);
+    s = l->s_shared;
+  }
+  HIP_TRY(hipSetDevice(ctx->device));
+  HIP_TRY(hs::launch_probe(static_cast<uint32_t*>(out_ids), n_groups, s));
+  return HS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,183 @@
+"""The C ABI on the CPU: exported symbols, host-only entry points (bit-exact
+against the reference's integer side) and argument validation that must fail
+before anything reaches a GPU."""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+from oracle import partition as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+LIB = os.path.join(ROOT, "paper_2608_01785_amd", "libhorizon.so")
+HEADER = os.path.join(ROOT, "include", "horizon.h")
+
+
+@pytest.fixture(scope="module")
+def b():
+    if not os.path.exists(LIB):
+        pytest.skip("libhorizon.so not built")
+    from paper_2608_01785_amd import binding
+    binding.lib()
+    return binding
+
+
+def declared_functions():
+    import re
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:hs_status|const char\*)\s+(hs_\w+)\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported(b):
+    names = declared_functions()
+    assert len(names) >= 14
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], stdout=subprocess.PIPE, text=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    assert set(b.SYMBOLS) == set(names)
+    for n in names:
+        getattr(b.lib(), n)
+
+
+def test_status_strings(b):
+    assert b.lib().hs_status_string(0) == b"HS_OK"
+    assert b.lib().hs_status_string(3) == b"HS_ERR_BUDGET"
+
+
+@pytest.mark.parametrize("c", [1, 7, 8, 63, 64, 96, 100, 128, 160, 192, 250, 256])
+def test_partition_matches_reference_default_topology(b, c):
+    t = b.hs_default_topology(256, 8)
+    xcc, se, cu = P.default_topology()
+    assert list(t.xcc) == xcc and list(t.se) == se and list(t.cu) == cu
+    assert b.hs_cu_partition(t, c) == P.cu_partition(xcc, se, cu, 8, c)
+
+
+def test_partition_matches_reference_random_topologies(b):
+    rng = np.random.default_rng(0)
+    for trial in range(20):
+        n_xcc = int(rng.choice([1, 2, 4, 8]))
+        per = int(rng.integers(4, 33))
+        n = n_xcc * per
+        xcc = rng.permutation(np.repeat(np.arange(n_xcc), per)).tolist()
+        se = rng.integers(0, 4, size=n).tolist()
+        cu = rng.integers(0, 16, size=n).tolist()
+        t = b.topology_from_lists(xcc, se, cu, n_xcc)
+        for c in rng.integers(1, n + 1, size=5).tolist() + [n]:
+            assert b.hs_cu_partition(t, c) == P.cu_partition(xcc, se, cu, n_xcc, c), (trial, c)
+
+
+@pytest.mark.parametrize("c", [0, -5, 257])
+def test_partition_rejects_budget(b, c):
+    t = b.hs_default_topology()
+    with pytest.raises(b.HorizonError) as e:
+        b.hs_cu_partition(t, c)
+    assert e.value.status == b.HS_ERR_BUDGET
+
+
+def test_plan_metadata_matches_reference(b):
+    from paper_2608_01785_amd import workloads as W
+    cases = [([0, 96, 224], None), ([0, 2, 2, 5], [3, 0, 7])]
+    lengths, ctx = W.thinker_mixed_layout()
+    off = np.concatenate([[0], np.cumsum(lengths)])
+    cases.append((off.tolist(), ctx.tolist()))
+    tb = W.thinker_batch(hidden=8)
+    cases.append((tb.seq_offsets.tolist(), None))
+    for off, ctx in cases:
+        pos, sid = b.hs_plan_metadata(off, ctx)
+        rpos, rsid = P.plan_metadata(off, ctx)
+        np.testing.assert_array_equal(pos, rpos)
+        np.testing.assert_array_equal(sid, rsid)
+    for bad in ([1, 3], [0, 5, 4]):
+        with pytest.raises(b.HorizonError) as e:
+            b.hs_plan_metadata(bad)
+        assert e.value.status == b.HS_ERR_INVALID_ARG
+
+
+def test_workspace_size_monotone_and_validated(b):
+    from paper_2608_01785_amd import workloads as W
+    s1 = b.hs_workspace_size(W.THINKER, 1000, 4, 1000)
+    s2 = b.hs_workspace_size(W.THINKER, 2000, 4, 1000)
+    s3 = b.hs_workspace_size(W.THINKER, 2000, 8, 4000)
+    assert 0 < s1 < s2 < s3
+    import dataclasses
+    bad = dataclasses.replace(W.THINKER, head_dim=96)
+    with pytest.raises(b.HorizonError) as e:
+        b.hs_workspace_size(bad, 10, 1, 10)
+    assert e.value.status == b.HS_ERR_UNSUPPORTED
+    bad = dataclasses.replace(W.THINKER, n_kv_heads=5)
+    with pytest.raises(b.HorizonError) as e:
+        b.hs_workspace_size(bad, 10, 1, 10)
+    assert e.value.status == b.HS_ERR_INVALID_ARG
+
+
+def _forward_null_ctx(b, cfg, offsets, ctx_lens=None, x_in=1 << 20, x_out=2 << 20, kv=None, n_layers=1):
+    """Call the forward with a null context and fake (never dereferenced) pointers."""
+    from paper_2608_01785_amd import binding
+    w = (binding.LayerWeights * n_layers)()
+    for i in range(n_layers):
+        for name in ("ln1", "w_qkv", "w_o", "ln2", "w_gate_up", "w_down"):
+            setattr(w[i], name, 0x1000)
+    off = (ctypes.c_int32 * len(offsets))(*offsets)
+    cl = None if ctx_lens is None else (ctypes.c_int32 * len(ctx_lens))(*ctx_lens)
+    st = b.lib().hs_shared_stage_forward(None, ctypes.byref(binding.LayerCfg.of(cfg)), w, n_layers, x_in, x_out,
+                                         off, cl, len(offsets) - 1, kv, 256, None, 0x3000, 1 << 30)
+    return st, b.hs_last_error()
+
+
+def test_forward_validation_fails_before_any_gpu_work(b):
+    from paper_2608_01785_amd import workloads as W
+    c = W.TINY
+    st, msg = _forward_null_ctx(b, c, [0, 4, 9])
+    assert st == b.HS_ERR_INVALID_ARG and "context" in msg
+    st, msg = _forward_null_ctx(b, c, [0, 4, 3])
+    assert st == b.HS_ERR_INVALID_ARG and "decrease" in msg
+    st, msg = _forward_null_ctx(b, c, [1, 4])
+    assert st == b.HS_ERR_INVALID_ARG
+    st, msg = _forward_null_ctx(b, c, [0, 4], x_in=5, x_out=5)
+    assert st == b.HS_ERR_INVALID_ARG and "alias" in msg
+    st, msg = _forward_null_ctx(b, c, [0, 4], ctx_lens=[3])
+    assert st == b.HS_ERR_INVALID_ARG and "cache" in msg
+    st, msg = _forward_null_ctx(b, c, [0, 4], ctx_lens=[-1])
+    assert st == b.HS_ERR_INVALID_ARG
+    import dataclasses
+    st, msg = _forward_null_ctx(b, dataclasses.replace(c, hidden=320), [0, 4])
+    assert st == b.HS_ERR_UNSUPPORTED
+
+
+def test_host_planner_under_sanitizers(tmp_path):
+    """Build the host-only planner with g++ and ASan/UBSan and drive its entry points."""
+    gxx = "g++"
+    drv = tmp_path / "drv.cpp"
+    drv.write_text(r'''
+#include "horizon.h"
+#include <stdio.h>
+#include <vector>
+int main() {
+  hs_topology t;
+  if (hs_default_topology(256, 8, &t) != HS_OK) return 1;
+  uint32_t s[8], d[8];
+  for (int c = 1; c <= 256; ++c) if (hs_cu_partition(&t, c, s, d) != HS_OK) return 2;
+  if (hs_cu_partition(&t, 0, s, d) != HS_ERR_BUDGET) return 3;
+  int off[] = {0, 3, 3, 10}; int ctx[] = {5, 0, 2};
+  std::vector<int> pos(10), sid(10);
+  if (hs_plan_metadata(off, ctx, 3, pos.data(), sid.data()) != HS_OK) return 4;
+  if (pos[9] != 8 || sid[9] != 2) return 5;
+  hs_layer_cfg c = {3584, 28, 4, 128, 18944, 1e-6f, 1e4f};
+  size_t n = 0;
+  if (hs_workspace_size(&c, 10515, 8, 2048, &n) != HS_OK || n == 0) return 6;
+  printf("ok %zu\n", n);
+  return 0;
+}
+''')
+    exe = tmp_path / "drv"
+    src = os.path.join(ROOT, "paper_2608_01785_amd", "csrc", "plan.cpp")
+    cmd = [gxx, "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           f"-I{os.path.join(ROOT, 'include')}", f"-I{os.path.join(ROOT, 'paper_2608_01785_amd', 'csrc')}",
+           str(drv), src, "-o", str(exe)]
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    assert r.returncode == 0, r.stdout
+    r = subprocess.run([str(exe)], stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    assert r.returncode == 0 and r.stdout.startswith("ok"), r.stdout

@@ -1,0 +1,213 @@
+"""GPU parity of the HIP path against the float64 reference, through the C ABI.
+
+Sizes here are small enough for the reference to run in seconds yet span
+several GEMM tiles, ragged tails, both head sizes, grouped-query heads,
+single-row (decode-path) sequences and cached prefixes.
+"""
+import numpy as np
+import pytest
+
+from oracle import layer as ref
+from paper_2608_01785_amd import workloads as W
+from tests.gpu_common import TOL, err_ratio, log, require_gpu, workspace
+from tests.util import f64, weights_f64
+
+pytestmark = pytest.mark.gpu
+
+BUDGETS = (64, 96, 128, 160, 192, 256)
+
+
+@pytest.fixture(scope="module")
+def env():
+    torch = require_gpu()
+    from paper_2608_01785_amd import binding
+    ctx = binding.Context(0, budgets=BUDGETS)
+    yield torch, ctx
+    torch.cuda.synchronize()
+    ctx.close()
+
+
+def run_prefill(env, shape, wdev, x_bits, offsets, ctx_lens=None, cache=None, budget=256):
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    from paper_2608_01785_amd.device_data import to_device, to_bits
+    offsets = [int(o) for o in offsets]
+    B = len(offsets) - 1
+    cl = [0] * B if ctx_lens is None else [int(c) for c in ctx_lens]
+    max_pos = max(cl[b] + offsets[b + 1] - offsets[b] for b in range(B))
+    ws = workspace(torch, shape, offsets[-1], B, max_pos)
+    x = to_device(x_bits)
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, offsets, ctx_lens,
+                                    cache.as_arg() if cache is not None else None, budget, None, ws)
+    torch.cuda.synchronize()
+    return to_bits(y)
+
+
+def seeded_layers(shape, n_layers, seed):
+    return W.make_weights(shape, n_layers, seed)
+
+
+def test_tiny_layer_all_budgets(env):
+    torch, _ = env
+    from paper_2608_01785_amd.device_data import upload_weights
+    shape = W.TINY
+    layers = seeded_layers(shape, 1, W.SEEDS["tiny"]["weights"])
+    batch = W.tiny_batch()
+    expect, _ = ref.stack_forward(f64(batch.x), weights_f64(layers), shape, batch.seq_offsets)
+    wdev = upload_weights(layers)
+    outs = {}
+    for b in BUDGETS:
+        log(f"[tiny layer] budget {b}, T={batch.n_tokens}")
+        outs[b] = run_prefill(env, shape, wdev, batch.x, batch.seq_offsets, budget=b)
+        e = err_ratio(f64(outs[b]), expect)
+        log(f"  max err / rms = {e:.3e}")
+        assert e <= TOL
+    for b in BUDGETS:
+        np.testing.assert_array_equal(outs[b], outs[256])
+
+
+@pytest.mark.parametrize("shape_name,lengths,n_layers", [
+    ("thinker", [300, 129, 1, 64, 2], 1),
+    ("tiny", [1, 5, 255, 257, 33], 2),
+    ("talker", [70, 1, 190], 1),
+])
+def test_ragged_prefill_parity(env, shape_name, lengths, n_layers):
+    from paper_2608_01785_amd.device_data import upload_weights
+    shape = {"thinker": W.THINKER, "tiny": W.TINY, "talker": W.TALKER}[shape_name]
+    layers = seeded_layers(shape, n_layers, 77)
+    batch = W.random_batch(shape.hidden, lengths, seed=78)
+    log(f"[ragged prefill] {shape_name} lengths={lengths} layers={n_layers}")
+    expect, _ = ref.stack_forward(f64(batch.x), weights_f64(layers), shape, batch.seq_offsets)
+    got = run_prefill(env, shape, upload_weights(layers), batch.x, batch.seq_offsets, budget=128)
+    e = err_ratio(f64(got), expect)
+    log(f"  max err / rms = {e:.3e}")
+    assert e <= TOL
+
+
+def test_residual_identity_bit_exact(env):
+    from paper_2608_01785_amd.device_data import upload_weights
+    shape = W.TINY
+    layers = seeded_layers(shape, 2, 5)
+    for lw in layers:
+        lw["w_o"][:] = 0
+        lw["w_down"][:] = 0
+    batch = W.random_batch(shape.hidden, [40, 300, 1], seed=6)
+    log("[residual identity] tiny, 2 layers, W_o = W_down = 0")
+    got = run_prefill(env, shape, upload_weights(layers), batch.x, batch.seq_offsets)
+    np.testing.assert_array_equal(got, batch.x)
+
+
+def test_causal_invariance_and_isolation(env):
+    from paper_2608_01785_amd.device_data import upload_weights
+    shape = W.TINY
+    wdev = upload_weights(seeded_layers(shape, 1, 9))
+    batch = W.random_batch(shape.hidden, [200, 150], seed=10)
+    log("[causal] tiny, perturb rows >= 120 of sequence 0")
+    y1 = run_prefill(env, shape, wdev, batch.x, batch.seq_offsets)
+    x2 = batch.x.copy()
+    x2[120:200] = W.token_rows(11, 80, shape.hidden)
+    y2 = run_prefill(env, shape, wdev, x2, batch.seq_offsets)
+    np.testing.assert_array_equal(y2[:120], y1[:120])
+    np.testing.assert_array_equal(y2[200:], y1[200:])   # the other sequence is untouched
+    assert np.any(y2[120:200] != y1[120:200])
+    # Swapping the two sequences swaps the outputs.
+    xs = np.concatenate([batch.x[200:], batch.x[:200]])
+    ys = run_prefill(env, shape, wdev, xs, [0, 150, 350])
+    np.testing.assert_array_equal(ys[:150], y1[200:])
+    np.testing.assert_array_equal(ys[150:], y1[:200])
+
+
+def test_cached_prefix_chunks_and_cache_writes(env):
+    torch, _ = env
+    from paper_2608_01785_amd.device_data import DeviceCache, upload_weights
+    shape = W.THINKER_MIXED
+    lengths, ctx_lens = [200, 1, 1, 130], [300, 70, 500, 0]
+    layers = seeded_layers(shape, 1, 21)
+    batch = W.random_batch(shape.hidden, lengths, seed=22, ctx_lens=ctx_lens)
+    prefix = W.make_cache(shape, 1, ctx_lens, seed=23)
+    cache = DeviceCache(1, 4, 640, shape.n_kv_heads, shape.head_dim, fill=7.0)
+    for b, c in enumerate(ctx_lens):
+        cache.load_prefix(0, b, prefix.k[0][b], prefix.v[0][b])
+    torch.cuda.synchronize()
+    log(f"[cached prefix] thinker-mixed shape lengths={lengths} ctx={ctx_lens}")
+    expect, k_new, v_new = ref.layer_forward(
+        f64(batch.x), weights_f64(layers)[0], shape, batch.seq_offsets, ctx_lens,
+        [f64(k) for k in prefix.k[0]], [f64(v) for v in prefix.v[0]])
+    got = run_prefill(env, shape, upload_weights(layers), batch.x, batch.seq_offsets, ctx_lens, cache, budget=96)
+    e = err_ratio(f64(got), expect)
+    log(f"  max err / rms = {e:.3e}")
+    assert e <= TOL
+    off = batch.seq_offsets
+    for b in range(4):
+        c, n = ctx_lens[b], lengths[b]
+        kb, vb = cache.rows(0, b, 0, 640)
+        # Prefix untouched, new rows match the reference, the rest still holds the fill value.
+        np.testing.assert_array_equal(kb[:c], prefix.k[0][b])
+        np.testing.assert_array_equal(vb[:c], prefix.v[0][b])
+        assert err_ratio(f64(kb[c:c + n]), k_new[off[b]:off[b + 1]]) <= TOL
+        assert err_ratio(f64(vb[c:c + n]), v_new[off[b]:off[b + 1]]) <= TOL
+        assert np.all(f64(kb[c + n:]) == 7.0) and np.all(f64(vb[c + n:]) == 7.0)
+
+
+def test_talker_decode_step_parity(env):
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    from paper_2608_01785_amd.device_data import DeviceCache, to_bits, to_device, upload_weights
+    shape = W.TALKER
+    n_layers, batch = 4, 8
+    rng = np.random.default_rng(31)
+    kv_lens = rng.integers(1, 300, size=batch).astype(np.int32)
+    kv_lens[0] = 255  # new key lands at the end of a 256-key chunk
+    kv_lens[1] = 256  # new key starts a chunk
+    layers = seeded_layers(shape, n_layers, 32)
+    x = W.token_rows(33, batch, shape.hidden)
+    prefix = W.make_cache(shape, n_layers, kv_lens, seed=34)
+    cache = DeviceCache(n_layers, batch, 320, shape.n_kv_heads, shape.head_dim, fill=0.0)
+    for l in range(n_layers):
+        for b in range(batch):
+            cache.load_prefix(l, b, prefix.k[l][b], prefix.v[l][b])
+    log(f"[talker decode] layers={n_layers} batch={batch} kv_lens={kv_lens.tolist()}")
+    expect, kv_new = ref.decode_step(f64(x), weights_f64(layers), shape, kv_lens,
+                                     [[f64(k) for k in prefix.k[l]] for l in range(n_layers)],
+                                     [[f64(v) for v in prefix.v[l]] for l in range(n_layers)])
+    ws = workspace(torch, shape, batch, batch, int(kv_lens.max()) + 1)
+    xd = to_device(x)
+    y = torch.empty_like(xd)
+    torch.cuda.synchronize()
+    binding.hs_downstream_decode_step(ctx, shape, upload_weights(layers), xd, y, cache.as_arg(), kv_lens, 128,
+                                      None, ws)
+    torch.cuda.synchronize()
+    e = err_ratio(f64(to_bits(y)), expect)
+    log(f"  max err / rms = {e:.3e}")
+    assert e <= TOL
+    for l in range(n_layers):
+        for b in range(batch):
+            kb, vb = cache.rows(l, b, int(kv_lens[b]), int(kv_lens[b]) + 1)
+            assert err_ratio(f64(kb[0]), kv_new[l][0][b]) <= TOL
+            assert err_ratio(f64(vb[0]), kv_new[l][1][b]) <= TOL
+
+
+def test_masks_hold_on_hardware(env):
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    for budget in (64, 128, 192):
+        sh, dn = binding.hs_context_masks(ctx, budget)
+        popc = lambda ws: sum(bin(w).count("1") for w in ws)
+        assert popc(sh) == budget and popc(dn) == 256 - budget
+        seen = {}
+        for role in (binding.HS_ROLE_SHARED, binding.HS_ROLE_DOWN):
+            s = binding.hs_context_stream(ctx, budget, role)
+            n = 4096
+            out = torch.zeros(n * 4, dtype=torch.int32, device="cuda")
+            torch.cuda.synchronize()
+            log(f"[probe] budget {budget} role {role}")
+            binding.hs_probe_hw_ids(ctx, s, n, out)
+            torch.cuda.synchronize()
+            ids = out.view(n, 4).cpu().numpy()
+            seen[role] = {(int(a), int(b_), int(c)) for a, b_, c, _ in ids}
+            log(f"  distinct CUs used: {len(seen[role])}")
+        assert not (seen[0] & seen[1])
+        assert len(seen[0]) <= budget and len(seen[1]) <= 256 - budget
+        assert len(seen[0]) >= 0.9 * budget  # 4096 blocks spread over (nearly) every CU of the mask
