@@ -80,7 +80,7 @@ def main():
     log(f"[bench] generated thinker weights/batch in {time.time() - t0:.1f}s, T={batch.n_tokens}")
     wdev = upload_weights(layers, dev)
     x = to_device(batch.x, dev)
-    y = torch.empty_like(x)
+    y = torch.empty(x.shape, dtype=torch.float32, device=dev)
     T, B = batch.n_tokens, batch.n_seqs
     max_pos = int(batch.lengths.max())
     ws = torch.empty(binding.hs_workspace_size(shape, T, B, max_pos), dtype=torch.uint8, device=dev)
@@ -189,7 +189,7 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
         for b in range(bt):
             cache.fill_random(l, b, int(kv_lens[b]), gen)
     xt = to_device(W.talker_batch(ts_shape, ts_layers, bt, seeds, with_cache=False).x, dev)
-    yt = torch.empty_like(xt)
+    yt = torch.empty(xt.shape, dtype=torch.float32, device=dev)
     wst = torch.empty(binding.hs_workspace_size(ts_shape, bt, bt, int(kv_lens.max()) + 1), dtype=torch.uint8, device=dev)
     step_bytes = talker_bytes(ts_shape, ts_layers, kv_lens)
     s_sh = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_SHARED))

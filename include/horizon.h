@@ -19,7 +19,12 @@
  *   - Device pointers are HIP device addresses; "host" arrays are ordinary
  *     host memory that the call reads before it returns (the caller may
  *     reuse them at once).  Streams are hipStream_t passed as void*.
- *   - bf16 means IEEE bfloat16 stored as 16-bit words.
+ *   - bf16 means IEEE bfloat16 and fp16 IEEE binary16, stored as 16-bit words.
+ *   - Precision: token rows and weights are bf16 in memory; every contraction
+ *     runs on fp16 MFMA operands with fp32 accumulation (weights are converted
+ *     bf16 -> fp16 on load, exact for magnitudes in [2^-14, 65504]); the
+ *     residual stream is fp32; intermediate activations and the key/value
+ *     cache are fp16 (finite values saturate at +-65504).
  *   - Weight matrices are [out, in] row-major, so y = x * W^T.
  *   - Every function returns an hs_status.  No C++ exception crosses the
  *     ABI.  On any error other than HS_ERR_HIP nothing has been enqueued.
@@ -79,8 +84,8 @@ typedef struct hs_layer_weights {
 
 /* Key/value cache.  k[l] and v[l] are device pointers for layer l (host
  * arrays of n_layers pointers, owned by the caller).  Per layer:
- *   K: bf16 [n_slots, max_ctx, Hkv, dh]   (row-major, token-major)
- *   V: bf16 [n_slots, Hkv, dh, max_ctx]   (dimension-major: the P.V
+ *   K: fp16 [n_slots, max_ctx, Hkv, dh]   (row-major, token-major)
+ *   V: fp16 [n_slots, Hkv, dh, max_ctx]   (dimension-major: the P.V
  *      contraction reads keys contiguously)
  * Sequence b of a call uses slot b.  max_ctx % 64 == 0. */
 typedef struct hs_kv_cache {
@@ -160,7 +165,9 @@ hs_status hs_workspace_size(const hs_layer_cfg* cfg, int32_t max_tokens, int32_t
                             int32_t max_pos, size_t* bytes);
 
 /* Shared-stage forward: n_layers decoder layers over a packed ragged batch.
- *   x_in, x_out  bf16 [T, hidden] device, T = seq_offsets[n_seqs]; must not alias.
+ *   x_in         bf16 [T, hidden] device, T = seq_offsets[n_seqs].
+ *   x_out        fp32 [T, hidden] device (the residual stream is carried in
+ *                fp32 between layers); must not overlap x_in.
  *   w            host array of n_layers weight sets.
  *   seq_offsets  host [n_seqs + 1];  ctx_lens host [n_seqs] or NULL.
  *   kv           NULL: keys/values live in the workspace only (plain prefill).
@@ -185,7 +192,8 @@ hs_status hs_shared_stage_forward(hs_context* ctx, const hs_layer_cfg* cfg,
 
 /* Downstream decode step (§2.1: decode re-reads weights and the cache):
  * one new row per sequence through n_layers layers.
- *   x_in, x_out  bf16 [batch, hidden] device; must not alias.
+ *   x_in         bf16 [batch, hidden] device.
+ *   x_out        fp32 [batch, hidden] device; must not overlap x_in.
  *   kv_lens      host [batch]: cached rows before the step.  The new row is at
  *                position kv_lens[b], its K/V are written there in slot b, and
  *                it attends to kv_lens[b] + 1 keys.  kv_lens[b] < max_ctx.

@@ -149,7 +149,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
           const int row = 32 * st + perm32(fr);
           const int phys = (c & ~7) | ((c & 7) ^ kswz(row));
           const u32x4 kf = *reinterpret_cast<const u32x4*>(ks + row * KROW + phys * 16);
-          s[st] = mfma32(as_bf16x8(kf), as_bf16x8(qf[kb]), s[st]);
+          s[st] = mfma32(kf, qf[kb], s[st]);
         }
       }
       // Register r of subtile st holds key kv0 + 32 st + 16 (r / 8) + 8 fh + r % 8.
@@ -187,7 +187,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
       for (int kb2 = 0; kb2 < 4; ++kb2) {
         const int st = kb2 >> 1, r0 = 8 * (kb2 & 1);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) pf[kb2][e] = pack2bf(s[st][r0 + 2 * e], s[st][r0 + 2 * e + 1]);
+        for (int e = 0; e < 4; ++e) pf[kb2][e] = pack2h(s[st][r0 + 2 * e], s[st][r0 + 2 * e + 1]);
       }
 #pragma unroll
       for (int i = 0; i < NDS; ++i) {
@@ -196,7 +196,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
         for (int kb2 = 0; kb2 < 4; ++kb2) {
           const int c = 2 * kb2 + fh;
           const u32x4 vf = *reinterpret_cast<const u32x4*>(vs + d * 128 + ((c ^ (d & 7)) * 16));
-          o[i] = mfma32(as_bf16x8(vf), as_bf16x8(pf[kb2]), o[i]);
+          o[i] = mfma32(vf, pf[kb2], o[i]);
         }
       }
     }
@@ -213,8 +213,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
     for (int i = 0; i < NDS; ++i)
 #pragma unroll
       for (int gq = 0; gq < 4; ++gq)
-        store_bf16x4(op + 32 * i + 8 * gq, o[i][4 * gq] * inv, o[i][4 * gq + 1] * inv,
-                     o[i][4 * gq + 2] * inv, o[i][4 * gq + 3] * inv);
+        store_h4(op + 32 * i + 8 * gq, o[i][4 * gq] * inv, o[i][4 * gq + 1] * inv, o[i][4 * gq + 2] * inv,
+                 o[i][4 * gq + 3] * inv);
   }
 }
 
@@ -253,7 +253,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_attn_kernel(DecodeAttnArgs
 
   for (int i = tid; i < G * DH; i += kThreads) {
     const int hh = i / DH, d = i % DH;
-    qs[hh][d] = bf2f(a.q[(int64_t(t) * a.hq + g * G + hh) * DH + d]);
+    qs[hh][d] = h2f(a.q[(int64_t(t) * a.hq + g * G + hh) * DH + d]);
   }
   for (int i = tid; i < CK * KCH; i += kThreads) {
     const int row = i / KCH, cc = i % KCH;
@@ -294,10 +294,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_attn_kernel(DecodeAttnArgs
       const u32x4 kv = *reinterpret_cast<const u32x4*>(ks + j * KROW + phys * 16);
       float kf[8];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        kf[2 * e] = __uint_as_float(kv[e] << 16);
-        kf[2 * e + 1] = __uint_as_float(kv[e] & 0xffff0000u);
-      }
+      for (int e = 0; e < 4; ++e) h2x_to_f(kv[e], kf[2 * e], kf[2 * e + 1]);
 #pragma unroll
       for (int hh = 0; hh < MAXG; ++hh) {
         if (hh < G) {
@@ -353,10 +350,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_attn_kernel(DecodeAttnArgs
       const u32x4 vv = *reinterpret_cast<const u32x4*>(vs + d * VROW + phys * 16);
       float vf[8];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vf[2 * e] = __uint_as_float(vv[e] << 16);
-        vf[2 * e + 1] = __uint_as_float(vv[e] & 0xffff0000u);
-      }
+      for (int e = 0; e < 4; ++e) h2x_to_f(vv[e], vf[2 * e], vf[2 * e + 1]);
 #pragma unroll
       for (int hh = 0; hh < MAXG; ++hh)
         if (hh < G) {
@@ -409,7 +403,7 @@ __global__ __launch_bounds__(128) void decode_combine_kernel(DecodeAttnArgs a) {
     den += w * a.part_ml[(item * G + hh) * 2 + 1];
     num += w * a.part_o[(item * G + hh) * DH + d];
   }
-  a.o[int64_t(t) * a.hq * DH + h * DH + d] = f2bf(num / den);
+  a.o[int64_t(t) * a.hq * DH + h * DH + d] = f2h(num / den);
 }
 
 }  // namespace

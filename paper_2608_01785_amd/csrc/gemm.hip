@@ -1,7 +1,10 @@
-// Persistent bf16 MFMA GEMM for gfx950 with fused epilogues.
+// Persistent fp16 MFMA GEMM for gfx950 with fused epilogues.
 //
-// Computes C[M, N] = A[M, K] * W[N, K]^T (activations times [out, in]
-// weights).  The MFMA is issued as C^T = W * A^T: the weight tile is the MFMA
+// Computes C[M, N] = A[M, K] * W[N, K]^T (fp16 activations times bf16 [out, in]
+// weights, fp32 accumulation).  Weight tiles are converted bf16 -> fp16 on
+// their way into LDS (exact for the weight range), so both MFMA operands are
+// fp16: the same MFMA rate as bf16 on gfx950 with 8x finer rounding of the
+// activations.  The MFMA is issued as C^T = W * A^T: the weight tile is the MFMA
 // A operand and the activation tile the B operand, so every lane of the 32x32
 // accumulator owns one activation row and four consecutive output columns per
 // register group.  That makes 8-byte output stores possible and keeps the
@@ -95,7 +98,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int off = (ld_row + 32 * j) * kRowBytes + ld_phys * 16;
-        *reinterpret_cast<u32x4*>(base + off) = rw[j];
+        *reinterpret_cast<u32x4*>(base + off) = bf8_to_h8(rw[j]);
         *reinterpret_cast<u32x4*>(base + kTileBytes + off) = ra[j];
       }
     };
@@ -129,7 +132,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(as_bf16x8(wf[i]), as_bf16x8(af[j]), acc[i][j]);
+          for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(wf[i], af[j], acc[i][j]);
       }
       if (kt + 1 < KT) lstore(cur ^ 1);
       __syncthreads();
@@ -141,21 +144,28 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     for (int j = 0; j < 4; ++j) {
       const int m = m0 + j * 32;
       if (m >= a.M) continue;
-      if constexpr (EPI == EPI_STORE || EPI == EPI_RESID) {
+      if constexpr (EPI == EPI_RESID) {
+        // out (fp32) = resid (bf16 or fp32) + acc: the residual stream stays in fp32.
         const int n_base = tile_n * BN + wn * 128 + 4 * fh;
+        float* orow = a.out_f32 + int64_t(m) * a.ldo;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const int n = n_base + i * 32 + 8 * g;
-            float v[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-            if constexpr (EPI == EPI_RESID) {
+            f32x4 v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+            if (a.resid_f32) {
+              const f32x4 r = *reinterpret_cast<const f32x4*>(a.resid_f32 + int64_t(m) * a.ldo + n);
+              v += r;
+            } else {
               float r[4];
               load_bf16x4(a.resid + int64_t(m) * a.ldo + n, r);
-#pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] += r[e];
+              v[0] += r[0];
+              v[1] += r[1];
+              v[2] += r[2];
+              v[3] += r[3];
             }
-            store_bf16x4(a.out + int64_t(m) * a.ldo + n, v[0], v[1], v[2], v[3]);
+            *reinterpret_cast<f32x4*>(orow + n) = v;
           }
       } else if constexpr (EPI == EPI_SWIGLU) {
         const int c_base = tile_n * 128 + wn * 64 + 4 * fh;
@@ -166,7 +176,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
             float v[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) v[e] = silu(acc[i][j][4 * g + e]) * acc[i + 2][j][4 * g + e];
-            store_bf16x4(a.out + int64_t(m) * a.ldo + c_base + i * 32 + 8 * g, v[0], v[1], v[2], v[3]);
+            store_h4(a.out + int64_t(m) * a.ldo + c_base + i * 32 + 8 * g, v[0], v[1], v[2], v[3]);
           }
       } else {  // EPI_QKV
         const int p = a.pos[m];
@@ -199,15 +209,15 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
               uint16_t* dst = (head < a.hq)
                                   ? a.q + (int64_t(m) * a.hq + head) * DH
                                   : a.kstore + a.k_off[m] + int64_t(head - a.hq) * DH;
-              store_bf16x4(dst + d, rl[0], rl[1], rl[2], rl[3]);
-              store_bf16x4(dst + d + DH / 2, rh[0], rh[1], rh[2], rh[3]);
+              store_h4(dst + d, rl[0], rl[1], rl[2], rl[3]);
+              store_h4(dst + d + DH / 2, rh[0], rh[1], rh[2], rh[3]);
             } else {
               const int gh = head - a.hq - a.hkv;
               uint16_t* dst = a.vstore + a.v_off[m];
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
-                dst[int64_t(gh * DH + d + e) * a.v_stride] = f2bf(lo[e]);
-                dst[int64_t(gh * DH + d + DH / 2 + e) * a.v_stride] = f2bf(hi[e]);
+                dst[int64_t(gh * DH + d + e) * a.v_stride] = f2h(lo[e]);
+                dst[int64_t(gh * DH + d + DH / 2 + e) * a.v_stride] = f2h(hi[e]);
               }
             }
           }
@@ -231,7 +241,6 @@ hipError_t launch_one(const GemmArgs& a, int max_blocks, hipStream_t s) {
 hipError_t launch_gemm(int epi, const GemmArgs& a, int max_blocks, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   switch (epi) {
-    case EPI_STORE: return launch_one<EPI_STORE, 128>(a, max_blocks, s);
     case EPI_RESID: return launch_one<EPI_RESID, 128>(a, max_blocks, s);
     case EPI_SWIGLU: return launch_one<EPI_SWIGLU, 128>(a, max_blocks, s);
     case EPI_QKV:

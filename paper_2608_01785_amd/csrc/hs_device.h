@@ -7,8 +7,7 @@
 
 namespace hs {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -16,33 +15,56 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 constexpr int kNumXcd = 8;
+constexpr float kF16Max = 65504.0f;
 
-// 32x32x16 bf16 MFMA, fp32 accumulate.
+// 32x32x16 fp16 MFMA, fp32 accumulate.  Operands are 8 packed fp16 values.
 //   A operand: lane l holds A[i = l % 32][k = 8 (l / 32) + 0..7]
 //   B operand: lane l holds B[k = 8 (l / 32) + 0..7][j = l % 32]
 //   D:         lane l, register r holds D[i = 8 (r / 4) + 4 (l / 32) + r % 4][j = l % 32]
-__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+__device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c,
+                                                0, 0, 0);
 }
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
 
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  __bf16 b = (__bf16)f;  // round to nearest even (v_cvt_pk_bf16_f32 on gfx950)
-  return __builtin_bit_cast(uint16_t, b);
+__device__ __forceinline__ float h2f(uint16_t h) { return float(__builtin_bit_cast(_Float16, h)); }
+
+// fp32 -> fp16, round to nearest even, saturated to the finite range.
+__device__ __forceinline__ uint16_t f2h(float f) {
+  f = fminf(fmaxf(f, -kF16Max), kF16Max);
+  return __builtin_bit_cast(uint16_t, (_Float16)f);
 }
 
-__device__ __forceinline__ uint32_t pack2bf(float lo, float hi) {
-  return uint32_t(f2bf(lo)) | (uint32_t(f2bf(hi)) << 16);
+__device__ __forceinline__ uint32_t pack2h(float lo, float hi) {
+  return uint32_t(f2h(lo)) | (uint32_t(f2h(hi)) << 16);
 }
 
-__device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& v) { return __builtin_bit_cast(bf16x8, v); }
+// Two bf16 values (one 32-bit word) -> two fp16 values.  Exact for
+// magnitudes in [2^-14, 65504]; smaller values become fp16 subnormals
+// (absolute error below 2^-24).  Round-toward-zero conversion is used because
+// it is a single packed instruction and is exact wherever fp16 can hold the
+// bf16 value.
+__device__ __forceinline__ uint32_t bf2x_to_h2x(uint32_t u) {
+  const float lo = __uint_as_float(u << 16);
+  const float hi = __uint_as_float(u & 0xffff0000u);
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(lo, hi));
+}
 
-// Store 4 consecutive bf16 values (8 bytes, 8-byte aligned).
-__device__ __forceinline__ void store_bf16x4(uint16_t* p, float a, float b, float c, float d) {
+__device__ __forceinline__ u32x4 bf8_to_h8(const u32x4& v) {
+  u32x4 r;
+  r.x = bf2x_to_h2x(v.x);
+  r.y = bf2x_to_h2x(v.y);
+  r.z = bf2x_to_h2x(v.z);
+  r.w = bf2x_to_h2x(v.w);
+  return r;
+}
+
+// Store 4 consecutive fp16 values (8 bytes, 8-byte aligned).
+__device__ __forceinline__ void store_h4(uint16_t* p, float a, float b, float c, float d) {
   u32x2 v;
-  v.x = pack2bf(a, b);
-  v.y = pack2bf(c, d);
+  v.x = pack2h(a, b);
+  v.y = pack2h(c, d);
   *reinterpret_cast<u32x2*>(p) = v;
 }
 
@@ -52,6 +74,12 @@ __device__ __forceinline__ void load_bf16x4(const uint16_t* p, float out[4]) {
   out[1] = __uint_as_float(v.x & 0xffff0000u);
   out[2] = __uint_as_float(v.y << 16);
   out[3] = __uint_as_float(v.y & 0xffff0000u);
+}
+
+// Two packed fp16 values -> floats.
+__device__ __forceinline__ void h2x_to_f(uint32_t u, float& lo, float& hi) {
+  lo = h2f(uint16_t(u & 0xffffu));
+  hi = h2f(uint16_t(u >> 16));
 }
 
 // Work-groups of a launch are handed to the 8 XCDs round-robin (block b runs

@@ -7,23 +7,24 @@
 namespace hs {
 
 enum Epilogue : int {
-  EPI_STORE = 0,   // out = acc
-  EPI_RESID = 1,   // out = resid + acc
+  EPI_RESID = 1,   // out_f32 = resid + acc
   EPI_SWIGLU = 2,  // out = silu(gate) * up, gate/up rows gathered from [gate | up]
   EPI_QKV = 3,     // RoPE on Q and K heads, Q -> q buffer, K/V -> key/value store
 };
 
 struct GemmArgs {
-  const uint16_t* A;  // activations [M, K] bf16 row-major
+  const uint16_t* A;  // activations [M, K] fp16 row-major
   const uint16_t* W;  // weights [N, K] bf16 row-major
   int M, K;
   int n_tiles_n;      // output tiles along N (256 weight rows each; 128 outputs for SWIGLU)
-  uint16_t* out;      // STORE / RESID / SWIGLU output, row stride ldo
+  uint16_t* out;      // SWIGLU output (fp16), row stride ldo
+  float* out_f32;     // RESID output (fp32), row stride ldo
   int ldo;
-  const uint16_t* resid;  // RESID: residual input with row stride ldo
+  const uint16_t* resid;     // RESID: bf16 residual input with row stride ldo, or
+  const float* resid_f32;    //        fp32 residual input (used when non-null)
   int ffn;                // SWIGLU: offset of the 'up' rows
   // QKV epilogue
-  uint16_t* q;            // [M, hq, dh]
+  uint16_t* q;            // [M, hq, dh] fp16
   uint16_t* kstore;       // keys: element k_off[m] + g * dh + d
   uint16_t* vstore;       // values (dimension-major): v_off[m] + (g * dh + d) * v_stride
   const int32_t* pos;     // [M] RoPE position of each row
@@ -79,8 +80,9 @@ constexpr int kDecodeChunk = 256;
 
 hipError_t launch_decode_attention(const DecodeAttnArgs& a, hipStream_t s);
 
-hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* gamma, uint16_t* y, int rows, int d,
-                          float eps, int max_blocks, hipStream_t s);
+// x is bf16 (x_f32 null) or fp32 (x_f32 non-null); y is fp16.
+hipError_t launch_rmsnorm(const uint16_t* x, const float* x_f32, const uint16_t* gamma, uint16_t* y, int rows,
+                          int d, float eps, int max_blocks, hipStream_t s);
 
 hipError_t launch_rope_table(float2* tab, int max_pos, int dh, float base, hipStream_t s);
 

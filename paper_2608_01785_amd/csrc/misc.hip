@@ -8,30 +8,41 @@ namespace {
 constexpr int kMaxChunksPerLane = 16;  // hidden <= 64 lanes * 16 chunks * 8 = 8192
 
 // One wave per row: y = x / sqrt(mean(x^2) + eps) * gamma, fp32 reduction,
-// bf16 output.  16-byte loads; the row stays in registers between passes.
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x,
-                                                      const uint16_t* __restrict__ gamma,
-                                                      uint16_t* __restrict__ y, int rows, int d,
-                                                      float eps) {
+// fp16 output (the next GEMM's operand).  The input row (bf16 or fp32) stays in registers between the
+// two passes; loads are 16 bytes wide.
+template <typename TIn>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const TIn* __restrict__ x, const uint16_t* __restrict__ gamma,
+                                                      uint16_t* __restrict__ y, int rows, int d, float eps) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int chunks = d >> 3;
+  const int chunks = d >> 3;  // 8 elements per chunk
   const float inv_d = 1.0f / float(d);
   for (int row = blockIdx.x * 4 + wave; row < rows; row += gridDim.x * 4) {
-    const uint16_t* xr = x + int64_t(row) * d;
-    u32x4 v[kMaxChunksPerLane];
+    const TIn* xr = x + int64_t(row) * d;
+    float v[kMaxChunksPerLane][8];
     float ss = 0.0f;
 #pragma unroll
     for (int i = 0; i < kMaxChunksPerLane; ++i) {
       const int c = lane + 64 * i;
       if (c < chunks) {
-        v[i] = *reinterpret_cast<const u32x4*>(xr + c * 8);
+        if constexpr (sizeof(TIn) == 2) {
+          const u32x4 u = *reinterpret_cast<const u32x4*>(xr + c * 8);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float lo = __uint_as_float(v[i][e] << 16);
-          const float hi = __uint_as_float(v[i][e] & 0xffff0000u);
-          ss += lo * lo + hi * hi;
+          for (int e = 0; e < 4; ++e) {
+            v[i][2 * e] = __uint_as_float(u[e] << 16);
+            v[i][2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+          }
+        } else {
+          const f32x4 lo = *reinterpret_cast<const f32x4*>(xr + c * 8);
+          const f32x4 hi = *reinterpret_cast<const f32x4*>(xr + c * 8 + 4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[i][e] = lo[e];
+            v[i][4 + e] = hi[e];
+          }
         }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ss += v[i][e] * v[i][e];
       }
     }
     ss = wave_sum(ss);
@@ -45,9 +56,9 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
         u32x4 out;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float lo = __uint_as_float(v[i][e] << 16) * r * __uint_as_float(gv[e] << 16);
-          const float hi = __uint_as_float(v[i][e] & 0xffff0000u) * r * __uint_as_float(gv[e] & 0xffff0000u);
-          out[e] = pack2bf(lo, hi);
+          const float lo = v[i][2 * e] * r * __uint_as_float(gv[e] << 16);
+          const float hi = v[i][2 * e + 1] * r * __uint_as_float(gv[e] & 0xffff0000u);
+          out[e] = pack2h(lo, hi);
         }
         *reinterpret_cast<u32x4*>(yr + c * 8) = out;
       }
@@ -93,12 +104,15 @@ __global__ void probe_kernel(uint32_t* out, int n) {
 
 }  // namespace
 
-hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* gamma, uint16_t* y, int rows, int d,
-                          float eps, int max_blocks, hipStream_t s) {
+hipError_t launch_rmsnorm(const uint16_t* x, const float* x_f32, const uint16_t* gamma, uint16_t* y, int rows,
+                          int d, float eps, int max_blocks, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   int grid = (rows + 3) / 4;
   if (grid > max_blocks) grid = max_blocks;
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3(grid), dim3(256), 0, s, x, gamma, y, rows, d, eps);
+  if (x_f32)
+    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(grid), dim3(256), 0, s, x_f32, gamma, y, rows, d, eps);
+  else
+    hipLaunchKernelGGL(rmsnorm_kernel<uint16_t>, dim3(grid), dim3(256), 0, s, x, gamma, y, rows, d, eps);
   return hipGetLastError();
 }
 

@@ -118,9 +118,9 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
   w.v_stride = int64_t(align_up(size_t(T), 64)) + 64;
   w.vpack = take(size_t(hkv) * dh * size_t(w.v_stride) * 2);
   w.o = take(size_t(T) * hq * dh * 2);
-  w.h = take(size_t(T) * d * 2);
+  w.h = take(size_t(T) * d * 4);
   w.a = take(size_t(T) * f * 2);
-  w.xtmp = take(size_t(T) * d * 2);
+  w.xtmp = take(size_t(T) * d * 4);
   w.rope = take(size_t(max_pos) * (dh / 2) * 8);
   const size_t group = hq / hkv;
   w.part_o = take(size_t(dec) * group * dh * 4);

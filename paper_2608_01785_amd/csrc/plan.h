@@ -40,9 +40,9 @@ struct WsLayout {
   size_t vpack;       // [hkv, dh, v_stride] values when no cache is given
   int64_t v_stride;   // round_up(T, 64) + 64
   size_t o;           // [T, hq * dh]
-  size_t h;           // [T, d]
+  size_t h;           // [T, d] fp32 residual after attention
   size_t a;           // [T, ffn]
-  size_t xtmp;        // [T, d]
+  size_t xtmp;        // [T, d] fp32 residual between layers
   size_t rope;        // [max_pos, dh / 2] float2
   size_t part_o;      // decode partials [items, group, dh] f32
   size_t part_ml;     // [items, group, 2] f32

@@ -224,25 +224,27 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
   uint16_t* n_buf = at<uint16_t>(ws, lay.n);
   uint16_t* q_buf = at<uint16_t>(ws, lay.q);
   uint16_t* o_buf = at<uint16_t>(ws, lay.o);
-  uint16_t* h_buf = at<uint16_t>(ws, lay.h);
+  float* h_buf = at<float>(ws, lay.h);
   uint16_t* a_buf = at<uint16_t>(ws, lay.a);
-  uint16_t* xtmp = at<uint16_t>(ws, lay.xtmp);
+  float* xtmp = at<float>(ws, lay.xtmp);
 
   TIMED(HS_KERNEL_ROPE_TABLE, hs::launch_rope_table(rope, max_pos, dh, cfg->rope_base, s));
 
   const int grid_cap = budget;  // persistent GEMM: one block per CU of the budget
   const float scale_log2 = 1.4426950408889634f / sqrtf(float(dh));
+  // The residual stream is bf16 only at the input; every layer writes fp32.
   const uint16_t* x_cur = static_cast<const uint16_t*>(x_in);
+  const float* x_cur_f32 = nullptr;
   for (int l = 0; l < n_layers; ++l) {
     // The last layer writes x_out; earlier layers alternate so that no layer
     // reads and writes the same buffer.
     const int remaining = n_layers - 1 - l;
-    uint16_t* x_next = (remaining % 2 == 0) ? static_cast<uint16_t*>(x_out) : xtmp;
+    float* x_next = (remaining % 2 == 0) ? static_cast<float*>(x_out) : xtmp;
     uint16_t* kstore = place.cache ? static_cast<uint16_t*>(kv->k[l]) : at<uint16_t>(ws, lay.kpack);
     uint16_t* vstore = place.cache ? static_cast<uint16_t*>(kv->v[l]) : at<uint16_t>(ws, lay.vpack);
 
-    TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(x_cur, static_cast<const uint16_t*>(w[l].ln1), n_buf, T, d,
-                                                cfg->rms_eps, 4 * budget, s));
+    TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(x_cur, x_cur_f32, static_cast<const uint16_t*>(w[l].ln1), n_buf,
+                                                T, d, cfg->rms_eps, 4 * budget, s));
     hs::GemmArgs g{};
     g.A = n_buf;
     g.W = static_cast<const uint16_t*>(w[l].w_qkv);
@@ -308,13 +310,14 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     go.M = T;
     go.K = hq * dh;
     go.n_tiles_n = d / 256;
-    go.out = h_buf;
+    go.out_f32 = h_buf;
     go.ldo = d;
     go.resid = x_cur;
+    go.resid_f32 = x_cur_f32;
     TIMED(HS_KERNEL_O_PROJ, hs::launch_gemm(hs::EPI_RESID, go, grid_cap, s));
 
-    TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(h_buf, static_cast<const uint16_t*>(w[l].ln2), n_buf, T, d,
-                                                cfg->rms_eps, 4 * budget, s));
+    TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(nullptr, h_buf, static_cast<const uint16_t*>(w[l].ln2), n_buf, T,
+                                                d, cfg->rms_eps, 4 * budget, s));
 
     hs::GemmArgs gu{};
     gu.A = n_buf;
@@ -333,11 +336,12 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     gd.M = T;
     gd.K = f;
     gd.n_tiles_n = d / 256;
-    gd.out = x_next;
+    gd.out_f32 = x_next;
     gd.ldo = d;
-    gd.resid = h_buf;
+    gd.resid_f32 = h_buf;
     TIMED(HS_KERNEL_DOWN, hs::launch_gemm(hs::EPI_RESID, gd, grid_cap, s));
-    x_cur = x_next;
+    x_cur = nullptr;
+    x_cur_f32 = x_next;
   }
   return HS_OK;
 }

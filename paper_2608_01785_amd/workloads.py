@@ -23,7 +23,8 @@ available, so every value is drawn from the recipes below):
 
 Weights are N(0, 0.02); RMSNorm gains are 1 + N(0, 0.02); token embeddings and
 cached keys/values are N(0, 1).  All values are drawn in float32 with NumPy's
-PCG64 generator and rounded to bfloat16 with round-to-nearest-even.
+PCG64 generator and rounded with round-to-nearest-even: to bfloat16 for
+weights and token rows, to IEEE half for cached keys/values.
 """
 from __future__ import annotations
 
@@ -53,6 +54,15 @@ def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
     """Expand raw bfloat16 bits to float32 (exact)."""
     bits = np.ascontiguousarray(bits, dtype=np.uint16)
     return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def f16_bits(a: np.ndarray) -> np.ndarray:
+    """Round float32 values to IEEE half (nearest even); return raw uint16 bits."""
+    return np.ascontiguousarray(a, dtype=np.float32).astype(np.float16).view(np.uint16)
+
+
+def f16_to_f32(bits: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(bits, dtype=np.uint16).view(np.float16).astype(np.float32)
 
 
 # ----------------------------------------------------------------------------
@@ -207,7 +217,7 @@ def random_batch(hidden: int, lengths, seed: int, ctx_lens=None) -> PrefillBatch
 
 @dataclasses.dataclass
 class CacheContents:
-    """Cached keys/values in logical order: per layer, per slot, [ctx, Hkv, dh] bf16 bits."""
+    """Cached keys/values in logical order: per layer, per slot, [ctx, Hkv, dh] fp16 bits."""
     k: List[List[np.ndarray]]
     v: List[List[np.ndarray]]
 
@@ -219,8 +229,8 @@ def make_cache(s: LayerShape, n_layers: int, ctx_lens, seed: int) -> CacheConten
         kl, vl = [], []
         for c in ctx_lens:
             shp = (int(c), s.n_kv_heads, s.head_dim)
-            kl.append(bf16_bits(rng.standard_normal(shp, dtype=np.float32)))
-            vl.append(bf16_bits(rng.standard_normal(shp, dtype=np.float32)))
+            kl.append(f16_bits(rng.standard_normal(shp, dtype=np.float32)))
+            vl.append(f16_bits(rng.standard_normal(shp, dtype=np.float32)))
         ks.append(kl)
         vs.append(vl)
     return CacheContents(ks, vs)

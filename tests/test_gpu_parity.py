@@ -10,7 +10,7 @@ import pytest
 from oracle import layer as ref
 from paper_2608_01785_amd import workloads as W
 from tests.gpu_common import TOL, err_ratio, log, require_gpu, workspace
-from tests.util import f64, weights_f64
+from tests.util import f64, h64, weights_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -37,12 +37,12 @@ def run_prefill(env, shape, wdev, x_bits, offsets, ctx_lens=None, cache=None, bu
     max_pos = max(cl[b] + offsets[b + 1] - offsets[b] for b in range(B))
     ws = workspace(torch, shape, offsets[-1], B, max_pos)
     x = to_device(x_bits)
-    y = torch.empty_like(x)
+    y = torch.empty(x.shape, dtype=torch.float32, device="cuda")
     torch.cuda.synchronize()
     binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, offsets, ctx_lens,
                                     cache.as_arg() if cache is not None else None, budget, None, ws)
     torch.cuda.synchronize()
-    return to_bits(y)
+    return y.cpu().numpy().astype(np.float64)
 
 
 def seeded_layers(shape, n_layers, seed):
@@ -61,7 +61,7 @@ def test_tiny_layer_all_budgets(env):
     for b in BUDGETS:
         log(f"[tiny layer] budget {b}, T={batch.n_tokens}")
         outs[b] = run_prefill(env, shape, wdev, batch.x, batch.seq_offsets, budget=b)
-        e = err_ratio(f64(outs[b]), expect)
+        e = err_ratio(outs[b], expect)
         log(f"  max err / rms = {e:.3e}")
         assert e <= TOL
     for b in BUDGETS:
@@ -81,7 +81,7 @@ def test_ragged_prefill_parity(env, shape_name, lengths, n_layers):
     log(f"[ragged prefill] {shape_name} lengths={lengths} layers={n_layers}")
     expect, _ = ref.stack_forward(f64(batch.x), weights_f64(layers), shape, batch.seq_offsets)
     got = run_prefill(env, shape, upload_weights(layers), batch.x, batch.seq_offsets, budget=128)
-    e = err_ratio(f64(got), expect)
+    e = err_ratio(got, expect)
     log(f"  max err / rms = {e:.3e}")
     assert e <= TOL
 
@@ -96,7 +96,7 @@ def test_residual_identity_bit_exact(env):
     batch = W.random_batch(shape.hidden, [40, 300, 1], seed=6)
     log("[residual identity] tiny, 2 layers, W_o = W_down = 0")
     got = run_prefill(env, shape, upload_weights(layers), batch.x, batch.seq_offsets)
-    np.testing.assert_array_equal(got, batch.x)
+    np.testing.assert_array_equal(got, f64(batch.x))
 
 
 def test_causal_invariance_and_isolation(env):
@@ -134,9 +134,9 @@ def test_cached_prefix_chunks_and_cache_writes(env):
     log(f"[cached prefix] thinker-mixed shape lengths={lengths} ctx={ctx_lens}")
     expect, k_new, v_new = ref.layer_forward(
         f64(batch.x), weights_f64(layers)[0], shape, batch.seq_offsets, ctx_lens,
-        [f64(k) for k in prefix.k[0]], [f64(v) for v in prefix.v[0]])
+        [h64(k) for k in prefix.k[0]], [h64(v) for v in prefix.v[0]])
     got = run_prefill(env, shape, upload_weights(layers), batch.x, batch.seq_offsets, ctx_lens, cache, budget=96)
-    e = err_ratio(f64(got), expect)
+    e = err_ratio(got, expect)
     log(f"  max err / rms = {e:.3e}")
     assert e <= TOL
     off = batch.seq_offsets
@@ -146,9 +146,9 @@ def test_cached_prefix_chunks_and_cache_writes(env):
         # Prefix untouched, new rows match the reference, the rest still holds the fill value.
         np.testing.assert_array_equal(kb[:c], prefix.k[0][b])
         np.testing.assert_array_equal(vb[:c], prefix.v[0][b])
-        assert err_ratio(f64(kb[c:c + n]), k_new[off[b]:off[b + 1]]) <= TOL
-        assert err_ratio(f64(vb[c:c + n]), v_new[off[b]:off[b + 1]]) <= TOL
-        assert np.all(f64(kb[c + n:]) == 7.0) and np.all(f64(vb[c + n:]) == 7.0)
+        assert err_ratio(h64(kb[c:c + n]), k_new[off[b]:off[b + 1]]) <= TOL
+        assert err_ratio(h64(vb[c:c + n]), v_new[off[b]:off[b + 1]]) <= TOL
+        assert np.all(h64(kb[c + n:]) == 7.0) and np.all(h64(vb[c + n:]) == 7.0)
 
 
 def test_talker_decode_step_parity(env):
@@ -170,23 +170,23 @@ def test_talker_decode_step_parity(env):
             cache.load_prefix(l, b, prefix.k[l][b], prefix.v[l][b])
     log(f"[talker decode] layers={n_layers} batch={batch} kv_lens={kv_lens.tolist()}")
     expect, kv_new = ref.decode_step(f64(x), weights_f64(layers), shape, kv_lens,
-                                     [[f64(k) for k in prefix.k[l]] for l in range(n_layers)],
-                                     [[f64(v) for v in prefix.v[l]] for l in range(n_layers)])
+                                     [[h64(k) for k in prefix.k[l]] for l in range(n_layers)],
+                                     [[h64(v) for v in prefix.v[l]] for l in range(n_layers)])
     ws = workspace(torch, shape, batch, batch, int(kv_lens.max()) + 1)
     xd = to_device(x)
-    y = torch.empty_like(xd)
+    y = torch.empty(xd.shape, dtype=torch.float32, device="cuda")
     torch.cuda.synchronize()
     binding.hs_downstream_decode_step(ctx, shape, upload_weights(layers), xd, y, cache.as_arg(), kv_lens, 128,
                                       None, ws)
     torch.cuda.synchronize()
-    e = err_ratio(f64(to_bits(y)), expect)
+    e = err_ratio(y.cpu().numpy(), expect)
     log(f"  max err / rms = {e:.3e}")
     assert e <= TOL
     for l in range(n_layers):
         for b in range(batch):
             kb, vb = cache.rows(l, b, int(kv_lens[b]), int(kv_lens[b]) + 1)
-            assert err_ratio(f64(kb[0]), kv_new[l][0][b]) <= TOL
-            assert err_ratio(f64(vb[0]), kv_new[l][1][b]) <= TOL
+            assert err_ratio(h64(kb[0]), kv_new[l][0][b]) <= TOL
+            assert err_ratio(h64(vb[0]), kv_new[l][1][b]) <= TOL
 
 
 def test_masks_hold_on_hardware(env):

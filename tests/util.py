@@ -1,11 +1,17 @@
 """Test helpers: conversions between the generator's bf16 bits and float64."""
 import numpy as np
 
-from paper_2608_01785_amd.workloads import bf16_to_f32, bf16_bits
+from paper_2608_01785_amd.workloads import bf16_to_f32, bf16_bits, f16_to_f32
 
 
 def f64(bits):
+    """bf16 bits -> float64."""
     return bf16_to_f32(bits).astype(np.float64)
+
+
+def h64(bits):
+    """fp16 bits -> float64."""
+    return f16_to_f32(bits).astype(np.float64)
 
 
 def weights_f64(layers):
