@@ -56,7 +56,10 @@ def main():
     ap.add_argument("--budgets", type=str, default="64,128,192")
     ap.add_argument("--no-corun", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=24, help="rows per sequence in the CPU-reference sample")
+    ap.add_argument("--cpu-rows", type=int, default=384, help="rows per sequence in the CPU-reference sample")
+    ap.add_argument("--quick", action="store_true", help="headline stack only (no budget sweep, co-run, CPU leg)")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run one device copy of this many MiB (counter calibration under a profiler)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only; the hot path is a single-GPU "
@@ -70,6 +73,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = "cuda:0"
     budgets = [int(b) for b in args.budgets.split(",") if b]
+    if args.quick:
+        budgets, args.no_corun, args.no_cpu_baseline = [], True, True
     ctx = binding.Context(0, budgets=sorted(set(budgets + [128, 256])))
 
     # ---------------------------------------------------------------- thinker stack
@@ -133,6 +138,16 @@ def main():
         log(f"[bench] thinker stack @{b} CUs: {mb:.3f} ms/step, {T / (mb / 1e3):,.0f} tok/s")
     per_budget["256"] = {"ms_per_step": round(ms, 3), "tok_s": round(tok_s),
                          "mfma_frac_cu_scaled": round(flops_step / (ms / 1e3) / PEAK_BF16, 4)}
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {args.calib_copy_mib} MiB done")
+        del src, dst
 
     # ---------------------------------------------------------------- co-run
     corun = None

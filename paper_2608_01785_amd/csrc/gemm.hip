@@ -1,21 +1,25 @@
 // Persistent fp16 MFMA GEMM for gfx950 with fused epilogues.
 //
 // Computes C[M, N] = A[M, K] * W[N, K]^T (fp16 activations times bf16 [out, in]
-// weights, fp32 accumulation).  Weight tiles are converted bf16 -> fp16 on
-// their way into LDS (exact for the weight range), so both MFMA operands are
+// weights, fp32 accumulation).  Weight fragments are converted bf16 -> fp16
+// after they leave LDS (exact for the weight range), so both MFMA operands are
 // fp16: the same MFMA rate as bf16 on gfx950 with 8x finer rounding of the
-// activations.  The MFMA is issued as C^T = W * A^T: the weight tile is the MFMA
-// A operand and the activation tile the B operand, so every lane of the 32x32
+// activations.
+//
+// The MFMA is issued as C^T = W * A^T: the weight tile is the MFMA A operand
+// and the activation tile the B operand, so every lane of the 32x32
 // accumulator owns one activation row and four consecutive output columns per
 // register group.  That makes 8-byte output stores possible and keeps the
 // pairs the epilogues need (RoPE's (j, j + dh/2), SwiGLU's gate/up) in the
 // same lane and register.
 //
-// Block tile 256 (weight rows) x 256 (activation rows) x 64 (K), 4 waves in a
-// 2 x 2 grid, each wave 128 x 128 = 4 x 4 MFMA tiles of 32x32x16.  Operands go
-// global -> registers -> LDS (two stages, XOR-swizzled 16-byte chunks) and
-// the next K slab is fetched while the current one feeds the MFMAs.  The grid
-// is persistent (at most one block per CU of the budget); blocks walk the
+// Block tile 256 (weight rows) x 256 (activation rows), 4 waves in a 2 x 2
+// grid, each wave 128 x 128 = 4 x 4 MFMA tiles of 32x32x16.  K advances in
+// slabs of 32 through a ring of 5 LDS stages (160 KB): both operands are
+// copied buffer -> LDS by the load unit itself (no staging registers), so
+// four slabs (128 KB per CU) are in flight while the fifth feeds the MFMAs.
+// That depth is what hides the latency of operands that miss the XCD's L2.
+// The grid is persistent (one block per CU of the budget); blocks walk the
 // tile space in grouped order, remapped so each XCD takes a contiguous range.
 #include "hs_device.h"
 #include "hs_kernels.h"
@@ -25,33 +29,63 @@ namespace {
 
 constexpr int BM = 256;   // activation rows per tile
 constexpr int BN = 256;   // weight rows per tile
-constexpr int BK = 64;
+constexpr int BK = 32;    // K per LDS stage
+constexpr int kStages = 5;
 constexpr int kThreads = 256;
-constexpr int kRowBytes = BK * 2;            // 128 bytes = 8 chunks of 16
-constexpr int kTileBytes = 256 * kRowBytes;  // 32 KB
+constexpr int kRowBytes = BK * 2;            // 64 bytes = 4 chunks of 16
+constexpr int kTileBytes = 256 * kRowBytes;  // 16 KB
 constexpr int kStageBytes = 2 * kTileBytes;  // weight tile + activation tile
 constexpr int kGroupM = 8;
 
+// Row of W that lands in tile row r (0..255) of output tile tile_n.
 template <int EPI>
-__device__ __forceinline__ int64_t weight_row(int tile_n, int j, int ld_row, int ffn) {
-  // Row of W loaded into tile row ld_row + 32 j.
+__device__ __forceinline__ uint32_t weight_row(int tile_n, int r, int ffn) {
   if constexpr (EPI == EPI_SWIGLU) {
     // Tile rows: [wave-n 0: gate 64 | up 64][wave-n 1: gate 64 | up 64] for
     // output columns tile_n * 128 .. +128.
-    const int half = j >> 2;            // which wave-n half (rows 128 * half ..)
-    const int up = (j & 3) >> 1;        // rows 64..127 of the half are 'up'
-    const int jj = ld_row + 32 * (j & 1);
-    return int64_t(up) * ffn + tile_n * 128 + half * 64 + jj;
+    const int half = r >> 7, rr = r & 127, up = rr >> 6, jj = rr & 63;
+    return uint32_t(up * ffn + tile_n * 128 + half * 64 + jj);
   } else {
-    return int64_t(tile_n) * BN + ld_row + 32 * j;
+    return uint32_t(tile_n * BN + r);
   }
 }
 
+// 16-byte chunk c of tile row r sits at physical chunk c ^ swz(r): the 8 rows
+// read by 8 consecutive lanes then cover all 32 banks.
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 3; }
+
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
 
-template <int EPI, int DH>
+using lds_ptr_t = __attribute__((address_space(3))) void*;
+
+// Buffer resource over [base, base + bytes): loads past the end return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
+
+// Workgroup barrier without the compiler's memory fence (which would wait for
+// every outstanding copy).  Callers wait for exactly the copies they need
+// first; LDS reads of the previous stage have completed because their results
+// were consumed.
+__device__ __forceinline__ void barrier_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Wait until at most n vector-memory operations of this wave are outstanding.
+__device__ __forceinline__ void wait_vm(int n) {
+  switch (n) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
+  }
+}
+
+template <int EPI, int DH, bool W_F16>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * kStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -64,45 +98,75 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
   const int n_m_tiles = (a.M + BM - 1) / BM;
   const int n_tiles = n_m_tiles * a.n_tiles_n;
   const int KT = a.K / BK;
-  const int ld_row = tid >> 3;   // 0..31
-  const int ld_chunk = tid & 7;
-  const int ld_phys = ld_chunk ^ (ld_row & 7);  // rows ld_row + 32 j share (row & 7)
+  const uint32_t row_bytes = uint32_t(a.K) * 2;
+  const uint32_t w_rows = (EPI == EPI_SWIGLU) ? uint32_t(2 * a.ffn) : uint32_t(a.n_tiles_n * BN);
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(a.W, w_rows * row_bytes);
+  const __amdgpu_buffer_rsrc_t ares = make_rsrc(a.A, uint32_t(a.M) * row_bytes);
+
+  // Loads: one wave instruction fills 16 consecutive tile rows (1 KB); lane i
+  // lands at byte 16 i = row i / 4, physical chunk i % 4, so it fetches logical
+  // chunk (i % 4) ^ swz(row).  Wave w fills rows 64 w .. 64 w + 63 of both tiles.
+  const int ld_sub = lane >> 2;
+  const int ld_chunk = (lane & 3) ^ swz(ld_sub);  // rows 16 j + ld_sub share swz with ld_sub
 
   const int per_group = kGroupM * a.n_tiles_n;
-  for (int L = xcd_remap(blockIdx.x, gridDim.x); L < n_tiles; L += gridDim.x) {
+  auto tile_coords = [&](int L, int& tile_m, int& tile_n) {
     const int group = L / per_group;
     const int first_m = group * kGroupM;
     const int gsize = min(n_m_tiles - first_m, kGroupM);
-    const int tile_m = first_m + (L % per_group) % gsize;
-    const int tile_n = (L % per_group) / gsize;
+    tile_m = first_m + (L % per_group) % gsize;
+    tile_n = (L % per_group) / gsize;
+  };
 
-    // Weight rows of one thread differ by wave-uniform offsets (scalar registers);
-    // activation rows are clamped to the last valid row in a ragged tail tile.
-    const uint16_t* wsrc = a.W + weight_row<EPI>(tile_n, 0, ld_row, a.ffn) * a.K + ld_chunk * 8;
-    const int arow0 = tile_m * BM + ld_row;
-    const bool a_full = tile_m * BM + BM <= a.M;
-    const uint16_t* asrc = a.A + int64_t(arow0) * a.K + ld_chunk * 8;
-
-    u32x4 rw[8], ra[8];
-    auto gload = [&](int kt) {
+  uint32_t w_off[4], a_off[4];
+  auto set_tile = [&](int tile_m, int tile_n) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int64_t wofs = (weight_row<EPI>(tile_n, j, 0, a.ffn) - weight_row<EPI>(tile_n, 0, 0, a.ffn)) * a.K;
-        rw[j] = *reinterpret_cast<const u32x4*>(wsrc + wofs + kt * BK);
-        const int64_t arow = a_full ? int64_t(32 * j) : int64_t(min(arow0 + 32 * j, a.M - 1) - arow0);
-        ra[j] = *reinterpret_cast<const u32x4*>(asrc + arow * a.K + kt * BK);
-      }
-    };
-    auto lstore = [&](int stage) {
-      uint8_t* base = smem + stage * kStageBytes;
+    for (int j = 0; j < 4; ++j) {
+      const int r = wave * 64 + 16 * j + ld_sub;
+      w_off[j] = weight_row<EPI>(tile_n, r, a.ffn) * row_bytes + ld_chunk * 16;
+      a_off[j] = uint32_t(tile_m * BM + r) * row_bytes + ld_chunk * 16;  // rows >= M read zero
+    }
+  };
+  auto issue_stage = [&](int kt, int buf) {
+    const int koff = kt * BK * 2;
+    uint8_t* wbase = smem + buf * kStageBytes + wave * 64 * kRowBytes;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int off = (ld_row + 32 * j) * kRowBytes + ld_phys * 16;
-        *reinterpret_cast<u32x4*>(base + off) = bf8_to_h8(rw[j]);
-        *reinterpret_cast<u32x4*>(base + kTileBytes + off) = ra[j];
-      }
-    };
+    for (int j = 0; j < 4; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lds_ptr_t)(wbase + j * 16 * kRowBytes), 16, w_off[j], koff,
+                                               0, 0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ares, (lds_ptr_t)(wbase + kTileBytes + j * 16 * kRowBytes), 16,
+                                               a_off[j], koff, 0, 0);
+  };
 
+  // Fragments of one stage: [kk][i] weight, [kk][j] activation.
+  typedef u32x4 Frags[2][4];
+  auto read_frags = [&](int buf, Frags& fw, Frags& fa) {
+    const uint8_t* base = smem + buf * kStageBytes;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int phys = (kk * 2 + fh) ^ swz(fr);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        fw[kk][i] = *reinterpret_cast<const u32x4*>(base + (wn * 128 + i * 32 + fr) * kRowBytes + phys * 16);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        fa[kk][j] =
+            *reinterpret_cast<const u32x4*>(base + kTileBytes + (wm * 128 + j * 32 + fr) * kRowBytes + phys * 16);
+    }
+  };
+
+  int L = xcd_remap(blockIdx.x, gridDim.x);
+  if (L >= n_tiles) return;
+  int tile_m, tile_n;
+  tile_coords(L, tile_m, tile_n);
+  set_tile(tile_m, tile_n);
+#pragma unroll
+  for (int st = 0; st < kStages - 1; ++st)
+    if (st < KT) issue_stage(st, st);
+
+  while (true) {
     f32x16 acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -111,31 +175,54 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    gload(0);
-    lstore(0);
-    __syncthreads();
-
-    for (int kt = 0; kt < KT; ++kt) {
-      const int cur = kt & 1;
-      if (kt + 1 < KT) gload(kt + 1);
-      const uint8_t* base = smem + cur * kStageBytes;
+    auto mfma_half = [&](const Frags& fw, const Frags& fa, int kk) {
 #pragma unroll
-      for (int kk = 0; kk < BK / 16; ++kk) {
-        const int phys = (kk * 2 + fh) ^ (fr & 7);
-        u32x4 wf[4], af[4];
+      for (int i = 0; i < 4; ++i) {
+        const u32x4 wh = W_F16 ? fw[kk][i] : bf8_to_h8(fw[kk][i]);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          wf[i] = *reinterpret_cast<const u32x4*>(base + (wn * 128 + i * 32 + fr) * kRowBytes + phys * 16);
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          af[j] = *reinterpret_cast<const u32x4*>(base + kTileBytes + (wm * 128 + j * 32 + fr) * kRowBytes + phys * 16);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(wf[i], af[j], acc[i][j]);
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(wh, fa[kk][j], acc[i][j]);
       }
-      if (kt + 1 < KT) lstore(cur ^ 1);
-      __syncthreads();
+    };
+
+    // Stage s lives in buffer s % kStages.  Its fragments are read into
+    // registers during the second half of stage s - 1, right after the
+    // barrier that publishes stage s; the first half of stage s then needs no
+    // LDS wait, and the reads overlap 16 MFMAs.
+    wait_vm(min(kStages - 2, KT - 1));
+    barrier_nofence();
+    if (kStages - 1 < KT) issue_stage(kStages - 1, kStages - 1);
+    Frags fwA, faA, fwB, faB;
+    read_frags(0, fwA, faA);
+
+    // One half-stage step: finish stage s with fragments (fw, fa) and prefetch
+    // stage s + 1 into (nw, na).
+    auto step = [&](int s, Frags& fw, Frags& fa, Frags& nw, Frags& na) {
+      mfma_half(fw, fa, 0);
+      if (s + 1 < KT) {
+        wait_vm(min(kStages - 2, KT - 2 - s));
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of stage s are done
+        barrier_nofence();
+        if (s + kStages < KT) issue_stage(s + kStages, s % kStages);
+        read_frags((s + 1) % kStages, nw, na);
+      }
+      mfma_half(fw, fa, 1);
+    };
+    for (int s = 0; s < KT; s += 2) {
+      step(s, fwA, faA, fwB, faB);
+      step(s + 1, fwB, faB, fwA, faA);
+    }
+
+    // All waves are done with every stage: start the next tile's copies so
+    // they overlap this tile's epilogue.
+    const int L_next = L + gridDim.x;
+    __syncthreads();
+    if (L_next < n_tiles) {
+      int nm, nn;
+      tile_coords(L_next, nm, nn);
+      set_tile(nm, nn);
+#pragma unroll
+      for (int st = 0; st < kStages - 1; ++st)
+        if (st < KT) issue_stage(st, st);
     }
 
     // ---------------------------------------------------------------- epilogue
@@ -224,6 +311,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
         }
       }
     }
+    if (L_next >= n_tiles) break;
+    L = L_next;
+    tile_coords(L, tile_m, tile_n);
   }
 }
 
@@ -232,7 +322,10 @@ hipError_t launch_one(const GemmArgs& a, int max_blocks, hipStream_t s) {
   const int n_tiles = ((a.M + BM - 1) / BM) * a.n_tiles_n;
   int grid = n_tiles < max_blocks ? n_tiles : max_blocks;
   if (grid < 1) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<EPI, DH>), dim3(grid), dim3(kThreads), 0, s, a);
+  if (a.w_f16)
+    hipLaunchKernelGGL((gemm_kernel<EPI, DH, true>), dim3(grid), dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((gemm_kernel<EPI, DH, false>), dim3(grid), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -14,7 +14,8 @@ enum Epilogue : int {
 
 struct GemmArgs {
   const uint16_t* A;  // activations [M, K] fp16 row-major
-  const uint16_t* W;  // weights [N, K] bf16 row-major
+  const uint16_t* W;  // weights [N, K] row-major, bf16 (w_f16 = 0) or fp16 (w_f16 = 1)
+  int w_f16;
   int M, K;
   int n_tiles_n;      // output tiles along N (256 weight rows each; 128 outputs for SWIGLU)
   uint16_t* out;      // SWIGLU output (fp16), row stride ldo
