@@ -67,12 +67,18 @@ typedef struct hs_layer_cfg {
   float rope_base; /* RoPE base; pair (j, j + dh/2) turns by pos * base^(-2j/dh) */
 } hs_layer_cfg;
 
-/* Device pointers to one layer's bf16 weights.
- *   ln1, ln2   [hidden]                              RMSNorm gains
+/* Storage format of the four projection matrices of a layer. */
+enum { HS_WEIGHTS_BF16 = 0, HS_WEIGHTS_F16 = 1 };
+
+/* Device pointers to one layer's weights.
+ *   ln1, ln2   [hidden] bf16                         RMSNorm gains
  *   w_qkv      [(Hq + 2 Hkv) * dh, hidden]           rows: Q heads | K heads | V heads
  *   w_o        [hidden, Hq * dh]
  *   w_gate_up  [2 * ffn, hidden]                      rows: gate | up
- *   w_down     [hidden, ffn]                                                    */
+ *   w_down     [hidden, ffn]
+ * format: HS_WEIGHTS_BF16 (the matrices are bf16 and each GEMM converts its
+ * tiles on the fly) or HS_WEIGHTS_F16 (the matrices were converted once with
+ * hs_convert_weights_f16; same values, no per-call conversion). */
 typedef struct hs_layer_weights {
   const void* ln1;
   const void* w_qkv;
@@ -80,6 +86,7 @@ typedef struct hs_layer_weights {
   const void* ln2;
   const void* w_gate_up;
   const void* w_down;
+  int32_t format;
 } hs_layer_weights;
 
 /* Key/value cache.  k[l] and v[l] are device pointers for layer l (host
@@ -212,6 +219,15 @@ hs_status hs_downstream_decode_step(hs_context* ctx, const hs_layer_cfg* cfg,
  * [n_groups * 4]): XCC id, shader engine, CU id, and the low 32 bits of the
  * constant-rate clock at its start.  Used to check that masks hold. */
 hs_status hs_probe_hw_ids(hs_context* ctx, void* stream, int32_t n_groups, void* out_ids);
+
+/* One-time weight preparation: dst[i] = fp16(src[i]) for n bf16 values
+ * (device pointers, 4-byte aligned, n even, no overlap), enqueued on stream
+ * (NULL = the context's full-budget stream).  Exact for magnitudes in
+ * [2^-14, 65504]; smaller magnitudes round toward zero to fp16 subnormals
+ * (error below 2^-24) and larger ones saturate at 65504.  For the four
+ * projection matrices of hs_layer_weights with format HS_WEIGHTS_F16. */
+hs_status hs_convert_weights_f16(hs_context* ctx, const void* src_bf16, void* dst_f16, int64_t n,
+                                 void* stream);
 
 /* Per-kernel timing with HIP events on the launch stream.  While enabled,
  * every launch of the compute calls is bracketed by a pair of events (a pool

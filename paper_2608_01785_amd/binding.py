@@ -23,8 +23,9 @@ SYMBOLS = (
     "hs_status_string", "hs_last_error", "hs_default_topology", "hs_cu_partition", "hs_plan_metadata",
     "hs_context_create", "hs_context_topology", "hs_context_stream", "hs_context_masks",
     "hs_context_destroy", "hs_workspace_size", "hs_shared_stage_forward", "hs_downstream_decode_step",
-    "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read",
+    "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read", "hs_convert_weights_f16",
 )
+HS_WEIGHTS_BF16, HS_WEIGHTS_F16 = 0, 1
 
 KERNEL_KINDS = {"rmsnorm": 0, "qkv": 1, "attention": 2, "decode_attn": 3, "o_proj": 4, "gate_up": 5,
                 "down": 6, "rope_table": 7}
@@ -40,8 +41,12 @@ class LayerCfg(ctypes.Structure):
         return cls(s.hidden, s.n_q_heads, s.n_kv_heads, s.head_dim, s.ffn, s.rms_eps, s.rope_base)
 
 
+MATRICES = ("w_qkv", "w_o", "w_gate_up", "w_down")
+
+
 class LayerWeights(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in ("ln1", "w_qkv", "w_o", "ln2", "w_gate_up", "w_down")]
+    _fields_ = [(n, ctypes.c_void_p) for n in ("ln1", "w_qkv", "w_o", "ln2", "w_gate_up", "w_down")] + \
+               [("format", ctypes.c_int32)]
 
 
 class KvCache(ctypes.Structure):
@@ -91,6 +96,7 @@ def lib() -> ctypes.CDLL:
             "hs_probe_hw_ids": [vp, vp, i32, vp],
             "hs_timing_enable": [vp, i32],
             "hs_timing_read": [vp, i32, ctypes.POINTER(ctypes.c_double), i32p],
+            "hs_convert_weights_f16": [vp, vp, vp, ctypes.c_int64, vp],
         }
         for name, args in sigs.items():
             fn = getattr(L, name)
@@ -229,6 +235,7 @@ def _weights_array(weights: List[Dict[str, object]]):
     for i, w in enumerate(weights):
         for name in ("ln1", "w_qkv", "w_o", "ln2", "w_gate_up", "w_down"):
             setattr(arr[i], name, _ptr(w[name]))
+        arr[i].format = int(w.get("format", HS_WEIGHTS_BF16))
     return arr
 
 
@@ -285,3 +292,9 @@ def hs_timing_read(ctx: Context, kind) -> Tuple[float, int]:
     n = ctypes.c_int32(0)
     _check(lib().hs_timing_read(ctx.handle, k, ctypes.byref(ms), ctypes.byref(n)))
     return float(ms.value), int(n.value)
+
+
+def hs_convert_weights_f16(ctx: Context, src, dst, n: Optional[int] = None, stream=None) -> None:
+    if n is None:
+        n = src.numel()
+    _check(lib().hs_convert_weights_f16(ctx.handle, _ptr(src), _ptr(dst), int(n), _ptr(stream)))

@@ -89,4 +89,7 @@ hipError_t launch_rope_table(float2* tab, int max_pos, int dh, float base, hipSt
 
 hipError_t launch_probe(uint32_t* out, int n_groups, hipStream_t s);
 
+// dst = fp16(src) for n bf16 values (n even).
+hipError_t launch_convert_bf16_f16(const uint16_t* src, uint16_t* dst, int64_t n, hipStream_t s);
+
 }  // namespace hs

@@ -102,7 +102,23 @@ __global__ void probe_kernel(uint32_t* out, int n) {
   }
 }
 
+// Weight preparation: pairs of bf16 values -> pairs of fp16 values.
+__global__ void convert_kernel(const uint32_t* __restrict__ src, uint32_t* __restrict__ dst, int64_t n2) {
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n2; i += int64_t(gridDim.x) * blockDim.x)
+    dst[i] = bf2x_to_h2x(src[i]);
+}
+
 }  // namespace
+
+hipError_t launch_convert_bf16_f16(const uint16_t* src, uint16_t* dst, int64_t n, hipStream_t s) {
+  const int64_t n2 = n / 2;
+  if (n2 <= 0) return hipSuccess;
+  int64_t grid = (n2 + 255) / 256;
+  if (grid > 8192) grid = 8192;
+  hipLaunchKernelGGL(convert_kernel, dim3(unsigned(grid)), dim3(256), 0, s, reinterpret_cast<const uint32_t*>(src),
+                     reinterpret_cast<uint32_t*>(dst), n2);
+  return hipGetLastError();
+}
 
 hipError_t launch_rmsnorm(const uint16_t* x, const float* x_f32, const uint16_t* gamma, uint16_t* y, int rows,
                           int d, float eps, int max_blocks, hipStream_t s) {

@@ -170,9 +170,12 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
   hs_status st = hs::validate_cfg(cfg);
   if (st != HS_OK) return st;
   if (!w || n_layers < 1) return hs::fail(HS_ERR_INVALID_ARG, "weights missing or n_layers %d < 1", n_layers);
-  for (int l = 0; l < n_layers; ++l)
+  for (int l = 0; l < n_layers; ++l) {
     if (!w[l].ln1 || !w[l].w_qkv || !w[l].w_o || !w[l].ln2 || !w[l].w_gate_up || !w[l].w_down)
       return hs::fail(HS_ERR_INVALID_ARG, "layer %d has a null weight pointer", l);
+    if (w[l].format != HS_WEIGHTS_BF16 && w[l].format != HS_WEIGHTS_F16)
+      return hs::fail(HS_ERR_INVALID_ARG, "layer %d has weight format %d", l, w[l].format);
+  }
   if (!x_in || !x_out) return hs::fail(HS_ERR_INVALID_ARG, "x_in / x_out is null");
   if (x_in == x_out) return hs::fail(HS_ERR_INVALID_ARG, "x_in and x_out must not alias");
   int32_t T = 0, max_pos = 0;
@@ -248,6 +251,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     hs::GemmArgs g{};
     g.A = n_buf;
     g.W = static_cast<const uint16_t*>(w[l].w_qkv);
+    g.w_f16 = w[l].format == HS_WEIGHTS_F16;
     g.M = T;
     g.K = d;
     g.n_tiles_n = (hq + 2 * hkv) * dh / 256;
@@ -307,6 +311,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     hs::GemmArgs go{};
     go.A = o_buf;
     go.W = static_cast<const uint16_t*>(w[l].w_o);
+    go.w_f16 = w[l].format == HS_WEIGHTS_F16;
     go.M = T;
     go.K = hq * dh;
     go.n_tiles_n = d / 256;
@@ -322,6 +327,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     hs::GemmArgs gu{};
     gu.A = n_buf;
     gu.W = static_cast<const uint16_t*>(w[l].w_gate_up);
+    gu.w_f16 = w[l].format == HS_WEIGHTS_F16;
     gu.M = T;
     gu.K = d;
     gu.n_tiles_n = f / 128;
@@ -333,6 +339,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     hs::GemmArgs gd{};
     gd.A = a_buf;
     gd.W = static_cast<const uint16_t*>(w[l].w_down);
+    gd.w_f16 = w[l].format == HS_WEIGHTS_F16;
     gd.M = T;
     gd.K = f;
     gd.n_tiles_n = d / 256;
@@ -472,6 +479,22 @@ hs_status hs_downstream_decode_step(hs_context* ctx, const hs_layer_cfg* cfg, co
   for (int32_t b = 0; b <= batch; ++b) off[b] = b;
   return run_stack(ctx, cfg, w, n_layers, x_in, x_out, off.data(), kv_lens, batch, kv, cu_budget,
                    HS_ROLE_DOWN, stream, workspace, ws_bytes);
+}
+
+hs_status hs_convert_weights_f16(hs_context* ctx, const void* src, void* dst, int64_t n, void* stream) {
+  hs::clear_error();
+  if (!ctx || !src || !dst) return hs::fail(HS_ERR_INVALID_ARG, "null argument");
+  if (n < 0 || n % 2 != 0) return hs::fail(HS_ERR_INVALID_ARG, "element count %lld must be even and >= 0", (long long)n);
+  if ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) % 4 != 0)
+    return hs::fail(HS_ERR_INVALID_ARG, "pointers must be 4-byte aligned");
+  const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+  const uintptr_t bytes = uintptr_t(n) * 2;
+  if (s0 < d0 + bytes && d0 < s0 + bytes) return hs::fail(HS_ERR_INVALID_ARG, "source and destination overlap");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (!s) s = find_level(ctx, ctx->n_cus)->s_shared;
+  HIP_TRY(hipSetDevice(ctx->device));
+  HIP_TRY(hs::launch_convert_bf16_f16(static_cast<const uint16_t*>(src), static_cast<uint16_t*>(dst), n, s));
+  return HS_OK;
 }
 
 hs_status hs_timing_enable(hs_context* ctx, int32_t enable) {

@@ -39,6 +39,21 @@ def upload_weights(layers: List[Dict[str, np.ndarray]], device="cuda") -> List[D
     return [{k: to_device(v, device) for k, v in lw.items()} for lw in layers]
 
 
+def prepare_f16(ctx, layers_dev: List[Dict[str, torch.Tensor]]) -> List[Dict[str, object]]:
+    """fp16 copies of the projection matrices (through the library's converter); gains stay bf16."""
+    from paper_2608_01785_amd import binding
+    out = []
+    for lw in layers_dev:
+        d = {"ln1": lw["ln1"], "ln2": lw["ln2"], "format": binding.HS_WEIGHTS_F16}
+        for name in binding.MATRICES:
+            dst = torch.empty(lw[name].shape, dtype=torch.float16, device=lw[name].device)
+            binding.hs_convert_weights_f16(ctx, lw[name], dst)
+            d[name] = dst
+        out.append(d)
+    torch.cuda.synchronize()
+    return out
+
+
 class DeviceCache:
     """Per-layer K/V device tensors for n_slots sequences of up to max_ctx positions."""
 

@@ -1,0 +1,230 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times, through the C ABI.
+
+The float64 reference cannot run whole 4-layer, 10,515-row stacks in seconds,
+so these tests check outputs it can compute independently:
+* a whole request (sequences never see each other, so request 0 alone through
+  the reference equals its rows of the batched run);
+* the first rows of every request (causality: they depend on nothing later);
+* properties that hold at any size (bit-identical results across CU budgets,
+  concurrency with a co-running decode stage changes nothing).
+"""
+import numpy as np
+import pytest
+
+from oracle import layer as ref
+from paper_2608_01785_amd import workloads as W
+from tests.gpu_common import TOL, err_ratio, log, require_gpu
+from tests.util import f64, h64, weights_f64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    torch = require_gpu()
+    from paper_2608_01785_amd import binding
+    ctx = binding.Context(0, budgets=(64, 96, 128, 192, 256))
+    yield torch, ctx
+    torch.cuda.synchronize()
+    ctx.close()
+
+
+@pytest.fixture(scope="module")
+def thinker(env):
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    from paper_2608_01785_amd.device_data import prepare_f16, to_device, upload_weights
+    log("[thinker] generating 4-layer weights and the 8-request batch")
+    layers = W.make_weights(W.THINKER, 4, W.SEEDS["thinker"]["weights"])
+    batch = W.thinker_batch()
+    wdev = prepare_f16(ctx, upload_weights(layers))
+    x = to_device(batch.x)
+    ws = torch.empty(binding.hs_workspace_size(W.THINKER, batch.n_tokens, batch.n_seqs, int(batch.lengths.max())),
+                     dtype=torch.uint8, device="cuda")
+    return layers, batch, wdev, x, ws
+
+
+def run_thinker(env, thinker, budget, stream=None):
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    layers, batch, wdev, x, ws = thinker
+    y = torch.empty(x.shape, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    binding.hs_shared_stage_forward(ctx, W.THINKER, wdev, x, y, batch.seq_offsets, None, None, budget, stream, ws)
+    return y
+
+
+def test_thinker_stack_request_and_prefixes(env, thinker):
+    torch, _ = env
+    layers, batch, _, _, _ = thinker
+    log("[thinker] full stack at 256 CUs")
+    y = run_thinker(env, thinker, 256)
+    torch.cuda.synchronize()
+    got = y.cpu().numpy().astype(np.float64)
+    assert np.all(np.isfinite(got))
+    w64 = weights_f64(layers)
+    off = batch.seq_offsets
+    # Whole request 0 (849 rows) through the reference on its own.
+    log("[thinker] reference on request 0")
+    exp0, _ = ref.stack_forward(f64(batch.x[off[0]:off[1]]), w64, W.THINKER, [0, off[1] - off[0]])
+    e = err_ratio(got[off[0]:off[1]], exp0)
+    log(f"  request 0: max err / rms = {e:.3e}")
+    assert e <= TOL
+    # First 24 rows of every request.
+    r = 24
+    xs = np.concatenate([batch.x[o:o + r] for o in off[:-1]])
+    exp, _ = ref.stack_forward(f64(xs), w64, W.THINKER, np.arange(batch.n_seqs + 1) * r)
+    gs = np.concatenate([got[o:o + r] for o in off[:-1]])
+    e = err_ratio(gs, exp)
+    log(f"  first {r} rows of all requests: max err / rms = {e:.3e}")
+    assert e <= TOL
+
+
+def test_thinker_budgets_bit_identical(env, thinker):
+    torch, _ = env
+    outs = {}
+    for b in (256, 192, 128, 64):
+        log(f"[thinker] budget {b}")
+        outs[b] = run_thinker(env, thinker, b)
+        torch.cuda.synchronize()
+    for b in (192, 128, 64):
+        assert torch.equal(outs[b], outs[256]), f"budget {b} differs from 256"
+
+
+def test_thinker_bf16_weights_match_prepared(env, thinker):
+    """Weights converted inside each GEMM give the same bits as prepared fp16 copies."""
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    from paper_2608_01785_amd.device_data import upload_weights
+    layers, batch, wdev, x, ws = thinker
+    y_f16 = run_thinker(env, thinker, 256)
+    wb = upload_weights(layers)
+    y = torch.empty(x.shape, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    log("[thinker] bf16 weights, converted in the GEMM")
+    binding.hs_shared_stage_forward(ctx, W.THINKER, wb, x, y, batch.seq_offsets, None, None, 256, None, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y_f16)
+
+
+def talker_setup(env, batch, seeds, n_layers=16):
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    from paper_2608_01785_amd.device_data import DeviceCache, prepare_f16, to_device, upload_weights
+    shape = W.TALKER
+    layers = W.make_weights(shape, n_layers, seeds["weights"])
+    d = W.talker_batch(shape, n_layers, batch, seeds)
+    max_ctx = int(np.ceil((d.kv_lens.max() + 1) / 64) * 64)
+    cache = DeviceCache(n_layers, batch, max_ctx, shape.n_kv_heads, shape.head_dim, fill=0.0)
+    for l in range(n_layers):
+        for b in range(batch):
+            cache.load_prefix(l, b, d.cache.k[l][b], d.cache.v[l][b])
+    wdev = prepare_f16(ctx, upload_weights(layers))
+    ws = torch.empty(binding.hs_workspace_size(shape, batch, batch, int(d.kv_lens.max()) + 1), dtype=torch.uint8,
+                     device="cuda")
+    return layers, d, cache, wdev, to_device(d.x), ws
+
+
+def test_talker_decode_step_full(env):
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    shape, n_layers, batch = W.TALKER, 16, 32
+    log("[talker] 16 layers, batch 32, seeded cache")
+    layers, d, cache, wdev, x, ws = talker_setup(env, batch, W.SEEDS["talker"])
+    y = torch.empty(x.shape, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    binding.hs_downstream_decode_step(ctx, shape, wdev, x, y, cache.as_arg(), d.kv_lens, 128, None, ws)
+    torch.cuda.synchronize()
+    expect, kv_new = ref.decode_step(f64(d.x), weights_f64(layers), shape, d.kv_lens,
+                                     [[h64(k) for k in d.cache.k[l]] for l in range(n_layers)],
+                                     [[h64(v) for v in d.cache.v[l]] for l in range(n_layers)])
+    e = err_ratio(y.cpu().numpy(), expect)
+    log(f"  max err / rms = {e:.3e}")
+    assert e <= TOL
+    for l in (0, 7, 15):
+        kn = np.stack([h64(cache.rows(l, b, int(d.kv_lens[b]), int(d.kv_lens[b]) + 1)[0][0]) for b in range(batch)])
+        vn = np.stack([h64(cache.rows(l, b, int(d.kv_lens[b]), int(d.kv_lens[b]) + 1)[1][0]) for b in range(batch)])
+        assert err_ratio(kn, kv_new[l][0]) <= TOL
+        assert err_ratio(vn, kv_new[l][1]) <= TOL
+
+
+def test_thinker_mixed_step_sampled(env):
+    """One layer at hidden 4096: four 2048-row chunks behind 0/2048/4096/6144 cached
+    rows and 64 single-row sequences behind 4096 cached rows, at 96 CUs."""
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    from paper_2608_01785_amd.device_data import DeviceCache, prepare_f16, to_device, upload_weights
+    shape = W.THINKER_MIXED
+    seeds = W.SEEDS["thinker_mixed"]
+    lengths, ctx_lens = W.thinker_mixed_layout()
+    layers = W.make_weights(shape, 1, seeds["weights"])
+    batch = W.random_batch(shape.hidden, lengths, seeds["tokens"], ctx_lens)
+    log("[mixed] generating prefix caches")
+    prefix = W.make_cache(shape, 1, ctx_lens, seeds["cache"])
+    B = len(lengths)
+    cache = DeviceCache(1, B, 8192, shape.n_kv_heads, shape.head_dim, fill=0.0)
+    for b in range(B):
+        cache.load_prefix(0, b, prefix.k[0][b], prefix.v[0][b])
+    wdev = prepare_f16(ctx, upload_weights(layers))
+    x = to_device(batch.x)
+    y = torch.empty(x.shape, dtype=torch.float32, device="cuda")
+    ws = torch.empty(binding.hs_workspace_size(shape, batch.n_tokens, B, 8192), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    log("[mixed] layer at 96 CUs")
+    binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, ctx_lens, cache.as_arg(), 96, None, ws)
+    torch.cuda.synchronize()
+    got = y.cpu().numpy().astype(np.float64)
+    # Reference on sampled rows: first 16 rows of each chunk, and 8 decode rows.
+    off = batch.seq_offsets
+    pick = [(b, 16) for b in range(4)] + [(b, 1) for b in range(4, B, 8)]
+    xs = np.concatenate([batch.x[off[b]:off[b] + n] for b, n in pick])
+    so = np.concatenate([[0], np.cumsum([n for _, n in pick])])
+    w64 = weights_f64(layers)[0]
+    exp, _, _ = ref.layer_forward(f64(xs), w64, shape, so, [int(ctx_lens[b]) for b, _ in pick],
+                                  [h64(prefix.k[0][b]) for b, _ in pick], [h64(prefix.v[0][b]) for b, _ in pick])
+    gs = np.concatenate([got[off[b]:off[b] + n] for b, n in pick])
+    e = err_ratio(gs, exp)
+    log(f"  sampled rows: max err / rms = {e:.3e}")
+    assert e <= TOL
+
+
+def test_corun_changes_nothing(env, thinker):
+    """Prefill on a 128-CU mask with talker steps on the other 128 CUs: both
+    outputs equal their solo runs bit for bit, and the two stages overlap."""
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    layers_t, d, cache, wdev_t, xt, ws_t = talker_setup(env, 32, W.SEEDS["talker"])
+    kv0 = [c.clone() for c in cache.k] + [c.clone() for c in cache.v]
+    yt_solo = torch.empty(xt.shape, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    binding.hs_downstream_decode_step(ctx, W.TALKER, wdev_t, xt, yt_solo, cache.as_arg(), d.kv_lens, 128, None, ws_t)
+    y_solo = run_thinker(env, thinker, 128)
+    torch.cuda.synchronize()
+    # The decode step rewrote the new rows with identical values; restore anyway.
+    for i, c in enumerate(cache.k + cache.v):
+        c.copy_(kv0[i])
+    torch.cuda.synchronize()
+    s_sh = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_SHARED))
+    s_dn = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_DOWN))
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    yt = torch.empty_like(yt_solo)
+    log("[co-run] prefill @128 + decode @128")
+    _, batch, wdev, x, ws = thinker
+    y = torch.empty(x.shape, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    ev[0].record(s_sh)
+    binding.hs_shared_stage_forward(ctx, W.THINKER, wdev, x, y, batch.seq_offsets, None, None, 128, None, ws)
+    ev[1].record(s_sh)
+    s_dn.wait_event(ev[0])
+    ev[2].record(s_dn)
+    for _ in range(3):
+        binding.hs_downstream_decode_step(ctx, W.TALKER, wdev_t, xt, yt, cache.as_arg(), d.kv_lens, 128, None, ws_t)
+    ev[3].record(s_dn)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y_solo)
+    assert torch.equal(yt, yt_solo)
+    t_pre = (ev[0].elapsed_time(ev[0]), ev[0].elapsed_time(ev[1]))
+    t_dec = (ev[0].elapsed_time(ev[2]), ev[0].elapsed_time(ev[3]))
+    log(f"  prefill window {t_pre}, decode window {t_dec} (ms from the common start)")
+    assert t_dec[0] < t_pre[1], "decode did not start before the prefill ended"

@@ -68,19 +68,24 @@ def test_tiny_layer_all_budgets(env):
         np.testing.assert_array_equal(outs[b], outs[256])
 
 
-@pytest.mark.parametrize("shape_name,lengths,n_layers", [
-    ("thinker", [300, 129, 1, 64, 2], 1),
-    ("tiny", [1, 5, 255, 257, 33], 2),
-    ("talker", [70, 1, 190], 1),
+@pytest.mark.parametrize("shape_name,lengths,n_layers,fmt", [
+    ("thinker", [300, 129, 1, 64, 2], 1, "bf16"),
+    ("thinker", [300, 129, 1, 64, 2], 1, "f16"),
+    ("tiny", [1, 5, 255, 257, 33], 2, "bf16"),
+    ("tiny", [1, 5, 255, 257, 33], 2, "f16"),
+    ("talker", [70, 1, 190], 1, "f16"),
 ])
-def test_ragged_prefill_parity(env, shape_name, lengths, n_layers):
-    from paper_2608_01785_amd.device_data import upload_weights
+def test_ragged_prefill_parity(env, shape_name, lengths, n_layers, fmt):
+    from paper_2608_01785_amd.device_data import prepare_f16, upload_weights
     shape = {"thinker": W.THINKER, "tiny": W.TINY, "talker": W.TALKER}[shape_name]
     layers = seeded_layers(shape, n_layers, 77)
     batch = W.random_batch(shape.hidden, lengths, seed=78)
-    log(f"[ragged prefill] {shape_name} lengths={lengths} layers={n_layers}")
+    log(f"[ragged prefill] {shape_name} lengths={lengths} layers={n_layers} weights={fmt}")
     expect, _ = ref.stack_forward(f64(batch.x), weights_f64(layers), shape, batch.seq_offsets)
-    got = run_prefill(env, shape, upload_weights(layers), batch.x, batch.seq_offsets, budget=128)
+    wdev = upload_weights(layers)
+    if fmt == "f16":
+        wdev = prepare_f16(env[1], wdev)
+    got = run_prefill(env, shape, wdev, batch.x, batch.seq_offsets, budget=128)
     e = err_ratio(got, expect)
     log(f"  max err / rms = {e:.3e}")
     assert e <= TOL
