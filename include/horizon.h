@@ -238,7 +238,7 @@ enum {
   HS_KERNEL_RMSNORM = 0,
   HS_KERNEL_QKV = 1,          /* QKV projection with RoPE and key/value store */
   HS_KERNEL_ATTENTION = 2,    /* multi-row causal attention */
-  HS_KERNEL_DECODE_ATTN = 3,  /* single-row attention (split keys + merge) */
+  HS_KERNEL_DECODE_ATTN = 3,  /* single-row attention */
   HS_KERNEL_O_PROJ = 4,       /* output projection + residual */
   HS_KERNEL_GATE_UP = 5,      /* gate/up projection + SwiGLU */
   HS_KERNEL_DOWN = 6,         /* down projection + residual */

@@ -219,191 +219,176 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
 }
 
 // ----------------------------------------------------------------------------
-// Single-row attention: one block per (row, kv head, key chunk) computes the
-// partial softmax statistics of all query heads of the group over its chunk;
-// a second kernel merges the chunks.
+// Single-row (decode) attention.  One block = one row r and one key/value head
+// g; the group's G query heads are the 32 MFMA columns (G <= 8 valid), so the
+// keys and values of the head are read once for the whole group.  The four
+// waves take interleaved key tiles; their K and V fragments come straight from
+// memory into registers in MFMA layout (double-buffered, no LDS), and the four
+// partial softmax states are merged through LDS at the end.
 
 template <int DH>
-__global__ __launch_bounds__(kThreads, 1) void decode_attn_kernel(DecodeAttnArgs a) {
-  constexpr int CK = kDecodeChunk;       // 256 keys, one per thread
-  constexpr int KROW = DH * 2;
-  constexpr int KCH = DH / 8;
-  constexpr int VROW = CK * 2;           // 512 bytes per value row
-  constexpr int VCH = CK / 8;            // 32 chunks
-  constexpr int MAXG = 8;
-  constexpr int PARTS = kThreads / DH;   // threads per value row in P.V
-  __shared__ __attribute__((aligned(16))) uint8_t ks[CK * KROW];
-  __shared__ __attribute__((aligned(16))) uint8_t vs[DH * VROW];
-  __shared__ float qs[MAXG][DH];
-  __shared__ float ps[MAXG][CK];
-  __shared__ float red[4][MAXG];
-  __shared__ float ored[PARTS][MAXG][DH];
+__global__ __launch_bounds__(kThreads, DH == 64 ? 2 : 1) void decode_attn_kernel(DecodeAttnArgs a) {
+  constexpr int TK = (DH == 64) ? 64 : 32;     // keys per tile
+  constexpr int NST = TK / 32;                 // 32-key score subtiles
+  constexpr int NKB = DH / 16;                 // 16-wide K steps of q.k
+  constexpr int NDS = DH / 32;                 // output subtiles along dh
+  constexpr int NPB = TK / 16;                 // 16-key P.V steps
+  __shared__ float red_m[4][32], red_l[4][32];
+  __shared__ float red_o[4][DH][33];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int4 it = a.items[blockIdx.x];
-  const int r = it.x, g = it.y, c = it.z;
+  const int fr = lane & 31, fh = lane >> 5;
+  const int r = blockIdx.x / a.hkv;
+  const int g = blockIdx.x % a.hkv;
   const int4 rw = a.rows[r];
   const int t = rw.x, b = rw.y;
   const int G = a.hq / a.hkv;
   const int n_keys = a.seq_ctx[b] + 1;
-  const int k0 = c * CK;
-  const int nk = min(CK, n_keys - k0);
-  const int64_t kbase = a.seq_kbase[b] + int64_t(g) * DH + int64_t(k0) * a.hkv * DH;
-  const int64_t vbase = a.seq_vbase[b] + int64_t(g) * DH * a.v_stride + k0;
+  const int n_tiles = (n_keys + TK - 1) / TK;
+  const int qh = min(fr, G - 1);  // query head of this lane's column (padding lanes repeat the last)
+  const int64_t kbase = a.seq_kbase[b] + int64_t(g) * DH;
+  const int64_t vbase = a.seq_vbase[b] + int64_t(g) * DH * a.v_stride;
+  const int kstride = a.hkv * DH;
 
-  for (int i = tid; i < G * DH; i += kThreads) {
-    const int hh = i / DH, d = i % DH;
-    qs[hh][d] = h2f(a.q[(int64_t(t) * a.hq + g * G + hh) * DH + d]);
-  }
-  for (int i = tid; i < CK * KCH; i += kThreads) {
-    const int row = i / KCH, cc = i % KCH;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (row < nk) v = *reinterpret_cast<const u32x4*>(a.kstore + kbase + int64_t(row) * a.hkv * DH + cc * 8);
-    const int phys = (cc & ~7) | ((cc & 7) ^ (row & 7));
-    *reinterpret_cast<u32x4*>(ks + row * KROW + phys * 16) = v;
-  }
-  for (int i = tid; i < DH * VCH; i += kThreads) {
-    const int d = i / VCH, cc = i % VCH;
-    const int key = cc * 8;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (key < nk) {
-      v = *reinterpret_cast<const u32x4*>(a.vstore + vbase + int64_t(d) * a.v_stride + key);
-      if (key + 8 > nk) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const uint32_t lo_ok = (key + 2 * e < nk) ? 0x0000ffffu : 0u;
-          const uint32_t hi_ok = (key + 2 * e + 1 < nk) ? 0xffff0000u : 0u;
-          v[e] &= (lo_ok | hi_ok);
-        }
-      }
-    }
-    const int phys = (cc & ~7) | ((cc & 7) ^ (d & 7));
-    *reinterpret_cast<u32x4*>(vs + d * VROW + phys * 16) = v;
-  }
-  __syncthreads();
-
-  // Scores: thread j owns key k0 + j.
-  float sc[MAXG];
+  u32x4 qf[NKB];
   {
-    const int j = tid;
+    const uint16_t* qp = a.q + (int64_t(t) * a.hq + g * G + qh) * DH + fh * 8;
 #pragma unroll
-    for (int hh = 0; hh < MAXG; ++hh) sc[hh] = 0.0f;
+    for (int kb = 0; kb < NKB; ++kb) qf[kb] = *reinterpret_cast<const u32x4*>(qp + kb * 16);
+  }
+
+  // Fragments of one tile: K rows (A operand of S^T = K Q^T, rows permuted by
+  // perm32) and V^T rows (A operand of O^T = V^T P^T).
+  struct Tile {
+    u32x4 k[NST][NKB];
+    u32x4 v[NDS][NPB];
+  };
+  auto load = [&](int tt, Tile& f) {
+    const int kv0 = tt * TK;
 #pragma unroll
-    for (int cc = 0; cc < KCH; ++cc) {
-      const int phys = (cc & ~7) | ((cc & 7) ^ (j & 7));
-      const u32x4 kv = *reinterpret_cast<const u32x4*>(ks + j * KROW + phys * 16);
-      float kf[8];
+    for (int st = 0; st < NST; ++st) {
+      const int key = kv0 + 32 * st + perm32(fr);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) h2x_to_f(kv[e], kf[2 * e], kf[2 * e + 1]);
+      for (int kb = 0; kb < NKB; ++kb)
+        f.k[st][kb] = *reinterpret_cast<const u32x4*>(a.kstore + kbase + int64_t(key) * kstride + kb * 16 + fh * 8);
+    }
 #pragma unroll
-      for (int hh = 0; hh < MAXG; ++hh) {
-        if (hh < G) {
+    for (int ds = 0; ds < NDS; ++ds)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) sc[hh] += qs[hh][cc * 8 + e] * kf[e];
+      for (int pb = 0; pb < NPB; ++pb) {
+        const int key = kv0 + 16 * pb + 8 * fh;
+        u32x4 v = *reinterpret_cast<const u32x4*>(a.vstore + vbase + int64_t(ds * 32 + fr) * a.v_stride + key);
+        if (key + 8 > n_keys) {  // zero values past the last key (P is 0 there; keep 0 * garbage out)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t lo_ok = (key + 2 * e < n_keys) ? 0x0000ffffu : 0u;
+            const uint32_t hi_ok = (key + 2 * e + 1 < n_keys) ? 0xffff0000u : 0u;
+            v[e] &= (lo_ok | hi_ok);
+          }
         }
+        f.v[ds][pb] = v;
       }
-    }
-#pragma unroll
-    for (int hh = 0; hh < MAXG; ++hh) sc[hh] = (j < nk) ? sc[hh] * a.scale_log2 : -INFINITY;
-  }
-  float mh[MAXG], lh[MAXG];
-#pragma unroll
-  for (int hh = 0; hh < MAXG; ++hh) {
-    if (hh < G) {
-      const float m = wave_max(sc[hh]);
-      if (lane == 0) red[wave][hh] = m;
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int hh = 0; hh < MAXG; ++hh) {
-    if (hh < G) {
-      mh[hh] = fmaxf(fmaxf(red[0][hh], red[1][hh]), fmaxf(red[2][hh], red[3][hh]));
-      const float p = exp2f(sc[hh] - mh[hh]);
-      ps[hh][tid] = p;
-      sc[hh] = p;
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int hh = 0; hh < MAXG; ++hh) {
-    if (hh < G) {
-      const float s = wave_sum(sc[hh]);
-      if (lane == 0) red[wave][hh] = s;
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int hh = 0; hh < MAXG; ++hh)
-    if (hh < G) lh[hh] = red[0][hh] + red[1][hh] + red[2][hh] + red[3][hh];
+  };
 
-  // P.V: thread -> (value row d, key part).
-  {
-    const int d = tid % DH, part = tid / DH;
-    constexpr int KPP = CK / PARTS;  // keys per part
-    float acc[MAXG];
+  f32x16 o[NDS];
 #pragma unroll
-    for (int hh = 0; hh < MAXG; ++hh) acc[hh] = 0.0f;
-#pragma unroll 4
-    for (int cc = part * (KPP / 8); cc < (part + 1) * (KPP / 8); ++cc) {
-      const int phys = (cc & ~7) | ((cc & 7) ^ (d & 7));
-      const u32x4 vv = *reinterpret_cast<const u32x4*>(vs + d * VROW + phys * 16);
-      float vf[8];
+  for (int i = 0; i < NDS; ++i)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) h2x_to_f(vv[e], vf[2 * e], vf[2 * e + 1]);
+    for (int e = 0; e < 16; ++e) o[i][e] = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
+
+  auto compute = [&](int tt, const Tile& f) {
+    const int kv0 = tt * TK;
+    f32x16 s[NST];
 #pragma unroll
-      for (int hh = 0; hh < MAXG; ++hh)
-        if (hh < G) {
+    for (int st = 0; st < NST; ++st) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc[hh] += ps[hh][cc * 8 + e] * vf[e];
-        }
+      for (int e = 0; e < 16; ++e) s[st][e] = 0.0f;
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) s[st] = mfma32(f.k[st][kb], qf[kb], s[st]);
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < NST; ++st)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = kv0 + 32 * st + 16 * (e >> 3) + 8 * fh + (e & 7);
+        const float v = (key < n_keys) ? s[st][e] * a.scale_log2 : -INFINITY;
+        s[st][e] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.0f;
+#pragma unroll
+    for (int st = 0; st < NST; ++st)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float p = exp2f(s[st][e] - m_new);
+        s[st][e] = p;
+        psum += p;
+      }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int i = 0; i < NDS; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[i][e] *= alpha;
+    u32x4 pf[NPB];
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      const int st = pb >> 1, r0 = 8 * (pb & 1);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pf[pb][e] = pack2h(s[st][r0 + 2 * e], s[st][r0 + 2 * e + 1]);
     }
 #pragma unroll
-    for (int hh = 0; hh < MAXG; ++hh)
-      if (hh < G) ored[part][hh][d] = acc[hh];
-  }
-  __syncthreads();
-  for (int i = tid; i < G * DH; i += kThreads) {
-    const int hh = i / DH, d = i % DH;
-    float s = 0.0f;
+    for (int i = 0; i < NDS; ++i)
 #pragma unroll
-    for (int p = 0; p < PARTS; ++p) s += ored[p][hh][d];
-    a.part_o[(int64_t(blockIdx.x) * G + hh) * DH + d] = s;
-  }
-  if (tid < G) {
-    // mh/lh are identical in every thread; thread hh publishes head hh.
-    float m = 0.0f, l = 0.0f;
-#pragma unroll
-    for (int hh = 0; hh < MAXG; ++hh)
-      if (hh == tid) { m = mh[hh]; l = lh[hh]; }
-    a.part_ml[(int64_t(blockIdx.x) * G + tid) * 2 + 0] = m;
-    a.part_ml[(int64_t(blockIdx.x) * G + tid) * 2 + 1] = l;
-  }
-}
+      for (int pb = 0; pb < NPB; ++pb) o[i] = mfma32(f.v[i][pb], pf[pb], o[i]);
+  };
 
-template <int DH>
-__global__ __launch_bounds__(128) void decode_combine_kernel(DecodeAttnArgs a) {
-  const int r = blockIdx.x / a.hq;
-  const int h = blockIdx.x % a.hq;
-  const int G = a.hq / a.hkv;
-  const int g = h / G, hh = h % G;
-  const int4 rw = a.rows[r];
-  const int t = rw.x, first = rw.z, nch = rw.w;
-  const int d = threadIdx.x;
-  if (d >= DH) return;
-  float m = -INFINITY;
-  for (int c = 0; c < nch; ++c) {
-    const int64_t item = first + int64_t(g) * nch + c;
-    m = fmaxf(m, a.part_ml[(item * G + hh) * 2]);
+  // Wave w takes tiles w, w + 4, ...; the next tile's fragments load while
+  // the current one is multiplied.
+  Tile f0, f1;
+  int tt = wave;
+  if (tt < n_tiles) load(tt, f0);
+  while (tt < n_tiles) {
+    if (tt + 4 < n_tiles) load(tt + 4, f1);
+    compute(tt, f0);
+    tt += 4;
+    if (tt >= n_tiles) break;
+    if (tt + 4 < n_tiles) load(tt + 4, f0);
+    compute(tt, f1);
+    tt += 4;
   }
-  float num = 0.0f, den = 0.0f;
-  for (int c = 0; c < nch; ++c) {
-    const int64_t item = first + int64_t(g) * nch + c;
-    const float w = exp2f(a.part_ml[(item * G + hh) * 2] - m);
-    den += w * a.part_ml[(item * G + hh) * 2 + 1];
-    num += w * a.part_o[(item * G + hh) * DH + d];
+
+  // Merge the four waves.  Lane (fr, fh) holds query column fr; both halves
+  // share the running max, each holds part of the sum.
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  if (fh == 0) {
+    red_m[wave][fr] = m_run;
+    red_l[wave][fr] = l_tot;
   }
-  a.o[int64_t(t) * a.hq * DH + h * DH + d] = f2h(num / den);
+#pragma unroll
+  for (int i = 0; i < NDS; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) red_o[wave][32 * i + 8 * (e >> 2) + 4 * fh + (e & 3)][fr] = o[i][e];
+  __syncthreads();
+  for (int idx = tid; idx < G * DH; idx += kThreads) {
+    const int q = idx / DH, d = idx % DH;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, red_m[w][q]);
+    float num = 0.0f, den = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float sc = exp2f(red_m[w][q] - M);  // waves without tiles hold -inf: weight 0
+      num += sc * red_o[w][d][q];
+      den += sc * red_l[w][q];
+    }
+    a.o[int64_t(t) * a.hq * DH + (g * G + q) * DH + d] = f2h(num / den);
+  }
 }
 
 }  // namespace
@@ -419,14 +404,12 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_decode_attention(const DecodeAttnArgs& a, hipStream_t s) {
-  if (a.n_items <= 0) return hipSuccess;
-  if (a.dh == 64) {
-    hipLaunchKernelGGL(decode_attn_kernel<64>, dim3(a.n_items), dim3(kThreads), 0, s, a);
-    hipLaunchKernelGGL(decode_combine_kernel<64>, dim3(a.n_rows * a.hq), dim3(64), 0, s, a);
-  } else {
-    hipLaunchKernelGGL(decode_attn_kernel<128>, dim3(a.n_items), dim3(kThreads), 0, s, a);
-    hipLaunchKernelGGL(decode_combine_kernel<128>, dim3(a.n_rows * a.hq), dim3(128), 0, s, a);
-  }
+  if (a.n_rows <= 0) return hipSuccess;
+  const int grid = a.n_rows * a.hkv;
+  if (a.dh == 64)
+    hipLaunchKernelGGL(decode_attn_kernel<64>, dim3(grid), dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(decode_attn_kernel<128>, dim3(grid), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -1,0 +1,280 @@
+// Skinny fp16 MFMA GEMM for decode-sized batches (M <= 128 rows), gfx950.
+//
+// Decode re-reads every weight for a handful of rows, so this kernel is built
+// to stream W at HBM speed rather than to reuse it: each block owns a thin
+// strip of weight rows (32, or 64 when the epilogue needs RoPE or gate/up
+// pairs) and all M rows, and walks K in 64-wide stages copied buffer -> LDS
+// by the load unit through an 8-deep ring (many strips in flight per CU).
+// The four waves split every stage's K: wave w multiplies the 16-wide slice w,
+// so no wave waits on another until the end, where partial accumulators are
+// summed through LDS and the same fused epilogues as the large GEMM run
+// (residual add into fp32, SwiGLU, or RoPE + key/value store).
+//
+// Layout conventions are those of the large GEMM: the weight strip is the
+// MFMA A operand, activation rows the B operand, so each lane of a 32x32
+// accumulator owns one activation row and 4 consecutive output columns per
+// register group.
+#include "hs_device.h"
+#include "hs_kernels.h"
+
+namespace hs {
+namespace {
+
+constexpr int BK = 64;                  // K per stage
+constexpr int kRowBytes = BK * 2;       // 128 bytes, 8 chunks of 16
+constexpr int kMaxStages = 8;
+constexpr int kLdsBytes = 160 * 1024;
+constexpr int kThreads = 256;
+
+using lds_ptr_t = __attribute__((address_space(3))) void*;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
+
+__device__ __forceinline__ void barrier_nofence() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's LDS reads are done
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+
+// Wait until at most n stages of this wave's copies are outstanding, with L
+// copies per stage.
+template <int L>
+__device__ __forceinline__ void wait_stages(int n) {
+  switch (n) {
+#define HS_CASE(k)                                                           \
+  case k:                                                                    \
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((k * L) < 63 ? (k * L) : 63) : "memory"); \
+    break;
+    HS_CASE(0) HS_CASE(1) HS_CASE(2) HS_CASE(3) HS_CASE(4) HS_CASE(5)
+    default:
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((6 * L) < 63 ? (6 * L) : 63) : "memory");
+      break;
+#undef HS_CASE
+  }
+}
+
+// Weight row held in row r of strip `tile` (NR rows per strip).
+template <int EPI, int NR>
+__device__ __forceinline__ uint32_t strip_row(int tile, int r, int ffn) {
+  if constexpr (EPI == EPI_SWIGLU) {
+    return uint32_t((r >> 5) * ffn + tile * 32 + (r & 31));  // [gate 32 | up 32]
+  } else {
+    return uint32_t(tile * NR + r);
+  }
+}
+
+// NS: n-subtiles of 32 weight rows per block (1 or 2); MT: m-subtiles of 32 rows.
+template <int EPI, int DH, bool W_F16, int NS, int MT>
+__global__ __launch_bounds__(kThreads) void skinny_kernel(GemmArgs a) {
+  constexpr int NR = 32 * NS;                 // weight rows per block
+  constexpr int MR = 32 * MT;                 // activation rows covered
+  constexpr int WBYTES = NR * kRowBytes;
+  constexpr int XBYTES = MR * kRowBytes;
+  constexpr int STAGE = WBYTES + XBYTES;
+  constexpr int WCOPIES = NR / 8 / 4;         // copies per wave per stage (8 rows each)
+  constexpr int XCOPIES = MR / 8 / 4;
+  constexpr int L = WCOPIES + XCOPIES;
+  constexpr int kStages = (kLdsBytes / STAGE) < kMaxStages ? (kLdsBytes / STAGE) : kMaxStages;
+  static_assert(NR % 32 == 0 && MR % 32 == 0, "tile shape");
+  static_assert(4 * NS * MT * 16 * 64 * 4 <= kStages * STAGE, "reduction buffer fits the ring");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int fr = lane & 31, fh = lane >> 5;
+  const int tile = blockIdx.x;
+  const int KT = a.K / BK;
+  const uint32_t row_bytes = uint32_t(a.K) * 2;
+
+  const uint32_t w_rows = (EPI == EPI_SWIGLU) ? uint32_t(2 * a.ffn) : uint32_t(a.n_tiles_n * 256);
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(a.W, w_rows * row_bytes);
+  const __amdgpu_buffer_rsrc_t xres = make_rsrc(a.A, uint32_t(a.M) * row_bytes);
+
+  // Copy assignment: one wave instruction fills 8 rows (1 KB); lane i lands at
+  // row i / 8, physical chunk i % 8 = logical chunk (i % 8) ^ (row % 8).
+  const int sub = lane >> 3;
+  const int chunk = (lane & 7) ^ sub;
+  // Fixed extents: arrays sized by the template's constants and captured by
+  // the lambda below make the host pass drop the kernel's launch stub.
+  static_assert(WCOPIES <= 2 && XCOPIES <= 4, "copy slots");
+  uint32_t w_off[2], x_off[4];
+#pragma unroll
+  for (int c = 0; c < WCOPIES; ++c)
+    w_off[c] = strip_row<EPI, NR>(tile, (wave * WCOPIES + c) * 8 + sub, a.ffn) * row_bytes + chunk * 16;
+#pragma unroll
+  for (int c = 0; c < XCOPIES; ++c) x_off[c] = uint32_t((wave * XCOPIES + c) * 8 + sub) * row_bytes + chunk * 16;
+
+  auto issue = [&](int kt, int buf) {
+    const int koff = kt * kRowBytes;
+    uint8_t* base = smem + buf * STAGE;
+#pragma unroll
+    for (int c = 0; c < WCOPIES; ++c)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lds_ptr_t)(base + (wave * WCOPIES + c) * 8 * kRowBytes), 16,
+                                               w_off[c], koff, 0, 0);
+#pragma unroll
+    for (int c = 0; c < XCOPIES; ++c)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xres,
+                                               (lds_ptr_t)(base + WBYTES + (wave * XCOPIES + c) * 8 * kRowBytes),
+                                               16, x_off[c], koff, 0, 0);
+  };
+
+  f32x16 acc[NS][MT];
+#pragma unroll
+  for (int i = 0; i < NS; ++i)
+#pragma unroll
+    for (int j = 0; j < MT; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+#pragma unroll
+  for (int st = 0; st < kStages - 1; ++st)
+    if (st < KT) issue(st, st);
+
+  const int phys = (2 * wave + fh) ^ (fr & 7);  // this wave's 16-wide K slice
+  int buf = 0;
+  for (int kt = 0; kt < KT; ++kt) {
+    wait_stages<L>(min(kStages - 2, KT - 1 - kt));
+    barrier_nofence();
+    if (kt + kStages - 1 < KT) issue(kt + kStages - 1, buf == 0 ? kStages - 1 : buf - 1);
+    const uint8_t* base = smem + buf * STAGE;
+    u32x4 fw[NS], fx[MT];
+#pragma unroll
+    for (int i = 0; i < NS; ++i) fw[i] = *reinterpret_cast<const u32x4*>(base + (i * 32 + fr) * kRowBytes + phys * 16);
+#pragma unroll
+    for (int j = 0; j < MT; ++j)
+      fx[j] = *reinterpret_cast<const u32x4*>(base + WBYTES + (j * 32 + fr) * kRowBytes + phys * 16);
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      const u32x4 wh = W_F16 ? fw[i] : bf8_to_h8(fw[i]);
+#pragma unroll
+      for (int j = 0; j < MT; ++j) acc[i][j] = mfma32(wh, fx[j], acc[i][j]);
+    }
+    buf = (buf == kStages - 1) ? 0 : buf + 1;
+  }
+
+  // Sum the four waves' partial accumulators through LDS; wave w then owns
+  // row subtiles j = w, w + 4, ... and runs their epilogue.
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int i = 0; i < NS; ++i)
+#pragma unroll
+    for (int j = 0; j < MT; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) red[(((wave * NS + i) * MT + j) * 16 + r) * 64 + lane] = acc[i][j][r];
+  __syncthreads();
+  for (int j = wave; j < MT; j += 4) {
+    const int m = j * 32 + fr;
+    f32x16 c[NS];
+#pragma unroll
+    for (int i = 0; i < NS; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float v = 0.0f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) v += red[(((w * NS + i) * MT + j) * 16 + r) * 64 + lane];
+        c[i][r] = v;
+      }
+    if (m >= a.M) continue;
+    if constexpr (EPI == EPI_RESID) {
+      float* orow = a.out_f32 + int64_t(m) * a.ldo;
+#pragma unroll
+      for (int i = 0; i < NS; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = tile * NR + i * 32 + 8 * g + 4 * fh;
+          f32x4 v = {c[i][4 * g], c[i][4 * g + 1], c[i][4 * g + 2], c[i][4 * g + 3]};
+          if (a.resid_f32) {
+            v += *reinterpret_cast<const f32x4*>(a.resid_f32 + int64_t(m) * a.ldo + n);
+          } else {
+            float r4[4];
+            load_bf16x4(a.resid + int64_t(m) * a.ldo + n, r4);
+            v[0] += r4[0];
+            v[1] += r4[1];
+            v[2] += r4[2];
+            v[3] += r4[3];
+          }
+          *reinterpret_cast<f32x4*>(orow + n) = v;
+        }
+    } else if constexpr (EPI == EPI_SWIGLU) {
+      static_assert(EPI != EPI_SWIGLU || NS == 2, "gate/up strips hold 32 + 32 rows");
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = silu(c[0][4 * g + e]) * c[1][4 * g + e];
+        store_h4(a.out + int64_t(m) * a.ldo + tile * 32 + 8 * g + 4 * fh, v[0], v[1], v[2], v[3]);
+      }
+    } else {  // EPI_QKV: the strip is one 64-wide head
+      static_assert(EPI != EPI_QKV || (NS == 2 && DH == 64), "QKV strips are one 64-wide head");
+      const int head = tile;
+      const int p = a.pos[m];
+      const float2* rt = a.rope + int64_t(p) * (DH / 2);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int d = 8 * g + 4 * fh;
+        if (head < a.hq + a.hkv) {
+          float rl[4], rh[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float2 cs = rt[d + e];
+            const float lo = c[0][4 * g + e], hi = c[1][4 * g + e];
+            rl[e] = lo * cs.x - hi * cs.y;
+            rh[e] = hi * cs.x + lo * cs.y;
+          }
+          uint16_t* dst = (head < a.hq) ? a.q + (int64_t(m) * a.hq + head) * DH
+                                        : a.kstore + a.k_off[m] + int64_t(head - a.hq) * DH;
+          store_h4(dst + d, rl[0], rl[1], rl[2], rl[3]);
+          store_h4(dst + d + DH / 2, rh[0], rh[1], rh[2], rh[3]);
+        } else {
+          const int gh = head - a.hq - a.hkv;
+          uint16_t* dst = a.vstore + a.v_off[m];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            dst[int64_t(gh * DH + d + e) * a.v_stride] = f2h(c[0][4 * g + e]);
+            dst[int64_t(gh * DH + d + DH / 2 + e) * a.v_stride] = f2h(c[1][4 * g + e]);
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int EPI, int DH, int NS, int MT>
+hipError_t launch_mt(const GemmArgs& a, int n_blocks, hipStream_t s) {
+  if (a.w_f16)
+    hipLaunchKernelGGL((skinny_kernel<EPI, DH, true, NS, MT>), dim3(n_blocks), dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((skinny_kernel<EPI, DH, false, NS, MT>), dim3(n_blocks), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int EPI, int DH, int NS>
+hipError_t launch_ns(const GemmArgs& a, int n_blocks, hipStream_t s) {
+  if (a.M <= 32) return launch_mt<EPI, DH, NS, 1>(a, n_blocks, s);
+  if (a.M <= 64) return launch_mt<EPI, DH, NS, 2>(a, n_blocks, s);
+  return launch_mt<EPI, DH, NS, 4>(a, n_blocks, s);
+}
+
+}  // namespace
+
+bool skinny_supported(int epi, const GemmArgs& a) {
+  if (a.M <= 0 || a.M > kSkinnyMaxRows || a.K % BK != 0) return false;
+  if (epi == EPI_QKV) return a.dh == 64;
+  return true;
+}
+
+hipError_t launch_gemm_skinny(int epi, const GemmArgs& a, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  switch (epi) {
+    case EPI_RESID: return launch_ns<EPI_RESID, 64, 1>(a, a.n_tiles_n * 8, s);      // 32-row strips
+    case EPI_SWIGLU: return launch_ns<EPI_SWIGLU, 64, 2>(a, a.ffn / 32, s);         // 32 outputs per strip
+    case EPI_QKV: return launch_ns<EPI_QKV, 64, 2>(a, a.hq + 2 * a.hkv, s);        // one head per strip
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace hs

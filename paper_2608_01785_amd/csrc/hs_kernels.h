@@ -38,6 +38,11 @@ struct GemmArgs {
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, int max_blocks, hipStream_t s);
 
+// Decode-sized GEMMs (M <= kSkinnyMaxRows): thin weight strips, one block each.
+constexpr int kSkinnyMaxRows = 128;
+bool skinny_supported(int epi, const GemmArgs& a);
+hipError_t launch_gemm_skinny(int epi, const GemmArgs& a, hipStream_t s);
+
 struct AttnArgs {
   const uint16_t* q;        // [T, hq, dh]
   const uint16_t* kstore;   // token-major keys
@@ -57,27 +62,21 @@ struct AttnArgs {
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 
-// Single-row (decode) attention, split over key chunks, then combined.
+// Single-row (decode) attention: one block per (row, key/value head).
 struct DecodeAttnArgs {
   const uint16_t* q;
   const uint16_t* kstore;
   const uint16_t* vstore;
   uint16_t* o;
-  const int4* items;        // [n_items] = (row index r, kv head g, chunk c, 0)
-  int n_items;
-  const int4* rows;         // [R] = (packed row t, sequence b, first item, n_chunks)
+  const int4* rows;         // [R] = (packed row t, sequence b, 0, 0)
   int n_rows;
-  const int32_t* seq_ctx;   // keys of row r's sequence: seq_ctx[b] + 1
+  const int32_t* seq_ctx;   // row r of sequence b attends to seq_ctx[b] + 1 keys
   const int64_t* seq_kbase;
   const int64_t* seq_vbase;
   int64_t v_stride;
-  float* part_o;            // [n_items, group, dh]
-  float* part_ml;           // [n_items, group, 2]
   int hq, hkv, dh;
   float scale_log2;
 };
-
-constexpr int kDecodeChunk = 256;
 
 hipError_t launch_decode_attention(const DecodeAttnArgs& a, hipStream_t s);
 

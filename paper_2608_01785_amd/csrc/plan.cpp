@@ -84,33 +84,27 @@ hs_status validate_batch(const int32_t* off, const int32_t* ctx, int32_t B, int3
 
 int64_t max_att_items(int32_t T, int32_t B) { return int64_t(T) / kAttnBlockQ + B + 1; }
 
-int64_t max_dec_items(const hs_layer_cfg& c, int32_t B, int32_t max_pos) {
-  return int64_t(B) * c.n_kv_heads * ((max_pos + kDecChunk - 1) / kDecChunk + 1);
-}
-
-static size_t meta_bytes(int32_t T, int32_t B, int64_t att, int64_t dec_items) {
+static size_t meta_bytes(int32_t T, int32_t B, int64_t att) {
   size_t s = 0;
   s += align_up(size_t(T) * 4, 16);       // pos
   s += align_up(size_t(T) * 8, 16) * 2;   // k_off, v_off
   s += align_up(size_t(B) * 4, 16) * 3;   // seq_start, seq_len, seq_ctx
   s += align_up(size_t(B) * 8, 16) * 2;   // seq_kbase, seq_vbase
   s += align_up(size_t(att) * 8, 16);     // att items
-  s += align_up(size_t(B) * 16, 16);      // dec rows
-  s += align_up(size_t(dec_items) * 16, 16);
+  s += align_up(size_t(B) * 16, 16);      // single-row (decode) rows
   return align_up(s, kAlign);
 }
 
 WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos) {
   WsLayout w{};
   const size_t d = c.hidden, hq = c.n_q_heads, hkv = c.n_kv_heads, dh = c.head_dim, f = c.ffn;
-  const int64_t dec = max_dec_items(c, B, max_pos);
   size_t p = 0;
   auto take = [&](size_t bytes) {
     const size_t at = p;
     p = align_up(p + bytes, kAlign);
     return at;
   };
-  w.meta_bytes = meta_bytes(T, B, max_att_items(T, B), dec);
+  w.meta_bytes = meta_bytes(T, B, max_att_items(T, B));
   w.meta = take(w.meta_bytes);
   w.n = take(size_t(T) * d * 2);
   w.q = take(size_t(T) * hq * dh * 2);
@@ -122,9 +116,6 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
   w.a = take(size_t(T) * f * 2);
   w.xtmp = take(size_t(T) * d * 4);
   w.rope = take(size_t(max_pos) * (dh / 2) * 8);
-  const size_t group = hq / hkv;
-  w.part_o = take(size_t(dec) * group * dh * 4);
-  w.part_ml = take(size_t(dec) * group * 2 * 4);
   w.total = p;
   return w;
 }
@@ -139,7 +130,7 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   const int64_t T = P.T;
 
   // Attention work: multi-row sequences in 128-row query blocks, longest
-  // key range first; single-row sequences take the split-key decode path.
+  // key range first; single-row sequences take the decode path.
   struct Item { int32_t b, q0, keys; };
   std::vector<Item> att;
   std::vector<int32_t> dec_seq;
@@ -155,13 +146,10 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   }
   std::stable_sort(att.begin(), att.end(), [](const Item& x, const Item& y) { return x.keys > y.keys; });
   P.n_att_items = int32_t(att.size());
+  // Longest key range first among single-row sequences as well.
+  std::stable_sort(dec_seq.begin(), dec_seq.end(),
+                   [&](int32_t x, int32_t y) { return (ctx ? ctx[x] : 0) > (ctx ? ctx[y] : 0); });
   P.n_dec_rows = int32_t(dec_seq.size());
-  int64_t n_dec_items = 0;
-  for (int32_t b : dec_seq) {
-    const int32_t keys = (ctx ? ctx[b] : 0) + 1;
-    n_dec_items += hkv * ((keys + kDecChunk - 1) / kDecChunk);
-  }
-  P.n_dec_items = int32_t(n_dec_items);
 
   // Image layout (must match meta_bytes' order and bounds).
   size_t p = 0;
@@ -180,7 +168,6 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   P.seq_vbase = take(size_t(B) * 8);
   P.att_items = take(size_t(P.n_att_items) * 8);
   P.dec_rows = take(size_t(P.n_dec_rows) * 16);
-  P.dec_items = take(size_t(P.n_dec_items) * 16);
   P.image.assign(align_up(p, kAlign), 0);
 
   auto i32 = [&](size_t at) { return reinterpret_cast<int32_t*>(P.image.data() + at); };
@@ -221,25 +208,13 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
     i32(P.att_items)[2 * i] = att[i].b;
     i32(P.att_items)[2 * i + 1] = att[i].q0;
   }
-  int32_t item = 0;
   for (int32_t r = 0; r < P.n_dec_rows; ++r) {
     const int32_t b = dec_seq[r];
-    const int32_t keys = (ctx ? ctx[b] : 0) + 1;
-    const int32_t nch = (keys + kDecChunk - 1) / kDecChunk;
     int32_t* row = i32(P.dec_rows) + 4 * r;
     row[0] = off[b];
     row[1] = b;
-    row[2] = item;
-    row[3] = nch;
-    for (int32_t g = 0; g < hkv; ++g)
-      for (int32_t ch = 0; ch < nch; ++ch) {
-        int32_t* it = i32(P.dec_items) + 4 * item;
-        it[0] = r;
-        it[1] = g;
-        it[2] = ch;
-        it[3] = 0;
-        ++item;
-      }
+    row[2] = 0;
+    row[3] = 0;
   }
   return HS_OK;
 }

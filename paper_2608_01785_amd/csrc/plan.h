@@ -19,7 +19,6 @@ void clear_error();
 constexpr int kMaxXcc = 8;
 constexpr size_t kAlign = 256;
 constexpr int kAttnBlockQ = 128;   // query rows per prefill-attention block
-constexpr int kDecChunk = 256;     // keys per decode-attention block
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -44,14 +43,11 @@ struct WsLayout {
   size_t a;           // [T, ffn]
   size_t xtmp;        // [T, d] fp32 residual between layers
   size_t rope;        // [max_pos, dh / 2] float2
-  size_t part_o;      // decode partials [items, group, dh] f32
-  size_t part_ml;     // [items, group, 2] f32
   size_t total;
 };
 
 // Upper bounds used for sizing: T rows, B sequences, positions < max_pos.
 int64_t max_att_items(int32_t T, int32_t B);
-int64_t max_dec_items(const hs_layer_cfg& c, int32_t B, int32_t max_pos);
 
 WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos);
 
@@ -62,8 +58,8 @@ struct Plan {
   // byte offsets inside image
   size_t pos = 0, k_off = 0, v_off = 0;
   size_t seq_start = 0, seq_len = 0, seq_ctx = 0, seq_kbase = 0, seq_vbase = 0;
-  size_t att_items = 0, dec_rows = 0, dec_items = 0;
-  int32_t n_att_items = 0, n_dec_rows = 0, n_dec_items = 0;
+  size_t att_items = 0, dec_rows = 0;
+  int32_t n_att_items = 0, n_dec_rows = 0;
   int64_t v_stride = 0;
 };
 

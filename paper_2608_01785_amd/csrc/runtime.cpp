@@ -161,6 +161,12 @@ void timing_end(hs_context* ctx, hipStream_t s, int kind, hipEvent_t a, hipEvent
     timing_end(ctx, s, kind, ta_, tb_);                \
   } while (0)
 
+// Large persistent GEMM, or the skinny variant for decode-sized batches.
+hipError_t gemm(int epi, const hs::GemmArgs& a, int grid_cap, hipStream_t s) {
+  if (hs::skinny_supported(epi, a)) return hs::launch_gemm_skinny(epi, a, s);
+  return hs::launch_gemm(epi, a, grid_cap, s);
+}
+
 // Shared body of the prefill forward and the decode step.
 hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w, int32_t n_layers,
                     const void* x_in, void* x_out, const int32_t* seq_offsets, const int32_t* ctx_lens,
@@ -266,7 +272,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     g.hq = hq;
     g.hkv = hkv;
     g.dh = dh;
-    TIMED(HS_KERNEL_QKV, hs::launch_gemm(hs::EPI_QKV, g, grid_cap, s));
+    TIMED(HS_KERNEL_QKV, gemm(hs::EPI_QKV, g, grid_cap, s));
 
     hs::AttnArgs at_args{};
     at_args.q = q_buf;
@@ -292,21 +298,17 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     da.kstore = kstore;
     da.vstore = vstore;
     da.o = o_buf;
-    da.items = reinterpret_cast<const int4*>(meta + plan.dec_items);
-    da.n_items = plan.n_dec_items;
     da.rows = reinterpret_cast<const int4*>(meta + plan.dec_rows);
     da.n_rows = plan.n_dec_rows;
     da.seq_ctx = at_args.seq_ctx;
     da.seq_kbase = at_args.seq_kbase;
     da.seq_vbase = at_args.seq_vbase;
     da.v_stride = plan.v_stride;
-    da.part_o = at<float>(ws, lay.part_o);
-    da.part_ml = at<float>(ws, lay.part_ml);
     da.hq = hq;
     da.hkv = hkv;
     da.dh = dh;
     da.scale_log2 = scale_log2;
-    if (plan.n_dec_items > 0) TIMED(HS_KERNEL_DECODE_ATTN, hs::launch_decode_attention(da, s));
+    if (plan.n_dec_rows > 0) TIMED(HS_KERNEL_DECODE_ATTN, hs::launch_decode_attention(da, s));
 
     hs::GemmArgs go{};
     go.A = o_buf;
@@ -319,7 +321,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     go.ldo = d;
     go.resid = x_cur;
     go.resid_f32 = x_cur_f32;
-    TIMED(HS_KERNEL_O_PROJ, hs::launch_gemm(hs::EPI_RESID, go, grid_cap, s));
+    TIMED(HS_KERNEL_O_PROJ, gemm(hs::EPI_RESID, go, grid_cap, s));
 
     TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(nullptr, h_buf, static_cast<const uint16_t*>(w[l].ln2), n_buf, T,
                                                 d, cfg->rms_eps, 4 * budget, s));
@@ -334,7 +336,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     gu.out = a_buf;
     gu.ldo = f;
     gu.ffn = f;
-    TIMED(HS_KERNEL_GATE_UP, hs::launch_gemm(hs::EPI_SWIGLU, gu, grid_cap, s));
+    TIMED(HS_KERNEL_GATE_UP, gemm(hs::EPI_SWIGLU, gu, grid_cap, s));
 
     hs::GemmArgs gd{};
     gd.A = a_buf;
@@ -346,7 +348,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     gd.out_f32 = x_next;
     gd.ldo = d;
     gd.resid_f32 = h_buf;
-    TIMED(HS_KERNEL_DOWN, hs::launch_gemm(hs::EPI_RESID, gd, grid_cap, s));
+    TIMED(HS_KERNEL_DOWN, gemm(hs::EPI_RESID, gd, grid_cap, s));
     x_cur = nullptr;
     x_cur_f32 = x_next;
   }

@@ -74,6 +74,12 @@ def test_tiny_layer_all_budgets(env):
     ("tiny", [1, 5, 255, 257, 33], 2, "bf16"),
     ("tiny", [1, 5, 255, 257, 33], 2, "f16"),
     ("talker", [70, 1, 190], 1, "f16"),
+    # 128 rows or fewer: the skinny GEMM (one, two and four 32-row subtiles).
+    ("tiny", [50, 1, 40], 1, "bf16"),
+    ("tiny", [17, 3, 1, 9], 1, "f16"),
+    ("talker", [33, 31], 2, "bf16"),
+    ("thinker", [60, 1, 3], 1, "bf16"),
+    ("thinker", [128], 1, "f16"),
 ])
 def test_ragged_prefill_parity(env, shape_name, lengths, n_layers, fmt):
     from paper_2608_01785_amd.device_data import prepare_f16, upload_weights
@@ -156,13 +162,14 @@ def test_cached_prefix_chunks_and_cache_writes(env):
         assert np.all(h64(kb[c + n:]) == 7.0) and np.all(h64(vb[c + n:]) == 7.0)
 
 
-def test_talker_decode_step_parity(env):
+@pytest.mark.parametrize("batch,fmt", [(8, "bf16"), (40, "f16"), (97, "bf16"), (128, "f16")])
+def test_talker_decode_step_parity(env, batch, fmt):
     torch, ctx = env
     from paper_2608_01785_amd import binding
-    from paper_2608_01785_amd.device_data import DeviceCache, to_bits, to_device, upload_weights
+    from paper_2608_01785_amd.device_data import DeviceCache, prepare_f16, to_device, upload_weights
     shape = W.TALKER
-    n_layers, batch = 4, 8
-    rng = np.random.default_rng(31)
+    n_layers = 4
+    rng = np.random.default_rng(31 + batch)
     kv_lens = rng.integers(1, 300, size=batch).astype(np.int32)
     kv_lens[0] = 255  # new key lands at the end of a 256-key chunk
     kv_lens[1] = 256  # new key starts a chunk
@@ -173,7 +180,7 @@ def test_talker_decode_step_parity(env):
     for l in range(n_layers):
         for b in range(batch):
             cache.load_prefix(l, b, prefix.k[l][b], prefix.v[l][b])
-    log(f"[talker decode] layers={n_layers} batch={batch} kv_lens={kv_lens.tolist()}")
+    log(f"[talker decode] layers={n_layers} batch={batch} weights={fmt} kv_lens={kv_lens.tolist()}")
     expect, kv_new = ref.decode_step(f64(x), weights_f64(layers), shape, kv_lens,
                                      [[h64(k) for k in prefix.k[l]] for l in range(n_layers)],
                                      [[h64(v) for v in prefix.v[l]] for l in range(n_layers)])
@@ -181,8 +188,10 @@ def test_talker_decode_step_parity(env):
     xd = to_device(x)
     y = torch.empty(xd.shape, dtype=torch.float32, device="cuda")
     torch.cuda.synchronize()
-    binding.hs_downstream_decode_step(ctx, shape, upload_weights(layers), xd, y, cache.as_arg(), kv_lens, 128,
-                                      None, ws)
+    wdev = upload_weights(layers)
+    if fmt == "f16":
+        wdev = prepare_f16(ctx, wdev)
+    binding.hs_downstream_decode_step(ctx, shape, wdev, xd, y, cache.as_arg(), kv_lens, 128, None, ws)
     torch.cuda.synchronize()
     e = err_ratio(y.cpu().numpy(), expect)
     log(f"  max err / rms = {e:.3e}")
@@ -192,6 +201,37 @@ def test_talker_decode_step_parity(env):
             kb, vb = cache.rows(l, b, int(kv_lens[b]), int(kv_lens[b]) + 1)
             assert err_ratio(h64(kb[0]), kv_new[l][0][b]) <= TOL
             assert err_ratio(h64(vb[0]), kv_new[l][1][b]) <= TOL
+
+
+def test_decode_rows_behind_long_prefixes(env):
+    """Single-row sequences of the 128-wide-head shape behind cached prefixes up to 2000 rows."""
+    torch, _ = env
+    from paper_2608_01785_amd.device_data import DeviceCache, upload_weights
+    shape = W.THINKER_MIXED
+    n = 24
+    rng = np.random.default_rng(41)
+    ctx_lens = rng.integers(0, 2000, size=n).astype(np.int32)
+    ctx_lens[:4] = [0, 31, 32, 1999]
+    lengths = [1] * n
+    layers = seeded_layers(shape, 1, 42)
+    batch = W.random_batch(shape.hidden, lengths, seed=43, ctx_lens=ctx_lens)
+    prefix = W.make_cache(shape, 1, ctx_lens, seed=44)
+    cache = DeviceCache(1, n, 2048, shape.n_kv_heads, shape.head_dim, fill=0.0)
+    for b in range(n):
+        cache.load_prefix(0, b, prefix.k[0][b], prefix.v[0][b])
+    torch.cuda.synchronize()
+    log(f"[decode rows] thinker-mixed shape, {n} rows, ctx={ctx_lens.tolist()}")
+    expect, k_new, v_new = ref.layer_forward(
+        f64(batch.x), weights_f64(layers)[0], shape, batch.seq_offsets, ctx_lens,
+        [h64(k) for k in prefix.k[0]], [h64(v) for v in prefix.v[0]])
+    got = run_prefill(env, shape, upload_weights(layers), batch.x, batch.seq_offsets, ctx_lens, cache, budget=192)
+    e = err_ratio(got, expect)
+    log(f"  max err / rms = {e:.3e}")
+    assert e <= TOL
+    for b in range(n):
+        kb, vb = cache.rows(0, b, int(ctx_lens[b]), int(ctx_lens[b]) + 1)
+        assert err_ratio(h64(kb), k_new[b:b + 1]) <= TOL
+        assert err_ratio(h64(vb), v_new[b:b + 1]) <= TOL
 
 
 def test_masks_hold_on_hardware(env):
