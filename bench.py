@@ -43,7 +43,7 @@ def thinker_flops(shape, lengths, ctx=None):
 
 def talker_bytes(shape, n_layers, kv_lens):
     """HBM bytes of one decode step: weights once + cached K/V read + new K/V written."""
-    per_tok = 2 * shape.n_kv_heads * shape.head_dim * 2  # K and V, bf16, per layer
+    per_tok = 2 * shape.n_kv_heads * shape.head_dim * 2  # K and V, fp16, per layer
     kv = np.asarray(kv_lens, np.int64)
     return n_layers * (shape.params_per_layer * 2 + per_tok * int(kv.sum()) + per_tok * len(kv))
 
@@ -56,7 +56,8 @@ def main():
     ap.add_argument("--budgets", type=str, default="64,128,192")
     ap.add_argument("--no-corun", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=384, help="rows per sequence in the CPU-reference sample")
+    ap.add_argument("--cpu-rows", type=int, default=0,
+                    help="rows per sequence in the CPU-reference sample (0: sized to take about 15 s)")
     ap.add_argument("--quick", action="store_true", help="headline stack only (no budget sweep, co-run, CPU leg)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration under a profiler)")
@@ -68,7 +69,7 @@ def main():
 
     import torch
     from paper_2608_01785_amd import binding, workloads as W
-    from paper_2608_01785_amd.device_data import DeviceCache, to_device, upload_weights
+    from paper_2608_01785_amd.device_data import DeviceCache, prepare_f16, to_device, upload_weights
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = "cuda:0"
@@ -83,7 +84,10 @@ def main():
     layers = W.make_weights(shape, n_layers, W.SEEDS["thinker"]["weights"])
     batch = W.thinker_batch()
     log(f"[bench] generated thinker weights/batch in {time.time() - t0:.1f}s, T={batch.n_tokens}")
-    wdev = upload_weights(layers, dev)
+    wbf16 = upload_weights(layers, dev)
+    # One-time weight preparation: fp16 copies of the projection matrices
+    # (the MFMA operand type); the bf16 originals are timed once as well.
+    wdev = prepare_f16(ctx, wbf16)
     x = to_device(batch.x, dev)
     y = torch.empty(x.shape, dtype=torch.float32, device=dev)
     T, B = batch.n_tokens, batch.n_seqs
@@ -93,14 +97,15 @@ def main():
     flops_step = n_layers * (lin + att)
     torch.cuda.synchronize()
 
-    def run(budget, k):
+    def run(budget, k, weights=None):
+        weights = wdev if weights is None else weights
         s = binding.hs_context_stream(ctx, budget, binding.HS_ROLE_SHARED)
         ts = torch.cuda.ExternalStream(s)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record(ts)
         for _ in range(k):
-            binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, None, None, budget, None, ws)
+            binding.hs_shared_stage_forward(ctx, shape, weights, x, y, batch.seq_offsets, None, None, budget, None, ws)
         e1.record(ts)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / k
@@ -126,6 +131,10 @@ def main():
     roofline = {"bound": "mfma", "kernel": "gate_up_swiglu_gemm", "achieved": round(achieved, 1),
                 "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s", "frac": round(achieved / (PEAK_BF16 / 1e12), 4),
                 "traffic": None, "avg_launch_ms": round(gu_ms, 4)}
+
+    run(256, 1, wbf16)
+    ms_bf16w = run(256, max(2, args.steps // 2), wbf16)
+    log(f"[bench] thinker stack @256 CUs with bf16 weights converted in the GEMM: {ms_bf16w:.3f} ms/step")
 
     per_budget = {}
     for b in budgets:
@@ -170,8 +179,9 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) token rows)",
+        "dtype": "f16",
+        "data": "synthetic (seeded N(0,0.02) bf16 weights, N(0,1) bf16 token rows); fp16 MFMA operands, "
+                "fp32 accumulation and residual stream",
         "config": {"workload": "thinker 4-layer stack prefill, hidden 3584, 28/4 heads, dh 128, ffn 18944, "
                                "8 ragged requests T=10515, 256 CUs",
                    "global_batch": B, "seq_len": int(batch.lengths.max()), "tokens": T,
@@ -180,6 +190,7 @@ def main():
         "mfma_frac": round(flops_step / (ms / 1e3) / PEAK_BF16, 4),
         "roofline": roofline,
         "kernel_ms": {k: round(v, 4) for k, v in kernel_ms.items() if v},
+        "ms_per_step_bf16_weights": round(ms_bf16w, 4),
         "budgets": per_budget,
         "corun": corun,
         "cpu_baseline": cpu,
@@ -195,7 +206,8 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
     ts_shape, ts_layers, bt = W.TALKER, 16, 32
     seeds = W.SEEDS["talker"]
     kv_lens = W.talker_kv_lens(bt, seeds["cache"])
-    tl = upload_weights(W.make_weights(ts_shape, ts_layers, seeds["weights"]), dev)
+    from paper_2608_01785_amd.device_data import prepare_f16
+    tl = prepare_f16(ctx, upload_weights(W.make_weights(ts_shape, ts_layers, seeds["weights"]), dev))
     max_ctx = int(np.ceil((kv_lens.max() + 1) / 64) * 64)
     cache = DeviceCache(ts_layers, bt, max_ctx, ts_shape.n_kv_heads, ts_shape.head_dim, dev)
     gen = torch.Generator(device=dev)
@@ -228,6 +240,30 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
     ev = decode(20)
     torch.cuda.synchronize()
     solo_ms = e0.elapsed_time(ev[-1]) / 20
+
+    # Per-kernel averages of the solo decode step (events on the decode stream).
+    binding.hs_timing_enable(ctx, True)
+    decode(10)
+    torch.cuda.synchronize()
+    dk = {k: binding.hs_timing_read(ctx, k) for k in binding.KERNEL_KINDS}
+    binding.hs_timing_enable(ctx, False)
+    dec_kernel_ms = {k: v[0] / v[1] for k, v in dk.items() if v[1]}
+    # Dominant decode kernel: single-row attention, which reads every cached key/value row once.
+    kv_bytes = 2 * ts_shape.n_kv_heads * ts_shape.head_dim * 2 * int(np.sum(kv_lens + 1))
+    da_ms = dec_kernel_ms["decode_attn"]
+    da_gbs = kv_bytes / (da_ms / 1e3) / 1e9
+    w_bytes = {"qkv": ts_shape.qkv_rows * ts_shape.hidden * 2, "o_proj": ts_shape.hidden * ts_shape.n_q_heads * ts_shape.head_dim * 2,
+               "gate_up": 2 * ts_shape.ffn * ts_shape.hidden * 2, "down": ts_shape.hidden * ts_shape.ffn * 2}
+    decode_roofline = {
+        "bound": "hbm", "kernel": "decode_attn", "cus": 128,
+        "achieved": round(da_gbs, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+        "frac": round(da_gbs / (PEAK_HBM / 1e9), 4),
+        "frac_cu_scaled": round(da_gbs / (PEAK_HBM / 1e9 * 128 / N_CUS), 4),
+        "bytes_per_launch": kv_bytes, "avg_launch_ms": round(da_ms, 4),
+        "gemm_weight_gbs": {k: round(w_bytes[k] / (dec_kernel_ms[k] / 1e3) / 1e9, 1) for k in w_bytes
+                            if k in dec_kernel_ms},
+    }
+    log("[bench] decode kernels: " + ", ".join(f"{k} {v * 1e3:.1f} us" for k, v in dec_kernel_ms.items()))
 
     # Solo prefill on its 128 CUs.
     p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -275,6 +311,8 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
         "decode_solo_tok_s": round(32 / (solo_ms / 1e3)),
         "decode_solo_hbm_frac_cu_scaled": round(step_bytes / (solo_ms / 1e3) / (PEAK_HBM * 128 / N_CUS), 4),
         "decode_bytes_per_step": int(step_bytes),
+        "decode_kernel_ms": {k: round(v, 4) for k, v in dec_kernel_ms.items()},
+        "decode_roofline": decode_roofline,
         "talker": "16 layers, hidden 1024, 16/16 heads, dh 64, ffn 4096, batch 32, kv_len U[128,1024] (sum 17437)",
     }
     log(f"[bench] co-run: prefill {window:.2f} ms (solo {prefill_solo:.2f}), decode {dec_ms:.3f} ms/step "
@@ -282,11 +320,12 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
     return res
 
 
-def cpu_baseline(W, layers, batch, shape, rows_per_seq):
+def cpu_baseline(W, layers, batch, shape, rows_per_seq, target_s=15.0):
     """The float64 reference on the host: first rows of every request through all layers.
 
     By causality the first r rows of a request depend only on themselves, so the
-    sample is a faithful slice of the same workload.
+    sample is a faithful slice of the same workload.  With rows_per_seq = 0 the
+    sample size is chosen from a short calibration run to take about target_s.
     """
     from oracle import layer as ref
     try:
@@ -294,16 +333,24 @@ def cpu_baseline(W, layers, batch, shape, rows_per_seq):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count()])
     except Exception:
         cores = os.cpu_count()
-    r = rows_per_seq
-    xs = np.concatenate([batch.x[o:o + r] for o in batch.seq_offsets[:-1]])
-    off = np.arange(batch.n_seqs + 1) * r
     w64 = [{k: W.bf16_to_f32(v).astype(np.float64) for k, v in lw.items()} for lw in layers]
-    x64 = W.bf16_to_f32(xs).astype(np.float64)
-    t0 = time.time()
-    ref.stack_forward(x64, w64, shape, off)
-    dt = time.time() - t0
-    rows = int(off[-1])
-    log(f"[bench] CPU reference: {rows} rows x {len(layers)} layers in {dt:.1f}s")
+
+    def sample(r, n_layers):
+        xs = np.concatenate([batch.x[o:o + r] for o in batch.seq_offsets[:-1]])
+        off = np.arange(batch.n_seqs + 1) * r
+        x64 = W.bf16_to_f32(xs).astype(np.float64)
+        t0 = time.time()
+        ref.stack_forward(x64, w64[:n_layers], shape, off)
+        return time.time() - t0, int(off[-1])
+
+    r = rows_per_seq
+    if r <= 0:
+        t_cal, rows_cal = sample(32, 1)
+        per_row_layer = t_cal / rows_cal
+        r = int(target_s / (per_row_layer * batch.n_seqs * len(layers)))
+        r = max(32, min(r, int(batch.lengths.min())))
+    dt, rows = sample(r, len(layers))
+    log(f"[bench] CPU reference: {rows} rows x {len(layers)} layers in {dt:.1f}s ({cores} threads)")
     return {"value": round(rows / dt, 2), "unit": "tok/s", "cores": int(cores), "kind": "oracle",
             "sample": f"first {r} rows of each of the {batch.n_seqs} requests through all {len(layers)} layers "
                       f"({rows} rows), float64 NumPy", "seconds": round(dt, 2)}
