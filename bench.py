@@ -23,9 +23,28 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-PEAK_BF16 = 2.5e15       # MI355X dense bf16 MFMA, FLOP/s, 256 CUs
+PEAK_BF16 = 2.5e15       # MI355X dense bf16/fp16 MFMA, FLOP/s, 256 CUs
 PEAK_HBM = 8.0e12        # bytes/s
 N_CUS = 256
+
+
+# HBM-side bytes per gate/up launch at 256 CUs from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE passes (KiB per dispatch), each scaled by what the counter reads for a
+# 1 GiB device copy (fetch x 2.000, write x 1.000).  Valid only for the GEMM
+# source these counters were taken on.
+MEASURED_TRAFFIC = {
+    "26a9c9bc6543aa7d": {"fetch_kib": 2248883.3, "fetch_scale": 2.0, "write_kib": 494602.9, "write_scale": 1.0},
+}
+
+
+def gemm_traffic_bytes():
+    import hashlib
+    with open(os.path.join(ROOT, "paper_2608_01785_amd", "csrc", "gemm.hip"), "rb") as f:
+        key = hashlib.sha256(f.read()).hexdigest()[:16]
+    m = MEASURED_TRAFFIC.get(key)
+    if m is None:
+        return None
+    return int(1024 * (m["fetch_kib"] * m["fetch_scale"] + m["write_kib"] * m["write_scale"]))
 
 
 def log(msg):
@@ -127,10 +146,11 @@ def main():
     # Dominant kernel: the gate/up projection (SwiGLU epilogue), ~58 % of the FLOPs.
     gu_flops = 2.0 * T * shape.hidden * 2 * shape.ffn
     gu_ms = kernel_ms["gate_up"]
+    gu_bytes = 2 * (T * shape.hidden + 2 * shape.ffn * shape.hidden + T * shape.ffn)  # A, W, a (fp16)
     achieved = gu_flops / (gu_ms / 1e3) / 1e12
     roofline = {"bound": "mfma", "kernel": "gate_up_swiglu_gemm", "achieved": round(achieved, 1),
                 "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s", "frac": round(achieved / (PEAK_BF16 / 1e12), 4),
-                "traffic": None, "avg_launch_ms": round(gu_ms, 4)}
+                "traffic": gemm_traffic_bytes(), "algorithmic_bytes": gu_bytes, "avg_launch_ms": round(gu_ms, 4)}
 
     run(256, 1, wbf16)
     ms_bf16w = run(256, max(2, args.steps // 2), wbf16)
