@@ -76,9 +76,10 @@ enum { HS_WEIGHTS_BF16 = 0, HS_WEIGHTS_F16 = 1 };
  *   w_o        [hidden, Hq * dh]
  *   w_gate_up  [2 * ffn, hidden]                      rows: gate | up
  *   w_down     [hidden, ffn]
- * format: HS_WEIGHTS_BF16 (the matrices are bf16 and each GEMM converts its
- * tiles on the fly) or HS_WEIGHTS_F16 (the matrices were converted once with
- * hs_convert_weights_f16; same values, no per-call conversion). */
+ * format: HS_WEIGHTS_BF16 (the matrices are bf16 row-major as above and each
+ * GEMM converts its tiles on the fly) or HS_WEIGHTS_F16 (the matrices were
+ * prepared once with hs_convert_weights_f16: same values as fp16 in
+ * panel-major order, no per-call conversion; the fastest format). */
 typedef struct hs_layer_weights {
   const void* ln1;
   const void* w_qkv;
@@ -220,13 +221,16 @@ hs_status hs_downstream_decode_step(hs_context* ctx, const hs_layer_cfg* cfg,
  * constant-rate clock at its start.  Used to check that masks hold. */
 hs_status hs_probe_hw_ids(hs_context* ctx, void* stream, int32_t n_groups, void* out_ids);
 
-/* One-time weight preparation: dst[i] = fp16(src[i]) for n bf16 values
- * (device pointers, 4-byte aligned, n even, no overlap), enqueued on stream
- * (NULL = the context's full-budget stream).  Exact for magnitudes in
- * [2^-14, 65504]; smaller magnitudes round toward zero to fp16 subnormals
- * (error below 2^-24) and larger ones saturate at 65504.  For the four
- * projection matrices of hs_layer_weights with format HS_WEIGHTS_F16. */
-hs_status hs_convert_weights_f16(hs_context* ctx, const void* src_bf16, void* dst_f16, int64_t n,
+/* One-time weight preparation for format HS_WEIGHTS_F16: src is a bf16
+ * [rows, cols] row-major matrix, dst receives the same values as fp16 in
+ * panel-major order [cols / 32][rows][32] (element (r, c) at
+ * ((c / 32) * rows + r) * 32 + c % 32).  That order makes every 32-wide K
+ * slice of a weight tile one contiguous run for the GEMMs' copy engine.
+ * Device pointers, 4-byte aligned, non-overlapping; cols a positive multiple
+ * of 32.  Enqueued on stream (NULL = the context's full-budget stream).
+ * Exact for magnitudes in [2^-14, 65504]; smaller magnitudes round toward
+ * zero to fp16 subnormals (error below 2^-24), larger ones saturate. */
+hs_status hs_convert_weights_f16(hs_context* ctx, const void* src_bf16, void* dst_f16, int64_t rows, int64_t cols,
                                  void* stream);
 
 /* Per-kernel timing with HIP events on the launch stream.  While enabled,

@@ -96,7 +96,7 @@ def lib() -> ctypes.CDLL:
             "hs_probe_hw_ids": [vp, vp, i32, vp],
             "hs_timing_enable": [vp, i32],
             "hs_timing_read": [vp, i32, ctypes.POINTER(ctypes.c_double), i32p],
-            "hs_convert_weights_f16": [vp, vp, vp, ctypes.c_int64, vp],
+            "hs_convert_weights_f16": [vp, vp, vp, ctypes.c_int64, ctypes.c_int64, vp],
         }
         for name, args in sigs.items():
             fn = getattr(L, name)
@@ -294,7 +294,9 @@ def hs_timing_read(ctx: Context, kind) -> Tuple[float, int]:
     return float(ms.value), int(n.value)
 
 
-def hs_convert_weights_f16(ctx: Context, src, dst, n: Optional[int] = None, stream=None) -> None:
-    if n is None:
-        n = src.numel()
-    _check(lib().hs_convert_weights_f16(ctx.handle, _ptr(src), _ptr(dst), int(n), _ptr(stream)))
+def hs_convert_weights_f16(ctx: Context, src, dst, rows: Optional[int] = None, cols: Optional[int] = None,
+                           stream=None) -> None:
+    """bf16 [rows, cols] -> fp16 panel-major [cols / 32][rows][32] (shape taken from src if not given)."""
+    if rows is None or cols is None:
+        rows, cols = int(src.shape[0]), int(src.shape[1])
+    _check(lib().hs_convert_weights_f16(ctx.handle, _ptr(src), _ptr(dst), int(rows), int(cols), _ptr(stream)))

@@ -1,10 +1,11 @@
 // Persistent fp16 MFMA GEMM for gfx950 with fused epilogues.
 //
-// Computes C[M, N] = A[M, K] * W[N, K]^T (fp16 activations times bf16 [out, in]
-// weights, fp32 accumulation).  Weight fragments are converted bf16 -> fp16
-// after they leave LDS (exact for the weight range), so both MFMA operands are
-// fp16: the same MFMA rate as bf16 on gfx950 with 8x finer rounding of the
-// activations.
+// Computes C[M, N] = A[M, K] * W[N, K]^T (fp16 activations times [out, in]
+// weights, fp32 accumulation).  Weights are either bf16 row-major, converted
+// to fp16 after they leave LDS (exact for the weight range), or prepared fp16
+// in panel-major order [K / 32][N][32], which makes every stage of a tile one
+// contiguous run.  Both MFMA operands are fp16: the same MFMA rate as bf16 on
+// gfx950 with 8x finer rounding of the activations.
 //
 // The MFMA is issued as C^T = W * A^T: the weight tile is the MFMA A operand
 // and the activation tile the B operand, so every lane of the 32x32
@@ -15,10 +16,12 @@
 //
 // Block tile 256 (weight rows) x 256 (activation rows), 4 waves in a 2 x 2
 // grid, each wave 128 x 128 = 4 x 4 MFMA tiles of 32x32x16.  K advances in
-// slabs of 32 through a ring of 5 LDS stages (160 KB): both operands are
+// slabs of 32 through a ring of 4 LDS stages (128 KB): both operands are
 // copied buffer -> LDS by the load unit itself (no staging registers), so
-// four slabs (128 KB per CU) are in flight while the fifth feeds the MFMAs.
-// That depth is what hides the latency of operands that miss the XCD's L2.
+// three slabs are in flight while the fourth feeds the MFMAs.  A five-stage
+// ring measured about 5 % slower on the large shapes and a three-stage one
+// the same as four (plausibly because 32 CUs x 5 x 32 KB in flight exceeds
+// the XCD's 4 MB L2, which neighbouring blocks share).
 // The grid is persistent (one block per CU of the budget); blocks walk the
 // tile space in grouped order, remapped so each XCD takes a contiguous range.
 #include "hs_device.h"
@@ -30,12 +33,12 @@ namespace {
 constexpr int BM = 256;   // activation rows per tile
 constexpr int BN = 256;   // weight rows per tile
 constexpr int BK = 32;    // K per LDS stage
-constexpr int kStages = 5;
+constexpr int kStages = 4;
 constexpr int kThreads = 256;
 constexpr int kRowBytes = BK * 2;            // 64 bytes = 4 chunks of 16
 constexpr int kTileBytes = 256 * kRowBytes;  // 16 KB
 constexpr int kStageBytes = 2 * kTileBytes;  // weight tile + activation tile
-constexpr int kGroupM = 8;
+constexpr int kGroupM = 4;
 
 // Row of W that lands in tile row r (0..255) of output tile tile_n.
 template <int EPI>
@@ -119,20 +122,25 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
   };
 
   uint32_t w_off[4], a_off[4];
+  // fp16 weights are panel-major ([K / 32][N][32]): one stage of a weight row
+  // is 64 contiguous bytes and a tile's stage one contiguous 16 KB run.
+  const uint32_t w_row_stride = W_F16 ? uint32_t(kRowBytes) : row_bytes;
+  const uint32_t w_stage_stride = W_F16 ? w_rows * kRowBytes : uint32_t(kRowBytes);
   auto set_tile = [&](int tile_m, int tile_n) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = wave * 64 + 16 * j + ld_sub;
-      w_off[j] = weight_row<EPI>(tile_n, r, a.ffn) * row_bytes + ld_chunk * 16;
+      w_off[j] = weight_row<EPI>(tile_n, r, a.ffn) * w_row_stride + ld_chunk * 16;
       a_off[j] = uint32_t(tile_m * BM + r) * row_bytes + ld_chunk * 16;  // rows >= M read zero
     }
   };
   auto issue_stage = [&](int kt, int buf) {
     const int koff = kt * BK * 2;
+    const uint32_t wkoff = uint32_t(kt) * w_stage_stride;
     uint8_t* wbase = smem + buf * kStageBytes + wave * 64 * kRowBytes;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lds_ptr_t)(wbase + j * 16 * kRowBytes), 16, w_off[j], koff,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lds_ptr_t)(wbase + j * 16 * kRowBytes), 16, w_off[j], wkoff,
                                                0, 0);
 #pragma unroll
     for (int j = 0; j < 4; ++j)

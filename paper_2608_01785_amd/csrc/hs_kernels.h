@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "skinny_policy.h"
+
 namespace hs {
 
 enum Epilogue : int {
@@ -34,12 +36,17 @@ struct GemmArgs {
   int64_t v_stride;
   const float2* rope;     // [max_pos, dh / 2] (cos, sin)
   int hq, hkv, dh;
+  // Skinny GEMM split along K: fp32 partial sums and one arrival counter per
+  // weight strip (zero on entry, left at zero on exit).
+  float* part;
+  int32_t* counters;
+  int n_split, k_per_split;  // set by the launcher
 };
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, int max_blocks, hipStream_t s);
 
-// Decode-sized GEMMs (M <= kSkinnyMaxRows): thin weight strips, one block each.
-constexpr int kSkinnyMaxRows = 128;
+// Decode-sized GEMMs (M <= kSkinnyMaxRows): thin weight strips, K split
+// across blocks as skinny_split() says.
 bool skinny_supported(int epi, const GemmArgs& a);
 hipError_t launch_gemm_skinny(int epi, const GemmArgs& a, hipStream_t s);
 
@@ -89,6 +96,6 @@ hipError_t launch_rope_table(float2* tab, int max_pos, int dh, float base, hipSt
 hipError_t launch_probe(uint32_t* out, int n_groups, hipStream_t s);
 
 // dst = fp16(src) for n bf16 values (n even).
-hipError_t launch_convert_bf16_f16(const uint16_t* src, uint16_t* dst, int64_t n, hipStream_t s);
+hipError_t launch_convert_bf16_f16(const uint16_t* src, uint16_t* dst, int64_t rows, int64_t cols, hipStream_t s);
 
 }  // namespace hs

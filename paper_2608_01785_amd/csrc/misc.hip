@@ -103,20 +103,26 @@ __global__ void probe_kernel(uint32_t* out, int n) {
 }
 
 // Weight preparation: pairs of bf16 values -> pairs of fp16 values.
-__global__ void convert_kernel(const uint32_t* __restrict__ src, uint32_t* __restrict__ dst, int64_t n2) {
-  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n2; i += int64_t(gridDim.x) * blockDim.x)
-    dst[i] = bf2x_to_h2x(src[i]);
+// bf16 [rows, cols] row-major -> fp16 panel-major [cols / 32][rows][32], two
+// elements per thread.
+__global__ void convert_kernel(const uint32_t* __restrict__ src, uint32_t* __restrict__ dst, int64_t rows,
+                               int64_t cols) {
+  const int64_t n2 = rows * cols / 2, half_cols = cols / 2;
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n2; i += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t r = i / half_cols, c = 2 * (i % half_cols);
+    dst[(((c >> 5) * rows + r) * 32 + (c & 31)) >> 1] = bf2x_to_h2x(src[i]);
+  }
 }
 
 }  // namespace
 
-hipError_t launch_convert_bf16_f16(const uint16_t* src, uint16_t* dst, int64_t n, hipStream_t s) {
-  const int64_t n2 = n / 2;
+hipError_t launch_convert_bf16_f16(const uint16_t* src, uint16_t* dst, int64_t rows, int64_t cols, hipStream_t s) {
+  const int64_t n2 = rows * cols / 2;
   if (n2 <= 0) return hipSuccess;
   int64_t grid = (n2 + 255) / 256;
   if (grid > 8192) grid = 8192;
   hipLaunchKernelGGL(convert_kernel, dim3(unsigned(grid)), dim3(256), 0, s, reinterpret_cast<const uint32_t*>(src),
-                     reinterpret_cast<uint32_t*>(dst), n2);
+                     reinterpret_cast<uint32_t*>(dst), rows, cols);
   return hipGetLastError();
 }
 

@@ -1,6 +1,7 @@
 // Host-only planner: status strings, thread-local errors, CU partition,
 // batch metadata, attention work lists and the workspace layout.
 #include "plan.h"
+#include "skinny_policy.h"
 
 #include <stdarg.h>
 #include <stdio.h>
@@ -84,7 +85,38 @@ hs_status validate_batch(const int32_t* off, const int32_t* ctx, int32_t B, int3
 
 int64_t max_att_items(int32_t T, int32_t B) { return int64_t(T) / kAttnBlockQ + B + 1; }
 
-static size_t meta_bytes(int32_t T, int32_t B, int64_t att) {
+// Split-K scratch of the skinny GEMM over the four projections of a layer:
+// the largest partial-sum buffer and the most weight strips of any of them.
+struct SkinnyNeeds {
+  size_t part_bytes = 0;
+  int32_t counters = 0;
+};
+
+static SkinnyNeeds skinny_needs(const hs_layer_cfg& c, int32_t T) {
+  SkinnyNeeds n;
+  if (T > kSkinnyMaxRows) return n;
+  const int mt = skinny_m_tiles(T);
+  struct G {
+    int strips, ns, k;
+    bool used;
+  };
+  const G gs[4] = {
+      {skinny_strips_qkv(c.n_q_heads, c.n_kv_heads), 2, c.hidden, c.head_dim == 64},
+      {skinny_strips_resid(c.hidden), 1, c.n_q_heads * c.head_dim, true},
+      {skinny_strips_swiglu(c.ffn), 2, c.hidden, true},
+      {skinny_strips_resid(c.hidden), 1, c.ffn, true},
+  };
+  for (const G& g : gs) {
+    if (!g.used) continue;
+    const SkinnySplit sp = skinny_split(g.strips, g.k / kSkinnyBK);
+    n.counters = std::max(n.counters, int32_t(g.strips));
+    if (sp.splits > 1)
+      n.part_bytes = std::max(n.part_bytes, size_t(g.strips) * sp.splits * skinny_partial_bytes(g.ns, mt));
+  }
+  return n;
+}
+
+static size_t meta_bytes(int32_t T, int32_t B, int64_t att, int32_t counters) {
   size_t s = 0;
   s += align_up(size_t(T) * 4, 16);       // pos
   s += align_up(size_t(T) * 8, 16) * 2;   // k_off, v_off
@@ -92,6 +124,7 @@ static size_t meta_bytes(int32_t T, int32_t B, int64_t att) {
   s += align_up(size_t(B) * 8, 16) * 2;   // seq_kbase, seq_vbase
   s += align_up(size_t(att) * 8, 16);     // att items
   s += align_up(size_t(B) * 16, 16);      // single-row (decode) rows
+  s += align_up(size_t(counters) * 4, 16); // split-K counters
   return align_up(s, kAlign);
 }
 
@@ -104,7 +137,8 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
     p = align_up(p + bytes, kAlign);
     return at;
   };
-  w.meta_bytes = meta_bytes(T, B, max_att_items(T, B));
+  const SkinnyNeeds sk = skinny_needs(c, T);
+  w.meta_bytes = meta_bytes(T, B, max_att_items(T, B), sk.counters);
   w.meta = take(w.meta_bytes);
   w.n = take(size_t(T) * d * 2);
   w.q = take(size_t(T) * hq * dh * 2);
@@ -116,6 +150,8 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
   w.a = take(size_t(T) * f * 2);
   w.xtmp = take(size_t(T) * d * 4);
   w.rope = take(size_t(max_pos) * (dh / 2) * 8);
+  w.part_bytes = sk.part_bytes;
+  w.part = take(sk.part_bytes);
   w.total = p;
   return w;
 }
@@ -168,6 +204,8 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   P.seq_vbase = take(size_t(B) * 8);
   P.att_items = take(size_t(P.n_att_items) * 8);
   P.dec_rows = take(size_t(P.n_dec_rows) * 16);
+  P.n_counters = skinny_needs(c, int32_t(T)).counters;
+  P.counters = take(size_t(P.n_counters) * 4);
   P.image.assign(align_up(p, kAlign), 0);
 
   auto i32 = [&](size_t at) { return reinterpret_cast<int32_t*>(P.image.data() + at); };

@@ -43,6 +43,8 @@ struct WsLayout {
   size_t a;           // [T, ffn]
   size_t xtmp;        // [T, d] fp32 residual between layers
   size_t rope;        // [max_pos, dh / 2] float2
+  size_t part;        // split-K partial sums of the skinny GEMM (T <= 128 rows only)
+  size_t part_bytes;
   size_t total;
 };
 
@@ -59,7 +61,8 @@ struct Plan {
   size_t pos = 0, k_off = 0, v_off = 0;
   size_t seq_start = 0, seq_len = 0, seq_ctx = 0, seq_kbase = 0, seq_vbase = 0;
   size_t att_items = 0, dec_rows = 0;
-  int32_t n_att_items = 0, n_dec_rows = 0;
+  size_t counters = 0;  // split-K arrival counters of the skinny GEMM, zero in the image
+  int32_t n_att_items = 0, n_dec_rows = 0, n_counters = 0;
   int64_t v_stride = 0;
 };
 

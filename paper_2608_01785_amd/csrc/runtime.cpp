@@ -236,6 +236,8 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
   float* h_buf = at<float>(ws, lay.h);
   uint16_t* a_buf = at<uint16_t>(ws, lay.a);
   float* xtmp = at<float>(ws, lay.xtmp);
+  float* sk_part = lay.part_bytes ? at<float>(ws, lay.part) : nullptr;
+  int32_t* sk_count = plan.n_counters ? reinterpret_cast<int32_t*>(meta + plan.counters) : nullptr;
 
   TIMED(HS_KERNEL_ROPE_TABLE, hs::launch_rope_table(rope, max_pos, dh, cfg->rope_base, s));
 
@@ -255,6 +257,8 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(x_cur, x_cur_f32, static_cast<const uint16_t*>(w[l].ln1), n_buf,
                                                 T, d, cfg->rms_eps, 4 * budget, s));
     hs::GemmArgs g{};
+    g.part = sk_part;
+    g.counters = sk_count;
     g.A = n_buf;
     g.W = static_cast<const uint16_t*>(w[l].w_qkv);
     g.w_f16 = w[l].format == HS_WEIGHTS_F16;
@@ -311,6 +315,8 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     if (plan.n_dec_rows > 0) TIMED(HS_KERNEL_DECODE_ATTN, hs::launch_decode_attention(da, s));
 
     hs::GemmArgs go{};
+    go.part = sk_part;
+    go.counters = sk_count;
     go.A = o_buf;
     go.W = static_cast<const uint16_t*>(w[l].w_o);
     go.w_f16 = w[l].format == HS_WEIGHTS_F16;
@@ -327,6 +333,8 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
                                                 d, cfg->rms_eps, 4 * budget, s));
 
     hs::GemmArgs gu{};
+    gu.part = sk_part;
+    gu.counters = sk_count;
     gu.A = n_buf;
     gu.W = static_cast<const uint16_t*>(w[l].w_gate_up);
     gu.w_f16 = w[l].format == HS_WEIGHTS_F16;
@@ -339,6 +347,8 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     TIMED(HS_KERNEL_GATE_UP, gemm(hs::EPI_SWIGLU, gu, grid_cap, s));
 
     hs::GemmArgs gd{};
+    gd.part = sk_part;
+    gd.counters = sk_count;
     gd.A = a_buf;
     gd.W = static_cast<const uint16_t*>(w[l].w_down);
     gd.w_f16 = w[l].format == HS_WEIGHTS_F16;
@@ -483,19 +493,22 @@ hs_status hs_downstream_decode_step(hs_context* ctx, const hs_layer_cfg* cfg, co
                    HS_ROLE_DOWN, stream, workspace, ws_bytes);
 }
 
-hs_status hs_convert_weights_f16(hs_context* ctx, const void* src, void* dst, int64_t n, void* stream) {
+hs_status hs_convert_weights_f16(hs_context* ctx, const void* src, void* dst, int64_t rows, int64_t cols,
+                                 void* stream) {
   hs::clear_error();
   if (!ctx || !src || !dst) return hs::fail(HS_ERR_INVALID_ARG, "null argument");
-  if (n < 0 || n % 2 != 0) return hs::fail(HS_ERR_INVALID_ARG, "element count %lld must be even and >= 0", (long long)n);
+  if (rows < 1 || cols < 32 || cols % 32 != 0)
+    return hs::fail(HS_ERR_INVALID_ARG, "shape [%lld, %lld]: need rows >= 1 and cols a positive multiple of 32",
+                    (long long)rows, (long long)cols);
   if ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) % 4 != 0)
     return hs::fail(HS_ERR_INVALID_ARG, "pointers must be 4-byte aligned");
   const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
-  const uintptr_t bytes = uintptr_t(n) * 2;
+  const uintptr_t bytes = uintptr_t(rows) * uintptr_t(cols) * 2;
   if (s0 < d0 + bytes && d0 < s0 + bytes) return hs::fail(HS_ERR_INVALID_ARG, "source and destination overlap");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if (!s) s = find_level(ctx, ctx->n_cus)->s_shared;
   HIP_TRY(hipSetDevice(ctx->device));
-  HIP_TRY(hs::launch_convert_bf16_f16(static_cast<const uint16_t*>(src), static_cast<uint16_t*>(dst), n, s));
+  HIP_TRY(hs::launch_convert_bf16_f16(static_cast<const uint16_t*>(src), static_cast<uint16_t*>(dst), rows, cols, s));
   return HS_OK;
 }
 

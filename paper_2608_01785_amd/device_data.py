@@ -40,14 +40,18 @@ def upload_weights(layers: List[Dict[str, np.ndarray]], device="cuda") -> List[D
 
 
 def prepare_f16(ctx, layers_dev: List[Dict[str, torch.Tensor]]) -> List[Dict[str, object]]:
-    """fp16 copies of the projection matrices (through the library's converter); gains stay bf16."""
+    """fp16 panel-major copies of the projection matrices (the library's converter); gains stay bf16.
+
+    Each copy is a flat buffer holding [K / 32][N][32] for an [N, K] matrix.
+    """
     from paper_2608_01785_amd import binding
     out = []
     for lw in layers_dev:
         d = {"ln1": lw["ln1"], "ln2": lw["ln2"], "format": binding.HS_WEIGHTS_F16}
         for name in binding.MATRICES:
-            dst = torch.empty(lw[name].shape, dtype=torch.float16, device=lw[name].device)
-            binding.hs_convert_weights_f16(ctx, lw[name], dst)
+            n, k = lw[name].shape
+            dst = torch.empty((k // 32, n, 32), dtype=torch.float16, device=lw[name].device)
+            binding.hs_convert_weights_f16(ctx, lw[name], dst, n, k)
             d[name] = dst
         out.append(d)
     torch.cuda.synchronize()

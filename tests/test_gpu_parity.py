@@ -97,6 +97,29 @@ def test_ragged_prefill_parity(env, shape_name, lengths, n_layers, fmt):
     assert e <= TOL
 
 
+def test_weight_preparation_layout(env):
+    """hs_convert_weights_f16: fp16 of every value, in panel-major order [K / 32][N][32]."""
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    from paper_2608_01785_amd.device_data import f16_bits_of, to_device
+    rng = np.random.default_rng(51)
+    n, k = 96, 160
+    w = W.bf16_bits(rng.standard_normal((n, k), dtype=np.float32) * np.float32(0.02))
+    w[0, :4] = W.bf16_bits(np.array([1e-6, -3e-5, 7.0, -59904.0], np.float32))  # subnormals, large normals
+    src = to_device(w)
+    dst = torch.empty((k // 32, n, 32), dtype=torch.float16, device="cuda")
+    binding.hs_convert_weights_f16(ctx, src, dst)
+    torch.cuda.synchronize()
+    got = f16_bits_of(dst).view(np.float16).astype(np.float64)
+    vals = W.bf16_to_f32(w).astype(np.float64)
+    expect = vals.reshape(n, k // 32, 32).transpose(1, 0, 2)
+    normal = np.abs(expect) >= 2.0 ** -14
+    np.testing.assert_array_equal(got[normal], expect[normal])              # exact in the normal range
+    assert np.all(np.abs(got[~normal] - expect[~normal]) < 2.0 ** -24)     # subnormals: toward zero
+    with pytest.raises(binding.HorizonError):
+        binding.hs_convert_weights_f16(ctx, src, dst, n, 100)              # cols not a multiple of 32
+
+
 def test_residual_identity_bit_exact(env):
     from paper_2608_01785_amd.device_data import upload_weights
     shape = W.TINY
@@ -196,6 +219,12 @@ def test_talker_decode_step_parity(env, batch, fmt):
     e = err_ratio(y.cpu().numpy(), expect)
     log(f"  max err / rms = {e:.3e}")
     assert e <= TOL
+    # Split-K partial sums are added in a fixed order: a repeat (same cache
+    # positions rewritten with the same rows) at another budget is bit-identical.
+    y2 = torch.empty_like(y)
+    binding.hs_downstream_decode_step(ctx, shape, wdev, xd, y2, cache.as_arg(), kv_lens, 64, None, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
     for l in range(n_layers):
         for b in range(batch):
             kb, vb = cache.rows(l, b, int(kv_lens[b]), int(kv_lens[b]) + 1)
