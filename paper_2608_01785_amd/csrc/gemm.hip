@@ -24,6 +24,8 @@
 // the XCD's 4 MB L2, which neighbouring blocks share).
 // The grid is persistent (one block per CU of the budget); blocks walk the
 // tile space in grouped order, remapped so each XCD takes a contiguous range.
+#include <type_traits>
+
 #include "hs_device.h"
 #include "hs_kernels.h"
 
@@ -126,12 +128,17 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
   // is 64 contiguous bytes and a tile's stage one contiguous 16 KB run.
   const uint32_t w_row_stride = W_F16 ? uint32_t(kRowBytes) : row_bytes;
   const uint32_t w_stage_stride = W_F16 ? w_rows * kRowBytes : uint32_t(kRowBytes);
-  auto set_tile = [&](int tile_m, int tile_n) {
+  // A half unit (hm = 0 or 1) covers activation rows hm * 128 .. + 127 of its
+  // tile: LDS activation rows 0..127 hold them (copied by waves 0 and 1);
+  // waves 2 and 3 copy the same rows again into the unused rows 128..255, so
+  // every stage still has exactly 8 copies per wave for the vmcnt accounting.
+  auto set_tile = [&](int tile_m, int tile_n, int hm) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = wave * 64 + 16 * j + ld_sub;
+      const int ar = hm < 0 ? r : hm * 128 + (r & 127);
       w_off[j] = weight_row<EPI>(tile_n, r, a.ffn) * w_row_stride + ld_chunk * 16;
-      a_off[j] = uint32_t(tile_m * BM + r) * row_bytes + ld_chunk * 16;  // rows >= M read zero
+      a_off[j] = uint32_t(tile_m * BM + ar) * row_bytes + ld_chunk * 16;  // rows >= M read zero
     }
   };
   auto issue_stage = [&](int kt, int buf) {
@@ -148,34 +155,55 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
                                                a_off[j], koff, 0, 0);
   };
 
-  // Fragments of one stage: [kk][i] weight, [kk][j] activation.
-  typedef u32x4 Frags[2][4];
-  auto read_frags = [&](int buf, Frags& fw, Frags& fa) {
+  // Fragments of one half stage (16-wide K step kk): [i] weight, [j] activation.
+  // JT = activation subtiles per wave: 4 (full tile, rows wm * 128 ..) or 2
+  // (half unit, rows wm * 64 ..).
+  struct Half {
+    u32x4 w[4], a[4];
+  };
+  auto read_half = [&](auto jt, int buf, int kk, Half& h) {
+    constexpr int JT = decltype(jt)::value;
     const uint8_t* base = smem + buf * kStageBytes;
+    const int phys = (kk * 2 + fh) ^ swz(fr);
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int phys = (kk * 2 + fh) ^ swz(fr);
+    for (int i = 0; i < 4; ++i)
+      h.w[i] = *reinterpret_cast<const u32x4*>(base + (wn * 128 + i * 32 + fr) * kRowBytes + phys * 16);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        fw[kk][i] = *reinterpret_cast<const u32x4*>(base + (wn * 128 + i * 32 + fr) * kRowBytes + phys * 16);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        fa[kk][j] =
-            *reinterpret_cast<const u32x4*>(base + kTileBytes + (wm * 128 + j * 32 + fr) * kRowBytes + phys * 16);
-    }
+    for (int j = 0; j < JT; ++j)
+      h.a[j] = *reinterpret_cast<const u32x4*>(base + kTileBytes + (wm * JT * 32 + j * 32 + fr) * kRowBytes +
+                                               phys * 16);
   };
 
-  int L = xcd_remap(blockIdx.x, gridDim.x);
-  if (L >= n_tiles) return;
-  int tile_m, tile_n;
-  tile_coords(L, tile_m, tile_n);
-  set_tile(tile_m, tile_n);
+  // Work units: full tiles, except that when the last round would leave more
+  // than half the blocks idle its tiles are split into two 128-row halves.
+  // Each output element is accumulated in the same order either way, so the
+  // result does not depend on the grid.
+  const int G = gridDim.x;
+  const int full_units = (n_tiles / G) * G;
+  const int tail = n_tiles - full_units;
+  const bool split_tail = tail > 0 && 2 * tail <= G;
+  const int n_units = split_tail ? full_units + 2 * tail : n_tiles;
+  auto unit_coords = [&](int u, int& tile_m, int& tile_n, int& hm) {
+    int t = u;
+    hm = -1;
+    if (split_tail && u >= full_units) {
+      t = full_units + (u - full_units) / 2;
+      hm = (u - full_units) % 2;
+    }
+    tile_coords(t, tile_m, tile_n);
+  };
+
+  int L = xcd_remap(blockIdx.x, G);
+  if (L >= n_units) return;
+  int tile_m, tile_n, hm;
+  unit_coords(L, tile_m, tile_n, hm);
+  set_tile(tile_m, tile_n, hm);
 #pragma unroll
   for (int st = 0; st < kStages - 1; ++st)
     if (st < KT) issue_stage(st, st);
 
+  f32x16 acc[4][4];
   while (true) {
-    f32x16 acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -183,62 +211,86 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    auto mfma_half = [&](const Frags& fw, const Frags& fa, int kk) {
+    auto mfma_half = [&](auto jt, const Half& h) {
+      constexpr int JT = decltype(jt)::value;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const u32x4 wh = W_F16 ? fw[kk][i] : bf8_to_h8(fw[kk][i]);
+        const u32x4 wh = W_F16 ? h.w[i] : bf8_to_h8(h.w[i]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(wh, fa[kk][j], acc[i][j]);
+        for (int j = 0; j < JT; ++j) acc[i][j] = mfma32(wh, h.a[j], acc[i][j]);
       }
     };
 
-    // Stage s lives in buffer s % kStages.  Its fragments are read into
-    // registers during the second half of stage s - 1, right after the
-    // barrier that publishes stage s; the first half of stage s then needs no
-    // LDS wait, and the reads overlap 16 MFMAs.
-    wait_vm(min(kStages - 2, KT - 1));
-    barrier_nofence();
-    if (kStages - 1 < KT) issue_stage(kStages - 1, kStages - 1);
-    Frags fwA, faA, fwB, faB;
-    read_frags(0, fwA, faA);
-
-    // One half-stage step: finish stage s with fragments (fw, fa) and prefetch
-    // stage s + 1 into (nw, na).
-    auto step = [&](int s, Frags& fw, Frags& fa, Frags& nw, Frags& na) {
-      mfma_half(fw, fa, 0);
-      if (s + 1 < KT) {
-        wait_vm(min(kStages - 2, KT - 2 - s));
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of stage s are done
-        barrier_nofence();
-        if (s + kStages < KT) issue_stage(s + kStages, s % kStages);
-        read_frags((s + 1) % kStages, nw, na);
+    // Stage s lives in buffer s % kStages.  Each 16-wide half of a stage is
+    // read from LDS while the previous half multiplies, so LDS reads are
+    // spread over the MFMA stream instead of bursting after the barrier.  The
+    // barrier of stage s sits between its two halves: by then every wave has
+    // read all of stage s, so its buffer can be refilled.
+    auto k_loop = [&](auto jt) {
+      constexpr int JT = decltype(jt)::value;
+      constexpr int NM = 4 * JT;  // MFMAs per half stage
+      wait_vm(min(kStages - 2, KT - 1));
+      barrier_nofence();
+      if (kStages - 1 < KT) issue_stage(kStages - 1, kStages - 1);
+      Half h0, h1;
+      read_half(jt, 0, 0, h0);
+      for (int s = 0; s < KT; ++s) {
+        const int buf = s % kStages;
+        // Phase A: the kk = 0 MFMAs of stage s, with the kk = 1 fragment
+        // reads of the same stage slotted between them.
+        read_half(jt, buf, 1, h1);
+        mfma_half(jt, h0);
+#pragma unroll
+        for (int q = 0; q < 4 + JT; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NM - 4 - JT, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (s + 1 < KT) {
+          wait_vm(min(kStages - 2, KT - 2 - s));
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of stage s are done
+          barrier_nofence();
+          if (s + kStages < KT) issue_stage(s + kStages, buf);
+          read_half(jt, (s + 1) % kStages, 0, h0);
+        }
+        // Phase B: the kk = 1 MFMAs, with the kk = 0 fragment reads of stage
+        // s + 1 slotted between them (the copies of stage s + kStages go first).
+        mfma_half(jt, h1);
+#pragma unroll
+        for (int q = 0; q < 4 + JT; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);  // one LDS read
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);  // one MFMA
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NM - 4 - JT, 1);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      mfma_half(fw, fa, 1);
     };
-    for (int s = 0; s < KT; s += 2) {
-      step(s, fwA, faA, fwB, faB);
-      step(s + 1, fwB, faB, fwA, faA);
-    }
+    if (hm < 0)
+      k_loop(std::integral_constant<int, 4>{});
+    else
+      k_loop(std::integral_constant<int, 2>{});
 
     // All waves are done with every stage: start the next tile's copies so
     // they overlap this tile's epilogue.
-    const int L_next = L + gridDim.x;
+    const int L_next = L + G;
     __syncthreads();
-    if (L_next < n_tiles) {
-      int nm, nn;
-      tile_coords(L_next, nm, nn);
-      set_tile(nm, nn);
+    if (L_next < n_units) {
+      int nm, nn, nh;
+      unit_coords(L_next, nm, nn, nh);
+      set_tile(nm, nn, nh);
 #pragma unroll
       for (int st = 0; st < kStages - 1; ++st)
         if (st < KT) issue_stage(st, st);
     }
 
     // ---------------------------------------------------------------- epilogue
-    const int m0 = tile_m * BM + wm * 128 + fr;
+    const int nj = hm < 0 ? 4 : 2;
+    const int m0 = tile_m * BM + (hm < 0 ? wm * 128 : hm * 128 + wm * 64) + fr;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int m = m0 + j * 32;
-      if (m >= a.M) continue;
+      if (j >= nj || m >= a.M) continue;
       if constexpr (EPI == EPI_RESID) {
         // out (fp32) = resid (bf16 or fp32) + acc: the residual stream stays in fp32.
         const int n_base = tile_n * BN + wn * 128 + 4 * fh;
@@ -319,9 +371,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
         }
       }
     }
-    if (L_next >= n_tiles) break;
+    if (L_next >= n_units) break;
     L = L_next;
-    tile_coords(L, tile_m, tile_n);
+    unit_coords(L, tile_m, tile_n, hm);
   }
 }
 
