@@ -219,93 +219,95 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
 }
 
 // ----------------------------------------------------------------------------
-// Single-row (decode) attention.  One block = one row r and one key/value head
-// g; the group's G query heads are the 32 MFMA columns (G <= 8 valid), so the
-// keys and values of the head are read once for the whole group.  The four
-// waves take interleaved key tiles; their K and V fragments come straight from
-// memory into registers in MFMA layout (double-buffered, no LDS), and the four
-// partial softmax states are merged through LDS at the end.
+// Single-row (decode) attention.  One block = one key range (a "split" of
+// dec_split_keys keys) of one row r and one key/value head g; the group's G
+// query heads are the 32 MFMA columns (G <= 8 valid), so the keys and values
+// of the head are read once for the whole group.  Each of the four waves
+// takes one tile of the range; its K and V fragments come straight from
+// memory into registers in MFMA layout (no LDS), and the four partial softmax
+// states are merged through LDS.  A row with one split writes its output
+// directly; otherwise every split publishes its state and the last split of
+// (r, g) to arrive merges them in split order.
+
+constexpr int kDeviceScope = 16;  // buffer cache-policy bit sc1: device-coherent access
 
 template <int DH>
-__global__ __launch_bounds__(kThreads, DH == 64 ? 2 : 1) void decode_attn_kernel(DecodeAttnArgs a) {
+__global__ __launch_bounds__(kThreads) void decode_attn_kernel(DecodeAttnArgs a) {
   constexpr int TK = (DH == 64) ? 64 : 32;     // keys per tile
+  static_assert(TK * 4 == (DH == 64 ? 256 : 128), "a split is one tile per wave");
   constexpr int NST = TK / 32;                 // 32-key score subtiles
   constexpr int NKB = DH / 16;                 // 16-wide K steps of q.k
   constexpr int NDS = DH / 32;                 // output subtiles along dh
   constexpr int NPB = TK / 16;                 // 16-key P.V steps
-  __shared__ float red_m[4][32], red_l[4][32];
-  __shared__ float red_o[4][DH][33];
+  __shared__ float red_m[4][8], red_l[4][8];
+  __shared__ float red_o[4][DH][9];  // [wave][d][query head], G <= 8
+  __shared__ int last;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 31, fh = lane >> 5;
-  const int r = blockIdx.x / a.hkv;
+  const int item = blockIdx.x / a.hkv;
   const int g = blockIdx.x % a.hkv;
-  const int4 rw = a.rows[r];
-  const int t = rw.x, b = rw.y;
+  const DecItem it = a.items[item];
+  const int t = it.t, n_keys = it.n_keys, split = it.split, n_split = it.n_split;
   const int G = a.hq / a.hkv;
-  const int n_keys = a.seq_ctx[b] + 1;
-  const int n_tiles = (n_keys + TK - 1) / TK;
+  const int kv0 = split * 4 * TK + wave * TK;  // this wave's tile
   const int qh = min(fr, G - 1);  // query head of this lane's column (padding lanes repeat the last)
-  const int64_t kbase = a.seq_kbase[b] + int64_t(g) * DH;
-  const int64_t vbase = a.seq_vbase[b] + int64_t(g) * DH * a.v_stride;
+  const int64_t kbase = it.kbase + int64_t(g) * DH;
+  const int64_t vbase = it.vbase + int64_t(g) * DH * a.v_stride;
   const int kstride = a.hkv * DH;
 
-  u32x4 qf[NKB];
-  {
-    const uint16_t* qp = a.q + (int64_t(t) * a.hq + g * G + qh) * DH + fh * 8;
-#pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) qf[kb] = *reinterpret_cast<const u32x4*>(qp + kb * 16);
-  }
-
-  // Fragments of one tile: K rows (A operand of S^T = K Q^T, rows permuted by
-  // perm32) and V^T rows (A operand of O^T = V^T P^T).
-  struct Tile {
-    u32x4 k[NST][NKB];
-    u32x4 v[NDS][NPB];
-  };
-  auto load = [&](int tt, Tile& f) {
-    const int kv0 = tt * TK;
-#pragma unroll
-    for (int st = 0; st < NST; ++st) {
-      const int key = kv0 + 32 * st + perm32(fr);
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb)
-        f.k[st][kb] = *reinterpret_cast<const u32x4*>(a.kstore + kbase + int64_t(key) * kstride + kb * 16 + fh * 8);
-    }
-#pragma unroll
-    for (int ds = 0; ds < NDS; ++ds)
-#pragma unroll
-      for (int pb = 0; pb < NPB; ++pb) {
-        const int key = kv0 + 16 * pb + 8 * fh;
-        u32x4 v = *reinterpret_cast<const u32x4*>(a.vstore + vbase + int64_t(ds * 32 + fr) * a.v_stride + key);
-        if (key + 8 > n_keys) {  // zero values past the last key (P is 0 there; keep 0 * garbage out)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const uint32_t lo_ok = (key + 2 * e < n_keys) ? 0x0000ffffu : 0u;
-            const uint32_t hi_ok = (key + 2 * e + 1 < n_keys) ? 0xffff0000u : 0u;
-            v[e] &= (lo_ok | hi_ok);
-          }
-        }
-        f.v[ds][pb] = v;
-      }
-  };
-
+  float m_run = -INFINITY, l_run = 0.0f;
   f32x16 o[NDS];
 #pragma unroll
   for (int i = 0; i < NDS; ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[i][e] = 0.0f;
-  float m_run = -INFINITY, l_run = 0.0f;
 
-  auto compute = [&](int tt, const Tile& f) {
-    const int kv0 = tt * TK;
-    f32x16 s[NST];
+  if (kv0 < n_keys) {
+    // K rows (A operand of S^T = K Q^T, rows permuted by perm32) and V^T rows
+    // (A operand of O^T = V^T P^T); all loads of the tile are issued first.
+    u32x4 kf[NST][NKB], vf[NDS][NPB], qf[NKB];
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+      const int key = kv0 + 32 * st + perm32(fr);
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb)
+        kf[st][kb] = *reinterpret_cast<const u32x4*>(a.kstore + kbase + int64_t(key) * kstride + kb * 16 + fh * 8);
+    }
+#pragma unroll
+    for (int ds = 0; ds < NDS; ++ds)
+#pragma unroll
+      for (int pb = 0; pb < NPB; ++pb)
+        vf[ds][pb] = *reinterpret_cast<const u32x4*>(a.vstore + vbase + int64_t(ds * 32 + fr) * a.v_stride + kv0 +
+                                                     16 * pb + 8 * fh);
+    {
+      const uint16_t* qp = a.q + (int64_t(t) * a.hq + g * G + qh) * DH + fh * 8;
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) qf[kb] = *reinterpret_cast<const u32x4*>(qp + kb * 16);
+    }
+    // Values past the last key: P is 0 there; keep 0 * garbage out.
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      const int key = kv0 + 16 * pb + 8 * fh;
+      if (key + 8 > n_keys) {
+#pragma unroll
+        for (int ds = 0; ds < NDS; ++ds)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t lo_ok = (key + 2 * e < n_keys) ? 0x0000ffffu : 0u;
+            const uint32_t hi_ok = (key + 2 * e + 1 < n_keys) ? 0xffff0000u : 0u;
+            vf[ds][pb][e] &= (lo_ok | hi_ok);
+          }
+      }
+    }
+
+    f32x16 sc[NST];
 #pragma unroll
     for (int st = 0; st < NST; ++st) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) s[st][e] = 0.0f;
+      for (int e = 0; e < 16; ++e) sc[st][e] = 0.0f;
 #pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) s[st] = mfma32(f.k[st][kb], qf[kb], s[st]);
+      for (int kb = 0; kb < NKB; ++kb) sc[st] = mfma32(kf[st][kb], qf[kb], sc[st]);
     }
     float mx = -INFINITY;
 #pragma unroll
@@ -313,68 +315,52 @@ __global__ __launch_bounds__(kThreads, DH == 64 ? 2 : 1) void decode_attn_kernel
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int key = kv0 + 32 * st + 16 * (e >> 3) + 8 * fh + (e & 7);
-        const float v = (key < n_keys) ? s[st][e] * a.scale_log2 : -INFINITY;
-        s[st][e] = v;
+        const float v = (key < n_keys) ? sc[st][e] * a.scale_log2 : -INFINITY;
+        sc[st][e] = v;
         mx = fmaxf(mx, v);
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
+    m_run = fmaxf(mx, __shfl_xor(mx, 32, 64));
     float psum = 0.0f;
 #pragma unroll
     for (int st = 0; st < NST; ++st)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const float p = exp2f(s[st][e] - m_new);
-        s[st][e] = p;
+        const float p = exp2f(sc[st][e] - m_run);
+        sc[st][e] = p;
         psum += p;
       }
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int i = 0; i < NDS; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[i][e] *= alpha;
+    l_run = psum;
     u32x4 pf[NPB];
 #pragma unroll
     for (int pb = 0; pb < NPB; ++pb) {
       const int st = pb >> 1, r0 = 8 * (pb & 1);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) pf[pb][e] = pack2h(s[st][r0 + 2 * e], s[st][r0 + 2 * e + 1]);
+      for (int e = 0; e < 4; ++e) pf[pb][e] = pack2h(sc[st][r0 + 2 * e], sc[st][r0 + 2 * e + 1]);
     }
 #pragma unroll
     for (int i = 0; i < NDS; ++i)
 #pragma unroll
-      for (int pb = 0; pb < NPB; ++pb) o[i] = mfma32(f.v[i][pb], pf[pb], o[i]);
-  };
-
-  // Wave w takes tiles w, w + 4, ...; the next tile's fragments load while
-  // the current one is multiplied.
-  Tile f0, f1;
-  int tt = wave;
-  if (tt < n_tiles) load(tt, f0);
-  while (tt < n_tiles) {
-    if (tt + 4 < n_tiles) load(tt + 4, f1);
-    compute(tt, f0);
-    tt += 4;
-    if (tt >= n_tiles) break;
-    if (tt + 4 < n_tiles) load(tt + 4, f0);
-    compute(tt, f1);
-    tt += 4;
+      for (int pb = 0; pb < NPB; ++pb) o[i] = mfma32(vf[i][pb], pf[pb], o[i]);
   }
 
   // Merge the four waves.  Lane (fr, fh) holds query column fr; both halves
-  // share the running max, each holds part of the sum.
+  // share the maximum, each holds part of the sum.  Waves without a tile hold
+  // -inf and weigh zero.
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  if (fh == 0) {
+  if (fh == 0 && fr < 8) {
     red_m[wave][fr] = m_run;
     red_l[wave][fr] = l_tot;
   }
+  if (fr < 8) {
 #pragma unroll
-  for (int i = 0; i < NDS; ++i)
+    for (int i = 0; i < NDS; ++i)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) red_o[wave][32 * i + 8 * (e >> 2) + 4 * fh + (e & 3)][fr] = o[i][e];
+      for (int e = 0; e < 16; ++e) red_o[wave][32 * i + 8 * (e >> 2) + 4 * fh + (e & 3)][fr] = o[i][e];
+  }
   __syncthreads();
+
+  const int pf_stride = dec_part_floats(G, DH);
+  const int64_t row_item0 = item - split;  // first split of this row
   for (int idx = tid; idx < G * DH; idx += kThreads) {
     const int q = idx / DH, d = idx % DH;
     float M = -INFINITY;
@@ -383,11 +369,68 @@ __global__ __launch_bounds__(kThreads, DH == 64 ? 2 : 1) void decode_attn_kernel
     float num = 0.0f, den = 0.0f;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      const float sc = exp2f(red_m[w][q] - M);  // waves without tiles hold -inf: weight 0
+      const float sc = exp2f(red_m[w][q] - M);
       num += sc * red_o[w][d][q];
       den += sc * red_l[w][q];
     }
-    a.o[int64_t(t) * a.hq * DH + (g * G + q) * DH + d] = f2h(num / den);
+    if (n_split == 1) {
+      a.o[int64_t(t) * a.hq * DH + (g * G + q) * DH + d] = f2h(num / den);
+    } else {
+      // Publish (unnormalised output, maximum, sum) with device-scope stores.
+      float* st = a.part + (int64_t(item) * a.hkv + g) * pf_stride;
+      __hip_atomic_store(st + idx, num, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (d == 0) {
+        __hip_atomic_store(st + G * DH + q, M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(st + G * DH + G + q, den, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
+  if (n_split == 1) return;
+
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // partial state complete before the arrival count
+  __syncthreads();
+  if (tid == 0) {
+    int32_t* cnt = a.counters + row_item0 * a.hkv + g;
+    last = atomicAdd(cnt, 1) == n_split - 1;
+    if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!last) return;
+
+  // Last arrival: combine the splits of (r, g) in split order, eight at a
+  // time (all loads of a batch in flight), with a running maximum.
+  const float* base = a.part + (row_item0 * a.hkv + g) * pf_stride;
+  const int64_t split_stride = int64_t(a.hkv) * pf_stride;
+  for (int idx = tid; idx < G * DH; idx += kThreads) {
+    const int q = idx / DH;
+    float M = -INFINITY, num = 0.0f, den = 0.0f;
+    for (int sp0 = 0; sp0 < n_split; sp0 += 8) {
+      float mv[8], lv[8], ov[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float* st = base + min(sp0 + k, n_split - 1) * split_stride;
+        mv[k] = __hip_atomic_load(st + G * DH + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        lv[k] = __hip_atomic_load(st + G * DH + G + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ov[k] = __hip_atomic_load(st + idx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      float bm = M;
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (sp0 + k < n_split) bm = fmaxf(bm, mv[k]);
+      const float rescale = exp2f(M - bm);  // M = -inf on the first batch: 0
+      num *= rescale;
+      den *= rescale;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        if (sp0 + k < n_split) {
+          const float sc = exp2f(mv[k] - bm);
+          num += sc * ov[k];
+          den += sc * lv[k];
+        }
+      }
+      M = bm;
+    }
+    a.o[int64_t(t) * a.hq * DH + (g * G + q) * DH + (idx % DH)] = f2h(num / den);
   }
 }
 
@@ -404,8 +447,8 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_decode_attention(const DecodeAttnArgs& a, hipStream_t s) {
-  if (a.n_rows <= 0) return hipSuccess;
-  const int grid = a.n_rows * a.hkv;
+  if (a.n_items <= 0) return hipSuccess;
+  const int grid = a.n_items * a.hkv;
   if (a.dh == 64)
     hipLaunchKernelGGL(decode_attn_kernel<64>, dim3(grid), dim3(kThreads), 0, s, a);
   else

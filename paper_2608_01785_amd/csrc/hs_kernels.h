@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "decode_policy.h"
 #include "skinny_policy.h"
 
 namespace hs {
@@ -69,17 +70,28 @@ struct AttnArgs {
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 
-// Single-row (decode) attention: one block per (row, key/value head).
+// Single-row (decode) attention: one block per (work item, key/value head);
+// a work item is one key range (dec_split_keys keys) of one row and carries
+// everything the block needs, so the K/V loads follow a single record load.
+struct DecItem {
+  int32_t t;        // packed row of the query
+  int32_t n_keys;   // keys the row attends to (cached prefix + itself)
+  int32_t split;    // key range split * dec_split_keys ..
+  int32_t n_split;  // splits of this row (its items are consecutive)
+  int64_t kbase;    // element offset of key position 0, head 0
+  int64_t vbase;    // element offset of value position 0, head 0, dim 0
+};
+static_assert(sizeof(DecItem) == 32, "decode item record");
+
 struct DecodeAttnArgs {
   const uint16_t* q;
-  const uint16_t* kstore;
-  const uint16_t* vstore;
+  const uint16_t* kstore;   // token-major keys
+  const uint16_t* vstore;   // dimension-major values
   uint16_t* o;
-  const int4* rows;         // [R] = (packed row t, sequence b, 0, 0)
-  int n_rows;
-  const int32_t* seq_ctx;   // row r of sequence b attends to seq_ctx[b] + 1 keys
-  const int64_t* seq_kbase;
-  const int64_t* seq_vbase;
+  const DecItem* items;
+  int n_items;
+  float* part;              // [n_items][hkv][dec_part_floats] partial states of split rows
+  int32_t* counters;        // [n_items * hkv] arrival counters (first item of a row), zero on entry and exit
   int64_t v_stride;
   int hq, hkv, dh;
   float scale_log2;

@@ -1,6 +1,7 @@
 // Host-only planner: status strings, thread-local errors, CU partition,
 // batch metadata, attention work lists and the workspace layout.
 #include "plan.h"
+#include "decode_policy.h"
 #include "skinny_policy.h"
 
 #include <stdarg.h>
@@ -116,7 +117,13 @@ static SkinnyNeeds skinny_needs(const hs_layer_cfg& c, int32_t T) {
   return n;
 }
 
-static size_t meta_bytes(int32_t T, int32_t B, int64_t att, int32_t counters) {
+// Upper bound on decode work items: every single-row sequence split by the
+// longest possible key range.
+static int64_t max_dec_items(int32_t T, int32_t B, int32_t max_pos, int dh) {
+  return int64_t(std::min(T, B)) * dec_splits(max_pos, dh);
+}
+
+static size_t meta_bytes(int32_t T, int32_t B, int64_t att, int32_t counters, int64_t dec_items, int64_t dec_count) {
   size_t s = 0;
   s += align_up(size_t(T) * 4, 16);       // pos
   s += align_up(size_t(T) * 8, 16) * 2;   // k_off, v_off
@@ -125,6 +132,8 @@ static size_t meta_bytes(int32_t T, int32_t B, int64_t att, int32_t counters) {
   s += align_up(size_t(att) * 8, 16);     // att items
   s += align_up(size_t(B) * 16, 16);      // single-row (decode) rows
   s += align_up(size_t(counters) * 4, 16); // split-K counters
+  s += align_up(size_t(dec_items) * 32, 16); // decode work items
+  s += align_up(size_t(dec_count) * 4, 16);  // decode arrival counters
   return align_up(s, kAlign);
 }
 
@@ -138,7 +147,8 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
     return at;
   };
   const SkinnyNeeds sk = skinny_needs(c, T);
-  w.meta_bytes = meta_bytes(T, B, max_att_items(T, B), sk.counters);
+  const int64_t dec_items = max_dec_items(T, B, max_pos, c.head_dim);
+  w.meta_bytes = meta_bytes(T, B, max_att_items(T, B), sk.counters, dec_items, dec_items * c.n_kv_heads);
   w.meta = take(w.meta_bytes);
   w.n = take(size_t(T) * d * 2);
   w.q = take(size_t(T) * hq * dh * 2);
@@ -152,6 +162,9 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
   w.rope = take(size_t(max_pos) * (dh / 2) * 8);
   w.part_bytes = sk.part_bytes;
   w.part = take(sk.part_bytes);
+  w.dec_part_bytes = size_t(dec_items) * c.n_kv_heads *
+                     dec_part_floats(c.n_q_heads / c.n_kv_heads, c.head_dim) * 4;
+  w.dec_part = take(w.dec_part_bytes);
   w.total = p;
   return w;
 }
@@ -206,6 +219,14 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   P.dec_rows = take(size_t(P.n_dec_rows) * 16);
   P.n_counters = skinny_needs(c, int32_t(T)).counters;
   P.counters = take(size_t(P.n_counters) * 4);
+  std::vector<int32_t> dec_nsplit(dec_seq.size());
+  P.n_dec_items = 0;
+  for (size_t r = 0; r < dec_seq.size(); ++r) {
+    dec_nsplit[r] = dec_splits((ctx ? ctx[dec_seq[r]] : 0) + 1, int(dh));
+    P.n_dec_items += dec_nsplit[r];
+  }
+  P.dec_items = take(size_t(P.n_dec_items) * 32);
+  P.dec_count = take(size_t(P.n_dec_items) * hkv * 4);
   P.image.assign(align_up(p, kAlign), 0);
 
   auto i32 = [&](size_t at) { return reinterpret_cast<int32_t*>(P.image.data() + at); };
@@ -246,6 +267,7 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
     i32(P.att_items)[2 * i] = att[i].b;
     i32(P.att_items)[2 * i + 1] = att[i].q0;
   }
+  int32_t item = 0;
   for (int32_t r = 0; r < P.n_dec_rows; ++r) {
     const int32_t b = dec_seq[r];
     int32_t* row = i32(P.dec_rows) + 4 * r;
@@ -253,6 +275,16 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
     row[1] = b;
     row[2] = 0;
     row[3] = 0;
+    for (int32_t sp = 0; sp < dec_nsplit[r]; ++sp, ++item) {
+      // Record layout: int32 t, n_keys, split, n_split; int64 K base, V base.
+      int32_t* it = i32(P.dec_items + size_t(item) * 32);
+      it[0] = off[b];
+      it[1] = (ctx ? ctx[b] : 0) + 1;
+      it[2] = sp;
+      it[3] = dec_nsplit[r];
+      i64(P.dec_items + size_t(item) * 32 + 16)[0] = i64(P.seq_kbase)[b];
+      i64(P.dec_items + size_t(item) * 32 + 16)[1] = i64(P.seq_vbase)[b];
+    }
   }
   return HS_OK;
 }

@@ -45,6 +45,8 @@ struct WsLayout {
   size_t rope;        // [max_pos, dh / 2] float2
   size_t part;        // split-K partial sums of the skinny GEMM (T <= 128 rows only)
   size_t part_bytes;
+  size_t dec_part;    // per-split partial states of single-row attention
+  size_t dec_part_bytes;
   size_t total;
 };
 
@@ -62,7 +64,9 @@ struct Plan {
   size_t seq_start = 0, seq_len = 0, seq_ctx = 0, seq_kbase = 0, seq_vbase = 0;
   size_t att_items = 0, dec_rows = 0;
   size_t counters = 0;  // split-K arrival counters of the skinny GEMM, zero in the image
-  int32_t n_att_items = 0, n_dec_rows = 0, n_counters = 0;
+  size_t dec_items = 0;  // [n_dec_items] 32-byte records (row, keys, split, splits, K base, V base)
+  size_t dec_count = 0;  // [n_dec_items * hkv] arrival counters, zero in the image
+  int32_t n_att_items = 0, n_dec_rows = 0, n_counters = 0, n_dec_items = 0;
   int64_t v_stride = 0;
 };
 

@@ -302,11 +302,10 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     da.kstore = kstore;
     da.vstore = vstore;
     da.o = o_buf;
-    da.rows = reinterpret_cast<const int4*>(meta + plan.dec_rows);
-    da.n_rows = plan.n_dec_rows;
-    da.seq_ctx = at_args.seq_ctx;
-    da.seq_kbase = at_args.seq_kbase;
-    da.seq_vbase = at_args.seq_vbase;
+    da.items = reinterpret_cast<const hs::DecItem*>(meta + plan.dec_items);
+    da.n_items = plan.n_dec_items;
+    da.part = lay.dec_part_bytes ? at<float>(ws, lay.dec_part) : nullptr;
+    da.counters = reinterpret_cast<int32_t*>(meta + plan.dec_count);
     da.v_stride = plan.v_stride;
     da.hq = hq;
     da.hkv = hkv;
