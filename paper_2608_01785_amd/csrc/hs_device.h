@@ -68,6 +68,74 @@ __device__ __forceinline__ void store_h4(uint16_t* p, float a, float b, float c,
   *reinterpret_cast<u32x2*>(p) = v;
 }
 
+// MFMA row i of a 32-key subtile reads key perm32(i): bits 2 and 3 swapped.
+__device__ __forceinline__ int perm32(int i) {
+  return (i & ~12) | ((i >> 1) & 4) | ((i << 1) & 8);
+}
+
+// Memory accesses whose data another block of the same launch reads or wrote
+// (DEV = true): device-scope relaxed atomics, which write through to, and read
+// from, the device-coherent level instead of an XCD's private L2.  With
+// DEV = false they are ordinary accesses.
+template <bool DEV>
+__device__ __forceinline__ void st_u64(void* p, uint64_t v) {
+  if constexpr (DEV)
+    __hip_atomic_store(static_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    *static_cast<uint64_t*>(p) = v;
+}
+template <bool DEV>
+__device__ __forceinline__ uint64_t ld_u64(const void* p) {
+  if constexpr (DEV)
+    return __hip_atomic_load(static_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    return *static_cast<const uint64_t*>(p);
+}
+template <bool DEV>
+__device__ __forceinline__ void st_u16(uint16_t* p, uint16_t v) {
+  if constexpr (DEV)
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    *p = v;
+}
+template <bool DEV>
+__device__ __forceinline__ u32x4 ld_u32x4(const void* p) {
+  if constexpr (DEV) {
+    const uint64_t lo = ld_u64<true>(p), hi = ld_u64<true>(static_cast<const uint8_t*>(p) + 8);
+    u32x4 r;
+    r[0] = uint32_t(lo);
+    r[1] = uint32_t(lo >> 32);
+    r[2] = uint32_t(hi);
+    r[3] = uint32_t(hi >> 32);
+    return r;
+  } else {
+    return *static_cast<const u32x4*>(p);
+  }
+}
+template <bool DEV>
+__device__ __forceinline__ void st_f32x4(float* p, f32x4 v) {
+  if constexpr (DEV) {
+    st_u64<true>(p, uint64_t(__float_as_uint(v[0])) | (uint64_t(__float_as_uint(v[1])) << 32));
+    st_u64<true>(p + 2, uint64_t(__float_as_uint(v[2])) | (uint64_t(__float_as_uint(v[3])) << 32));
+  } else {
+    *reinterpret_cast<f32x4*>(p) = v;
+  }
+}
+template <bool DEV>
+__device__ __forceinline__ f32x4 ld_f32x4(const float* p) {
+  if constexpr (DEV) {
+    const uint64_t lo = ld_u64<true>(p), hi = ld_u64<true>(p + 2);
+    return f32x4{__uint_as_float(uint32_t(lo)), __uint_as_float(uint32_t(lo >> 32)), __uint_as_float(uint32_t(hi)),
+                 __uint_as_float(uint32_t(hi >> 32))};
+  } else {
+    return *reinterpret_cast<const f32x4*>(p);
+  }
+}
+template <bool DEV>
+__device__ __forceinline__ void st_h4(uint16_t* p, float a, float b, float c, float d) {
+  st_u64<DEV>(p, uint64_t(pack2h(a, b)) | (uint64_t(pack2h(c, d)) << 32));
+}
+
 __device__ __forceinline__ void load_bf16x4(const uint16_t* p, float out[4]) {
   u32x2 v = *reinterpret_cast<const u32x2*>(p);
   out[0] = __uint_as_float(v.x << 16);
