@@ -56,7 +56,7 @@ typedef enum hs_status {
 /* Shape of one decoder layer (all layers of a stack share it).
  * Requirements: hidden % 256 == 0, head_dim in {64, 128},
  * n_q_heads % n_kv_heads == 0, (n_q_heads + 2 n_kv_heads) * head_dim % 256 == 0,
- * n_q_heads * head_dim % 64 == 0, ffn % 128 == 0. */
+ * n_q_heads * head_dim % 128 == 0, ffn % 128 == 0. */
 typedef struct hs_layer_cfg {
   int32_t hidden;
   int32_t n_q_heads;

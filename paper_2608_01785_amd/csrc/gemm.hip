@@ -14,14 +14,26 @@
 // pairs the epilogues need (RoPE's (j, j + dh/2), SwiGLU's gate/up) in the
 // same lane and register.
 //
-// Block tile 256 (weight rows) x 256 (activation rows), 4 waves in a 2 x 2
-// grid, each wave 128 x 128 = 4 x 4 MFMA tiles of 32x32x16.  K advances in
-// slabs of 32 through a ring of 4 LDS stages (128 KB): both operands are
-// copied buffer -> LDS by the load unit itself (no staging registers), so
-// three slabs are in flight while the fourth feeds the MFMAs.  A five-stage
-// ring measured about 5 % slower on the large shapes and a three-stage one
-// the same as four (plausibly because 32 CUs x 5 x 32 KB in flight exceeds
-// the XCD's 4 MB L2, which neighbouring blocks share).
+// Block tile 256 (weight rows) x 256 (activation rows), 8 waves (two per
+// SIMD) in a 2 x 4 grid, each wave 128 weight rows x 64 activation rows =
+// 4 x 2 MFMA tiles of 32x32x16.  K advances in stages of 32.
+//
+// Operand staging.  Copies straight from the buffer unit into LDS occupy the
+// LDS for far longer per byte than ds_write_b128 and serialise with the
+// fragment reads, and a wave can keep only a few vector-memory instructions
+// moving at a time.  So each stage is fetched with plain 16-byte loads into a
+// ring of registers (waves 0-3 the weight tile, waves 4-7 the activation
+// tile, 4 x 1 KB per wave) and written to LDS by the same wave:
+//   stage t is loaded during stage t - 4, written to LDS buffer t % 2 in the
+//   first half of stage t - 1 and multiplied during stage t.
+// One barrier per stage, between its two 16-wide halves, after each wave's
+// writes of stage t + 1 and fragment reads of stage t have completed: that
+// makes the writes visible to the second half's reads of stage t + 1 and
+// retires every read of the buffer the next stage overwrites.  K must be a
+// multiple of 128, so every tile starts on buffer 0 and register slot 0, and
+// the loads of a tile's last four stages already fetch the next tile's first
+// four: the pipeline runs across tiles and the epilogue overlaps them.
+//
 // The grid is persistent (one block per CU of the budget); blocks walk the
 // tile space in grouped order, remapped so each XCD takes a contiguous range.
 #include <type_traits>
@@ -34,12 +46,13 @@ namespace {
 
 constexpr int BM = 256;   // activation rows per tile
 constexpr int BN = 256;   // weight rows per tile
-constexpr int BK = 32;    // K per LDS stage
-constexpr int kStages = 4;
-constexpr int kThreads = 256;
+constexpr int BK = 32;    // K per stage
+constexpr int kThreads = 512;
 constexpr int kRowBytes = BK * 2;            // 64 bytes = 4 chunks of 16
 constexpr int kTileBytes = 256 * kRowBytes;  // 16 KB
 constexpr int kStageBytes = 2 * kTileBytes;  // weight tile + activation tile
+constexpr int kLoads = 4;                    // 1 KB loads per wave per stage
+constexpr int kUnroll = 4;                   // stages per loop body
 constexpr int kGroupM = 4;
 
 // Row of W that lands in tile row r (0..255) of output tile tile_n.
@@ -55,48 +68,28 @@ __device__ __forceinline__ uint32_t weight_row(int tile_n, int r, int ffn) {
   }
 }
 
-// 16-byte chunk c of tile row r sits at physical chunk c ^ swz(r): the 8 rows
-// read by 8 consecutive lanes then cover all 32 banks.
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & 3; }
+// 16-byte chunk c of tile row r sits at physical chunk c ^ swz(r).  A
+// 16-lane pass of fragment reads covers rows r0 .. r0 + 15 at one logical
+// chunk; (r & 3, c ^ swz(r)) is then distinct for all 16 rows, so the pass
+// touches each of the 64 banks once (and any 8 consecutive rows each of 32).
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
-
-using lds_ptr_t = __attribute__((address_space(3))) void*;
 
 // Buffer resource over [base, base + bytes): loads past the end return zero.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
 }
 
-// Workgroup barrier without the compiler's memory fence (which would wait for
-// every outstanding copy).  Callers wait for exactly the copies they need
-// first; LDS reads of the previous stage have completed because their results
-// were consumed.
-__device__ __forceinline__ void barrier_nofence() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-// Wait until at most n vector-memory operations of this wave are outstanding.
-__device__ __forceinline__ void wait_vm(int n) {
-  switch (n) {
-    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-    case 1: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
-    case 2: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
-    default: asm volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
-  }
-}
-
 template <int EPI, int DH, bool W_F16>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * kStageBytes];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wn = wave & 1;   // weight-row half of the tile
-  const int wm = wave >> 1;  // activation-row half of the tile
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wn = wave & 1;   // weight-row half of the tile (128 rows)
+  const int wm = wave >> 1;  // activation-row quarter (64 rows; 32 in a half unit)
   const int fr = lane & 31;
   const int fh = lane >> 5;
 
@@ -105,63 +98,60 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
   const int KT = a.K / BK;
   const uint32_t row_bytes = uint32_t(a.K) * 2;
   const uint32_t w_rows = (EPI == EPI_SWIGLU) ? uint32_t(2 * a.ffn) : uint32_t(a.n_tiles_n * BN);
-  const __amdgpu_buffer_rsrc_t wres = make_rsrc(a.W, w_rows * row_bytes);
-  const __amdgpu_buffer_rsrc_t ares = make_rsrc(a.A, uint32_t(a.M) * row_bytes);
 
-  // Loads: one wave instruction fills 16 consecutive tile rows (1 KB); lane i
-  // lands at byte 16 i = row i / 4, physical chunk i % 4, so it fetches logical
-  // chunk (i % 4) ^ swz(row).  Wave w fills rows 64 w .. 64 w + 63 of both tiles.
+  // Loads: waves 0-3 fetch the weight tile, waves 4-7 the activation tile.
+  // Load l of a wave covers tile rows 64 (wave % 4) + 16 l .. + 15; lane i
+  // fetches chunk i % 4 of row 16 l + i / 4 and writes it to LDS at its
+  // swizzled position.
+  const bool w_wave = wave < 4;
+  const __amdgpu_buffer_rsrc_t res =
+      w_wave ? make_rsrc(a.W, w_rows * row_bytes) : make_rsrc(a.A, uint32_t(a.M) * row_bytes);
+  // Bytes between consecutive stages of one row.  fp16 weights are
+  // panel-major ([K / 32][N][32]): a stage of a weight row is 64 contiguous
+  // bytes and the next stage w_rows * 64 bytes further on.
+  const uint32_t kstride = (w_wave && W_F16) ? w_rows * kRowBytes : uint32_t(kRowBytes);
   const int ld_sub = lane >> 2;
-  const int ld_chunk = (lane & 3) ^ swz(ld_sub);  // rows 16 j + ld_sub share swz with ld_sub
-
-  const int per_group = kGroupM * a.n_tiles_n;
-  auto tile_coords = [&](int L, int& tile_m, int& tile_n) {
-    const int group = L / per_group;
-    const int first_m = group * kGroupM;
-    const int gsize = min(n_m_tiles - first_m, kGroupM);
-    tile_m = first_m + (L % per_group) % gsize;
-    tile_n = (L % per_group) / gsize;
-  };
-
-  uint32_t w_off[4], a_off[4];
-  // fp16 weights are panel-major ([K / 32][N][32]): one stage of a weight row
-  // is 64 contiguous bytes and a tile's stage one contiguous 16 KB run.
-  const uint32_t w_row_stride = W_F16 ? uint32_t(kRowBytes) : row_bytes;
-  const uint32_t w_stage_stride = W_F16 ? w_rows * kRowBytes : uint32_t(kRowBytes);
-  // A half unit (hm = 0 or 1) covers activation rows hm * 128 .. + 127 of its
-  // tile: LDS activation rows 0..127 hold them (copied by waves 0 and 1);
-  // waves 2 and 3 copy the same rows again into the unused rows 128..255, so
-  // every stage still has exactly 8 copies per wave for the vmcnt accounting.
-  auto set_tile = [&](int tile_m, int tile_n, int hm) {
+  const int ld_chunk = lane & 3;
+  const int lrow0 = (wave & 3) * 64 + ld_sub;
+  uint32_t off[kLoads];
+  // A half unit (hm = 0 or 1) covers activation rows hm * 128 .. + 127 of
+  // its tile: LDS activation rows 0..127 hold them; waves 6 and 7 fetch the
+  // same rows again into the unused rows 128..255, so every wave still issues
+  // four loads per stage.
+  auto set_loads = [&](int tile_m, int tile_n, int hm) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = wave * 64 + 16 * j + ld_sub;
-      const int ar = hm < 0 ? r : hm * 128 + (r & 127);
-      w_off[j] = weight_row<EPI>(tile_n, r, a.ffn) * w_row_stride + ld_chunk * 16;
-      a_off[j] = uint32_t(tile_m * BM + ar) * row_bytes + ld_chunk * 16;  // rows >= M read zero
+    for (int l = 0; l < kLoads; ++l) {
+      const int r = lrow0 + 16 * l;
+      if (w_wave) {
+        off[l] = weight_row<EPI>(tile_n, r, a.ffn) * (W_F16 ? uint32_t(kRowBytes) : row_bytes) + ld_chunk * 16;
+      } else {
+        const int ar = hm < 0 ? r : hm * 128 + (r & 127);
+        off[l] = uint32_t(tile_m * BM + ar) * row_bytes + ld_chunk * 16;  // rows >= M read zero
+      }
     }
   };
-  auto issue_stage = [&](int kt, int buf) {
-    const int koff = kt * BK * 2;
-    const uint32_t wkoff = uint32_t(kt) * w_stage_stride;
-    uint8_t* wbase = smem + buf * kStageBytes + wave * 64 * kRowBytes;
+  const uint32_t wr_off = (w_wave ? 0u : uint32_t(kTileBytes)) + uint32_t(lrow0 * kRowBytes) +
+                          uint32_t((ld_chunk ^ swz(ld_sub)) * 16);
+
+  u32x4 g[kUnroll][kLoads];  // register ring: stage t in slot t % 4
+  auto gload = [&](int kt, u32x4* dst) {
+    const uint32_t so = uint32_t(kt) * kstride;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lds_ptr_t)(wbase + j * 16 * kRowBytes), 16, w_off[j], wkoff,
-                                               0, 0);
+    for (int l = 0; l < kLoads; ++l)
+      dst[l] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(res, off[l], so, 0));
+  };
+  auto lwrite = [&](int buf, const u32x4* v) {
+    uint8_t* base = smem + buf * kStageBytes + wr_off;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ares, (lds_ptr_t)(wbase + kTileBytes + j * 16 * kRowBytes), 16,
-                                               a_off[j], koff, 0, 0);
+    for (int l = 0; l < kLoads; ++l) *reinterpret_cast<u32x4*>(base + l * 16 * kRowBytes) = v[l];
   };
 
-  // Fragments of one half stage (16-wide K step kk): [i] weight, [j] activation.
-  // JT = activation subtiles per wave: 4 (full tile, rows wm * 128 ..) or 2
-  // (half unit, rows wm * 64 ..).
-  struct Half {
-    u32x4 w[4], a[4];
+  // Fragments of one 16-wide half stage: [i] weight subtile, [j] activation
+  // subtile.  JT = activation subtiles per wave: 2 (full tile) or 1 (half unit).
+  struct Frag {
+    u32x4 w[4], a[2];
   };
-  auto read_half = [&](auto jt, int buf, int kk, Half& h) {
+  auto read_frag = [&](auto jt, int buf, int kk, Frag& h) {
     constexpr int JT = decltype(jt)::value;
     const uint8_t* base = smem + buf * kStageBytes;
     const int phys = (kk * 2 + fh) ^ swz(fr);
@@ -178,6 +168,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
   // than half the blocks idle its tiles are split into two 128-row halves.
   // Each output element is accumulated in the same order either way, so the
   // result does not depend on the grid.
+  const int per_group = kGroupM * a.n_tiles_n;
+  auto tile_coords = [&](int L, int& tile_m, int& tile_n) {
+    const int group = L / per_group;
+    const int first_m = group * kGroupM;
+    const int gsize = min(n_m_tiles - first_m, kGroupM);
+    tile_m = first_m + (L % per_group) % gsize;
+    tile_n = (L % per_group) / gsize;
+  };
   const int G = gridDim.x;
   const int full_units = (n_tiles / G) * G;
   const int tail = n_tiles - full_units;
@@ -197,21 +195,24 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
   if (L >= n_units) return;
   int tile_m, tile_n, hm;
   unit_coords(L, tile_m, tile_n, hm);
-  set_tile(tile_m, tile_n, hm);
+  set_loads(tile_m, tile_n, hm);
 #pragma unroll
-  for (int st = 0; st < kStages - 1; ++st)
-    if (st < KT) issue_stage(st, st);
+  for (int q = 0; q < kUnroll; ++q) gload(q, g[q]);
+  lwrite(0, g[0]);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
   while (true) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    const int L_next = L + G;
 
-    auto mfma_half = [&](auto jt, const Half& h) {
+    auto mfma_half = [&](auto jt, const Frag& h) {
       constexpr int JT = decltype(jt)::value;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -221,74 +222,81 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
       }
     };
 
-    // Stage s lives in buffer s % kStages.  Each 16-wide half of a stage is
-    // read from LDS while the previous half multiplies, so LDS reads are
-    // spread over the MFMA stream instead of bursting after the barrier.  The
-    // barrier of stage s sits between its two halves: by then every wave has
-    // read all of stage s, so its buffer can be refilled.
+    // Stage s of the unit: buffer s % 2, register slot s % 4 (K % 128 == 0).
     auto k_loop = [&](auto jt) {
       constexpr int JT = decltype(jt)::value;
-      constexpr int NM = 4 * JT;  // MFMAs per half stage
-      wait_vm(min(kStages - 2, KT - 1));
-      barrier_nofence();
-      if (kStages - 1 < KT) issue_stage(kStages - 1, kStages - 1);
-      Half h0, h1;
-      read_half(jt, 0, 0, h0);
-      for (int s = 0; s < KT; ++s) {
-        const int buf = s % kStages;
-        // Phase A: the kk = 0 MFMAs of stage s, with the kk = 1 fragment
-        // reads of the same stage slotted between them.
-        read_half(jt, buf, 1, h1);
-        mfma_half(jt, h0);
+      constexpr int NM = 4 * JT;      // MFMAs per half stage
+      constexpr int NR = 4 + JT;      // fragment reads per half stage
+      Frag h0, h1;
+      read_frag(jt, 0, 0, h0);
+      for (int kt = 0; kt < KT; kt += kUnroll) {
+        const bool last = kt + kUnroll == KT;
+        if (last && L_next < n_units) {
+          // The loads of this body fetch the next unit's first four stages.
+          int nm, nn, nh;
+          unit_coords(L_next, nm, nn, nh);
+          set_loads(nm, nn, nh);
+        }
+        // After the last unit the loads repeat its first stages (in bounds,
+        // never used).
+        const int kl = last ? 0 : kt + kUnroll;
 #pragma unroll
-        for (int q = 0; q < 4 + JT; ++q) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, NM - 4 - JT, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        if (s + 1 < KT) {
-          wait_vm(min(kStages - 2, KT - 2 - s));
-          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of stage s are done
-          barrier_nofence();
-          if (s + kStages < KT) issue_stage(s + kStages, buf);
-          read_half(jt, (s + 1) % kStages, 0, h0);
-        }
-        // Phase B: the kk = 1 MFMAs, with the kk = 0 fragment reads of stage
-        // s + 1 slotted between them (the copies of stage s + kStages go first).
-        mfma_half(jt, h1);
+        for (int u = 0; u < kUnroll; ++u) {
+          // First half: the kk = 0 MFMAs of stage s, with the LDS writes of
+          // stage s + 1, the loads of stage s + 4 and the kk = 1 fragment
+          // reads of stage s slotted between them.
+          read_frag(jt, u & 1, 1, h1);
+          lwrite((u + 1) & 1, g[(u + 1) & 3]);
+          gload(kl + u, g[u]);
+          mfma_half(jt, h0);
+          // LDS traffic first (the barrier below waits for it), then the
+          // loads, one per MFMA.
 #pragma unroll
-        for (int q = 0; q < 4 + JT; ++q) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);  // one LDS read
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);  // one MFMA
+          for (int q = 0; q < kLoads; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+            __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // one LDS write
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+          }
+#pragma unroll
+          for (int q = kLoads; q < NR; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one load
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+          }
+#pragma unroll
+          for (int q = NR - kLoads; q < kLoads; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one load
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          // Writes of stage s + 1 and reads of stage s are done on this
+          // wave; after the barrier on every wave.
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+          __builtin_amdgcn_s_barrier();
+          // Second half: the kk = 1 MFMAs, with the kk = 0 fragment reads of
+          // stage s + 1 (the next unit re-reads its own first fragments).
+          if (u + 1 < kUnroll || !last) read_frag(jt, (u + 1) & 1, 0, h0);
+          mfma_half(jt, h1);
+#pragma unroll
+          for (int q = 0; q < NR; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);  // one LDS read
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);  // one MFMA
+          }
+          __builtin_amdgcn_sched_barrier(0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, NM - 4 - JT, 1);
-        __builtin_amdgcn_sched_barrier(0);
       }
+      (void)NM;
     };
     if (hm < 0)
-      k_loop(std::integral_constant<int, 4>{});
-    else
       k_loop(std::integral_constant<int, 2>{});
-
-    // All waves are done with every stage: start the next tile's copies so
-    // they overlap this tile's epilogue.
-    const int L_next = L + G;
-    __syncthreads();
-    if (L_next < n_units) {
-      int nm, nn, nh;
-      unit_coords(L_next, nm, nn, nh);
-      set_tile(nm, nn, nh);
-#pragma unroll
-      for (int st = 0; st < kStages - 1; ++st)
-        if (st < KT) issue_stage(st, st);
-    }
+    else
+      k_loop(std::integral_constant<int, 1>{});
 
     // ---------------------------------------------------------------- epilogue
-    const int nj = hm < 0 ? 4 : 2;
-    const int m0 = tile_m * BM + (hm < 0 ? wm * 128 : hm * 128 + wm * 64) + fr;
+    const int nj = hm < 0 ? 2 : 1;
+    const int m0 = tile_m * BM + (hm < 0 ? wm * 64 : hm * 128 + wm * 32) + fr;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 2; ++j) {
       const int m = m0 + j * 32;
       if (j >= nj || m >= a.M) continue;
       if constexpr (EPI == EPI_RESID) {
@@ -375,6 +383,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     L = L_next;
     unit_coords(L, tile_m, tile_n, hm);
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 template <int EPI, int DH>
@@ -393,6 +402,7 @@ hipError_t launch_one(const GemmArgs& a, int max_blocks, hipStream_t s) {
 
 hipError_t launch_gemm(int epi, const GemmArgs& a, int max_blocks, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
+  if (a.K < BK * kUnroll || a.K % (BK * kUnroll) != 0) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_RESID: return launch_one<EPI_RESID, 128>(a, max_blocks, s);
     case EPI_SWIGLU: return launch_one<EPI_SWIGLU, 128>(a, max_blocks, s);

@@ -54,8 +54,10 @@ hs_status validate_cfg(const hs_layer_cfg* c) {
                 c->n_q_heads / c->n_kv_heads);
   if (((c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim) % 256 != 0)
     return fail(HS_ERR_UNSUPPORTED, "(Hq + 2 Hkv) * head_dim must be a multiple of 256");
-  if ((c->n_q_heads * c->head_dim) % 64 != 0)
-    return fail(HS_ERR_UNSUPPORTED, "Hq * head_dim must be a multiple of 64");
+  // Hq * head_dim is the K of the output projection; the prefill GEMM walks K
+  // in groups of four 32-wide stages.
+  if ((c->n_q_heads * c->head_dim) % 128 != 0)
+    return fail(HS_ERR_UNSUPPORTED, "Hq * head_dim must be a multiple of 128");
   if (c->ffn <= 0 || c->ffn % 128 != 0)
     return fail(HS_ERR_UNSUPPORTED, "ffn %d must be a positive multiple of 128", c->ffn);
   if (!(c->rms_eps > 0.0f) || !(c->rope_base > 1.0f))
