@@ -403,6 +403,7 @@ hipError_t launch_one(const GemmArgs& a, int max_blocks, hipStream_t s) {
 hipError_t launch_gemm(int epi, const GemmArgs& a, int max_blocks, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (a.K < BK * kUnroll || a.K % (BK * kUnroll) != 0) return hipErrorInvalidValue;
+  if (a.sumsq_out || a.scaled_out || a.row_sumsq) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_RESID: return launch_one<EPI_RESID, 128>(a, max_blocks, s);
     case EPI_SWIGLU: return launch_one<EPI_SWIGLU, 128>(a, max_blocks, s);

@@ -99,6 +99,20 @@ __device__ __forceinline__ void st_u16(uint16_t* p, uint16_t v) {
     *p = v;
 }
 template <bool DEV>
+__device__ __forceinline__ void st_f32(float* p, float v) {
+  if constexpr (DEV)
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    *p = v;
+}
+template <bool DEV>
+__device__ __forceinline__ float ld_f32(const float* p) {
+  if constexpr (DEV)
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    return *p;
+}
+template <bool DEV>
 __device__ __forceinline__ u32x4 ld_u32x4(const void* p) {
   if constexpr (DEV) {
     const uint64_t lo = ld_u64<true>(p), hi = ld_u64<true>(static_cast<const uint8_t*>(p) + 8);

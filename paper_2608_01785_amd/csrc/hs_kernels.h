@@ -42,8 +42,22 @@ struct GemmArgs {
   float* part;
   int32_t* counters;
   int n_split, k_per_split;  // set by the launcher
+  // RMSNorm folded into the skinny GEMMs around it.  RESID, optional: the
+  // new residual's per-row partial sums of squares over each 32-column strip
+  // (sumsq_out[m * strips + strip]) and the residual times a per-column gain
+  // in fp16 (scaled_out, row stride ldo).
+  float* sumsq_out;
+  uint16_t* scaled_out;
+  const uint16_t* gain;      // bf16 [ldo]
+  // QKV / SWIGLU, optional: row m of the product is multiplied by
+  // rsqrt(sum_p row_sumsq[m * row_parts + p] / K + eps) before RoPE or SiLU
+  // (row_parts a multiple of 4, at most kSkinnyMaxNormParts).
+  const float* row_sumsq;
+  int row_parts;
+  float eps;
 };
 
+// The large GEMM does not take the folded-RMSNorm fields (they must be null).
 hipError_t launch_gemm(int epi, const GemmArgs& a, int max_blocks, hipStream_t s);
 
 // Decode-sized GEMMs (M <= kSkinnyMaxRows): thin weight strips, K split

@@ -161,6 +161,7 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
   w.h = take(size_t(T) * d * 4);
   w.a = take(size_t(T) * f * 2);
   w.xtmp = take(size_t(T) * d * 4);
+  w.sumsq = take(size_t(T) * (d / 32) * 4);
   w.rope = take(size_t(max_pos) * (dh / 2) * 8);
   w.part_bytes = sk.part_bytes;
   w.part = take(sk.part_bytes);

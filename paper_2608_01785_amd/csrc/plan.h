@@ -42,6 +42,7 @@ struct WsLayout {
   size_t h;           // [T, d] fp32 residual after attention
   size_t a;           // [T, ffn]
   size_t xtmp;        // [T, d] fp32 residual between layers
+  size_t sumsq;       // [T, d / 32] fp32 partial sums of squares of the residual (folded RMSNorm)
   size_t rope;        // [max_pos, dh / 2] float2
   size_t part;        // split-K partial sums of the skinny GEMM (T <= 128 rows only)
   size_t part_bytes;

@@ -167,6 +167,21 @@ hipError_t gemm(int epi, const hs::GemmArgs& a, int grid_cap, hipStream_t s) {
   return hs::launch_gemm(epi, a, grid_cap, s);
 }
 
+// Residual GEMM a also produces the next RMSNorm's input: its output times
+// gain in fp16 (into n_buf) and per-row partial sums of squares (into sumsq).
+void fold_norm(hs::GemmArgs& a, float* sumsq, uint16_t* n_buf, const void* gain) {
+  a.sumsq_out = sumsq;
+  a.scaled_out = n_buf;
+  a.gain = static_cast<const uint16_t*>(gain);
+}
+
+// The next projection scales its rows from those partial sums.
+void use_norm(hs::GemmArgs& a, const float* sumsq, int parts, float eps) {
+  a.row_sumsq = sumsq;
+  a.row_parts = parts;
+  a.eps = eps;
+}
+
 // Shared body of the prefill forward and the decode step.
 hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w, int32_t n_layers,
                     const void* x_in, void* x_out, const int32_t* seq_offsets, const int32_t* ctx_lens,
@@ -238,6 +253,14 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
   float* xtmp = at<float>(ws, lay.xtmp);
   float* sk_part = lay.part_bytes ? at<float>(ws, lay.part) : nullptr;
   int32_t* sk_count = plan.n_counters ? reinterpret_cast<int32_t*>(meta + plan.counters) : nullptr;
+  // Decode-sized layers (every GEMM on the skinny path) fold RMSNorm into the
+  // GEMMs around it after layer 0's: each residual GEMM writes its output
+  // times the next norm's gain (fp16, into n_buf) and per-row partial sums of
+  // squares over its 32-column strips; the next projection scales its rows by
+  // rsqrt(mean square + eps).  Larger batches keep the norm kernel.
+  float* sumsq = at<float>(ws, lay.sumsq);
+  const int norm_parts = d / 32;
+  bool folded = false;  // n_buf holds x * gain, sumsq its partial sums
 
   TIMED(HS_KERNEL_ROPE_TABLE, hs::launch_rope_table(rope, max_pos, dh, cfg->rope_base, s));
 
@@ -254,8 +277,9 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     uint16_t* kstore = place.cache ? static_cast<uint16_t*>(kv->k[l]) : at<uint16_t>(ws, lay.kpack);
     uint16_t* vstore = place.cache ? static_cast<uint16_t*>(kv->v[l]) : at<uint16_t>(ws, lay.vpack);
 
-    TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(x_cur, x_cur_f32, static_cast<const uint16_t*>(w[l].ln1), n_buf,
-                                                T, d, cfg->rms_eps, 4 * budget, s));
+    if (!folded)
+      TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(x_cur, x_cur_f32, static_cast<const uint16_t*>(w[l].ln1), n_buf,
+                                                  T, d, cfg->rms_eps, 4 * budget, s));
     hs::GemmArgs g{};
     g.part = sk_part;
     g.counters = sk_count;
@@ -276,6 +300,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     g.hq = hq;
     g.hkv = hkv;
     g.dh = dh;
+    if (folded) use_norm(g, sumsq, norm_parts, cfg->rms_eps);
     TIMED(HS_KERNEL_QKV, gemm(hs::EPI_QKV, g, grid_cap, s));
 
     hs::AttnArgs at_args{};
@@ -326,10 +351,17 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     go.ldo = d;
     go.resid = x_cur;
     go.resid_f32 = x_cur_f32;
+    // Fold when every GEMM of the layer takes the skinny path.
+    // Fold when every GEMM of the layer takes the skinny path (gate/up and
+    // down share M, and their K are multiples of 64) and a consumer can
+    // prefetch a row's partial sums.
+    const bool fold = hs::skinny_supported(hs::EPI_QKV, g) && hs::skinny_supported(hs::EPI_RESID, go) &&
+                      norm_parts <= hs::kSkinnyMaxNormParts;
+    if (fold) fold_norm(go, sumsq, n_buf, w[l].ln2);
     TIMED(HS_KERNEL_O_PROJ, gemm(hs::EPI_RESID, go, grid_cap, s));
-
-    TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(nullptr, h_buf, static_cast<const uint16_t*>(w[l].ln2), n_buf, T,
-                                                d, cfg->rms_eps, 4 * budget, s));
+    if (!fold)
+      TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(nullptr, h_buf, static_cast<const uint16_t*>(w[l].ln2), n_buf, T,
+                                                  d, cfg->rms_eps, 4 * budget, s));
 
     hs::GemmArgs gu{};
     gu.part = sk_part;
@@ -343,6 +375,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     gu.out = a_buf;
     gu.ldo = f;
     gu.ffn = f;
+    if (fold) use_norm(gu, sumsq, norm_parts, cfg->rms_eps);
     TIMED(HS_KERNEL_GATE_UP, gemm(hs::EPI_SWIGLU, gu, grid_cap, s));
 
     hs::GemmArgs gd{};
@@ -357,6 +390,8 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     gd.out_f32 = x_next;
     gd.ldo = d;
     gd.resid_f32 = h_buf;
+    folded = fold && l + 1 < n_layers;
+    if (folded) fold_norm(gd, sumsq, n_buf, w[l + 1].ln1);
     TIMED(HS_KERNEL_DOWN, gemm(hs::EPI_RESID, gd, grid_cap, s));
     x_cur = nullptr;
     x_cur_f32 = x_next;

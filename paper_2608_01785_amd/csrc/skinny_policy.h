@@ -15,6 +15,7 @@ constexpr int kSkinnyMaxSplits = 8;
 constexpr int kSkinnyMinStages = 8;      // K stages per split at least
 constexpr int kSkinnySplitBelow = 128;   // only GEMMs with fewer strips split K ...
 constexpr int kSkinnySplitFrom = 32;     // ... and only when K has this many stages
+constexpr int kSkinnyMaxNormParts = 64;  // folded RMSNorm: partial sums per row a consumer prefetches
 
 // 32-row activation subtiles covering M rows (1, 2 or 4).
 inline int skinny_m_tiles(int M) { return M <= 32 ? 1 : (M <= 64 ? 2 : 4); }

@@ -107,6 +107,20 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 31, fh = lane >> 5;
   const int n_split = a.n_split;
+  // Folded RMSNorm: this lane's row's partial sums of squares, loaded now and
+  // summed in the epilogue (wave w owns rows 32 w .. 32 w + 31 there).  Rows
+  // past M fall outside the buffer range and read zero.
+  constexpr int kPre = (EPI == EPI_RESID) ? 1 : kSkinnyMaxNormParts / 4;
+  u32x4 pre[kPre];
+  const bool want_rs = EPI != EPI_RESID && a.row_sumsq && wave < MT;
+  if (want_rs) {
+    const __amdgpu_buffer_rsrc_t pr = make_rsrc(a.row_sumsq, uint32_t(a.M) * a.row_parts * 4);
+    const uint32_t row_off = uint32_t((wave * 32 + fr) * a.row_parts) * 4;
+#pragma unroll
+    for (int u = 0; u < kPre; ++u)
+      if (4 * u < a.row_parts)
+        pre[u] = __builtin_amdgcn_raw_buffer_load_b128(pr, row_off + uint32_t(u * 16), 0, DEV ? kDeviceScope : 0);
+  }
   const int kt0 = ks * a.k_per_split;
   const int KT = min(a.K / BK - kt0, a.k_per_split);  // stages of this split
   const uint32_t row_bytes = uint32_t(a.K) * 2;
@@ -280,28 +294,63 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
   }
 
   const int m = j * 32 + fr;
-  if (!owner || m >= a.M) return;
   if constexpr (EPI == EPI_RESID) {
-    float* orow = a.out_f32 + int64_t(m) * a.ldo;
+    const int strips = a.n_tiles_n * 256 / NR;
+    if (owner && m < a.M) {
+      float* orow = a.out_f32 + int64_t(m) * a.ldo;
+      float ss = 0.0f;
 #pragma unroll
-    for (int i = 0; i < NS; ++i)
+      for (int i = 0; i < NS; ++i)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int n = tile * NR + i * 32 + 8 * g + 4 * fh;
-        f32x4 v = {c[i][4 * g], c[i][4 * g + 1], c[i][4 * g + 2], c[i][4 * g + 3]};
-        if (a.resid_f32) {
-          v += ld_f32x4<DEV>(a.resid_f32 + int64_t(m) * a.ldo + n);
-        } else {
-          float r4[4];
-          load_bf16x4(a.resid + int64_t(m) * a.ldo + n, r4);
-          v[0] += r4[0];
-          v[1] += r4[1];
-          v[2] += r4[2];
-          v[3] += r4[3];
+        for (int g = 0; g < 4; ++g) {
+          const int n = tile * NR + i * 32 + 8 * g + 4 * fh;
+          f32x4 v = {c[i][4 * g], c[i][4 * g + 1], c[i][4 * g + 2], c[i][4 * g + 3]};
+          if (a.resid_f32) {
+            v += ld_f32x4<DEV>(a.resid_f32 + int64_t(m) * a.ldo + n);
+          } else {
+            float r4[4];
+            load_bf16x4(a.resid + int64_t(m) * a.ldo + n, r4);
+            v[0] += r4[0];
+            v[1] += r4[1];
+            v[2] += r4[2];
+            v[3] += r4[3];
+          }
+          st_f32x4<DEV>(orow + n, v);
+          ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+          if (a.scaled_out) {
+            float gm[4];
+            load_bf16x4(a.gain + n, gm);
+            st_h4<DEV>(a.scaled_out + int64_t(m) * a.ldo + n, v[0] * gm[0], v[1] * gm[1], v[2] * gm[2], v[3] * gm[3]);
+          }
         }
-        st_f32x4<DEV>(orow + n, v);
+      if (a.sumsq_out) {
+        // The lane pair (fh = 0, 1) holds this row's NR columns of the strip.
+        ss += __shfl_xor(ss, 32, 64);
+        if (fh == 0) st_f32<DEV>(a.sumsq_out + int64_t(m) * strips + tile, ss);
       }
-  } else if constexpr (EPI == EPI_SWIGLU) {
+    }
+    return;
+  } else {
+    if (!owner || m >= a.M) return;
+    if (want_rs) {
+      float sum = 0.0f;
+#pragma unroll
+      for (int u = 0; u < kPre; ++u) {
+        if (4 * u >= a.row_parts) break;
+        const f32x4 f = __builtin_bit_cast(f32x4, pre[u]);
+        sum += f[0];
+        sum += f[1];
+        sum += f[2];
+        sum += f[3];
+      }
+      const float rs = rsqrtf(sum / float(a.K) + a.eps);
+#pragma unroll
+      for (int i = 0; i < NS; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) c[i][r] *= rs;
+    }
+  }
+  if constexpr (EPI == EPI_SWIGLU) {
     static_assert(EPI != EPI_SWIGLU || NS == 2, "gate/up strips hold 32 + 32 rows");
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
