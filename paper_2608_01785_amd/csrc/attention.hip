@@ -215,22 +215,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
 }
 
 // ----------------------------------------------------------------------------
-// Single-row (decode) attention.  One block = one key range (a "split" of
-// dec_split_keys keys) of one row r and one key/value head g; the group's G
-// query heads are the 32 MFMA columns (G <= 8 valid), so the keys and values
-// of the head are read once for the whole group.  Each of the four waves
-// takes one tile of the range; its K and V fragments come straight from
-// memory into registers in MFMA layout (no LDS), and the four partial softmax
-// states are merged through LDS.  A row with one split writes its output
-// directly; otherwise every split publishes its state and the last split of
-// (r, g) to arrive merges them in split order.
-
 // Single-row (decode) attention: one block per (work item, key/value head);
 // the unit is in decode_unit.h.
 template <int DH>
-__global__ __launch_bounds__(kThreads) void decode_attn_kernel(DecodeAttnArgs a) {
+__global__ __launch_bounds__(kThreads, 2) void decode_attn_kernel(DecodeAttnArgs a) {
   __shared__ decode::DecodeSmem<DH> sm;
-  decode::decode_attn_unit<DH, false>(a, blockIdx.x / a.hkv, blockIdx.x % a.hkv, sm);
+  decode::decode_attn_unit<DH>(a, blockIdx.x / a.hkv, blockIdx.x % a.hkv, sm);
 }
 
 }  // namespace

@@ -7,10 +7,10 @@
 
 namespace hs {
 
-// Keys per tile (one wave's unit of work) and per split (one block: a tile
-// per wave), by head size.
-constexpr int dec_tile_keys(int dh) { return dh == 64 ? 64 : 32; }
-constexpr int dec_split_keys(int dh) { return 4 * dec_tile_keys(dh); }
+// Keys per tile (a wave's step: 32 keys, 8 or 16 KB of keys and values) and
+// per split (one block; its four waves take every fourth tile), by head size.
+constexpr int dec_tile_keys(int dh) { return dh == 64 ? 32 : 32; }
+constexpr int dec_split_keys(int dh) { return dh == 64 ? 1024 : 512; }
 constexpr int dec_splits(int n_keys, int dh) { return (n_keys + dec_split_keys(dh) - 1) / dec_split_keys(dh); }
 
 // Partial state of one split for one key/value head: G x dh unnormalised

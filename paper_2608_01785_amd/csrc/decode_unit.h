@@ -1,14 +1,16 @@
-// Single-row (decode) attention unit, shared by the standalone decode
-// attention kernel and the persistent decode-layer kernel.
+// Single-row (decode) attention unit.
 //
 // A unit is one key range (a "split" of dec_split_keys keys) of one row r and
 // one key/value head g; the group's G query heads are the 32 MFMA columns
 // (G <= 8 valid), so the keys and values of the head are read once for the
-// whole group.  Each of the four waves takes one tile of the range; its K and
-// V fragments come straight from memory into registers in MFMA layout (no
-// LDS), and the four partial softmax states are merged through LDS.  A row
-// with one split writes its output directly; otherwise every split publishes
-// its state and the last split of (r, g) to arrive merges them in split order.
+// whole group.  The range is cut into tiles (dec_tile_keys keys); wave w takes
+// tiles w, w + 4, w + 8, ... and keeps its own running softmax state over
+// them.  A tile's K and V fragments go from memory straight into registers in
+// MFMA layout (no LDS), two register sets deep, so the next tile's loads are
+// in flight while the current tile is multiplied.  The four waves' states are
+// merged through LDS.  A row with one split writes its output directly;
+// otherwise every split publishes its state and the last split of (r, g) to
+// arrive merges them in split order.
 #pragma once
 
 #include "hs_device.h"
@@ -27,27 +29,29 @@ struct DecodeSmem {
 };
 
 // One work item (a key range of one row) for one key/value head g, by one
-// block of 256 threads.  DEV: q, K/V and the output are shared with other
-// blocks of the same launch (device-scope accesses).
-template <int DH, bool DEV>
+// block of 256 threads.
+template <int DH>
 __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int item, int g, DecodeSmem<DH>& sm) {
-  constexpr int TK = (DH == 64) ? 64 : 32;     // keys per tile
-  static_assert(TK * 4 == (DH == 64 ? 256 : 128), "a split is one tile per wave");
+  constexpr int TK = dec_tile_keys(DH);        // keys per tile
   constexpr int NST = TK / 32;                 // 32-key score subtiles
   constexpr int NKB = DH / 16;                 // 16-wide K steps of q.k
   constexpr int NDS = DH / 32;                 // output subtiles along dh
   constexpr int NPB = TK / 16;                 // 16-key P.V steps
+  constexpr int SPLIT = dec_split_keys(DH);
   auto& red_m = sm.red_m;
   auto& red_l = sm.red_l;
   auto& red_o = sm.red_o;
   int& last = sm.last;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int fr = lane & 31, fh = lane >> 5;
   const DecItem it = a.items[item];
   const int t = it.t, n_keys = it.n_keys, split = it.split, n_split = it.n_split;
   const int G = a.hq / a.hkv;
-  const int kv0 = split * 4 * TK + wave * TK;  // this wave's tile
+  const int k_begin = split * SPLIT;
+  const int n_tiles = (min(n_keys - k_begin, SPLIT) + TK - 1) / TK;
+  const int my_tiles = n_tiles > wave ? (n_tiles - wave + 3) / 4 : 0;
   const int qh = min(fr, G - 1);  // query head of this lane's column (padding lanes repeat the last)
   const int64_t kbase = it.kbase + int64_t(g) * DH;
   const int64_t vbase = it.vbase + int64_t(g) * DH * a.v_stride;
@@ -60,50 +64,70 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[i][e] = 0.0f;
 
-  if (kv0 < n_keys) {
-    // K rows (A operand of S^T = K Q^T, rows permuted by perm32) and V^T rows
-    // (A operand of O^T = V^T P^T); all loads of the tile are issued first.
-    u32x4 kf[NST][NKB], vf[NDS][NPB], qf[NKB];
+  u32x4 qf[NKB];
+  {
+    const uint16_t* qp = a.q + (int64_t(t) * a.hq + g * G + qh) * DH + fh * 8;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) qf[kb] = *reinterpret_cast<const u32x4*>(qp + kb * 16);
+  }
+
+  // K rows (A operand of S^T = K Q^T, rows permuted by perm32) and V^T rows
+  // (A operand of O^T = V^T P^T) of tile `ti` of the range, through buffer
+  // resources based at this row's slot and head: per-lane offsets are fixed,
+  // the tile moves the scalar offset.  Keys past the last one stay inside the
+  // slot (ranges are whole tiles of a slot whose length is a multiple of 64);
+  // their scores are masked below.
+  const __amdgpu_buffer_rsrc_t kres =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.kstore + kbase), 0, 0x7ffffff0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vres =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.vstore + vbase), 0, 0x7ffffff0, 0x00020000);
+  const uint32_t k_lane = uint32_t(perm32(fr) * kstride * 2 + fh * 16);
+  const uint32_t v_lane = uint32_t(int64_t(fr) * a.v_stride * 2 + fh * 16);
+  const uint32_t v_sub = uint32_t(32 * a.v_stride * 2);  // bytes between 32-row V^T subtiles
+  struct Tile {
+    u32x4 k[NST][NKB];
+    u32x4 v[NDS][NPB];
+  };
+  auto load_tile = [&](int ti, Tile& tl) {
+    const int kv0 = k_begin + ti * TK;
 #pragma unroll
     for (int st = 0; st < NST; ++st) {
-      const int key = kv0 + 32 * st + perm32(fr);
+      const uint32_t so = uint32_t((kv0 + 32 * st) * kstride * 2);
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
-        kf[st][kb] = ld_u32x4<DEV>(a.kstore + kbase + int64_t(key) * kstride + kb * 16 + fh * 8);
+        tl.k[st][kb] = __builtin_amdgcn_raw_buffer_load_b128(kres, k_lane + kb * 32, so, 0);
     }
 #pragma unroll
     for (int ds = 0; ds < NDS; ++ds)
 #pragma unroll
       for (int pb = 0; pb < NPB; ++pb)
-        vf[ds][pb] = ld_u32x4<DEV>(a.vstore + vbase + int64_t(ds * 32 + fr) * a.v_stride + kv0 + 16 * pb + 8 * fh);
-    {
-      const uint16_t* qp = a.q + (int64_t(t) * a.hq + g * G + qh) * DH + fh * 8;
+        tl.v[ds][pb] = __builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + pb * 32, uint32_t(ds) * v_sub + uint32_t(kv0 * 2), 0);
+  };
+  // Online softmax over this wave's tiles, in the exp2 domain.
+  auto compute_tile = [&](int ti, Tile& tl) {
+    const int kv0 = k_begin + ti * TK;
+    if (kv0 + TK > n_keys) {
+      // Values past the last key: P is 0 there; keep 0 * garbage out.
 #pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) qf[kb] = ld_u32x4<DEV>(qp + kb * 16);
-    }
-    // Values past the last key: P is 0 there; keep 0 * garbage out.
-#pragma unroll
-    for (int pb = 0; pb < NPB; ++pb) {
-      const int key = kv0 + 16 * pb + 8 * fh;
-      if (key + 8 > n_keys) {
+      for (int pb = 0; pb < NPB; ++pb) {
+        const int key = kv0 + 16 * pb + 8 * fh;
 #pragma unroll
         for (int ds = 0; ds < NDS; ++ds)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const uint32_t lo_ok = (key + 2 * e < n_keys) ? 0x0000ffffu : 0u;
             const uint32_t hi_ok = (key + 2 * e + 1 < n_keys) ? 0xffff0000u : 0u;
-            vf[ds][pb][e] &= (lo_ok | hi_ok);
+            tl.v[ds][pb][e] &= (lo_ok | hi_ok);
           }
       }
     }
-
     f32x16 sc[NST];
 #pragma unroll
     for (int st = 0; st < NST; ++st) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) sc[st][e] = 0.0f;
 #pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) sc[st] = mfma32(kf[st][kb], qf[kb], sc[st]);
+      for (int kb = 0; kb < NKB; ++kb) sc[st] = mfma32(tl.k[st][kb], qf[kb], sc[st]);
     }
     float mx = -INFINITY;
 #pragma unroll
@@ -115,17 +139,20 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
         sc[st][e] = v;
         mx = fmaxf(mx, v);
       }
-    m_run = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    // Every tile holds at least one valid key, so m_new is finite.
+    const float m_new = fmaxf(m_run, fmaxf(mx, __shfl_xor(mx, 32, 64)));
+    const float alpha = exp2f(m_run - m_new);  // 0 on the first tile
+    m_run = m_new;
     float psum = 0.0f;
 #pragma unroll
     for (int st = 0; st < NST; ++st)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const float p = exp2f(sc[st][e] - m_run);
+        const float p = exp2f(sc[st][e] - m_new);
         sc[st][e] = p;
         psum += p;
       }
-    l_run = psum;
+    l_run = l_run * alpha + psum;
     u32x4 pf[NPB];
 #pragma unroll
     for (int pb = 0; pb < NPB; ++pb) {
@@ -134,9 +161,51 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
       for (int e = 0; e < 4; ++e) pf[pb][e] = pack2h(sc[st][r0 + 2 * e], sc[st][r0 + 2 * e + 1]);
     }
 #pragma unroll
-    for (int i = 0; i < NDS; ++i)
+    for (int i = 0; i < NDS; ++i) {
 #pragma unroll
-      for (int pb = 0; pb < NPB; ++pb) o[i] = mfma32(vf[i][pb], pf[pb], o[i]);
+      for (int e = 0; e < 16; ++e) o[i][e] *= alpha;
+#pragma unroll
+      for (int pb = 0; pb < NPB; ++pb) o[i] = mfma32(tl.v[i][pb], pf[pb], o[i]);
+    }
+  };
+
+  if constexpr (DH == 64) {
+    // Two register sets.  The first load is unconditional (a wave without
+    // tiles reads tile 0 and discards it); later loads run only for tiles the
+    // wave owns, so the compiler's wait counts stay exact.  The scheduling
+    // barriers keep each tile's loads ahead of the previous tile's math.
+    Tile t0, t1;
+    load_tile(my_tiles > 0 ? wave : 0, t0);
+    __builtin_amdgcn_sched_barrier(0);
+    int i = 0;
+    for (; i + 2 < my_tiles; i += 2) {
+      load_tile(wave + 4 * (i + 1), t1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_tile(wave + 4 * i, t0);
+      __builtin_amdgcn_sched_barrier(0);
+      load_tile(wave + 4 * (i + 2), t0);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_tile(wave + 4 * (i + 1), t1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (my_tiles - i == 2) {
+      load_tile(wave + 4 * (i + 1), t1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_tile(wave + 4 * i, t0);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_tile(wave + 4 * (i + 1), t1);
+    } else if (my_tiles - i == 1) {
+      compute_tile(wave + 4 * i, t0);
+    }
+  } else {
+    // head_dim 128: a tile's fragments and the larger output and query
+    // registers leave room for one register set; other waves of the CU
+    // overlap the loads.
+    Tile t0;
+    for (int i = 0; i < my_tiles; ++i) {
+      load_tile(wave + 4 * i, t0);
+      compute_tile(wave + 4 * i, t0);
+    }
   }
 
   // Merge the four waves.  Lane (fr, fh) holds query column fr; both halves
@@ -170,7 +239,7 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
       den += sc * red_l[w][q];
     }
     if (n_split == 1) {
-      st_u16<DEV>(a.o + int64_t(t) * a.hq * DH + (g * G + q) * DH + d, f2h(num / den));
+      st_u16<false>(a.o + int64_t(t) * a.hq * DH + (g * G + q) * DH + d, f2h(num / den));
     } else {
       // Publish (unnormalised output, maximum, sum) with device-scope stores.
       float* st = a.part + (int64_t(item) * a.hkv + g) * pf_stride;
@@ -226,7 +295,7 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
       }
       M = bm;
     }
-    st_u16<DEV>(a.o + int64_t(t) * a.hq * DH + (g * G + q) * DH + (idx % DH), f2h(num / den));
+    st_u16<false>(a.o + int64_t(t) * a.hq * DH + (g * G + q) * DH + (idx % DH), f2h(num / den));
   }
 }
 

@@ -8,28 +8,20 @@ namespace {
 using namespace skinny;
 
 // NS: n-subtiles of 32 weight rows per block (1 or 2); MT: m-subtiles of 32
-// rows; ST: ring depth wanted (a short K split needs a shallow ring, which
-// leaves LDS for more resident blocks).
-template <int EPI, int DH, bool W_F16, int NS, int MT, int ST>
+// rows.
+template <int EPI, int DH, bool W_F16, int NS, int MT>
 __global__ __launch_bounds__(kThreads) void skinny_kernel(GemmArgs a) {
-  using S = SkinnyShape<EPI, DH, W_F16, NS, MT, ST>;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[S::SMEM];
-  skinny_unit<EPI, DH, W_F16, NS, MT, ST, false>(a, blockIdx.x / a.n_split, blockIdx.x % a.n_split, smem);
-}
-
-template <int EPI, int DH, int NS, int MT, int ST>
-hipError_t launch_st(const GemmArgs& a, int n_blocks, hipStream_t s) {
-  if (a.w_f16)
-    hipLaunchKernelGGL((skinny_kernel<EPI, DH, true, NS, MT, ST>), dim3(n_blocks), dim3(kThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL((skinny_kernel<EPI, DH, false, NS, MT, ST>), dim3(n_blocks), dim3(kThreads), 0, s, a);
-  return hipGetLastError();
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[SkinnyShape<NS, MT>::SMEM];
+  skinny_unit<EPI, DH, W_F16, NS, MT>(a, blockIdx.x / a.n_split, blockIdx.x % a.n_split, smem);
 }
 
 template <int EPI, int DH, int NS, int MT>
 hipError_t launch_mt(const GemmArgs& a, int n_blocks, hipStream_t s) {
-  if (a.k_per_split <= 4) return launch_st<EPI, DH, NS, MT, 4>(a, n_blocks, s);
-  return launch_st<EPI, DH, NS, MT, kMaxStages>(a, n_blocks, s);
+  if (a.w_f16)
+    hipLaunchKernelGGL((skinny_kernel<EPI, DH, true, NS, MT>), dim3(n_blocks), dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((skinny_kernel<EPI, DH, false, NS, MT>), dim3(n_blocks), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
 }
 
 template <int EPI, int DH, int NS>
@@ -49,7 +41,7 @@ hipError_t launch_ns(const GemmArgs& a_in, int strips, hipStream_t s) {
 
 bool skinny_supported(int epi, const GemmArgs& a) {
   if (a.M <= 0 || a.M > kSkinnyMaxRows || a.K % BK != 0) return false;
-  if (epi == EPI_QKV) return a.dh == 64;
+  if (epi == EPI_QKV) return a.dh == 64 || a.dh == 128;
   return true;
 }
 
@@ -58,7 +50,9 @@ hipError_t launch_gemm_skinny(int epi, const GemmArgs& a, hipStream_t s) {
   switch (epi) {
     case EPI_RESID: return launch_ns<EPI_RESID, 64, 1>(a, skinny_strips_resid(a.n_tiles_n * 256), s);
     case EPI_SWIGLU: return launch_ns<EPI_SWIGLU, 64, 2>(a, skinny_strips_swiglu(a.ffn), s);
-    case EPI_QKV: return launch_ns<EPI_QKV, 64, 2>(a, skinny_strips_qkv(a.hq, a.hkv), s);
+    case EPI_QKV:
+      return a.dh == 64 ? launch_ns<EPI_QKV, 64, 1>(a, skinny_strips_qkv(a.hq, a.hkv, 64), s)
+                        : launch_ns<EPI_QKV, 128, 1>(a, skinny_strips_qkv(a.hq, a.hkv, 128), s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -104,7 +104,7 @@ static SkinnyNeeds skinny_needs(const hs_layer_cfg& c, int32_t T) {
     bool used;
   };
   const G gs[4] = {
-      {skinny_strips_qkv(c.n_q_heads, c.n_kv_heads), 2, c.hidden, c.head_dim == 64},
+      {skinny_strips_qkv(c.n_q_heads, c.n_kv_heads, c.head_dim), 1, c.hidden, true},
       {skinny_strips_resid(c.hidden), 1, c.n_q_heads * c.head_dim, true},
       {skinny_strips_swiglu(c.ffn), 2, c.hidden, true},
       {skinny_strips_resid(c.hidden), 1, c.ffn, true},

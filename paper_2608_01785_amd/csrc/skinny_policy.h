@@ -10,7 +10,7 @@ namespace hs {
 
 constexpr int kSkinnyMaxRows = 128;      // M at or below this takes the skinny GEMM
 constexpr int kSkinnyBK = 64;            // K per pipeline stage
-constexpr int kSkinnyTargetBlocks = 256; // blocks wanted per launch
+constexpr int kSkinnyTargetBlocks = 128; // blocks wanted per launch
 constexpr int kSkinnyMaxSplits = 8;
 constexpr int kSkinnyMinStages = 8;      // K stages per split at least
 constexpr int kSkinnySplitBelow = 128;   // only GEMMs with fewer strips split K ...
@@ -40,10 +40,10 @@ inline SkinnySplit skinny_split(int strips, int k_stages) {
 }
 
 // Weight strips per GEMM: 32 output rows (residual GEMMs), 32 gate + 32 up
-// rows (SwiGLU), one 64-wide head (QKV, head_dim 64 only).
+// rows (SwiGLU), 16 dimensions of one head and their RoPE partners (QKV).
 inline int skinny_strips_resid(int n_out) { return n_out / 32; }
 inline int skinny_strips_swiglu(int ffn) { return ffn / 32; }
-inline int skinny_strips_qkv(int hq, int hkv) { return hq + 2 * hkv; }
+inline int skinny_strips_qkv(int hq, int hkv, int dh) { return (hq + 2 * hkv) * (dh / 32); }
 
 // fp32 partial sums of one split of one strip: NS x MT accumulator images of
 // 16 registers x 64 lanes.

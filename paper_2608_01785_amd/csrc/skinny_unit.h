@@ -1,13 +1,12 @@
-// One block's unit of the skinny (decode-sized) fp16 MFMA GEMM, shared by the
-// standalone skinny kernel and the persistent decode-layer kernel.
+// One block's unit of the skinny (decode-sized) fp16 MFMA GEMM.
 //
 // Decode re-reads every weight for a handful of rows, so the unit streams W
 // rather than reusing it: a block owns a thin strip of weight rows (32, or 64
-// when the epilogue needs RoPE or gate/up pairs) and all M rows, and walks K
-// in 64-wide stages copied buffer -> LDS by the load unit through a ring.
-// The four waves split every stage's K: wave w multiplies the 16-wide slice w,
-// so no wave waits on another until the end, where partial accumulators are
-// summed through LDS and the fused epilogues run (residual add into fp32,
+// when the epilogue needs RoPE or gate/up pairs), all M rows and one K range.
+// The four waves split the range into interleaved 32-wide panels whose
+// fragments they load straight into registers, several panels in flight per
+// wave, so no wave waits on another until the end, where partial accumulators
+// are summed through LDS and the fused epilogues run (residual add into fp32,
 // SwiGLU, or RoPE + key/value store).  A K split publishes fp32 partial sums;
 // the last split of a strip to arrive adds them in split order.
 //
@@ -24,87 +23,58 @@ namespace hs {
 namespace skinny {
 
 constexpr int BK = kSkinnyBK;           // K per stage
-constexpr int kRowBytes = BK * 2;       // 128 bytes, 8 chunks of 16
-constexpr int kMaxStages = 8;
 constexpr int kLdsBytes = 160 * 1024;
 constexpr int kThreads = 256;
 constexpr int kDeviceScope = 16;        // buffer cache-policy bit sc1: device-coherent access
-
-using lds_ptr_t = __attribute__((address_space(3))) void*;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
 }
 
-__device__ __forceinline__ void barrier_nofence() {
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's LDS reads are done
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
 
-// Wait until at most n stages of this wave's copies are outstanding, with L
-// copies per stage.
-template <int L>
-__device__ __forceinline__ void wait_stages(int n) {
-  switch (n) {
-#define HS_CASE(k)                                                           \
-  case k:                                                                    \
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((k * L) < 63 ? (k * L) : 63) : "memory"); \
-    break;
-    HS_CASE(0) HS_CASE(1) HS_CASE(2) HS_CASE(3) HS_CASE(4) HS_CASE(5)
-    default:
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((6 * L) < 63 ? (6 * L) : 63) : "memory");
-      break;
-#undef HS_CASE
-  }
-}
-
-// 16-byte chunk c of a 64-byte panel row r sits at physical chunk c ^ swz4(r).
-__device__ __forceinline__ int swz4(int r) { return (r >> 1) & 3; }
-
 // Weight row held in row r of strip `tile` (NR rows per strip).
-template <int EPI, int NR>
+//   SWIGLU: [gate 32 | up 32] for output columns 32 tile .. + 31.
+//   QKV: strip s of head h (DH / 32 strips per head) holds dimensions
+//     16 s .. 16 s + 15 then their rotation partners DH / 2 + 16 s .. + 15,
+//     so an accumulator lane's registers 4 g + e and 4 (g + 2) + e (g < 2)
+//     hold a RoPE pair.
+template <int EPI, int NR, int DH>
 __device__ __forceinline__ uint32_t strip_row(int tile, int r, int ffn) {
   if constexpr (EPI == EPI_SWIGLU) {
-    return uint32_t((r >> 5) * ffn + tile * 32 + (r & 31));  // [gate 32 | up 32]
+    return uint32_t((r >> 5) * ffn + tile * 32 + (r & 31));
+  } else if constexpr (EPI == EPI_QKV) {
+    constexpr int SPH = DH / 32;  // strips per head
+    const int head = tile / SPH, sub = tile % SPH;
+    return uint32_t(head * DH + (r < 16 ? 16 * sub + r : DH / 2 + 16 * sub + (r - 16)));
   } else {
     return uint32_t(tile * NR + r);
   }
 }
 
-template <int EPI, int DH, bool W_F16, int NS, int MT, int ST>
+// LDS of one block: the cross-wave reduction buffer and an arrival flag.
+template <int NS, int MT>
 struct SkinnyShape {
-  static constexpr int NR = 32 * NS;
-  static constexpr int MR = 32 * MT;
-  static constexpr int STAGE = (NR + MR) * kRowBytes;
-  static constexpr int kStages = (kLdsBytes / STAGE) < ST ? (kLdsBytes / STAGE) : ST;
   static constexpr int RED = 4 * NS * MT * 16 * 64 * 4;
-  static constexpr int SMEM = (kStages * STAGE > RED + 16) ? kStages * STAGE : RED + 16;
+  static constexpr int SMEM = RED + 16;
 };
+
+// 32-wide K panels per chunk (a chunk is 2 (NS + MT) fragment loads).
+template <int NS, int MT>
+constexpr int skinny_chunk() { return NS + MT <= 3 ? 2 : 1; }
 
 // One weight strip (`tile`) and one K split (`ks`) of a skinny GEMM, by one
 // block of kThreads threads, in LDS `smem` (SkinnyShape::SMEM bytes, 1 KB
-// aligned).  DEV: the activations, residual and outputs are shared with other
-// blocks of the same launch (device-scope accesses).
-template <int EPI, int DH, bool W_F16, int NS, int MT, int ST, bool DEV>
+// aligned).
+template <int EPI, int DH, bool W_F16, int NS, int MT>
 __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks, uint8_t* smem) {
   constexpr int NR = 32 * NS;                 // weight rows per block
-  constexpr int MR = 32 * MT;                 // activation rows covered
-  constexpr int WBYTES = NR * kRowBytes;
-  constexpr int XBYTES = MR * kRowBytes;
-  constexpr int STAGE = WBYTES + XBYTES;
-  constexpr int WCOPIES = NR / 8 / 4;         // copies per wave per stage (8 rows each)
-  constexpr int XCOPIES = MR / 8 / 4;
-  constexpr int L = WCOPIES + XCOPIES;
-  constexpr int kStages = (kLdsBytes / STAGE) < ST ? (kLdsBytes / STAGE) : ST;
-  constexpr int RED = 4 * NS * MT * 16 * 64 * 4;  // cross-wave reduction buffer
-  constexpr int SMEM = (kStages * STAGE > RED + 16) ? kStages * STAGE : RED + 16;
-  static_assert(NR % 32 == 0 && MR % 32 == 0, "tile shape");
+  constexpr int CH = skinny_chunk<NS, MT>();
+  constexpr int SMEM = SkinnyShape<NS, MT>::SMEM;
   static_assert(SMEM <= kLdsBytes, "LDS");
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int fr = lane & 31, fh = lane >> 5;
   const int n_split = a.n_split;
   // Folded RMSNorm: this lane's row's partial sums of squares, loaded now and
@@ -119,7 +89,28 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
 #pragma unroll
     for (int u = 0; u < kPre; ++u)
       if (4 * u < a.row_parts)
-        pre[u] = __builtin_amdgcn_raw_buffer_load_b128(pr, row_off + uint32_t(u * 16), 0, DEV ? kDeviceScope : 0);
+        pre[u] = __builtin_amdgcn_raw_buffer_load_b128(pr, row_off + uint32_t(u * 16), 0, 0);
+  }
+  // Residual of the RESID epilogue, loaded now so that it is in registers by
+  // the epilogue (wave w owns rows 32 w .. 32 w + 31 there).
+  f32x4 res_pre[EPI == EPI_RESID ? NS : 1][4];
+  if constexpr (EPI == EPI_RESID) {
+    const int m = wave * 32 + fr;
+    if (wave < MT && m < a.M) {
+#pragma unroll
+      for (int i = 0; i < NS; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = tile * NR + i * 32 + 8 * g + 4 * fh;
+          if (a.resid_f32) {
+            res_pre[i][g] = *reinterpret_cast<const f32x4*>(a.resid_f32 + int64_t(m) * a.ldo + n);
+          } else {
+            float r4[4];
+            load_bf16x4(a.resid + int64_t(m) * a.ldo + n, r4);
+            res_pre[i][g] = f32x4{r4[0], r4[1], r4[2], r4[3]};
+          }
+        }
+    }
   }
   const int kt0 = ks * a.k_per_split;
   const int KT = min(a.K / BK - kt0, a.k_per_split);  // stages of this split
@@ -129,52 +120,27 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
   const __amdgpu_buffer_rsrc_t wres = make_rsrc(a.W, w_rows * row_bytes);
   const __amdgpu_buffer_rsrc_t xres = make_rsrc(a.A, uint32_t(a.M) * row_bytes);
 
-  // Activation copies: one wave instruction fills 8 rows of 128 bytes; lane i
-  // lands at row i / 8, physical chunk i % 8 = logical chunk (i % 8) ^ (row % 8).
-  const int sub = lane >> 3;
-  const int chunk = (lane & 7) ^ sub;
-  // Weight copies.  Row-major bf16: as the activations.  Panel-major fp16
-  // ([K / 32][N][32]): a stage is two 32-wide panels, stored in LDS as
-  // [panel][NR rows][64 bytes]; one instruction fills 16 rows of one panel,
-  // lane i at row i / 4, physical chunk i % 4 = logical (i % 4) ^ swz4(row).
-  const int psub = lane >> 2;
-  const int pchunk = (lane & 3) ^ swz4(psub);
-  // Fixed extents: arrays sized by the template's constants and captured by
-  // the lambda below make the host pass drop the kernel's launch stub.
-  static_assert(WCOPIES <= 2 && XCOPIES <= 4, "copy slots");
-  uint32_t w_off[2], x_off[4];
-  int w_panel[2];
+  // Fragments go from memory straight into registers in MFMA operand layout.
+  // The split's K range is cut into 32-wide panels; wave w takes panels w,
+  // w + 4, w + 8, ... in chunks of CH panels and loads chunk c + 1 while it
+  // multiplies chunk c.  A panel past the range is read through an empty
+  // buffer resource, so it returns zeros and moves no data.
+  //   weight fragment (A operand): rows strip_row(i * 32 + fr), K 16 s + 8 fh .. + 7
+  //   activation fragment (B operand): rows j * 32 + fr, the same K
+  static_assert(NS <= 2 && MT <= 4, "fragment slots");
+  const __amdgpu_buffer_rsrc_t zres = make_rsrc(a.W, 0);
+  uint32_t w_off[NS], x_off[MT];
 #pragma unroll
-  for (int c = 0; c < WCOPIES; ++c) {
-    const int q = wave * WCOPIES + c;
-    if constexpr (W_F16) {
-      w_panel[c] = q / (NR / 16);
-      w_off[c] = strip_row<EPI, NR>(tile, (q % (NR / 16)) * 16 + psub, a.ffn) * 64 + pchunk * 16;
-    } else {
-      w_panel[c] = 0;
-      w_off[c] = strip_row<EPI, NR>(tile, q * 8 + sub, a.ffn) * row_bytes + chunk * 16;
-    }
+  for (int i = 0; i < NS; ++i) {
+    const uint32_t r = strip_row<EPI, NR, DH>(tile, i * 32 + fr, a.ffn);
+    w_off[i] = (W_F16 ? r * 64u : r * row_bytes) + uint32_t(fh * 16);
   }
 #pragma unroll
-  for (int c = 0; c < XCOPIES; ++c) x_off[c] = uint32_t((wave * XCOPIES + c) * 8 + sub) * row_bytes + chunk * 16;
+  for (int j = 0; j < MT; ++j) x_off[j] = uint32_t(j * 32 + fr) * row_bytes + uint32_t(fh * 16);
   const uint32_t panel_bytes = w_rows * 64;
-
-  auto issue = [&](int kt, int buf) {
-    const int koff = (kt0 + kt) * kRowBytes;
-    uint8_t* base = smem + buf * STAGE;
-#pragma unroll
-    for (int c = 0; c < WCOPIES; ++c) {
-      // Both layouts put copy q at byte q * 1 KB of the stage's weight area.
-      const int q = wave * WCOPIES + c;
-      const uint32_t soff = W_F16 ? (2 * (kt0 + kt) + w_panel[c]) * panel_bytes : uint32_t(koff);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lds_ptr_t)(base + q * 1024), 16, w_off[c], soff, 0, 0);
-    }
-#pragma unroll
-    for (int c = 0; c < XCOPIES; ++c)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(xres,
-                                               (lds_ptr_t)(base + WBYTES + (wave * XCOPIES + c) * 8 * kRowBytes),
-                                               16, x_off[c], koff, 0, DEV ? kDeviceScope : 0);
-  };
+  const int n_panels = 2 * KT;
+  const int my_panels = n_panels > wave ? (n_panels - wave + 3) / 4 : 0;
+  const int n_chunks = (my_panels + CH - 1) / CH;
 
   f32x16 acc[NS][MT];
 #pragma unroll
@@ -184,47 +150,84 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+  struct Chunk {
+    u32x4 w[CH][2][NS];
+    u32x4 x[CH][2][MT];
+  };
+  auto load_chunk = [&](int c, Chunk& b) {
 #pragma unroll
-  for (int st = 0; st < kStages - 1; ++st)
-    if (st < KT) issue(st, st);
-
-  const int phys = (2 * wave + fh) ^ (fr & 7);  // this wave's 16-wide K slice
-  // Panel-major weights: slice w is chunks 2 (w % 2) + fh of panel w / 2.
-  const int pphys = (2 * (wave & 1) + fh) ^ swz4(fr);
-  const int pbase = (wave >> 1) * NR * 64;
-  int buf = 0;
-  for (int kt = 0; kt < KT; ++kt) {
-    wait_stages<L>(min(kStages - 2, KT - 1 - kt));
-    barrier_nofence();
-    if (kt + kStages - 1 < KT) issue(kt + kStages - 1, buf == 0 ? kStages - 1 : buf - 1);
-    const uint8_t* base = smem + buf * STAGE;
-    u32x4 fw[NS], fx[MT];
+    for (int q = 0; q < CH; ++q) {
+      const int p = wave + 4 * (c * CH + q);  // panel of this split
+      const bool ok = p < n_panels;
+      const __amdgpu_buffer_rsrc_t wr = ok ? wres : zres;
+      const __amdgpu_buffer_rsrc_t xr = ok ? xres : zres;
+      const uint32_t P = uint32_t(2 * kt0 + p);  // panel of the matrix
+      const uint32_t wso = W_F16 ? P * panel_bytes : P * 64u;
 #pragma unroll
-    for (int i = 0; i < NS; ++i)
-      fw[i] = W_F16 ? *reinterpret_cast<const u32x4*>(base + pbase + (i * 32 + fr) * 64 + pphys * 16)
-                    : *reinterpret_cast<const u32x4*>(base + (i * 32 + fr) * kRowBytes + phys * 16);
+      for (int s = 0; s < 2; ++s) {
 #pragma unroll
-    for (int j = 0; j < MT; ++j)
-      fx[j] = *reinterpret_cast<const u32x4*>(base + WBYTES + (j * 32 + fr) * kRowBytes + phys * 16);
+        for (int i = 0; i < NS; ++i)
+          b.w[q][s][i] = __builtin_amdgcn_raw_buffer_load_b128(wr, w_off[i] + 32 * s, wso, 0);
 #pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      const u32x4 wh = W_F16 ? fw[i] : bf8_to_h8(fw[i]);
-#pragma unroll
-      for (int j = 0; j < MT; ++j) acc[i][j] = mfma32(wh, fx[j], acc[i][j]);
+        for (int j = 0; j < MT; ++j)
+          b.x[q][s][j] = __builtin_amdgcn_raw_buffer_load_b128(xr, x_off[j] + 32 * s, P * 64u, 0);
+      }
     }
-    buf = (buf == kStages - 1) ? 0 : buf + 1;
+  };
+  auto mma_chunk = [&](const Chunk& b) {
+#pragma unroll
+    for (int q = 0; q < CH; ++q)
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int i = 0; i < NS; ++i) {
+          const u32x4 wh = W_F16 ? b.w[q][s][i] : bf8_to_h8(b.w[q][s][i]);
+#pragma unroll
+          for (int j = 0; j < MT; ++j) acc[i][j] = mfma32(wh, b.x[q][s][j], acc[i][j]);
+        }
+  };
+
+  // Two register sets.  Chunk 0 is always loaded (a wave without panels
+  // reads zeros); later chunks are loaded only when they hold panels of this
+  // wave, so the compiler's wait counts stay exact, and the scheduling
+  // barriers keep each chunk's loads ahead of the previous chunk's MFMAs.
+  Chunk b0, b1;
+  load_chunk(0, b0);
+  __builtin_amdgcn_sched_barrier(0);
+  int ch = 0;
+  for (; ch + 2 < n_chunks; ch += 2) {
+    load_chunk(ch + 1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_chunk(b0);
+    __builtin_amdgcn_sched_barrier(0);
+    load_chunk(ch + 2, b0);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_chunk(b1);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (n_chunks - ch == 2) {
+    load_chunk(ch + 1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_chunk(b0);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_chunk(b1);
+  } else if (n_chunks - ch == 1) {
+    mma_chunk(b0);
   }
 
-  // Sum the four waves' partial accumulators through LDS; wave w then owns
-  // row subtile j = w (MT <= 4).
+  // Sum the four waves' partial accumulators through LDS ([wave][i][j][lane]
+  // images of 16 floats, moved 16 bytes at a time); wave w then owns row
+  // subtile j = w (MT <= 4).
   __syncthreads();
-  float* red = reinterpret_cast<float*>(smem);
+  f32x4* red = reinterpret_cast<f32x4*>(smem);
 #pragma unroll
   for (int i = 0; i < NS; ++i)
 #pragma unroll
     for (int j = 0; j < MT; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) red[(((wave * NS + i) * MT + j) * 16 + r) * 64 + lane] = acc[i][j][r];
+      for (int q = 0; q < 4; ++q)
+        red[(((wave * NS + i) * MT + j) * 64 + lane) * 4 + q] =
+            f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
   __syncthreads();
   const int j = wave;
   const bool owner = j < MT;
@@ -232,13 +235,14 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
 #pragma unroll
   for (int i = 0; i < NS; ++i)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float v = 0.0f;
+    for (int q = 0; q < 4; ++q) {
+      f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
       if (owner) {
 #pragma unroll
-        for (int w = 0; w < 4; ++w) v += red[(((w * NS + i) * MT + j) * 16 + r) * 64 + lane];
+        for (int w = 0; w < 4; ++w) v += red[(((w * NS + i) * MT + j) * 64 + lane) * 4 + q];
       }
-      c[i][r] = v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) c[i][4 * q + e] = v[e];
     }
 
   if (n_split > 1) {
@@ -305,28 +309,19 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
         for (int g = 0; g < 4; ++g) {
           const int n = tile * NR + i * 32 + 8 * g + 4 * fh;
           f32x4 v = {c[i][4 * g], c[i][4 * g + 1], c[i][4 * g + 2], c[i][4 * g + 3]};
-          if (a.resid_f32) {
-            v += ld_f32x4<DEV>(a.resid_f32 + int64_t(m) * a.ldo + n);
-          } else {
-            float r4[4];
-            load_bf16x4(a.resid + int64_t(m) * a.ldo + n, r4);
-            v[0] += r4[0];
-            v[1] += r4[1];
-            v[2] += r4[2];
-            v[3] += r4[3];
-          }
-          st_f32x4<DEV>(orow + n, v);
+          v += res_pre[i][g];
+          *reinterpret_cast<f32x4*>(orow + n) = v;
           ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
           if (a.scaled_out) {
             float gm[4];
             load_bf16x4(a.gain + n, gm);
-            st_h4<DEV>(a.scaled_out + int64_t(m) * a.ldo + n, v[0] * gm[0], v[1] * gm[1], v[2] * gm[2], v[3] * gm[3]);
+            st_h4<false>(a.scaled_out + int64_t(m) * a.ldo + n, v[0] * gm[0], v[1] * gm[1], v[2] * gm[2], v[3] * gm[3]);
           }
         }
       if (a.sumsq_out) {
         // The lane pair (fh = 0, 1) holds this row's NR columns of the strip.
         ss += __shfl_xor(ss, 32, 64);
-        if (fh == 0) st_f32<DEV>(a.sumsq_out + int64_t(m) * strips + tile, ss);
+        if (fh == 0) st_f32<false>(a.sumsq_out + int64_t(m) * strips + tile, ss);
       }
     }
     return;
@@ -357,36 +352,37 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
       float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) v[e] = silu(c[0][4 * g + e]) * c[1][4 * g + e];
-      st_h4<DEV>(a.out + int64_t(m) * a.ldo + tile * 32 + 8 * g + 4 * fh, v[0], v[1], v[2], v[3]);
+      st_h4<false>(a.out + int64_t(m) * a.ldo + tile * 32 + 8 * g + 4 * fh, v[0], v[1], v[2], v[3]);
     }
-  } else {  // EPI_QKV: the strip is one 64-wide head
-    static_assert(EPI != EPI_QKV || (NS == 2 && DH == 64), "QKV strips are one 64-wide head");
-    const int head = tile;
+  } else {  // EPI_QKV: a strip holds 16 dimensions of one head and their RoPE partners
+    static_assert(EPI != EPI_QKV || NS == 1, "QKV strips are 32 rows");
+    constexpr int SPH = DH / 32;
+    const int head = tile / SPH, sub = tile % SPH;
     const int p = a.pos[m];
     const float2* rt = a.rope + int64_t(p) * (DH / 2);
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int d = 8 * g + 4 * fh;
+    for (int g = 0; g < 2; ++g) {
+      const int d = 16 * sub + 8 * g + 4 * fh;  // < DH / 2; partner d + DH / 2
       if (head < a.hq + a.hkv) {
         float rl[4], rh[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float2 cs = rt[d + e];
-          const float lo = c[0][4 * g + e], hi = c[1][4 * g + e];
+          const float lo = c[0][4 * g + e], hi = c[0][4 * (g + 2) + e];
           rl[e] = lo * cs.x - hi * cs.y;
           rh[e] = hi * cs.x + lo * cs.y;
         }
         uint16_t* dst = (head < a.hq) ? a.q + (int64_t(m) * a.hq + head) * DH
                                       : a.kstore + a.k_off[m] + int64_t(head - a.hq) * DH;
-        st_h4<DEV>(dst + d, rl[0], rl[1], rl[2], rl[3]);
-        st_h4<DEV>(dst + d + DH / 2, rh[0], rh[1], rh[2], rh[3]);
+        store_h4(dst + d, rl[0], rl[1], rl[2], rl[3]);
+        store_h4(dst + d + DH / 2, rh[0], rh[1], rh[2], rh[3]);
       } else {
         const int gh = head - a.hq - a.hkv;
         uint16_t* dst = a.vstore + a.v_off[m];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          st_u16<DEV>(dst + int64_t(gh * DH + d + e) * a.v_stride, f2h(c[0][4 * g + e]));
-          st_u16<DEV>(dst + int64_t(gh * DH + d + DH / 2 + e) * a.v_stride, f2h(c[1][4 * g + e]));
+          dst[int64_t(gh * DH + d + e) * a.v_stride] = f2h(c[0][4 * g + e]);
+          dst[int64_t(gh * DH + d + DH / 2 + e) * a.v_stride] = f2h(c[0][4 * (g + 2) + e]);
         }
       }
     }
