@@ -92,9 +92,11 @@ typedef struct hs_layer_weights {
 
 /* Key/value cache.  k[l] and v[l] are device pointers for layer l (host
  * arrays of n_layers pointers, owned by the caller).  Per layer:
- *   K: fp16 [n_slots, max_ctx, Hkv, dh]   (row-major, token-major)
- *   V: fp16 [n_slots, Hkv, dh, max_ctx]   (dimension-major: the P.V
- *      contraction reads keys contiguously)
+ *   K: fp16 [n_slots, Hkv, max_ctx, dh]            (the key rows of one head
+ *      are contiguous)
+ *   V: fp16 [n_slots, Hkv, max_ctx / 32, dh, 32]   (values transposed in
+ *      tiles of 32 positions: the P.V contraction reads keys contiguously and
+ *      a tile of one head is one contiguous block)
  * Sequence b of a call uses slot b.  max_ctx % 64 == 0. */
 typedef struct hs_kv_cache {
   void* const* k;

@@ -51,9 +51,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
   const int len = a.seq_len[b];
   const int ctx = a.seq_ctx[b];
   const int row0 = a.seq_start[b];
-  const int64_t kbase = a.seq_kbase[b] + int64_t(g) * DH;
-  const int64_t vbase = a.seq_vbase[b] + int64_t(g) * DH * a.v_stride;
-  const int kv_row_stride = a.hkv * DH;
+  const int64_t kbase = a.seq_kbase[b] + int64_t(g) * a.kv_head_stride;
+  const int64_t vbase = a.seq_vbase[b] + int64_t(g) * a.kv_head_stride;
+  const int kv_row_stride = DH;
 
   const int n_keys = ctx + min(q0 + BQ, len);      // keys any query of the block may see
   const int n_tiles = (n_keys + BKV - 1) / BKV;
@@ -83,7 +83,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
       const int idx = tid + j * kThreads;
       const int d = idx >> 3, c = idx & 7;
       const int key = kv0 + c * 8;
-      u32x4 v = *reinterpret_cast<const u32x4*>(a.vstore + vbase + int64_t(d) * a.v_stride + key);
+      // 8 keys of dimension d inside the value tile of 32 keys holding them.
+      u32x4 v = *reinterpret_cast<const u32x4*>(a.vstore + vbase + int64_t(key / kv_tile_keys) * kv_tile_keys * DH +
+                                                d * kv_tile_keys + key % kv_tile_keys);
       if (key + 8 > n_keys) {
         // Keys past the last visible one may hold uninitialised data; P is 0
         // there, but 0 * NaN would still poison the sum, so zero them.

@@ -53,9 +53,8 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
   const int n_tiles = (min(n_keys - k_begin, SPLIT) + TK - 1) / TK;
   const int my_tiles = n_tiles > wave ? (n_tiles - wave + 3) / 4 : 0;
   const int qh = min(fr, G - 1);  // query head of this lane's column (padding lanes repeat the last)
-  const int64_t kbase = it.kbase + int64_t(g) * DH;
-  const int64_t vbase = it.vbase + int64_t(g) * DH * a.v_stride;
-  const int kstride = a.hkv * DH;
+  const int64_t kbase = it.kbase + int64_t(g) * a.kv_head_stride;
+  const int64_t vbase = it.vbase + int64_t(g) * a.kv_head_stride;
 
   float m_run = -INFINITY, l_run = 0.0f;
   f32x16 o[NDS];
@@ -74,16 +73,18 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
   // K rows (A operand of S^T = K Q^T, rows permuted by perm32) and V^T rows
   // (A operand of O^T = V^T P^T) of tile `ti` of the range, through buffer
   // resources based at this row's slot and head: per-lane offsets are fixed,
-  // the tile moves the scalar offset.  Keys past the last one stay inside the
-  // slot (ranges are whole tiles of a slot whose length is a multiple of 64);
-  // their scores are masked below.
+  // the tile moves the scalar offset.  A tile is one 32-key value tile of the
+  // cache, and its key rows are contiguous too.  Keys past the last one stay
+  // inside the slot (ranges are whole tiles of a slot whose length is a
+  // multiple of 64); their scores are masked below.
+  static_assert(TK == kv_tile_keys, "a tile is one value tile of the cache");
   const __amdgpu_buffer_rsrc_t kres =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.kstore + kbase), 0, 0x7ffffff0, 0x00020000);
   const __amdgpu_buffer_rsrc_t vres =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.vstore + vbase), 0, 0x7ffffff0, 0x00020000);
-  const uint32_t k_lane = uint32_t(perm32(fr) * kstride * 2 + fh * 16);
-  const uint32_t v_lane = uint32_t(int64_t(fr) * a.v_stride * 2 + fh * 16);
-  const uint32_t v_sub = uint32_t(32 * a.v_stride * 2);  // bytes between 32-row V^T subtiles
+  const uint32_t k_lane = uint32_t(perm32(fr) * DH * 2 + fh * 16);
+  const uint32_t v_lane = uint32_t(fr * TK * 2 + fh * 16);
+  constexpr uint32_t v_sub = 32 * TK * 2;  // bytes between 32-dimension subtiles of a value tile
   struct Tile {
     u32x4 k[NST][NKB];
     u32x4 v[NDS][NPB];
@@ -92,7 +93,7 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
     const int kv0 = k_begin + ti * TK;
 #pragma unroll
     for (int st = 0; st < NST; ++st) {
-      const uint32_t so = uint32_t((kv0 + 32 * st) * kstride * 2);
+      const uint32_t so = uint32_t((kv0 + 32 * st) * DH * 2);
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
         tl.k[st][kb] = __builtin_amdgcn_raw_buffer_load_b128(kres, k_lane + kb * 32, so, 0);
@@ -101,7 +102,8 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
     for (int ds = 0; ds < NDS; ++ds)
 #pragma unroll
       for (int pb = 0; pb < NPB; ++pb)
-        tl.v[ds][pb] = __builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + pb * 32, uint32_t(ds) * v_sub + uint32_t(kv0 * 2), 0);
+        tl.v[ds][pb] = __builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + pb * 32,
+                                                             uint32_t(ds) * v_sub + uint32_t(kv0 * DH * 2), 0);
   };
   // Online softmax over this wave's tiles, in the exp2 domain.
   auto compute_tile = [&](int ti, Tile& tl) {

@@ -363,16 +363,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
               }
               uint16_t* dst = (head < a.hq)
                                   ? a.q + (int64_t(m) * a.hq + head) * DH
-                                  : a.kstore + a.k_off[m] + int64_t(head - a.hq) * DH;
+                                  : a.kstore + a.k_off[m] + int64_t(head - a.hq) * a.kv_head_stride;
               store_h4(dst + d, rl[0], rl[1], rl[2], rl[3]);
               store_h4(dst + d + DH / 2, rh[0], rh[1], rh[2], rh[3]);
             } else {
               const int gh = head - a.hq - a.hkv;
-              uint16_t* dst = a.vstore + a.v_off[m];
+              uint16_t* dst = a.vstore + a.v_off[m] + int64_t(gh) * a.kv_head_stride;
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
-                dst[int64_t(gh * DH + d + e) * a.v_stride] = f2h(lo[e]);
-                dst[int64_t(gh * DH + d + DH / 2 + e) * a.v_stride] = f2h(hi[e]);
+                dst[(d + e) * kv_tile_keys] = f2h(lo[e]);
+                dst[(d + DH / 2 + e) * kv_tile_keys] = f2h(hi[e]);
               }
             }
           }

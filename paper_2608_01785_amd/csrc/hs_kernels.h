@@ -29,12 +29,12 @@ struct GemmArgs {
   int ffn;                // SWIGLU: offset of the 'up' rows
   // QKV epilogue
   uint16_t* q;            // [M, hq, dh] fp16
-  uint16_t* kstore;       // keys: element k_off[m] + g * dh + d
-  uint16_t* vstore;       // values (dimension-major): v_off[m] + (g * dh + d) * v_stride
+  uint16_t* kstore;       // keys: element k_off[m] + g * kv_head_stride + d
+  uint16_t* vstore;       // values: element v_off[m] + g * kv_head_stride + d * kv_tile_keys
   const int32_t* pos;     // [M] RoPE position of each row
   const int64_t* k_off;   // [M]
   const int64_t* v_off;   // [M]
-  int64_t v_stride;
+  int64_t kv_head_stride; // elements between the heads of one slot (max_ctx * dh)
   const float2* rope;     // [max_pos, dh / 2] (cos, sin)
   int hq, hkv, dh;
   // Skinny GEMM split along K: fp32 partial sums and one arrival counter per
@@ -67,8 +67,8 @@ hipError_t launch_gemm_skinny(int epi, const GemmArgs& a, hipStream_t s);
 
 struct AttnArgs {
   const uint16_t* q;        // [T, hq, dh]
-  const uint16_t* kstore;   // token-major keys
-  const uint16_t* vstore;   // dimension-major values
+  const uint16_t* kstore;   // keys, layout as the cache (kv_tile_keys)
+  const uint16_t* vstore;   // values in transposed tiles, layout as the cache
   uint16_t* o;              // [T, hq * dh]
   const int32_t* items;     // [n_items][2] = (sequence, first query row within it)
   int n_items;
@@ -76,8 +76,8 @@ struct AttnArgs {
   const int32_t* seq_len;   // [B] query rows
   const int32_t* seq_ctx;   // [B] cached rows before the chunk
   const int64_t* seq_kbase; // [B] element offset of key position 0 (head 0)
-  const int64_t* seq_vbase; // [B] element offset of value position 0 (head 0, dim 0)
-  int64_t v_stride;
+  const int64_t* seq_vbase; // [B] element offset of value position 0 (head 0, dim 0), tile aligned
+  int64_t kv_head_stride;
   int hq, hkv, dh;
   float scale_log2;         // log2(e) / sqrt(dh)
 };
@@ -99,14 +99,14 @@ static_assert(sizeof(DecItem) == 32, "decode item record");
 
 struct DecodeAttnArgs {
   const uint16_t* q;
-  const uint16_t* kstore;   // token-major keys
-  const uint16_t* vstore;   // dimension-major values
+  const uint16_t* kstore;   // keys, layout as the cache (kv_tile_keys)
+  const uint16_t* vstore;   // values in transposed tiles, layout as the cache
   uint16_t* o;
   const DecItem* items;
   int n_items;
   float* part;              // [n_items][hkv][dec_part_floats] partial states of split rows
   int32_t* counters;        // [n_items * hkv] arrival counters (first item of a row), zero on entry and exit
-  int64_t v_stride;
+  int64_t kv_head_stride;
   int hq, hkv, dh;
   float scale_log2;
 };

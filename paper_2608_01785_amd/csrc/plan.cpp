@@ -154,9 +154,12 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
   w.meta = take(w.meta_bytes);
   w.n = take(size_t(T) * d * 2);
   w.q = take(size_t(T) * hq * dh * 2);
-  w.kpack = take(size_t(T + 64) * hkv * dh * 2);
-  w.v_stride = int64_t(align_up(size_t(T), 64)) + 64;
-  w.vpack = take(size_t(hkv) * dh * size_t(w.v_stride) * 2);
+  // Packed keys/values: sequence b starts at the 64-aligned position
+  // sum_{b' < b} round_up(len_b', 64); 64 more positions cover the last
+  // tile's overhang.
+  w.packed_ctx = int64_t(align_up(size_t(T) + 64 * size_t(B), 64)) + 64;
+  w.kpack = take(size_t(hkv) * size_t(w.packed_ctx) * dh * 2);
+  w.vpack = take(size_t(hkv) * size_t(w.packed_ctx) * dh * 2);
   w.o = take(size_t(T) * hq * dh * 2);
   w.h = take(size_t(T) * d * 4);
   w.a = take(size_t(T) * f * 2);
@@ -235,37 +238,36 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   auto i32 = [&](size_t at) { return reinterpret_cast<int32_t*>(P.image.data() + at); };
   auto i64 = [&](size_t at) { return reinterpret_cast<int64_t*>(P.image.data() + at); };
 
-  if (kv.cache) {
-    P.v_stride = kv.max_ctx;
-  } else {
-    P.v_stride = kv.packed_v_stride;
-  }
-  const int64_t slot_k = int64_t(kv.max_ctx) * hkv * dh;  // elements per cache slot (K)
-  const int64_t slot_v = hkv * dh * int64_t(kv.max_ctx);  // elements per cache slot (V)
+  // Cache: slot b holds hkv heads of max_ctx positions.  Packed (no cache):
+  // one slot of packed_ctx positions in which sequence b starts at the
+  // 64-aligned position base_b, so its key tiles line up with the value
+  // tiles.  Position p of a sequence: key element (base + p) * dh of head 0,
+  // value element ((base + p) / 32) * 32 dh + (base + p) % 32.
+  const int64_t slot_ctx = kv.cache ? kv.max_ctx : kv.packed_ctx;
+  P.kv_head_stride = slot_ctx * dh;
+  const int64_t slot = hkv * slot_ctx * dh;  // elements per cache slot (K and V alike)
+  constexpr int64_t VT = kv_tile_keys;
+  int64_t packed_base = 0;
   for (int32_t b = 0; b < B; ++b) {
     const int32_t cx = ctx ? ctx[b] : 0;
+    const int32_t len = off[b + 1] - off[b];
     i32(P.seq_start)[b] = off[b];
-    i32(P.seq_len)[b] = off[b + 1] - off[b];
+    i32(P.seq_len)[b] = len;
     i32(P.seq_ctx)[b] = cx;
-    if (kv.cache) {
-      i64(P.seq_kbase)[b] = int64_t(b) * slot_k;
-      i64(P.seq_vbase)[b] = int64_t(b) * slot_v;
-    } else {
-      i64(P.seq_kbase)[b] = int64_t(off[b]) * hkv * dh;
-      i64(P.seq_vbase)[b] = off[b];
-    }
+    const int64_t base = kv.cache ? int64_t(b) * slot : packed_base * dh;  // element of position 0, head 0
+    i64(P.seq_kbase)[b] = base;
+    i64(P.seq_vbase)[b] = base;
     for (int32_t t = off[b]; t < off[b + 1]; ++t) {
-      const int32_t pos = cx + (t - off[b]);
-      i32(P.pos)[t] = pos;
-      if (kv.cache) {
-        i64(P.k_off)[t] = (int64_t(b) * kv.max_ctx + pos) * hkv * dh;
-        i64(P.v_off)[t] = int64_t(b) * slot_v + pos;
-      } else {
-        i64(P.k_off)[t] = int64_t(t) * hkv * dh;
-        i64(P.v_off)[t] = t;
-      }
+      const int64_t pos = cx + (t - off[b]);
+      i32(P.pos)[t] = int32_t(pos);
+      i64(P.k_off)[t] = base + pos * dh;
+      i64(P.v_off)[t] = base + (pos / VT) * VT * dh + pos % VT;
     }
+    if (!kv.cache) packed_base += int64_t(align_up(size_t(len), 64));
   }
+  if (!kv.cache && packed_base + 64 > kv.packed_ctx)
+    return fail(HS_ERR_INTERNAL, "packed keys need %lld positions, %lld planned", (long long)(packed_base + 64),
+                (long long)kv.packed_ctx);
   for (int32_t i = 0; i < P.n_att_items; ++i) {
     i32(P.att_items)[2 * i] = att[i].b;
     i32(P.att_items)[2 * i + 1] = att[i].q0;

@@ -35,9 +35,9 @@ struct WsLayout {
   size_t meta_bytes;
   size_t n;           // [T, d] normalised rows
   size_t q;           // [T, hq, dh]
-  size_t kpack;       // [T + 64, hkv, dh]   keys when no cache is given
-  size_t vpack;       // [hkv, dh, v_stride] values when no cache is given
-  int64_t v_stride;   // round_up(T, 64) + 64
+  size_t kpack;       // keys when no cache is given: one slot of packed_ctx positions
+  size_t vpack;       // values when no cache is given, same
+  int64_t packed_ctx; // positions of that slot: every sequence starts 64-aligned, plus 64
   size_t o;           // [T, hq * dh]
   size_t h;           // [T, d] fp32 residual after attention
   size_t a;           // [T, ffn]
@@ -68,14 +68,14 @@ struct Plan {
   size_t dec_items = 0;  // [n_dec_items] 32-byte records (row, keys, split, splits, K base, V base)
   size_t dec_count = 0;  // [n_dec_items * hkv] arrival counters, zero in the image
   int32_t n_att_items = 0, n_dec_rows = 0, n_counters = 0, n_dec_items = 0;
-  int64_t v_stride = 0;
+  int64_t kv_head_stride = 0;
 };
 
 // Key/value placement: packed (no cache, rows in the workspace) or cache slots.
 struct KvPlacement {
   bool cache = false;
   int32_t max_ctx = 0;
-  int64_t packed_v_stride = 0;
+  int64_t packed_ctx = 0;
 };
 
 hs_status build_plan(const hs_layer_cfg& c, const int32_t* seq_offsets, const int32_t* ctx_lens,

@@ -229,7 +229,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
   const hs::WsLayout lay = hs::ws_layout(*cfg, T, n_seqs, max_pos);
   if (ws_bytes < lay.total)
     return hs::fail(HS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, lay.total);
-  place.packed_v_stride = lay.v_stride;
+  place.packed_ctx = lay.packed_ctx;
   hs::Plan plan;
   st = hs::build_plan(*cfg, seq_offsets, ctx_lens, n_seqs, place, &plan);
   if (st != HS_OK) return st;
@@ -295,7 +295,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     g.pos = d_pos;
     g.k_off = d_koff;
     g.v_off = d_voff;
-    g.v_stride = plan.v_stride;
+    g.kv_head_stride = plan.kv_head_stride;
     g.rope = rope;
     g.hq = hq;
     g.hkv = hkv;
@@ -315,7 +315,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     at_args.seq_ctx = reinterpret_cast<const int32_t*>(meta + plan.seq_ctx);
     at_args.seq_kbase = reinterpret_cast<const int64_t*>(meta + plan.seq_kbase);
     at_args.seq_vbase = reinterpret_cast<const int64_t*>(meta + plan.seq_vbase);
-    at_args.v_stride = plan.v_stride;
+    at_args.kv_head_stride = plan.kv_head_stride;
     at_args.hq = hq;
     at_args.hkv = hkv;
     at_args.dh = dh;
@@ -331,7 +331,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     da.n_items = plan.n_dec_items;
     da.part = lay.dec_part_bytes ? at<float>(ws, lay.dec_part) : nullptr;
     da.counters = reinterpret_cast<int32_t*>(meta + plan.dec_count);
-    da.v_stride = plan.v_stride;
+    da.kv_head_stride = plan.kv_head_stride;
     da.hq = hq;
     da.hkv = hkv;
     da.dh = dh;

@@ -1,10 +1,10 @@
 """Device-side placement of seeded inputs (data layout only, no layer arithmetic).
 
 Moves generator output (raw bf16 bits) into torch device tensors and builds
-key/value caches in the layout the library expects:
+key/value caches in the layout the library expects (fp16, per layer):
 
-* K: fp16 [n_slots, max_ctx, Hkv, dh]   (token-major)
-* V: fp16 [n_slots, Hkv, dh, max_ctx]   (dimension-major)
+* K: [n_slots, Hkv, max_ctx, dh]              (key rows of a head contiguous)
+* V: [n_slots, Hkv, max_ctx / 32, dh, 32]     (values transposed in 32-key tiles)
 """
 from __future__ import annotations
 
@@ -61,6 +61,8 @@ def prepare_f16(ctx, layers_dev: List[Dict[str, torch.Tensor]]) -> List[Dict[str
 class DeviceCache:
     """Per-layer K/V device tensors for n_slots sequences of up to max_ctx positions."""
 
+    TILE = 32  # keys per value tile
+
     def __init__(self, n_layers: int, n_slots: int, max_ctx: int, n_kv_heads: int, head_dim: int,
                  device="cuda", fill: Optional[float] = None):
         assert max_ctx % 64 == 0
@@ -68,19 +70,29 @@ class DeviceCache:
         self.hkv, self.dh = n_kv_heads, head_dim
         mk = (lambda shape: torch.full(shape, fill, dtype=torch.float16, device=device)) if fill is not None \
             else (lambda shape: torch.empty(shape, dtype=torch.float16, device=device))
-        self.k = [mk((n_slots, max_ctx, n_kv_heads, head_dim)) for _ in range(n_layers)]
-        self.v = [mk((n_slots, n_kv_heads, head_dim, max_ctx)) for _ in range(n_layers)]
+        self.k = [mk((n_slots, n_kv_heads, max_ctx, head_dim)) for _ in range(n_layers)]
+        self.v = [mk((n_slots, n_kv_heads, max_ctx // self.TILE, head_dim, self.TILE)) for _ in range(n_layers)]
 
     def as_arg(self):
         return (self.k, self.v, self.n_slots, self.max_ctx)
 
+    def _put(self, layer: int, slot: int, k: torch.Tensor, v: torch.Tensor) -> None:
+        """Store logical [n, Hkv, dh] fp16 rows at positions 0..n-1 (later positions untouched)."""
+        n, T = k.shape[0], self.TILE
+        self.k[layer][slot, :, :n] = k.permute(1, 0, 2)
+        full = n // T
+        vt = v.permute(1, 0, 2)  # [Hkv, n, dh]
+        if full:
+            self.v[layer][slot, :, :full] = vt[:, :full * T].reshape(self.hkv, full, T, self.dh).transpose(2, 3)
+        if n % T:
+            self.v[layer][slot, :, full, :, :n % T] = vt[:, full * T:].transpose(1, 2)
+
     def load_prefix(self, layer: int, slot: int, k_bits: np.ndarray, v_bits: np.ndarray) -> None:
         """Place logical [n, Hkv, dh] rows at positions 0..n-1 of a slot."""
-        n = k_bits.shape[0]
-        if n == 0:
+        if k_bits.shape[0] == 0:
             return
-        self.k[layer][slot, :n] = to_device_f16(k_bits, self.k[layer].device)
-        self.v[layer][slot, :, :, :n] = to_device_f16(v_bits, self.v[layer].device).permute(1, 2, 0)
+        dev = self.k[layer].device
+        self._put(layer, slot, to_device_f16(k_bits, dev), to_device_f16(v_bits, dev))
 
     def fill_random(self, layer: int, slot: int, n: int, gen: torch.Generator) -> None:
         """Seeded N(0, 1) rows (torch's device generator, rounded to fp16) at positions 0..n-1."""
@@ -88,11 +100,11 @@ class DeviceCache:
             return
         dev = self.k[layer].device
         kv = torch.randn((2, n, self.hkv, self.dh), generator=gen, device=dev, dtype=torch.float32)
-        self.k[layer][slot, :n] = kv[0].to(torch.float16)
-        self.v[layer][slot, :, :, :n] = kv[1].to(torch.float16).permute(1, 2, 0)
+        self._put(layer, slot, kv[0].to(torch.float16), kv[1].to(torch.float16))
 
     def rows(self, layer: int, slot: int, start: int, stop: int):
         """Logical [stop - start, Hkv, dh] K and V rows as fp16 bits on the host."""
-        k = f16_bits_of(self.k[layer][slot, start:stop])
-        v = f16_bits_of(self.v[layer][slot, :, :, start:stop].permute(2, 0, 1))
+        k = f16_bits_of(self.k[layer][slot, :, start:stop].permute(1, 0, 2))
+        v_all = self.v[layer][slot].transpose(2, 3).reshape(self.hkv, self.max_ctx, self.dh)
+        v = f16_bits_of(v_all[:, start:stop].permute(1, 0, 2))
         return k, v
