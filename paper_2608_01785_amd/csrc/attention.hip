@@ -206,13 +206,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
   const float inv = 1.0f / l_tot;
   const int qw = q0 + wave * 32 + fr;
   if (qw < len) {
-    uint16_t* op = a.o + int64_t(row0 + qw) * (a.hq * DH) + head * DH + 4 * fh;
 #pragma unroll
     for (int i = 0; i < NDS; ++i)
 #pragma unroll
       for (int gq = 0; gq < 4; ++gq)
-        store_h4(op + 32 * i + 8 * gq, o[i][4 * gq] * inv, o[i][4 * gq + 1] * inv, o[i][4 * gq + 2] * inv,
-                 o[i][4 * gq + 3] * inv);
+        store_h4(a.o + act_index(row0 + qw, head * DH + 32 * i + 8 * gq + 4 * fh, a.hq * DH, a.o_k8_rows),
+                 o[i][4 * gq] * inv, o[i][4 * gq + 1] * inv, o[i][4 * gq + 2] * inv, o[i][4 * gq + 3] * inv);
   }
 }
 

@@ -241,7 +241,7 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
       den += sc * red_l[w][q];
     }
     if (n_split == 1) {
-      st_u16<false>(a.o + int64_t(t) * a.hq * DH + (g * G + q) * DH + d, f2h(num / den));
+      a.o[act_index(t, (g * G + q) * DH + d, a.hq * DH, a.o_k8_rows)] = f2h(num / den);
     } else {
       // Publish (unnormalised output, maximum, sum) with device-scope stores.
       float* st = a.part + (int64_t(item) * a.hkv + g) * pf_stride;
@@ -297,7 +297,7 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
       }
       M = bm;
     }
-    st_u16<false>(a.o + int64_t(t) * a.hq * DH + (g * G + q) * DH + (idx % DH), f2h(num / den));
+    a.o[act_index(t, (g * G + q) * DH + idx % DH, a.hq * DH, a.o_k8_rows)] = f2h(num / den);
   }
 }
 

@@ -68,6 +68,14 @@ __device__ __forceinline__ void store_h4(uint16_t* p, float a, float b, float c,
   *reinterpret_cast<u32x2*>(p) = v;
 }
 
+// Element offset of activation (m, k): row-major with row stride ld, or, when
+// k8_rows > 0, k-group-major ((k / 8) * k8_rows + m) * 8 + k % 8, the layout
+// in which a 32-row MFMA operand fragment of 8 k values per lane is one
+// contiguous 512-byte run.
+__device__ __forceinline__ int64_t act_index(int m, int k, int ld, int k8_rows) {
+  return k8_rows ? (int64_t(k >> 3) * k8_rows + m) * 8 + (k & 7) : int64_t(m) * ld + k;
+}
+
 // MFMA row i of a 32-key subtile reads key perm32(i): bits 2 and 3 swapped.
 __device__ __forceinline__ int perm32(int i) {
   return (i & ~12) | ((i >> 1) & 4) | ((i << 1) & 8);

@@ -16,12 +16,12 @@ enum Epilogue : int {
 };
 
 struct GemmArgs {
-  const uint16_t* A;  // activations [M, K] fp16 row-major
+  const uint16_t* A;  // activations [M, K] fp16: row-major, or k-group-major when k8_rows > 0
   const uint16_t* W;  // weights [N, K] row-major, bf16 (w_f16 = 0) or fp16 (w_f16 = 1)
   int w_f16;
   int M, K;
   int n_tiles_n;      // output tiles along N (256 weight rows each; 128 outputs for SWIGLU)
-  uint16_t* out;      // SWIGLU output (fp16), row stride ldo
+  uint16_t* out;      // SWIGLU output (fp16), row stride ldo, or k-group-major when k8_rows > 0
   float* out_f32;     // RESID output (fp32), row stride ldo
   int ldo;
   const uint16_t* resid;     // RESID: bf16 residual input with row stride ldo, or
@@ -47,7 +47,7 @@ struct GemmArgs {
   // (sumsq_out[m * strips + strip]) and the residual times a per-column gain
   // in fp16 (scaled_out, row stride ldo).
   float* sumsq_out;
-  uint16_t* scaled_out;
+  uint16_t* scaled_out;      // row stride ldo, or k-group-major when k8_rows > 0
   const uint16_t* gain;      // bf16 [ldo]
   // QKV / SWIGLU, optional: row m of the product is multiplied by
   // rsqrt(sum_p row_sumsq[m * row_parts + p] / K + eps) before RoPE or SiLU
@@ -55,6 +55,9 @@ struct GemmArgs {
   const float* row_sumsq;
   int row_parts;
   float eps;
+  // Skinny GEMM only: A, out and scaled_out are k-group-major with this many
+  // padded rows (skinny_k8_rows(M)); 0 = row-major.
+  int k8_rows;
 };
 
 // The large GEMM does not take the folded-RMSNorm fields (they must be null).
@@ -69,7 +72,8 @@ struct AttnArgs {
   const uint16_t* q;        // [T, hq, dh]
   const uint16_t* kstore;   // keys, layout as the cache (kv_tile_keys)
   const uint16_t* vstore;   // values in transposed tiles, layout as the cache
-  uint16_t* o;              // [T, hq * dh]
+  uint16_t* o;              // [T, hq * dh], k-group-major when o_k8_rows > 0
+  int o_k8_rows;
   const int32_t* items;     // [n_items][2] = (sequence, first query row within it)
   int n_items;
   const int32_t* seq_start; // [B] first packed row
@@ -101,7 +105,8 @@ struct DecodeAttnArgs {
   const uint16_t* q;
   const uint16_t* kstore;   // keys, layout as the cache (kv_tile_keys)
   const uint16_t* vstore;   // values in transposed tiles, layout as the cache
-  uint16_t* o;
+  uint16_t* o;               // [T, hq * dh], k-group-major when o_k8_rows > 0
+  int o_k8_rows;
   const DecItem* items;
   int n_items;
   float* part;              // [n_items][hkv][dec_part_floats] partial states of split rows
@@ -113,9 +118,10 @@ struct DecodeAttnArgs {
 
 hipError_t launch_decode_attention(const DecodeAttnArgs& a, hipStream_t s);
 
-// x is bf16 (x_f32 null) or fp32 (x_f32 non-null); y is fp16.
+// x is bf16 (x_f32 null) or fp32 (x_f32 non-null); y is fp16, row-major or
+// k-group-major with k8_rows padded rows (k8_rows > 0).
 hipError_t launch_rmsnorm(const uint16_t* x, const float* x_f32, const uint16_t* gamma, uint16_t* y, int rows,
-                          int d, float eps, int max_blocks, hipStream_t s);
+                          int d, float eps, int k8_rows, int max_blocks, hipStream_t s);
 
 hipError_t launch_rope_table(float2* tab, int max_pos, int dh, float base, hipStream_t s);
 

@@ -12,7 +12,8 @@ constexpr int kMaxChunksPerLane = 16;  // hidden <= 64 lanes * 16 chunks * 8 = 8
 // two passes; loads are 16 bytes wide.
 template <typename TIn>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const TIn* __restrict__ x, const uint16_t* __restrict__ gamma,
-                                                      uint16_t* __restrict__ y, int rows, int d, float eps) {
+                                                      uint16_t* __restrict__ y, int rows, int d, float eps,
+                                                      int k8_rows) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int chunks = d >> 3;  // 8 elements per chunk
@@ -47,7 +48,6 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const TIn* __restrict__ x,
     }
     ss = wave_sum(ss);
     const float r = rsqrtf(ss * inv_d + eps);
-    uint16_t* yr = y + int64_t(row) * d;
 #pragma unroll
     for (int i = 0; i < kMaxChunksPerLane; ++i) {
       const int c = lane + 64 * i;
@@ -60,7 +60,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const TIn* __restrict__ x,
           const float hi = v[i][2 * e + 1] * r * __uint_as_float(gv[e] & 0xffff0000u);
           out[e] = pack2h(lo, hi);
         }
-        *reinterpret_cast<u32x4*>(yr + c * 8) = out;
+        *reinterpret_cast<u32x4*>(y + act_index(row, c * 8, d, k8_rows)) = out;
       }
     }
   }
@@ -127,14 +127,14 @@ hipError_t launch_convert_bf16_f16(const uint16_t* src, uint16_t* dst, int64_t r
 }
 
 hipError_t launch_rmsnorm(const uint16_t* x, const float* x_f32, const uint16_t* gamma, uint16_t* y, int rows,
-                          int d, float eps, int max_blocks, hipStream_t s) {
+                          int d, float eps, int k8_rows, int max_blocks, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   int grid = (rows + 3) / 4;
   if (grid > max_blocks) grid = max_blocks;
   if (x_f32)
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(grid), dim3(256), 0, s, x_f32, gamma, y, rows, d, eps);
+    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(grid), dim3(256), 0, s, x_f32, gamma, y, rows, d, eps, k8_rows);
   else
-    hipLaunchKernelGGL(rmsnorm_kernel<uint16_t>, dim3(grid), dim3(256), 0, s, x, gamma, y, rows, d, eps);
+    hipLaunchKernelGGL(rmsnorm_kernel<uint16_t>, dim3(grid), dim3(256), 0, s, x, gamma, y, rows, d, eps, k8_rows);
   return hipGetLastError();
 }
 

@@ -152,7 +152,9 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
   const int64_t dec_items = max_dec_items(T, B, max_pos, c.head_dim);
   w.meta_bytes = meta_bytes(T, B, max_att_items(T, B), sk.counters, dec_items, dec_items * c.n_kv_heads);
   w.meta = take(w.meta_bytes);
-  w.n = take(size_t(T) * d * 2);
+  // GEMM inputs of decode-sized batches are k-group-major over padded rows.
+  const size_t act_rows = T <= kSkinnyMaxRows ? size_t(skinny_k8_rows(T)) : size_t(T);
+  w.n = take(act_rows * d * 2);
   w.q = take(size_t(T) * hq * dh * 2);
   // Packed keys/values: sequence b starts at the 64-aligned position
   // sum_{b' < b} round_up(len_b', 64); 64 more positions cover the last
@@ -160,9 +162,9 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
   w.packed_ctx = int64_t(align_up(size_t(T) + 64 * size_t(B), 64)) + 64;
   w.kpack = take(size_t(hkv) * size_t(w.packed_ctx) * dh * 2);
   w.vpack = take(size_t(hkv) * size_t(w.packed_ctx) * dh * 2);
-  w.o = take(size_t(T) * hq * dh * 2);
+  w.o = take(act_rows * hq * dh * 2);
   w.h = take(size_t(T) * d * 4);
-  w.a = take(size_t(T) * f * 2);
+  w.a = take(act_rows * f * 2);
   w.xtmp = take(size_t(T) * d * 4);
   w.sumsq = take(size_t(T) * (d / 32) * 4);
   w.rope = take(size_t(max_pos) * (dh / 2) * 8);

@@ -261,6 +261,9 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
   float* sumsq = at<float>(ws, lay.sumsq);
   const int norm_parts = d / 32;
   bool folded = false;  // n_buf holds x * gain, sumsq its partial sums
+  // Decode-sized batches keep the GEMM inputs (normed rows, attention output,
+  // SwiGLU output) k-group-major, the skinny GEMM's operand layout.
+  const int k8 = T <= hs::kSkinnyMaxRows ? hs::skinny_k8_rows(T) : 0;
 
   TIMED(HS_KERNEL_ROPE_TABLE, hs::launch_rope_table(rope, max_pos, dh, cfg->rope_base, s));
 
@@ -279,7 +282,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
 
     if (!folded)
       TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(x_cur, x_cur_f32, static_cast<const uint16_t*>(w[l].ln1), n_buf,
-                                                  T, d, cfg->rms_eps, 4 * budget, s));
+                                                  T, d, cfg->rms_eps, k8, 4 * budget, s));
     hs::GemmArgs g{};
     g.part = sk_part;
     g.counters = sk_count;
@@ -300,6 +303,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     g.hq = hq;
     g.hkv = hkv;
     g.dh = dh;
+    g.k8_rows = k8;
     if (folded) use_norm(g, sumsq, norm_parts, cfg->rms_eps);
     TIMED(HS_KERNEL_QKV, gemm(hs::EPI_QKV, g, grid_cap, s));
 
@@ -308,6 +312,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     at_args.kstore = kstore;
     at_args.vstore = vstore;
     at_args.o = o_buf;
+    at_args.o_k8_rows = k8;
     at_args.items = reinterpret_cast<const int32_t*>(meta + plan.att_items);
     at_args.n_items = plan.n_att_items;
     at_args.seq_start = reinterpret_cast<const int32_t*>(meta + plan.seq_start);
@@ -327,6 +332,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     da.kstore = kstore;
     da.vstore = vstore;
     da.o = o_buf;
+    da.o_k8_rows = k8;
     da.items = reinterpret_cast<const hs::DecItem*>(meta + plan.dec_items);
     da.n_items = plan.n_dec_items;
     da.part = lay.dec_part_bytes ? at<float>(ws, lay.dec_part) : nullptr;
@@ -351,6 +357,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     go.ldo = d;
     go.resid = x_cur;
     go.resid_f32 = x_cur_f32;
+    go.k8_rows = k8;
     // Fold when every GEMM of the layer takes the skinny path.
     // Fold when every GEMM of the layer takes the skinny path (gate/up and
     // down share M, and their K are multiples of 64) and a consumer can
@@ -361,7 +368,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     TIMED(HS_KERNEL_O_PROJ, gemm(hs::EPI_RESID, go, grid_cap, s));
     if (!fold)
       TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(nullptr, h_buf, static_cast<const uint16_t*>(w[l].ln2), n_buf, T,
-                                                  d, cfg->rms_eps, 4 * budget, s));
+                                                  d, cfg->rms_eps, k8, 4 * budget, s));
 
     hs::GemmArgs gu{};
     gu.part = sk_part;
@@ -375,6 +382,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     gu.out = a_buf;
     gu.ldo = f;
     gu.ffn = f;
+    gu.k8_rows = k8;
     if (fold) use_norm(gu, sumsq, norm_parts, cfg->rms_eps);
     TIMED(HS_KERNEL_GATE_UP, gemm(hs::EPI_SWIGLU, gu, grid_cap, s));
 
@@ -390,6 +398,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     gd.out_f32 = x_next;
     gd.ldo = d;
     gd.resid_f32 = h_buf;
+    gd.k8_rows = k8;
     folded = fold && l + 1 < n_layers;
     if (folded) fold_norm(gd, sumsq, n_buf, w[l + 1].ln1);
     TIMED(HS_KERNEL_DOWN, gemm(hs::EPI_RESID, gd, grid_cap, s));

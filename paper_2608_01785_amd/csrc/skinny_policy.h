@@ -20,6 +20,11 @@ constexpr int kSkinnyMaxNormParts = 64;  // folded RMSNorm: partial sums per row
 // 32-row activation subtiles covering M rows (1, 2 or 4).
 inline int skinny_m_tiles(int M) { return M <= 32 ? 1 : (M <= 64 ? 2 : 4); }
 
+// Activations of decode-sized batches are stored k-group-major with this many
+// (padded) rows: element (m, k) at ((k / 8) * rows + m) * 8 + k % 8.  Rows
+// M .. rows - 1 are never written; the GEMM discards their products.
+inline int skinny_k8_rows(int M) { return 32 * skinny_m_tiles(M); }
+
 struct SkinnySplit {
   int splits;  // blocks along K per weight strip
   int per;     // K stages per split (the last split may hold fewer)

@@ -91,25 +91,44 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
       if (4 * u < a.row_parts)
         pre[u] = __builtin_amdgcn_raw_buffer_load_b128(pr, row_off + uint32_t(u * 16), 0, 0);
   }
-  // Residual of the RESID epilogue, loaded now so that it is in registers by
-  // the epilogue (wave w owns rows 32 w .. 32 w + 31 there).
+  // Operands of the epilogue that do not depend on the product, loaded now
+  // so that they are in registers by then (wave w owns rows 32 w .. 32 w + 31
+  // there): RESID the residual and the next norm's gains; QKV the row's
+  // position, cache offsets and RoPE table entries (issued after the first
+  // chunk's loads, see below).
   f32x4 res_pre[EPI == EPI_RESID ? NS : 1][4];
+  f32x4 gain_pre[EPI == EPI_RESID ? NS : 1][4];
+  const int m_own = wave * 32 + fr;
+  const bool row_own = wave < MT && m_own < a.M;
   if constexpr (EPI == EPI_RESID) {
-    const int m = wave * 32 + fr;
-    if (wave < MT && m < a.M) {
+    if (row_own) {
 #pragma unroll
       for (int i = 0; i < NS; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int n = tile * NR + i * 32 + 8 * g + 4 * fh;
           if (a.resid_f32) {
-            res_pre[i][g] = *reinterpret_cast<const f32x4*>(a.resid_f32 + int64_t(m) * a.ldo + n);
+            res_pre[i][g] = *reinterpret_cast<const f32x4*>(a.resid_f32 + int64_t(m_own) * a.ldo + n);
           } else {
             float r4[4];
-            load_bf16x4(a.resid + int64_t(m) * a.ldo + n, r4);
+            load_bf16x4(a.resid + int64_t(m_own) * a.ldo + n, r4);
             res_pre[i][g] = f32x4{r4[0], r4[1], r4[2], r4[3]};
           }
+          if (a.scaled_out) {
+            float gm[4];
+            load_bf16x4(a.gain + n, gm);
+            gain_pre[i][g] = f32x4{gm[0], gm[1], gm[2], gm[3]};
+          }
         }
+    }
+  }
+  int qkv_pos = 0;
+  int64_t qkv_koff = 0, qkv_voff = 0;
+  if constexpr (EPI == EPI_QKV) {
+    if (row_own) {
+      qkv_pos = a.pos[m_own];
+      qkv_koff = a.k_off[m_own];
+      qkv_voff = a.v_off[m_own];
     }
   }
   const int kt0 = ks * a.k_per_split;
@@ -118,7 +137,8 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
 
   const uint32_t w_rows = (EPI == EPI_SWIGLU) ? uint32_t(2 * a.ffn) : uint32_t(a.n_tiles_n * 256);
   const __amdgpu_buffer_rsrc_t wres = make_rsrc(a.W, w_rows * row_bytes);
-  const __amdgpu_buffer_rsrc_t xres = make_rsrc(a.A, uint32_t(a.M) * row_bytes);
+  const __amdgpu_buffer_rsrc_t xres =
+      make_rsrc(a.A, a.k8_rows ? uint32_t(a.K) * uint32_t(a.k8_rows) * 2 : uint32_t(a.M) * row_bytes);
 
   // Fragments go from memory straight into registers in MFMA operand layout.
   // The split's K range is cut into 32-wide panels; wave w takes panels w,
@@ -135,8 +155,15 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
     const uint32_t r = strip_row<EPI, NR, DH>(tile, i * 32 + fr, a.ffn);
     w_off[i] = (W_F16 ? r * 64u : r * row_bytes) + uint32_t(fh * 16);
   }
+  // Activations row-major: a step is 32 bytes along the row, a panel 64.
+  // k-group-major (k8_rows padded rows): a fragment is 512 contiguous bytes,
+  // a step 2 k-groups and a panel 4.
+  const int k8 = a.k8_rows;
 #pragma unroll
-  for (int j = 0; j < MT; ++j) x_off[j] = uint32_t(j * 32 + fr) * row_bytes + uint32_t(fh * 16);
+  for (int j = 0; j < MT; ++j)
+    x_off[j] = k8 ? uint32_t((fh * k8 + j * 32 + fr) * 16) : uint32_t(j * 32 + fr) * row_bytes + uint32_t(fh * 16);
+  const uint32_t x_step = k8 ? uint32_t(2 * k8 * 16) : 32u;
+  const uint32_t x_panel = k8 ? uint32_t(4 * k8 * 16) : 64u;
   const uint32_t panel_bytes = w_rows * 64;
   const int n_panels = 2 * KT;
   const int my_panels = n_panels > wave ? (n_panels - wave + 3) / 4 : 0;
@@ -170,7 +197,7 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
           b.w[q][s][i] = __builtin_amdgcn_raw_buffer_load_b128(wr, w_off[i] + 32 * s, wso, 0);
 #pragma unroll
         for (int j = 0; j < MT; ++j)
-          b.x[q][s][j] = __builtin_amdgcn_raw_buffer_load_b128(xr, x_off[j] + 32 * s, P * 64u, 0);
+          b.x[q][s][j] = __builtin_amdgcn_raw_buffer_load_b128(xr, x_off[j] + x_step * s, P * x_panel, 0);
       }
     }
   };
@@ -193,6 +220,17 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
   // barriers keep each chunk's loads ahead of the previous chunk's MFMAs.
   Chunk b0, b1;
   load_chunk(0, b0);
+  // QKV: the RoPE table entries of this lane's dimension pairs.
+  float2 rope_pre[EPI == EPI_QKV ? 8 : 1];
+  if constexpr (EPI == EPI_QKV) {
+    if (row_own) {
+      const float2* rt = a.rope + int64_t(qkv_pos) * (DH / 2) + 16 * (tile % (DH / 32)) + 4 * fh;
+#pragma unroll
+      for (int g = 0; g < 2; ++g)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) rope_pre[4 * g + e] = rt[8 * g + e];
+    }
+  }
   __builtin_amdgcn_sched_barrier(0);
   int ch = 0;
   for (; ch + 2 < n_chunks; ch += 2) {
@@ -313,9 +351,9 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
           *reinterpret_cast<f32x4*>(orow + n) = v;
           ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
           if (a.scaled_out) {
-            float gm[4];
-            load_bf16x4(a.gain + n, gm);
-            st_h4<false>(a.scaled_out + int64_t(m) * a.ldo + n, v[0] * gm[0], v[1] * gm[1], v[2] * gm[2], v[3] * gm[3]);
+            const f32x4 gm = gain_pre[i][g];
+            store_h4(a.scaled_out + act_index(m, n, a.ldo, a.k8_rows), v[0] * gm[0], v[1] * gm[1], v[2] * gm[2],
+                     v[3] * gm[3]);
           }
         }
       if (a.sumsq_out) {
@@ -352,14 +390,12 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
       float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) v[e] = silu(c[0][4 * g + e]) * c[1][4 * g + e];
-      st_h4<false>(a.out + int64_t(m) * a.ldo + tile * 32 + 8 * g + 4 * fh, v[0], v[1], v[2], v[3]);
+      store_h4(a.out + act_index(m, tile * 32 + 8 * g + 4 * fh, a.ldo, a.k8_rows), v[0], v[1], v[2], v[3]);
     }
   } else {  // EPI_QKV: a strip holds 16 dimensions of one head and their RoPE partners
     static_assert(EPI != EPI_QKV || NS == 1, "QKV strips are 32 rows");
     constexpr int SPH = DH / 32;
     const int head = tile / SPH, sub = tile % SPH;
-    const int p = a.pos[m];
-    const float2* rt = a.rope + int64_t(p) * (DH / 2);
 #pragma unroll
     for (int g = 0; g < 2; ++g) {
       const int d = 16 * sub + 8 * g + 4 * fh;  // < DH / 2; partner d + DH / 2
@@ -367,18 +403,18 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
         float rl[4], rh[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float2 cs = rt[d + e];
+          const float2 cs = rope_pre[4 * g + e];
           const float lo = c[0][4 * g + e], hi = c[0][4 * (g + 2) + e];
           rl[e] = lo * cs.x - hi * cs.y;
           rh[e] = hi * cs.x + lo * cs.y;
         }
         uint16_t* dst = (head < a.hq) ? a.q + (int64_t(m) * a.hq + head) * DH
-                                      : a.kstore + a.k_off[m] + int64_t(head - a.hq) * a.kv_head_stride;
+                                      : a.kstore + qkv_koff + int64_t(head - a.hq) * a.kv_head_stride;
         store_h4(dst + d, rl[0], rl[1], rl[2], rl[3]);
         store_h4(dst + d + DH / 2, rh[0], rh[1], rh[2], rh[3]);
       } else {
         const int gh = head - a.hq - a.hkv;
-        uint16_t* dst = a.vstore + a.v_off[m] + int64_t(gh) * a.kv_head_stride;
+        uint16_t* dst = a.vstore + qkv_voff + int64_t(gh) * a.kv_head_stride;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           dst[(d + e) * kv_tile_keys] = f2h(c[0][4 * g + e]);
