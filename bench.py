@@ -75,6 +75,7 @@ def main():
     ap.add_argument("--budgets", type=str, default="64,128,192")
     ap.add_argument("--no-corun", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-controller", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows per sequence in the CPU-reference sample (0: sized to take about 15 s)")
     ap.add_argument("--quick", action="store_true", help="headline stack only (no budget sweep, co-run, CPU leg)")
@@ -94,8 +95,9 @@ def main():
     dev = "cuda:0"
     budgets = [int(b) for b in args.budgets.split(",") if b]
     if args.quick:
-        budgets, args.no_corun, args.no_cpu_baseline = [], True, True
-    ctx = binding.Context(0, budgets=sorted(set(budgets + [128, 256])))
+        budgets, args.no_corun, args.no_cpu_baseline, args.no_controller = [], True, True, True
+    ladder = sorted(set(budgets + [128, 256]))
+    ctx = binding.Context(0, budgets=ladder)
 
     # ---------------------------------------------------------------- thinker stack
     shape, n_layers = W.THINKER, 4
@@ -183,6 +185,11 @@ def main():
     if not args.no_corun:
         corun = corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flops_step)
 
+    # ---------------------------------------------------------------- spatial controller costs
+    controller = None
+    if not args.no_controller:
+        controller = controller_measure(torch, binding, ctx, [b for b in ladder if b < N_CUS], dev)
+
     # ---------------------------------------------------------------- CPU reference sample
     cpu = None
     if not args.no_cpu_baseline:
@@ -213,6 +220,7 @@ def main():
         "ms_per_step_bf16_weights": round(ms_bf16w, 4),
         "budgets": per_budget,
         "corun": corun,
+        "controller": controller,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
@@ -337,6 +345,79 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
     }
     log(f"[bench] co-run: prefill {window:.2f} ms (solo {prefill_solo:.2f}), decode {dec_ms:.3f} ms/step "
         f"(solo {solo_ms:.3f}), {n_in} steps in window")
+    return res
+
+
+def controller_measure(torch, binding, ctx, ladder, dev):
+    """Costs of the spatial controller's control path on the GPU machine.
+
+    * switch_us: extra GPU-side delay when consecutive dependent launches move
+      from the SHARED stream of one ladder level to that of another (an event
+      on the old stream, a wait on the new one), against staying on one stream.
+      Each launch is one probe work-group that spins ~20 us and stamps its
+      start on the constant-rate clock, so the host stays ahead of the GPU.
+    * switch_synced_us: the same when the host waits for each launch before
+      issuing the next (a serving loop reads every step's output), so the new
+      level's stream is idle when it receives work.
+    * decide_us: host time of one controller step plus the stream lookup.
+    * pressure_sample_us / pressure: one AMD SMI memory-activity reading.
+    """
+    n = 64
+    s_a = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_SHARED))
+    s_b = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 256, binding.HS_ROLE_SHARED))
+    out = torch.zeros((n, 4), dtype=torch.int32, device=dev)
+
+    def chain(alternate, synced=False):
+        torch.cuda.synchronize()
+        prev = s_a
+        for i in range(n):
+            cur = (s_a if i % 2 == 0 else s_b) if alternate else s_a
+            if cur is not prev and not synced:
+                ev = torch.cuda.Event()
+                ev.record(prev)
+                cur.wait_event(ev)
+            binding.hs_probe_hw_ids(ctx, cur.cuda_stream, 1, out[i])
+            if synced:
+                cur.synchronize()
+            prev = cur
+        torch.cuda.synchronize()
+        t = out[:, 3].cpu().numpy().astype(np.int64)
+        d = np.diff(t) % (1 << 32)
+        return float(np.median(d[1:])) / 100.0  # 100 MHz clock -> us
+
+    chain(False)
+    same = chain(False)
+    alt = chain(True)
+    same_synced = chain(False, synced=True)
+    alt_synced = chain(True, synced=True)
+
+    ctrl = binding.Controller(N_CUS, N_CUS, ladder, 0.4, 0.8, 1)
+    k = 20000
+    t0 = time.perf_counter()
+    for i in range(k):
+        sp = binding.hs_controller_step(ctrl, i % 3 != 0, (i % 10) / 10.0)
+        binding.hs_context_stream(ctx, sp.shared_cus, binding.HS_ROLE_SHARED)
+    decide_us = (time.perf_counter() - t0) / k * 1e6
+    ctrl.close()
+
+    pressure, sample_us = None, None
+    try:
+        binding.hs_pressure_sample(0)
+        t0 = time.perf_counter()
+        for _ in range(200):
+            pressure = binding.hs_pressure_sample(0)
+        sample_us = (time.perf_counter() - t0) / 200 * 1e6
+    except binding.HorizonError as e:
+        log(f"[bench] AMD SMI pressure sample unavailable: {e}")
+    res = {"same_stream_gap_us": round(same, 2), "switch_gap_us": round(alt, 2),
+           "switch_us": round(alt - same, 2), "switch_synced_us": round(alt_synced - same_synced, 2),
+           "synced_gap_us": round(same_synced, 2), "decide_us": round(decide_us, 2),
+           "pressure_sample_us": None if sample_us is None else round(sample_us, 1), "pressure": pressure,
+           "note": "switch = event on the old level's stream + wait on the new one; decide = controller step "
+                   "+ stream lookup through the Python binding"}
+    log(f"[bench] controller: switch {alt - same:.2f} us (gap {alt:.2f} vs {same:.2f} us), host-synced switch "
+        f"{alt_synced - same_synced:.2f} us (gap {alt_synced:.2f} vs {same_synced:.2f}), decide {decide_us:.2f} us, "
+        f"pressure sample {sample_us} us = {pressure}")
     return res
 
 

@@ -255,6 +255,65 @@ enum {
 hs_status hs_timing_enable(hs_context* ctx, int32_t enable);
 hs_status hs_timing_read(hs_context* ctx, int32_t kernel_kind, double* total_ms, int32_t* n_launches);
 
+/* ------------------------------------------------------------------------
+ * Spatial controller: the bandwidth-guided shared-stage cap of §4.4
+ * ("Bandwidth-pressure signal", "SM ladder", Eq. (1)) applied as in step 3 of
+ * Algorithm 1.  Host only; no HIP call.  Per scheduling step:
+ *   B_hat = ewma_weight * B + (1 - ewma_weight) * B_hat   (the first sample
+ *           initialises B_hat)
+ *   rho   = clamp(B_hat / saturation, 0, 1)
+ *   s*    = aggressive_cus                       if downstream is inactive
+ *         = snap(S_min + rho * (S_cap - S_min))  otherwise, snap = the nearest
+ *           ladder level, ties to the larger one
+ *   s*  is applied when downstream is inactive, on the first step, when the
+ *       current cap is not a ladder level, or when its ladder index is at
+ *       least hysteresis_steps away from the current level; otherwise the
+ *       current cap is kept.  down_cus = max(0, total_cus - shared_cus).
+ * Ladder levels are meant to be budgets of a context's ladder, so a decision
+ * selects a pre-built stream pair with hs_context_stream (§5). */
+typedef struct hs_controller_cfg {
+  int32_t total_cus;        /* S_tot */
+  int32_t aggressive_cus;   /* S_aggr, the cap with no downstream activity */
+  const int32_t* ladder;    /* host [n_ladder]: co-running levels S_min .. S_cap,
+                               strictly increasing, >= 1; S_cap < S_aggr <= S_tot */
+  int32_t n_ladder;
+  double ewma_weight;       /* gamma, weight of the newest sample, in (0, 1] */
+  double saturation;        /* B_sat > 0, in the units of the samples */
+  int32_t hysteresis_steps; /* Delta_step >= 1, in ladder levels */
+} hs_controller_cfg;
+
+typedef struct hs_split {
+  int32_t shared_cus;       /* s_shared: cap of the shared stage */
+  int32_t down_cus;         /* s_down = max(0, S_tot - s_shared) */
+  int32_t level;            /* index of s_shared in the ladder, -1 for S_aggr */
+  int32_t changed;          /* 1 when this step moved the cap */
+  double pressure;          /* B_hat after this step's sample */
+  double rho;               /* clamp(B_hat / saturation, 0, 1) */
+} hs_split;
+
+typedef struct hs_controller hs_controller;
+
+/* The controller copies cfg (and the ladder).  Errors: HS_ERR_INVALID_ARG for
+ * a null pointer, an empty or non-increasing ladder, S_cap >= S_aggr,
+ * S_aggr > S_tot, ewma_weight outside (0, 1], saturation <= 0 or
+ * hysteresis_steps < 1. */
+hs_status hs_controller_create(const hs_controller_cfg* cfg, hs_controller** out);
+
+/* One scheduling step: downstream_active is A(t) (non-zero when a downstream
+ * stage runs), sample is B(t).  Writes the split to *out.  Errors:
+ * HS_ERR_INVALID_ARG for null pointers or a non-finite sample (the state is
+ * then unchanged). */
+hs_status hs_controller_step(hs_controller* ctrl, int32_t downstream_active, double sample, hs_split* out);
+
+hs_status hs_controller_destroy(hs_controller* ctrl);
+
+/* Memory-system activity of a GPU in [0, 1]: the memory-controller (UMC)
+ * activity that AMD SMI reports, the AMD counterpart of the NVML memory
+ * activity the paper samples (§4.4, §5).  device is the index in AMD SMI's
+ * enumeration.  The library is loaded on first use; HS_ERR_UNSUPPORTED when
+ * it, or the reading, is unavailable. */
+hs_status hs_pressure_sample(int32_t device, double* activity);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,6 +24,7 @@ SYMBOLS = (
     "hs_context_create", "hs_context_topology", "hs_context_stream", "hs_context_masks",
     "hs_context_destroy", "hs_workspace_size", "hs_shared_stage_forward", "hs_downstream_decode_step",
     "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read", "hs_convert_weights_f16",
+    "hs_controller_create", "hs_controller_step", "hs_controller_destroy", "hs_pressure_sample",
 )
 HS_WEIGHTS_BF16, HS_WEIGHTS_F16 = 0, 1
 
@@ -57,6 +58,18 @@ class KvCache(ctypes.Structure):
 class Topology(ctypes.Structure):
     _fields_ = [("n_cus", ctypes.c_int32), ("n_xcc", ctypes.c_int32), ("xcc", ctypes.c_uint8 * 256),
                 ("se", ctypes.c_uint8 * 256), ("cu", ctypes.c_uint8 * 256)]
+
+
+class ControllerCfg(ctypes.Structure):
+    _fields_ = [("total_cus", ctypes.c_int32), ("aggressive_cus", ctypes.c_int32),
+                ("ladder", ctypes.POINTER(ctypes.c_int32)), ("n_ladder", ctypes.c_int32),
+                ("ewma_weight", ctypes.c_double), ("saturation", ctypes.c_double),
+                ("hysteresis_steps", ctypes.c_int32)]
+
+
+class Split(ctypes.Structure):
+    _fields_ = [("shared_cus", ctypes.c_int32), ("down_cus", ctypes.c_int32), ("level", ctypes.c_int32),
+                ("changed", ctypes.c_int32), ("pressure", ctypes.c_double), ("rho", ctypes.c_double)]
 
 
 class HorizonError(RuntimeError):
@@ -97,6 +110,10 @@ def lib() -> ctypes.CDLL:
             "hs_timing_enable": [vp, i32],
             "hs_timing_read": [vp, i32, ctypes.POINTER(ctypes.c_double), i32p],
             "hs_convert_weights_f16": [vp, vp, vp, ctypes.c_int64, ctypes.c_int64, vp],
+            "hs_controller_create": [ctypes.POINTER(ControllerCfg), ctypes.POINTER(vp)],
+            "hs_controller_step": [vp, i32, ctypes.c_double, ctypes.POINTER(Split)],
+            "hs_controller_destroy": [vp],
+            "hs_pressure_sample": [i32, ctypes.POINTER(ctypes.c_double)],
         }
         for name, args in sigs.items():
             fn = getattr(L, name)
@@ -173,6 +190,44 @@ def hs_workspace_size(cfg, max_tokens: int, max_seqs: int, max_pos: int) -> int:
     n = ctypes.c_size_t(0)
     _check(lib().hs_workspace_size(ctypes.byref(LayerCfg.of(cfg)), max_tokens, max_seqs, max_pos, ctypes.byref(n)))
     return int(n.value)
+
+
+# --------------------------------------------------------------------------- spatial controller
+
+class Controller:
+    """Owns an hs_controller handle (the C object copies the configuration)."""
+
+    def __init__(self, total_cus: int, aggressive_cus: int, ladder: Sequence[int], ewma_weight: float,
+                 saturation: float, hysteresis_steps: int = 1):
+        self._ladder = _i32_array(ladder)
+        cfg = ControllerCfg(total_cus, aggressive_cus, self._ladder, len(ladder), ewma_weight, saturation,
+                            hysteresis_steps)
+        h = ctypes.c_void_p()
+        _check(lib().hs_controller_create(ctypes.byref(cfg), ctypes.byref(h)))
+        self.handle = h
+
+    def close(self):
+        if self.handle:
+            lib().hs_controller_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):  # pragma: no cover
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def hs_controller_step(ctrl: Controller, downstream_active: bool, sample: float) -> Split:
+    out = Split()
+    _check(lib().hs_controller_step(ctrl.handle, 1 if downstream_active else 0, float(sample), ctypes.byref(out)))
+    return out
+
+
+def hs_pressure_sample(device: int = 0) -> float:
+    v = ctypes.c_double(0.0)
+    _check(lib().hs_pressure_sample(device, ctypes.byref(v)))
+    return float(v.value)
 
 
 # --------------------------------------------------------------------------- context

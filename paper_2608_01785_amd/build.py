@@ -20,7 +20,7 @@ LIB = os.path.join(PKG, "libhorizon.so")
 
 ARCH = "gfx950"
 HIP_SOURCES = ["gemm.hip", "gemm_skinny.hip", "attention.hip", "misc.hip"]
-HOST_SOURCES = ["plan.cpp", "runtime.cpp"]
+HOST_SOURCES = ["plan.cpp", "runtime.cpp", "controller.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}"]
 # Keep the compiler from forming packed fp32 instructions.
@@ -57,7 +57,7 @@ def build(verbose: bool = False) -> str:
                 print(out)
     objs = [os.path.join(BUILD, s + ".o") for s in HIP_SOURCES + HOST_SOURCES]
     tmp = LIB + ".tmp"
-    _run([cc, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *objs])
+    _run([cc, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *objs, "-ldl"])
     os.replace(tmp, LIB)
     return LIB
 

@@ -148,7 +148,7 @@ def test_forward_validation_fails_before_any_gpu_work(b):
 
 
 def test_host_planner_under_sanitizers(tmp_path):
-    """Build the host-only planner with g++ and ASan/UBSan and drive its entry points."""
+    """Build the host-only planner and controller with g++ and ASan/UBSan and drive their entry points."""
     gxx = "g++"
     drv = tmp_path / "drv.cpp"
     drv.write_text(r'''
@@ -168,15 +168,26 @@ int main() {
   hs_layer_cfg c = {3584, 28, 4, 128, 18944, 1e-6f, 1e4f};
   size_t n = 0;
   if (hs_workspace_size(&c, 10515, 8, 2048, &n) != HS_OK || n == 0) return 6;
+  int ladder[] = {64, 96, 128, 160, 192};
+  hs_controller_cfg cc = {256, 256, ladder, 5, 0.4, 0.8, 1};
+  hs_controller* ctrl = nullptr;
+  if (hs_controller_create(&cc, &ctrl) != HS_OK) return 7;
+  hs_split sp;
+  for (int i = 0; i < 1000; ++i)
+    if (hs_controller_step(ctrl, i % 7 != 0, (i % 13) / 10.0, &sp) != HS_OK || sp.shared_cus + sp.down_cus != 256)
+      return 8;
+  hs_controller_destroy(ctrl);
+  cc.n_ladder = 0;
+  if (hs_controller_create(&cc, &ctrl) != HS_ERR_INVALID_ARG) return 9;
   printf("ok %zu\n", n);
   return 0;
 }
 ''')
     exe = tmp_path / "drv"
-    src = os.path.join(ROOT, "paper_2608_01785_amd", "csrc", "plan.cpp")
+    srcs = [os.path.join(ROOT, "paper_2608_01785_amd", "csrc", f) for f in ("plan.cpp", "controller.cpp")]
     cmd = [gxx, "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
            f"-I{os.path.join(ROOT, 'include')}", f"-I{os.path.join(ROOT, 'paper_2608_01785_amd', 'csrc')}",
-           str(drv), src, "-o", str(exe)]
+           str(drv), *srcs, "-o", str(exe), "-ldl"]
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     assert r.returncode == 0, r.stdout
     r = subprocess.run([str(exe)], stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
