@@ -60,6 +60,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
   const int qi = min(q0 + wave * 32 + fr, len - 1);  // clamped query row (tail lanes recompute the last row)
   const int qpos = ctx + qi;
   const int wave_last = ctx + min(q0 + wave * 32 + 31, len - 1);  // last key this wave needs
+  const int wave_first = ctx + min(q0 + wave * 32, len - 1);      // position of the wave's first row
 
   // Query fragments: B operand of S^T = K Q^T, lane = query, k = head dimension.
   u32x4 qf[DH / 16];
@@ -151,41 +152,53 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
         }
       }
       // Register r of subtile st holds key kv0 + 32 st + 16 (r / 8) + 8 fh + r % 8.
+      // Only tiles reaching past the wave's first query position need the
+      // causal mask (every key of an earlier tile is visible to all of the
+      // wave's rows and lies inside the sequence).  The maximum is taken on
+      // the raw scores (the scale is positive) and the scale is folded into
+      // the exponent's FMA; masked scores are -inf and give 0.
+      if (kv0 + BKV - 1 > wave_first) {
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kv0 + 32 * st + 16 * (r >> 3) + 8 * fh + (r & 7);
+            if (key > qpos) s[st][r] = -INFINITY;
+          }
+      }
       float mx = -INFINITY;
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kv0 + 32 * st + 16 * (r >> 3) + 8 * fh + (r & 7);
-          const float v = (key <= qpos) ? s[st][r] * a.scale_log2 : -INFINITY;
-          s[st][r] = v;
-          mx = fmaxf(mx, v);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[st][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2;
       const float m_new = fmaxf(m_run, mx);
-      const float alpha = exp2f(m_run - m_new);
+      const float alpha = exp2_raw(m_run - m_new);
       m_run = m_new;
       float psum = 0.0f;
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = exp2f(s[st][r] - m_new);
+          const float p = exp2_raw(fmaf(s[st][r], a.scale_log2, -m_new));
           s[st][r] = p;
           psum += p;
         }
       l_run = l_run * alpha + psum;
+      // Rescale the outputs only when some lane's running maximum moved.
+      if (__ballot(alpha != 1.0f) != 0) {
 #pragma unroll
-      for (int i = 0; i < NDS; ++i)
+        for (int i = 0; i < NDS; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+          for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+      }
       // P^T fragments: key block kb2 (16 keys) = registers 8 (kb2 % 2) .. +8 of subtile kb2 / 2.
       u32x4 pf[4];
 #pragma unroll
       for (int kb2 = 0; kb2 < 4; ++kb2) {
         const int st = kb2 >> 1, r0 = 8 * (kb2 & 1);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) pf[kb2][e] = pack2h(s[st][r0 + 2 * e], s[st][r0 + 2 * e + 1]);
+        for (int e = 0; e < 4; ++e) pf[kb2][e] = pack2h_unit(s[st][r0 + 2 * e], s[st][r0 + 2 * e + 1]);
       }
 #pragma unroll
       for (int i = 0; i < NDS; ++i) {

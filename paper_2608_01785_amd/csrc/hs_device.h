@@ -40,6 +40,16 @@ __device__ __forceinline__ uint32_t pack2h(float lo, float hi) {
   return uint32_t(f2h(lo)) | (uint32_t(f2h(hi)) << 16);
 }
 
+// Two values in [0, 1] (softmax probabilities) -> two fp16 values, round to
+// nearest even; no saturation is needed in that range.
+__device__ __forceinline__ uint32_t pack2h_unit(float lo, float hi) {
+  return uint32_t(__builtin_bit_cast(uint16_t, (_Float16)lo)) | (uint32_t(__builtin_bit_cast(uint16_t, (_Float16)hi)) << 16);
+}
+
+// 2^x with the hardware instruction alone (about 1 ulp; results below the
+// normal range flush to zero, which softmax weights can afford).
+__device__ __forceinline__ float exp2_raw(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // Two bf16 values (one 32-bit word) -> two fp16 values.  Exact for
 // magnitudes in [2^-14, 65504]; smaller values become fp16 subnormals
 // (absolute error below 2^-24).  Round-toward-zero conversion is used because
