@@ -42,7 +42,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 31, fh = lane >> 5;
 
-  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  // Units L = item * hq + head are ordered longest key range first, and the
+  // Gq = hq / hkv consecutive units of a group share one key/value head.
+  // Work-groups go to the XCDs round-robin (block b to XCD b % 8), so XCD x
+  // takes groups x, x + 8, x + 16, ... in order: every XCD gets an equal share
+  // of the longest-first list, and a group's units run on one XCD, where its
+  // keys and values stay in that XCD's L2.  The grid is padded to whole rounds
+  // of groups; padding blocks exit.
+  const int Gq = a.hq / a.hkv;
+  const int xcd = blockIdx.x % kNumXcd, kx = blockIdx.x / kNumXcd;
+  const int L = ((kx / Gq) * kNumXcd + xcd) * Gq + kx % Gq;
+  if (L >= a.n_items * a.hq) return;
   const int item = L / a.hq;
   const int head = L % a.hq;
   const int g = head / (a.hq / a.hkv);
@@ -241,7 +251,9 @@ __global__ __launch_bounds__(kThreads, 2) void decode_attn_kernel(DecodeAttnArgs
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.n_items <= 0) return hipSuccess;
-  const int grid = a.n_items * a.hq;
+  // Whole rounds of key/value-head groups over the XCDs (see attn_kernel).
+  const int groups = a.n_items * a.hkv;
+  const int grid = (groups + kNumXcd - 1) / kNumXcd * kNumXcd * (a.hq / a.hkv);
   if (a.dh == 64)
     hipLaunchKernelGGL(attn_kernel<64>, dim3(grid), dim3(kThreads), 0, s, a);
   else
