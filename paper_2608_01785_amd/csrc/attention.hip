@@ -24,8 +24,20 @@ constexpr int BQ = 128;
 constexpr int BKV = 64;
 constexpr int kThreads = 256;
 
-// LDS swizzle of a key row: distinct for the rows perm32(0..7) read by 8 lanes.
-__device__ __forceinline__ int kswz(int row) { return (row & 3) | ((row >> 1) & 4); }
+// LDS placement of 16-byte chunk c of key row r (DH * 2 bytes per row).  A
+// 16-lane pass of fragment reads takes one logical chunk of 16 distinct rows
+// (perm32 of 16 consecutive indices).  With 256-byte rows every row starts on
+// bank 0, so the 16 rows need 16 different physical chunks (c ^ (r & 15));
+// with 128-byte rows odd rows start on bank 32, so the chunks need only
+// differ within each parity (c ^ ((r >> 1) & 7)).
+template <int DH>
+__device__ __forceinline__ int kphys(int r, int c) {
+  return DH == 128 ? (c ^ (r & 15)) : (c ^ ((r >> 1) & 7));
+}
+
+// Chunk c (8 keys) of value row d (64 keys, 128 bytes): odd rows start on bank
+// 32, so a pass over 16 consecutive rows needs distinct chunks per parity.
+__device__ __forceinline__ int vphys(int d, int c) { return c ^ ((d >> 1) & 7); }
 
 template <int DH>
 __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
@@ -117,14 +129,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
     for (int j = 0; j < KLOADS; ++j) {
       const int idx = tid + j * kThreads;
       const int row = idx / KCH, c = idx % KCH;
-      const int phys = (c & ~7) | ((c & 7) ^ kswz(row));
+      const int phys = kphys<DH>(row, c);
       *reinterpret_cast<u32x4*>(ks + row * KROW + phys * 16) = rk[j];
     }
 #pragma unroll
     for (int j = 0; j < VLOADS; ++j) {
       const int idx = tid + j * kThreads;
       const int d = idx >> 3, c = idx & 7;
-      *reinterpret_cast<u32x4*>(vs + d * 128 + ((c ^ (d & 7)) * 16)) = rv[j];
+      *reinterpret_cast<u32x4*>(vs + d * 128 + vphys(d, c) * 16) = rv[j];
     }
   };
 
@@ -156,7 +168,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int st = 0; st < 2; ++st) {
           const int row = 32 * st + perm32(fr);
-          const int phys = (c & ~7) | ((c & 7) ^ kswz(row));
+          const int phys = kphys<DH>(row, c);
           const u32x4 kf = *reinterpret_cast<const u32x4*>(ks + row * KROW + phys * 16);
           s[st] = mfma32(kf, qf[kb], s[st]);
         }
@@ -216,7 +228,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int kb2 = 0; kb2 < 4; ++kb2) {
           const int c = 2 * kb2 + fh;
-          const u32x4 vf = *reinterpret_cast<const u32x4*>(vs + d * 128 + ((c ^ (d & 7)) * 16));
+          const u32x4 vf = *reinterpret_cast<const u32x4*>(vs + d * 128 + vphys(d, c) * 16);
           o[i] = mfma32(vf, pf[kb2], o[i]);
         }
       }
