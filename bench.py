@@ -76,6 +76,7 @@ def main():
     ap.add_argument("--no-corun", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-controller", action="store_true")
+    ap.add_argument("--no-tpot", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows per sequence in the CPU-reference sample (0: sized to take about 15 s)")
     ap.add_argument("--quick", action="store_true", help="headline stack only (no budget sweep, co-run, CPU leg)")
@@ -95,7 +96,7 @@ def main():
     dev = "cuda:0"
     budgets = [int(b) for b in args.budgets.split(",") if b]
     if args.quick:
-        budgets, args.no_corun, args.no_cpu_baseline, args.no_controller = [], True, True, True
+        budgets, args.no_corun, args.no_cpu_baseline, args.no_controller, args.no_tpot = [], True, True, True, True
     ladder = sorted(set(budgets + [128, 256]))
     ctx = binding.Context(0, budgets=ladder)
 
@@ -185,6 +186,11 @@ def main():
     if not args.no_corun:
         corun = corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flops_step)
 
+    # ---------------------------------------------------------------- shared-stage decode TPOT vs CU cap
+    tpot = None
+    if not args.no_tpot:
+        tpot = thinker_decode_sweep(torch, binding, W, shape, wdev, n_layers, dev)
+
     # ---------------------------------------------------------------- spatial controller costs
     controller = None
     if not args.no_controller:
@@ -220,6 +226,7 @@ def main():
         "ms_per_step_bf16_weights": round(ms_bf16w, 4),
         "budgets": per_budget,
         "corun": corun,
+        "decode_tpot_vs_cus": tpot,
         "controller": controller,
         "cpu_baseline": cpu,
     }
@@ -346,6 +353,59 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
     log(f"[bench] co-run: prefill {window:.2f} ms (solo {prefill_solo:.2f}), decode {dec_ms:.3f} ms/step "
         f"(solo {solo_ms:.3f}), {n_in} steps in window")
     return res
+
+
+def thinker_decode_sweep(torch, binding, W, shape, wdev, n_layers, dev, batch=16):
+    """Decode step of the thinker stack (one new row for each of `batch` sequences
+    behind 1024-2048 cached rows) at each CU cap: the shared stage's TPOT curve."""
+    from paper_2608_01785_amd.device_data import DeviceCache, to_device
+    caps = [16, 32, 48, 64, 96, 128, 192, 256]
+    ctx = binding.Context(0, budgets=caps)
+    try:
+        rng = np.random.default_rng(5001)
+        ctx_lens = rng.integers(1024, 2048, size=batch, endpoint=True).astype(np.int32)
+        max_ctx = int(np.ceil((ctx_lens.max() + 1) / 64) * 64)
+        cache = DeviceCache(n_layers, batch, max_ctx, shape.n_kv_heads, shape.head_dim, dev)
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(5002)
+        for l in range(n_layers):
+            for b in range(batch):
+                cache.fill_random(l, b, int(ctx_lens[b]), gen)
+        x = to_device(W.token_rows(5003, batch, shape.hidden), dev)
+        y = torch.empty(x.shape, dtype=torch.float32, device=dev)
+        offsets = list(range(batch + 1))
+        ws = torch.empty(binding.hs_workspace_size(shape, batch, batch, int(ctx_lens.max()) + 1), dtype=torch.uint8,
+                         device=dev)
+        step_bytes = talker_bytes(shape, n_layers, ctx_lens)
+        out = {"workload": f"thinker {n_layers}-layer stack, {batch} single-row sequences behind "
+                           f"{int(ctx_lens.min())}-{int(ctx_lens.max())} cached rows (sum {int(ctx_lens.sum())})",
+               "bytes_per_step": int(step_bytes), "cus": [], "tpot_ms": [], "hbm_frac_cu_scaled": []}
+        for c in caps:
+            s = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, c, binding.HS_ROLE_SHARED))
+
+            def step(k):
+                for _ in range(k):
+                    binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, offsets, ctx_lens, cache.as_arg(), c, None,
+                                                    ws)
+            step(3)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            step(20)
+            e1.record(s)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / 20
+            out["cus"].append(c)
+            out["tpot_ms"].append(round(ms, 4))
+            out["hbm_frac_cu_scaled"].append(round(step_bytes / (ms / 1e3) / (PEAK_HBM * c / N_CUS), 4))
+        best = min(out["tpot_ms"])
+        out["saturation_cus"] = next(c for c, t in zip(out["cus"], out["tpot_ms"]) if t <= 1.05 * best)
+        log("[bench] thinker decode TPOT vs CUs: " + ", ".join(f"{c}: {t:.3f} ms" for c, t in zip(out["cus"], out["tpot_ms"]))
+            + f"; within 5 % of the best from {out['saturation_cus']} CUs")
+        return out
+    finally:
+        torch.cuda.synchronize()
+        ctx.close()
 
 
 def controller_measure(torch, binding, ctx, ladder, dev):
