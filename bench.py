@@ -77,6 +77,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-controller", action="store_true")
     ap.add_argument("--no-tpot", action="store_true")
+    ap.add_argument("--no-mixed", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows per sequence in the CPU-reference sample (0: sized to take about 15 s)")
     ap.add_argument("--quick", action="store_true", help="headline stack only (no budget sweep, co-run, CPU leg)")
@@ -97,7 +98,8 @@ def main():
     budgets = [int(b) for b in args.budgets.split(",") if b]
     if args.quick:
         budgets, args.no_corun, args.no_cpu_baseline, args.no_controller, args.no_tpot = [], True, True, True, True
-    ladder = sorted(set(budgets + [128, 256]))
+        args.no_mixed = True
+    ladder = sorted(set(budgets + [96, 128, 256]))
     ctx = binding.Context(0, budgets=ladder)
 
     # ---------------------------------------------------------------- thinker stack
@@ -186,6 +188,11 @@ def main():
     if not args.no_corun:
         corun = corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flops_step)
 
+    # ---------------------------------------------------------------- downstream-heavy mixed step
+    mixed = None
+    if not args.no_mixed:
+        mixed = corun_mixed(torch, binding, W, ctx, dev)
+
     # ---------------------------------------------------------------- shared-stage decode TPOT vs CU cap
     tpot = None
     if not args.no_tpot:
@@ -226,6 +233,7 @@ def main():
         "ms_per_step_bf16_weights": round(ms_bf16w, 4),
         "budgets": per_budget,
         "corun": corun,
+        "mixed_corun": mixed,
         "decode_tpot_vs_cus": tpot,
         "controller": controller,
         "cpu_baseline": cpu,
@@ -352,6 +360,117 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
     }
     log(f"[bench] co-run: prefill {window:.2f} ms (solo {prefill_solo:.2f}), decode {dec_ms:.3f} ms/step "
         f"(solo {solo_ms:.3f}), {n_in} steps in window")
+    return res
+
+
+def corun_mixed(torch, binding, W, ctx, dev, steps=4):
+    """Downstream-heavy mix: one 4096-wide thinker layer over four 2048-row chunks
+    behind 0/2048/4096/6144 cached rows plus 64 decode rows behind 4096, throttled
+    to 96 CUs, while the 16-layer talker decodes a batch of 128 on the other 160."""
+    from paper_2608_01785_amd.device_data import DeviceCache, prepare_f16, to_device, upload_weights
+    shape = W.THINKER_MIXED
+    seeds = W.SEEDS["thinker_mixed"]
+    lengths, ctx_lens = W.thinker_mixed_layout()
+    B = len(lengths)
+    wth = prepare_f16(ctx, upload_weights(W.make_weights(shape, 1, seeds["weights"]), dev))
+    batch = W.random_batch(shape.hidden, lengths, seeds["tokens"], ctx_lens)
+    cache = DeviceCache(1, B, 8192, shape.n_kv_heads, shape.head_dim, dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seeds["cache"])
+    for b in range(B):
+        cache.fill_random(0, b, int(ctx_lens[b]), gen)
+    x = to_device(batch.x, dev)
+    y = torch.empty(x.shape, dtype=torch.float32, device=dev)
+    ws = torch.empty(binding.hs_workspace_size(shape, batch.n_tokens, B, 8192), dtype=torch.uint8, device=dev)
+    lin, att = thinker_flops(shape, lengths, ctx_lens)
+    th_flops = lin + att
+
+    ts_shape, ts_layers, bt = W.TALKER, 16, 128
+    tseeds = W.SEEDS["talker"]
+    kv_lens = W.talker_kv_lens(bt, 4004)
+    tl = prepare_f16(ctx, upload_weights(W.make_weights(ts_shape, ts_layers, tseeds["weights"]), dev))
+    max_ctx = int(np.ceil((kv_lens.max() + 1) / 64) * 64)
+    tcache = DeviceCache(ts_layers, bt, max_ctx, ts_shape.n_kv_heads, ts_shape.head_dim, dev)
+    for l in range(ts_layers):
+        for b in range(bt):
+            tcache.fill_random(l, b, int(kv_lens[b]), gen)
+    xt = to_device(W.token_rows(tseeds["tokens"] + 17, bt, ts_shape.hidden), dev)
+    yt = torch.empty(xt.shape, dtype=torch.float32, device=dev)
+    wst = torch.empty(binding.hs_workspace_size(ts_shape, bt, bt, int(kv_lens.max()) + 1), dtype=torch.uint8,
+                      device=dev)
+    t_bytes = talker_bytes(ts_shape, ts_layers, kv_lens)
+    s_sh = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 96, binding.HS_ROLE_SHARED))
+    s_dn = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 96, binding.HS_ROLE_DOWN))
+
+    def thinker(k):
+        for _ in range(k):
+            binding.hs_shared_stage_forward(ctx, shape, wth, x, y, batch.seq_offsets, ctx_lens, cache.as_arg(), 96,
+                                            None, ws)
+
+    def talker(n):
+        ev = []
+        for _ in range(n):
+            binding.hs_downstream_decode_step(ctx, ts_shape, tl, xt, yt, tcache.as_arg(), kv_lens, 160, None, wst)
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(s_dn)
+            ev.append(e)
+        return ev
+
+    # Solo figures on the same masks.
+    thinker(1)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s_sh)
+    thinker(steps)
+    e1.record(s_sh)
+    torch.cuda.synchronize()
+    th_solo = e0.elapsed_time(e1) / steps
+    talker(2)
+    torch.cuda.synchronize()
+    e0.record(s_dn)
+    ev = talker(10)
+    torch.cuda.synchronize()
+    tk_solo = e0.elapsed_time(ev[-1]) / 10
+
+    # Co-run: talker steps loop on the 160 CUs while the thinker runs `steps` steps on 96.
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    start.record(s_sh)
+    s_dn.wait_event(start)
+    thinker(steps)
+    end = torch.cuda.Event(enable_timing=True)
+    end.record(s_sh)
+    dec = []
+    while True:
+        dec += talker(1)
+        if end.query() or len(dec) > 500:
+            break
+        if len(dec) > 3:
+            dec[-3].synchronize()
+    torch.cuda.synchronize()
+    window = start.elapsed_time(end)
+    done = [start.elapsed_time(e) for e in dec]
+    n_in = sum(1 for t in done if t <= window)
+    t_last = max([t for t in done if t <= window], default=0.0)
+    tk_ms = t_last / n_in if n_in else float("nan")
+    th_ms = window / steps
+    res = {
+        "workload": "thinker layer hidden 4096, 32/8 heads, ffn 14336: 4 x 2048-row chunks behind 0/2048/4096/6144 "
+                    "cached rows + 64 decode rows behind 4096, 96 CUs; talker 16 layers, batch 128, "
+                    f"kv_len U[128,1024] (sum {int(kv_lens.sum())}), 160 CUs",
+        "thinker_ms": round(th_ms, 3), "thinker_solo_ms": round(th_solo, 3),
+        "thinker_tflops": round(th_flops / (th_ms / 1e3) / 1e12, 1),
+        "thinker_mfma_frac_cu_scaled": round(th_flops / (th_ms / 1e3) / (PEAK_BF16 * 96 / N_CUS), 4),
+        "thinker_solo_mfma_frac_cu_scaled": round(th_flops / (th_solo / 1e3) / (PEAK_BF16 * 96 / N_CUS), 4),
+        "talker_ms_per_step": round(tk_ms, 4), "talker_solo_ms_per_step": round(tk_solo, 4),
+        "talker_tok_s": round(bt / (tk_ms / 1e3)) if n_in else None,
+        "talker_hbm_frac_cu_scaled": round(t_bytes / (tk_ms / 1e3) / (PEAK_HBM * 160 / N_CUS), 4) if n_in else None,
+        "talker_solo_hbm_frac_cu_scaled": round(t_bytes / (tk_solo / 1e3) / (PEAK_HBM * 160 / N_CUS), 4),
+        "talker_steps_in_window": n_in, "thinker_flops": th_flops, "talker_bytes_per_step": int(t_bytes),
+    }
+    log(f"[bench] mixed co-run: thinker {th_ms:.3f} ms/step (solo {th_solo:.3f}), talker {tk_ms:.3f} ms/step "
+        f"(solo {tk_solo:.3f}), {n_in} talker steps in window")
+    del wth, tl, cache, tcache
     return res
 
 

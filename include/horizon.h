@@ -152,7 +152,9 @@ hs_status hs_plan_metadata(const int32_t* seq_offsets, const int32_t* ctx_lens, 
  * pairs, one pair per budget in budgets[n_budgets] (each in [1, n_cus]).
  * Budget n_cus has a SHARED stream only.  topo may be NULL (default
  * topology); the masks are hs_cu_partition(topo, budget).  The context owns
- * its streams and a small pinned staging ring. */
+ * its streams and a pool of pinned staging slots for the calls' metadata (4,
+ * growing to at most 64 while calls queued on several streams are pending, so
+ * that a call never waits for another stream's queued work). */
 hs_status hs_context_create(int32_t device, const int32_t* budgets, int32_t n_budgets,
                             const hs_topology* topo, hs_context** out);
 

@@ -11,7 +11,13 @@
 
 namespace {
 
+// Pinned staging slots for the per-call metadata image.  Calls on different
+// streams (the two stages of a co-run) must not wait for each other's queued
+// work, so a call takes any slot whose copy has completed and adds a slot when
+// all are still pending, up to kMaxStagingSlots; only then does it wait for
+// the oldest.
 constexpr int kStagingSlots = 4;
+constexpr int kMaxStagingSlots = 64;
 
 struct Level {
   int budget = 0;
@@ -26,6 +32,7 @@ struct Slot {
   size_t cap = 0;
   hipEvent_t ev = nullptr;
   bool pending = false;
+  uint64_t used = 0;  // call counter at the last use (oldest = smallest)
 };
 
 int popcount8(const uint32_t m[8]) {
@@ -47,8 +54,8 @@ struct hs_context {
   int n_cus = 0;
   hs_topology topo{};
   std::vector<Level> levels;
-  Slot slots[kStagingSlots];
-  int next_slot = 0;
+  std::vector<Slot> slots;
+  uint64_t calls = 0;
   // Optional per-launch event timing.
   struct TimingRec {
     int kind;
@@ -88,12 +95,33 @@ void destroy_context(hs_context* ctx) {
 
 // Copy the plan's metadata image to the workspace through a pinned slot.
 hs_status stage_metadata(hs_context* ctx, const hs::Plan& plan, void* dst, hipStream_t s) {
-  Slot& slot = ctx->slots[ctx->next_slot];
-  ctx->next_slot = (ctx->next_slot + 1) % kStagingSlots;
-  if (slot.pending) {
-    HIP_TRY(hipEventSynchronize(slot.ev));
-    slot.pending = false;
+  Slot* free_slot = nullptr;
+  Slot* oldest = nullptr;
+  for (Slot& sl : ctx->slots) {
+    if (sl.pending) {
+      const hipError_t q = hipEventQuery(sl.ev);
+      if (q == hipSuccess) {
+        sl.pending = false;
+      } else if (q != hipErrorNotReady) {
+        return hs::fail(HS_ERR_HIP, "hipEventQuery failed: %s", hipGetErrorString(q));
+      }
+    }
+    if (!sl.pending && !free_slot) free_slot = &sl;
+    if (!oldest || sl.used < oldest->used) oldest = &sl;
   }
+  if (!free_slot && ctx->slots.size() < size_t(kMaxStagingSlots)) {
+    Slot fresh;
+    HIP_TRY(hipEventCreateWithFlags(&fresh.ev, hipEventDisableTiming));
+    ctx->slots.push_back(fresh);
+    free_slot = &ctx->slots.back();
+  }
+  if (!free_slot) {
+    HIP_TRY(hipEventSynchronize(oldest->ev));
+    oldest->pending = false;
+    free_slot = oldest;
+  }
+  Slot& slot = *free_slot;
+  slot.used = ++ctx->calls;
   const size_t bytes = plan.image.size();
   if (slot.cap < bytes) {
     if (slot.host) HIP_TRY(hipHostFree(slot.host));
@@ -472,6 +500,7 @@ hs_status hs_context_create(int32_t device, const int32_t* budgets, int32_t n_bu
     }
     ctx->levels.push_back(l);
   }
+  ctx->slots.resize(kStagingSlots);
   for (Slot& s : ctx->slots) {
     hipError_t e = hipEventCreateWithFlags(&s.ev, hipEventDisableTiming);
     if (e != hipSuccess) {
