@@ -228,3 +228,31 @@ def test_corun_changes_nothing(env, thinker):
     t_dec = (ev[0].elapsed_time(ev[2]), ev[0].elapsed_time(ev[3]))
     log(f"  prefill window {t_pre}, decode window {t_dec} (ms from the common start)")
     assert t_dec[0] < t_pre[1], "decode did not start before the prefill ended"
+
+
+def test_queued_prefill_never_blocks_decode_calls(env, thinker):
+    """Several thinker forwards queued on the shared stream must not make a
+    decode call on the downstream stream wait on the host (the calls' metadata
+    staging must not serialise the two stages)."""
+    import time
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    layers_t, d, cache, wdev_t, xt, ws_t = talker_setup(env, 32, W.SEEDS["talker"])
+    _, batch, wdev, x, ws = thinker
+    y = torch.empty(x.shape, dtype=torch.float32, device="cuda")
+    yt = torch.empty(xt.shape, dtype=torch.float32, device="cuda")
+    s_sh = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_SHARED))
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s_sh)
+    for _ in range(6):
+        binding.hs_shared_stage_forward(ctx, W.THINKER, wdev, x, y, batch.seq_offsets, None, None, 128, None, ws)
+    e1.record(s_sh)
+    t0 = time.perf_counter()
+    for _ in range(6):
+        binding.hs_downstream_decode_step(ctx, W.TALKER, wdev_t, xt, yt, cache.as_arg(), d.kv_lens, 128, None, ws_t)
+    host_ms = (time.perf_counter() - t0) * 1e3
+    torch.cuda.synchronize()
+    queued_ms = e0.elapsed_time(e1)
+    log(f"  6 decode calls issued in {host_ms:.1f} ms on the host behind {queued_ms:.1f} ms of queued prefill")
+    assert host_ms < queued_ms / 4
