@@ -8,7 +8,10 @@ runtime unchanged (§5) and states no layer formula, so the layer below is the
 standard pre-norm decoder layer, with these readings of unstated details:
 
 * RMSNorm: ``x / sqrt(mean(x^2) + eps) * gamma``, eps inside the root.
-* No biases.  Residual after attention and after the FFN.  No final norm.
+* No biases, except an optional bias ``b_qkv`` [(Hq + 2 Hkv) dh] added to the
+  QKV projection before RoPE (the thinker's model family carries one there;
+  the paper is silent).  Residual after attention and after the FFN.  No
+  final norm.
 * ``w_qkv`` rows are [query heads | key heads | value heads], ``head_dim``
   rows per head; query head ``h`` reads key/value head ``h // (Hq / Hkv)``.
 * RoPE rotates the pairs (j, j + dh/2), j < dh/2, by ``pos * base^(-2j/dh)``;
@@ -97,7 +100,7 @@ def layer_forward(x: np.ndarray, w: Dict[str, np.ndarray], cfg, seq_offsets: Seq
     """One pre-norm decoder layer over a packed ragged batch.
 
     x: [T, d] float64; w: float64 weights ('ln1', 'w_qkv', 'w_o', 'ln2',
-    'w_gate_up', 'w_down'); seq_offsets: [B+1]; ctx_lens: [B] cached rows per
+    'w_gate_up', 'w_down', optional 'b_qkv'); seq_offsets: [B+1]; ctx_lens: [B] cached rows per
     sequence (None = no prefix); prefix_k/v: per sequence [ctx_b, Hkv, dh].
     ``seqs`` restricts the attention to those sequences (their rows of the
     output are exact; other rows keep only the row-local parts and must not
@@ -116,6 +119,8 @@ def layer_forward(x: np.ndarray, w: Dict[str, np.ndarray], cfg, seq_offsets: Seq
 
     n = rms_norm(x, w["ln1"], cfg.rms_eps)
     qkv = n @ w["w_qkv"].T
+    if w.get("b_qkv") is not None:
+        qkv = qkv + np.asarray(w["b_qkv"], dtype=np.float64)
     q = qkv[:, : hq * dh].reshape(T, hq, dh)
     k = qkv[:, hq * dh: (hq + hkv) * dh].reshape(T, hkv, dh)
     v = qkv[:, (hq + hkv) * dh:].reshape(T, hkv, dh)

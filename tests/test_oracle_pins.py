@@ -206,6 +206,8 @@ def brute_force_layer(x, w, c, offsets, ctx_lens=None, pk=None, pv=None):
         for i, t in enumerate(rows):
             n = norm(list(x[t]), w["ln1"])
             qkv = matvec(w["w_qkv"], n)
+            if w.get("b_qkv") is not None:
+                qkv = [v + w["b_qkv"][o] for o, v in enumerate(qkv)]
             p = ctx[b] + i
             qs.append([rot(qkv[h * dh:(h + 1) * dh], p) for h in range(hq)])
             ks.append([rot(qkv[(hq + g) * dh:(hq + g + 1) * dh], p) for g in range(hkv)])
@@ -240,6 +242,42 @@ def test_layer_matches_brute_force_loops():
     got, _, _ = L.layer_forward(x, w, c, off)
     ref = brute_force_layer(x, w, c, off)
     np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-11)
+
+
+def test_layer_with_qkv_bias_matches_brute_force_loops():
+    c = cfg(d=8, hq=2, hkv=1, dh=4, f=6)
+    rng = np.random.default_rng(18)
+    w = rand_weights(c, rng)
+    w["b_qkv"] = rng.standard_normal((c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim)
+    off, ctx = [0, 2, 5], [3, 1]
+    pk = [rng.standard_normal((n, 1, 4)) for n in ctx]
+    pv = [rng.standard_normal((n, 1, 4)) for n in ctx]
+    x = rng.standard_normal((5, 8))
+    got, _, _ = L.layer_forward(x, w, c, off, ctx, pk, pv)
+    ref = brute_force_layer(x, w, c, off, ctx, pk, pv)
+    np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-11)
+
+
+def test_qkv_bias_alone_gives_rotated_bias_keys_and_bias_values():
+    # With W_qkv = 0 every row's key is RoPE(b_k) at its position and its value is b_v.
+    c = cfg(d=8, hq=2, hkv=1, dh=4, f=6)
+    rng = np.random.default_rng(19)
+    w = rand_weights(c, rng)
+    w["w_qkv"] = np.zeros_like(w["w_qkv"])
+    b = rng.standard_normal((c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim)
+    w["b_qkv"] = b
+    x = rng.standard_normal((5, 8))
+    _, k, v = L.layer_forward(x, w, c, [0, 5])
+    bk, bv = b[8:12], b[12:16]
+    for t in range(5):
+        th = t * c.rope_base ** (-2.0 * np.arange(2) / 4)
+        exp = np.concatenate([bk[:2] * np.cos(th) - bk[2:] * np.sin(th), bk[2:] * np.cos(th) + bk[:2] * np.sin(th)])
+        np.testing.assert_allclose(k[t, 0], exp, rtol=1e-13, atol=1e-13)
+        np.testing.assert_array_equal(v[t, 0], bv)
+    w0 = dict(w, w_qkv=rand_weights(c, rng)["w_qkv"])
+    y_none, _, _ = L.layer_forward(x, dict(w0, b_qkv=None), c, [0, 5])
+    y_zero, _, _ = L.layer_forward(x, dict(w0, b_qkv=np.zeros_like(b)), c, [0, 5])
+    np.testing.assert_array_equal(y_none, y_zero)
 
 
 def test_layer_with_prefix_matches_brute_force_loops():
