@@ -73,6 +73,8 @@ enum { HS_WEIGHTS_BF16 = 0, HS_WEIGHTS_F16 = 1 };
 /* Device pointers to one layer's weights.
  *   ln1, ln2   [hidden] bf16                         RMSNorm gains
  *   w_qkv      [(Hq + 2 Hkv) * dh, hidden]           rows: Q heads | K heads | V heads
+ *   b_qkv      [(Hq + 2 Hkv) * dh] bf16, or NULL     bias of the QKV projection, added
+ *                                                    before RoPE (same row order)
  *   w_o        [hidden, Hq * dh]
  *   w_gate_up  [2 * ffn, hidden]                      rows: gate | up
  *   w_down     [hidden, ffn]
@@ -88,6 +90,7 @@ typedef struct hs_layer_weights {
   const void* w_gate_up;
   const void* w_down;
   int32_t format;
+  const void* b_qkv;
 } hs_layer_weights;
 
 /* Key/value cache.  k[l] and v[l] are device pointers for layer l (host

@@ -47,7 +47,7 @@ MATRICES = ("w_qkv", "w_o", "w_gate_up", "w_down")
 
 class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("ln1", "w_qkv", "w_o", "ln2", "w_gate_up", "w_down")] + \
-               [("format", ctypes.c_int32)]
+               [("format", ctypes.c_int32), ("b_qkv", ctypes.c_void_p)]
 
 
 class KvCache(ctypes.Structure):
@@ -291,6 +291,7 @@ def _weights_array(weights: List[Dict[str, object]]):
         for name in ("ln1", "w_qkv", "w_o", "ln2", "w_gate_up", "w_down"):
             setattr(arr[i], name, _ptr(w[name]))
         arr[i].format = int(w.get("format", HS_WEIGHTS_BF16))
+        arr[i].b_qkv = _ptr(w.get("b_qkv"))
     return arr
 
 

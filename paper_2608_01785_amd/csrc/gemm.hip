@@ -353,6 +353,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
               lo[e] = acc[lo_i][j][4 * g + e];
               hi[e] = acc[hi_i][j][4 * g + e];
             }
+            if (a.bias) {
+              float bl[4], bh[4];
+              load_bf16x4(a.bias + head * DH + d, bl);
+              load_bf16x4(a.bias + head * DH + d + DH / 2, bh);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                lo[e] += bl[e];
+                hi[e] += bh[e];
+              }
+            }
             if (head < a.hq + a.hkv) {
               float rl[4], rh[4];
 #pragma unroll

@@ -36,6 +36,7 @@ struct GemmArgs {
   const int64_t* v_off;   // [M]
   int64_t kv_head_stride; // elements between the heads of one slot (max_ctx * dh)
   const float2* rope;     // [max_pos, dh / 2] (cos, sin)
+  const uint16_t* bias;   // QKV: bf16 [(hq + 2 hkv) * dh] added before RoPE, or null
   int hq, hkv, dh;
   // Skinny GEMM split along K: fp32 partial sums and one arrival counter per
   // weight strip (zero on entry, left at zero on exit).

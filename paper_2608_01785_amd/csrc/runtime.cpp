@@ -328,6 +328,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     g.v_off = d_voff;
     g.kv_head_stride = plan.kv_head_stride;
     g.rope = rope;
+    g.bias = static_cast<const uint16_t*>(w[l].b_qkv);
     g.hq = hq;
     g.hkv = hkv;
     g.dh = dh;
@@ -386,7 +387,6 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     go.resid = x_cur;
     go.resid_f32 = x_cur_f32;
     go.k8_rows = k8;
-    // Fold when every GEMM of the layer takes the skinny path.
     // Fold when every GEMM of the layer takes the skinny path (gate/up and
     // down share M, and their K are multiples of 64) and a consumer can
     // prefetch a row's partial sums.

@@ -220,8 +220,11 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
   // barriers keep each chunk's loads ahead of the previous chunk's MFMAs.
   Chunk b0, b1;
   load_chunk(0, b0);
-  // QKV: the RoPE table entries of this lane's dimension pairs.
+  // QKV: the RoPE table entries of this lane's dimension pairs and, with a
+  // bias, the bias of its columns (registers 4 g + e: dimension
+  // 16 sub + 8 g + 4 fh + e, registers 4 (g + 2) + e: that plus DH / 2).
   float2 rope_pre[EPI == EPI_QKV ? 8 : 1];
+  float bias_pre[EPI == EPI_QKV ? 16 : 1];
   if constexpr (EPI == EPI_QKV) {
     if (row_own) {
       const float2* rt = a.rope + int64_t(qkv_pos) * (DH / 2) + 16 * (tile % (DH / 32)) + 4 * fh;
@@ -229,6 +232,16 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
       for (int g = 0; g < 2; ++g)
 #pragma unroll
         for (int e = 0; e < 4; ++e) rope_pre[4 * g + e] = rt[8 * g + e];
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) bias_pre[r] = 0.0f;
+    if (a.bias && wave < MT) {
+      const uint16_t* bp = a.bias + (tile / (DH / 32)) * DH + 16 * (tile % (DH / 32)) + 4 * fh;
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        load_bf16x4(bp + 8 * g, &bias_pre[4 * g]);
+        load_bf16x4(bp + 8 * g + DH / 2, &bias_pre[4 * (g + 2)]);
+      }
     }
   }
   __builtin_amdgcn_sched_barrier(0);
@@ -381,6 +394,10 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
       for (int i = 0; i < NS; ++i)
 #pragma unroll
         for (int r = 0; r < 16; ++r) c[i][r] *= rs;
+    }
+    if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) c[0][r] += bias_pre[r];
     }
   }
   if constexpr (EPI == EPI_SWIGLU) {

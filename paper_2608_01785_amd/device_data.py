@@ -48,6 +48,8 @@ def prepare_f16(ctx, layers_dev: List[Dict[str, torch.Tensor]]) -> List[Dict[str
     out = []
     for lw in layers_dev:
         d = {"ln1": lw["ln1"], "ln2": lw["ln2"], "format": binding.HS_WEIGHTS_F16}
+        if lw.get("b_qkv") is not None:
+            d["b_qkv"] = lw["b_qkv"]
         for name in binding.MATRICES:
             n, k = lw[name].shape
             dst = torch.empty((k // 32, n, 32), dtype=torch.float16, device=lw[name].device)

@@ -21,7 +21,9 @@ available, so every value is drawn from the recipes below):
                   prefixes of 0/2048/4096/6144 rows, plus 64 single-row decode
                   sequences behind 4096 cached rows.
 
-Weights are N(0, 0.02); RMSNorm gains are 1 + N(0, 0.02); token embeddings and
+Weights are N(0, 0.02); RMSNorm gains are 1 + N(0, 0.02); the optional QKV
+bias (models of the Qwen2 family carry one) is N(0, sigma) with sigma chosen
+by the caller; token embeddings and
 cached keys/values are N(0, 1).  All values are drawn in float32 with NumPy's
 PCG64 generator and rounded with round-to-nearest-even: to bfloat16 for
 weights and token rows, to IEEE half for cached keys/values.
@@ -124,11 +126,15 @@ def weight_shapes(s: LayerShape) -> Dict[str, tuple]:
     }
 
 
-def make_weights(s: LayerShape, n_layers: int, seed: int, std: float = 0.02) -> List[Dict[str, np.ndarray]]:
+def make_weights(s: LayerShape, n_layers: int, seed: int, std: float = 0.02,
+                 qkv_bias_std: float = 0.0) -> List[Dict[str, np.ndarray]]:
     """Per-layer dict of raw bf16 bits, drawn layer by layer in WEIGHT_NAMES order.
 
     ``w_qkv`` rows are [query heads | key heads | value heads], ``head_dim``
     rows each; ``w_gate_up`` rows are [gate | up]. Matrices are [out, in].
+    With ``qkv_bias_std`` > 0 each layer also gets ``b_qkv`` [qkv_rows],
+    N(0, qkv_bias_std), drawn afterwards from a generator of its own so that
+    the other weights do not depend on whether biases are drawn.
     """
     rng = np.random.default_rng(seed)
     shapes = weight_shapes(s)
@@ -144,6 +150,12 @@ def make_weights(s: LayerShape, n_layers: int, seed: int, std: float = 0.02) -> 
             lw[name] = bf16_bits(v)
             del v
         layers.append(lw)
+    if qkv_bias_std > 0.0:
+        brng = np.random.default_rng([seed, 1])
+        for lw in layers:
+            v = brng.standard_normal(s.qkv_rows, dtype=np.float32)
+            v *= np.float32(qkv_bias_std)
+            lw["b_qkv"] = bf16_bits(v)
     return layers
 
 

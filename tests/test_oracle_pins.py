@@ -447,6 +447,17 @@ def test_bf16_rounding_is_nearest_even():
     assert abs(f64(w["w_qkv"]).std() - 0.02) < 0.001
 
 
+def test_qkv_bias_draw_leaves_other_weights_unchanged():
+    plain = W.make_weights(W.TINY, 2, 1000)
+    biased = W.make_weights(W.TINY, 2, 1000, qkv_bias_std=0.5)
+    for p_, b_ in zip(plain, biased):
+        assert "b_qkv" not in p_ and b_["b_qkv"].shape == (W.TINY.qkv_rows,)
+        for name in W.WEIGHT_NAMES:
+            np.testing.assert_array_equal(p_[name], b_[name])
+    assert abs(f64(biased[0]["b_qkv"]).std() - 0.5) < 0.05
+    assert not np.array_equal(biased[0]["b_qkv"], biased[1]["b_qkv"])
+
+
 def test_tiny_workload_layer_is_finite_and_row_local_residual():
     # End-to-end on the tiny workload's real inputs (the parity case of the GPU tests).
     c = W.TINY
