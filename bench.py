@@ -13,6 +13,7 @@ same workload (rank 0, N = 1 only).
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -99,7 +100,14 @@ def main():
     if args.quick:
         budgets, args.no_corun, args.no_cpu_baseline, args.no_controller, args.no_tpot = [], True, True, True, True
         args.no_mixed = True
-    ladder = sorted(set(budgets + [96, 128, 256]))
+    # One context holds every level the sections below use (each level is a
+    # pair of CU-masked hardware queues).
+    # The timed loops issue many short library calls from Python.  A cyclic
+    # garbage-collection pass over the objects that earlier sections built
+    # stalled one call by ~37 ms inside a timed loop, so the collector runs
+    # only between sections.
+    gc.disable()
+    ladder = sorted(set(budgets + [96, 128, 256] + ([] if args.no_tpot else TPOT_CAPS)))
     ctx = binding.Context(0, budgets=ladder)
 
     # ---------------------------------------------------------------- thinker stack
@@ -184,21 +192,25 @@ def main():
         del src, dst
 
     # ---------------------------------------------------------------- co-run
+    gc.collect()
     corun = None
     if not args.no_corun:
         corun = corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flops_step)
 
     # ---------------------------------------------------------------- downstream-heavy mixed step
+    gc.collect()
     mixed = None
     if not args.no_mixed:
         mixed = corun_mixed(torch, binding, W, ctx, dev)
 
     # ---------------------------------------------------------------- shared-stage decode TPOT vs CU cap
+    gc.collect()
     tpot = None
     if not args.no_tpot:
-        tpot = thinker_decode_sweep(torch, binding, W, shape, wdev, n_layers, dev)
+        tpot = thinker_decode_sweep(torch, binding, W, ctx, shape, wdev, n_layers, dev)
 
     # ---------------------------------------------------------------- spatial controller costs
+    gc.collect()
     controller = None
     if not args.no_controller:
         controller = controller_measure(torch, binding, ctx, [b for b in ladder if b < N_CUS], dev)
@@ -474,12 +486,14 @@ def corun_mixed(torch, binding, W, ctx, dev, steps=4):
     return res
 
 
-def thinker_decode_sweep(torch, binding, W, shape, wdev, n_layers, dev, batch=16):
+TPOT_CAPS = [16, 32, 48, 64, 96, 128, 192, 256]
+
+
+def thinker_decode_sweep(torch, binding, W, ctx, shape, wdev, n_layers, dev, batch=16):
     """Decode step of the thinker stack (one new row for each of `batch` sequences
     behind 1024-2048 cached rows) at each CU cap: the shared stage's TPOT curve."""
     from paper_2608_01785_amd.device_data import DeviceCache, to_device
-    caps = [16, 32, 48, 64, 96, 128, 192, 256]
-    ctx = binding.Context(0, budgets=caps)
+    caps = TPOT_CAPS
     try:
         rng = np.random.default_rng(5001)
         ctx_lens = rng.integers(1024, 2048, size=batch, endpoint=True).astype(np.int32)
@@ -498,7 +512,8 @@ def thinker_decode_sweep(torch, binding, W, shape, wdev, n_layers, dev, batch=16
         step_bytes = talker_bytes(shape, n_layers, ctx_lens)
         out = {"workload": f"thinker {n_layers}-layer stack, {batch} single-row sequences behind "
                            f"{int(ctx_lens.min())}-{int(ctx_lens.max())} cached rows (sum {int(ctx_lens.sum())})",
-               "bytes_per_step": int(step_bytes), "cus": [], "tpot_ms": [], "hbm_frac_cu_scaled": []}
+               "bytes_per_step": int(step_bytes), "cus": [], "tpot_ms": [], "hbm_frac_cu_scaled": [],
+               "host_ms_per_call": []}
         for c in caps:
             s = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, c, binding.HS_ROLE_SHARED))
 
@@ -510,21 +525,24 @@ def thinker_decode_sweep(torch, binding, W, shape, wdev, n_layers, dev, batch=16
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(s)
+            h0 = time.perf_counter()
             step(20)
+            host_ms = (time.perf_counter() - h0) * 1e3 / 20
             e1.record(s)
             torch.cuda.synchronize()
             ms = e0.elapsed_time(e1) / 20
+            out["host_ms_per_call"].append(round(host_ms, 4))
             out["cus"].append(c)
             out["tpot_ms"].append(round(ms, 4))
             out["hbm_frac_cu_scaled"].append(round(step_bytes / (ms / 1e3) / (PEAK_HBM * c / N_CUS), 4))
         best = min(out["tpot_ms"])
         out["saturation_cus"] = next(c for c, t in zip(out["cus"], out["tpot_ms"]) if t <= 1.05 * best)
-        log("[bench] thinker decode TPOT vs CUs: " + ", ".join(f"{c}: {t:.3f} ms" for c, t in zip(out["cus"], out["tpot_ms"]))
+        log("[bench] thinker decode TPOT vs CUs: " + ", ".join(
+            f"{c}: {t:.3f} ms (host {h:.3f})" for c, t, h in zip(out["cus"], out["tpot_ms"], out["host_ms_per_call"]))
             + f"; within 5 % of the best from {out['saturation_cus']} CUs")
         return out
     finally:
         torch.cuda.synchronize()
-        ctx.close()
 
 
 def controller_measure(torch, binding, ctx, ladder, dev):

@@ -157,7 +157,8 @@ hs_status hs_plan_metadata(const int32_t* seq_offsets, const int32_t* ctx_lens, 
  * topology); the masks are hs_cu_partition(topo, budget).  The context owns
  * its streams and a pool of pinned staging slots for the calls' metadata (4,
  * growing to at most 64 while calls queued on several streams are pending, so
- * that a call never waits for another stream's queued work). */
+ * that a call never waits for another stream's queued work).  Each stream
+ * is a hardware queue of its own (2 per level, 1 at n_cus). */
 hs_status hs_context_create(int32_t device, const int32_t* budgets, int32_t n_budgets,
                             const hs_topology* topo, hs_context** out);
 
