@@ -93,19 +93,38 @@ typedef struct hs_layer_weights {
   const void* b_qkv;
 } hs_layer_weights;
 
-/* Key/value cache.  k[l] and v[l] are device pointers for layer l (host
- * arrays of n_layers pointers, owned by the caller).  Per layer:
+/* Key/value cache (§2.1: prefill builds it, decode re-reads it).  k[l] and
+ * v[l] are device pointers for layer l (host arrays of n_layers pointers,
+ * owned by the caller).  The cache of a layer is a pool of n_slots slots of
+ * max_ctx positions each:
  *   K: fp16 [n_slots, Hkv, max_ctx, dh]            (the key rows of one head
  *      are contiguous)
  *   V: fp16 [n_slots, Hkv, max_ctx / 32, dh, 32]   (values transposed in
  *      tiles of 32 positions: the P.V contraction reads keys contiguously and
  *      a tile of one head is one contiguous block)
- * Sequence b of a call uses slot b.  max_ctx % 64 == 0. */
+ * max_ctx % 64 == 0.
+ *
+ * block_table NULL: sequence b of a call uses slot b; its positions are
+ *   < max_ctx.
+ * block_table non-NULL (paged cache): a slot is a page of max_ctx positions.
+ *   block_table is a host array [n_seqs][pages_per_seq] of slot indices;
+ *   position p of sequence b lives in slot block_table[b * pages_per_seq +
+ *   p / max_ctx] at position p % max_ctx.  Positions are
+ *   < pages_per_seq * max_ctx.  Entries for pages a sequence does not reach
+ *   are not read.  Sequences may share pages they only read (a common
+ *   prefix); a page that receives new rows in a call must belong to one
+ *   sequence only and appear once in its row of the table, else the call
+ *   fails with HS_ERR_INVALID_ARG.  Single-row attention splits its key range
+ *   at page boundaries, so pages of 512 (head_dim 128) or 1024 (head_dim 64)
+ *   positions or a multiple keep its work units whole; the workspace comes
+ *   from hs_workspace_size_paged. */
 typedef struct hs_kv_cache {
   void* const* k;
   void* const* v;
   int32_t n_slots;
   int32_t max_ctx;
+  const int32_t* block_table;
+  int32_t pages_per_seq;
 } hs_kv_cache;
 
 /* Per mask bit i (bit i%32 of word i/32): hardware XCD, shader engine and CU
@@ -180,6 +199,12 @@ hs_status hs_context_destroy(hs_context* ctx);
 hs_status hs_workspace_size(const hs_layer_cfg* cfg, int32_t max_tokens, int32_t max_seqs,
                             int32_t max_pos, size_t* bytes);
 
+/* The same for calls on a paged cache (hs_kv_cache.block_table non-NULL)
+ * whose pages hold page_positions positions (its max_ctx); 0 means no block
+ * table.  page_positions must be 0 or a positive multiple of 64. */
+hs_status hs_workspace_size_paged(const hs_layer_cfg* cfg, int32_t max_tokens, int32_t max_seqs,
+                                  int32_t max_pos, int32_t page_positions, size_t* bytes);
+
 /* Shared-stage forward: n_layers decoder layers over a packed ragged batch.
  *   x_in         bf16 [T, hidden] device, T = seq_offsets[n_seqs].
  *   x_out        fp32 [T, hidden] device (the residual stream is carried in
@@ -187,15 +212,17 @@ hs_status hs_workspace_size(const hs_layer_cfg* cfg, int32_t max_tokens, int32_t
  *   w            host array of n_layers weight sets.
  *   seq_offsets  host [n_seqs + 1];  ctx_lens host [n_seqs] or NULL.
  *   kv           NULL: keys/values live in the workspace only (plain prefill).
- *                non-NULL: row i of sequence b is written to slot b at
- *                position ctx_lens[b] + i of every layer's cache, and the
- *                sequence attends to cache positions 0 .. ctx_lens[b] + i
- *                (§2.1: prefill builds the cache).  Requires ctx_lens.
+ *                non-NULL: row i of sequence b is written to position
+ *                ctx_lens[b] + i of sequence b in every layer's cache (slot
+ *                b, or the page its block table names), and the sequence
+ *                attends to its cache positions 0 .. ctx_lens[b] + i (§2.1:
+ *                prefill builds the cache).  Requires ctx_lens.
  *   cu_budget    CU cap s_shared (§4.5, Algorithm 1, step 4).  stream NULL
  *                selects the context's SHARED stream of that budget; a
  *                non-NULL stream must carry exactly cu_budget CUs.
  *   workspace    device buffer of ws_bytes >= hs_workspace_size(cfg, T,
- *                n_seqs, max position + 1), owned by the caller; must not
+ *                n_seqs, max position + 1) (hs_workspace_size_paged with the
+ *                page size for a paged cache), owned by the caller; must not
  *                overlap the inputs or outputs.  It may be reused as soon as
  *                the stream has passed this call.
  * The output is the residual stream after the last layer (no final norm). */
@@ -211,8 +238,10 @@ hs_status hs_shared_stage_forward(hs_context* ctx, const hs_layer_cfg* cfg,
  *   x_in         bf16 [batch, hidden] device.
  *   x_out        fp32 [batch, hidden] device; must not overlap x_in.
  *   kv_lens      host [batch]: cached rows before the step.  The new row is at
- *                position kv_lens[b], its K/V are written there in slot b, and
- *                it attends to kv_lens[b] + 1 keys.  kv_lens[b] < max_ctx.
+ *                position kv_lens[b], its K/V are written there (slot b, or
+ *                the page its block table names), and it attends to
+ *                kv_lens[b] + 1 keys.  kv_lens[b] < max_ctx without a block
+ *                table, < pages_per_seq * max_ctx with one.
  *   cu_budget, stream, workspace as for hs_shared_stage_forward, with the
  *   DOWN role: stream NULL selects the context's DOWN stream for the ladder
  *   level whose SHARED budget is n_cus - cu_budget.

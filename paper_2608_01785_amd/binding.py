@@ -22,7 +22,7 @@ HS_ROLE_SHARED, HS_ROLE_DOWN = 0, 1
 SYMBOLS = (
     "hs_status_string", "hs_last_error", "hs_default_topology", "hs_cu_partition", "hs_plan_metadata",
     "hs_context_create", "hs_context_topology", "hs_context_stream", "hs_context_masks",
-    "hs_context_destroy", "hs_workspace_size", "hs_shared_stage_forward", "hs_downstream_decode_step",
+    "hs_context_destroy", "hs_workspace_size", "hs_workspace_size_paged", "hs_shared_stage_forward", "hs_downstream_decode_step",
     "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read", "hs_convert_weights_f16",
     "hs_controller_create", "hs_controller_step", "hs_controller_destroy", "hs_pressure_sample",
 )
@@ -52,7 +52,8 @@ class LayerWeights(ctypes.Structure):
 
 class KvCache(ctypes.Structure):
     _fields_ = [("k", ctypes.POINTER(ctypes.c_void_p)), ("v", ctypes.POINTER(ctypes.c_void_p)),
-                ("n_slots", ctypes.c_int32), ("max_ctx", ctypes.c_int32)]
+                ("n_slots", ctypes.c_int32), ("max_ctx", ctypes.c_int32),
+                ("block_table", ctypes.POINTER(ctypes.c_int32)), ("pages_per_seq", ctypes.c_int32)]
 
 
 class Topology(ctypes.Structure):
@@ -102,6 +103,8 @@ def lib() -> ctypes.CDLL:
             "hs_context_masks": [vp, i32, u32p, u32p],
             "hs_context_destroy": [vp],
             "hs_workspace_size": [ctypes.POINTER(LayerCfg), i32, i32, i32, ctypes.POINTER(ctypes.c_size_t)],
+            "hs_workspace_size_paged": [ctypes.POINTER(LayerCfg), i32, i32, i32, i32,
+                                        ctypes.POINTER(ctypes.c_size_t)],
             "hs_shared_stage_forward": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp, vp,
                                         i32p, i32p, i32, ctypes.POINTER(KvCache), i32, vp, vp, ctypes.c_size_t],
             "hs_downstream_decode_step": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp, vp,
@@ -189,6 +192,13 @@ def hs_plan_metadata(seq_offsets, ctx_lens=None) -> Tuple[np.ndarray, np.ndarray
 def hs_workspace_size(cfg, max_tokens: int, max_seqs: int, max_pos: int) -> int:
     n = ctypes.c_size_t(0)
     _check(lib().hs_workspace_size(ctypes.byref(LayerCfg.of(cfg)), max_tokens, max_seqs, max_pos, ctypes.byref(n)))
+    return int(n.value)
+
+
+def hs_workspace_size_paged(cfg, max_tokens: int, max_seqs: int, max_pos: int, page_positions: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().hs_workspace_size_paged(ctypes.byref(LayerCfg.of(cfg)), max_tokens, max_seqs, max_pos,
+                                         page_positions, ctypes.byref(n)))
     return int(n.value)
 
 
@@ -296,15 +306,23 @@ def _weights_array(weights: List[Dict[str, object]]):
 
 
 def _kv_struct(kv) -> Optional[KvCache]:
-    """kv: None or (k_list, v_list, n_slots, max_ctx) of device tensors / pointers."""
+    """kv: None, (k_list, v_list, n_slots, max_ctx) of device tensors / pointers, or the same
+    plus a host block table [n_seqs, pages_per_seq] of slot indices (a paged cache)."""
     if kv is None:
         return None
-    k_list, v_list, n_slots, max_ctx = kv
+    k_list, v_list, n_slots, max_ctx = kv[:4]
+    table = kv[4] if len(kv) > 4 else None
     kp = (ctypes.c_void_p * len(k_list))(*[_ptr(t) for t in k_list])
     vp = (ctypes.c_void_p * len(v_list))(*[_ptr(t) for t in v_list])
+    tp, pps = None, 0
+    if table is not None:
+        table = np.ascontiguousarray(table, dtype=np.int32)
+        assert table.ndim == 2
+        pps = table.shape[1]
+        tp = table.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
     s = KvCache(ctypes.cast(kp, ctypes.POINTER(ctypes.c_void_p)), ctypes.cast(vp, ctypes.POINTER(ctypes.c_void_p)),
-                n_slots, max_ctx)
-    s._keep = (kp, vp)
+                n_slots, max_ctx, tp, pps)
+    s._keep = (kp, vp, table)
     return s
 
 

@@ -73,8 +73,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
   const int len = a.seq_len[b];
   const int ctx = a.seq_ctx[b];
   const int row0 = a.seq_start[b];
-  const int64_t kbase = a.seq_kbase[b] + int64_t(g) * a.kv_head_stride;
-  const int64_t vbase = a.seq_vbase[b] + int64_t(g) * a.kv_head_stride;
+  const int64_t* pages = a.page_base + a.seq_page0[b];
+  const int64_t head_off = int64_t(g) * a.kv_head_stride;
   const int kv_row_stride = DH;
 
   const int n_keys = ctx + min(q0 + BQ, len);      // keys any query of the block may see
@@ -95,20 +95,24 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
   u32x4 rk[KLOADS], rv[VLOADS];
   auto gload = [&](int t) {
     const int kv0 = t * BKV;
+    // The tile's page and its first key's place in it (page_keys % BKV == 0).
+    const int pg = kv0 / a.page_keys;
+    const int in0 = kv0 - pg * a.page_keys;
+    const int64_t base = pages[pg] + head_off;
 #pragma unroll
     for (int j = 0; j < KLOADS; ++j) {
       const int idx = tid + j * kThreads;
       const int row = idx / KCH, c = idx % KCH;
-      rk[j] = *reinterpret_cast<const u32x4*>(a.kstore + kbase + int64_t(kv0 + row) * kv_row_stride + c * 8);
+      rk[j] = *reinterpret_cast<const u32x4*>(a.kstore + base + int64_t(in0 + row) * kv_row_stride + c * 8);
     }
 #pragma unroll
     for (int j = 0; j < VLOADS; ++j) {
       const int idx = tid + j * kThreads;
       const int d = idx >> 3, c = idx & 7;
-      const int key = kv0 + c * 8;
+      const int key = kv0 + c * 8, ki = in0 + c * 8;
       // 8 keys of dimension d inside the value tile of 32 keys holding them.
-      u32x4 v = *reinterpret_cast<const u32x4*>(a.vstore + vbase + int64_t(key / kv_tile_keys) * kv_tile_keys * DH +
-                                                d * kv_tile_keys + key % kv_tile_keys);
+      u32x4 v = *reinterpret_cast<const u32x4*>(a.vstore + base + int64_t(ki / kv_tile_keys) * kv_tile_keys * DH +
+                                                d * kv_tile_keys + ki % kv_tile_keys);
       if (key + 8 > n_keys) {
         // Keys past the last visible one may hold uninitialised data; P is 0
         // there, but 0 * NaN would still poison the sum, so zero them.

@@ -1,6 +1,7 @@
 // Single-row (decode) attention unit.
 //
-// A unit is one key range (a "split" of dec_split_keys keys) of one row r and
+// A unit is one key range (a "split" of unit_keys keys, inside one page of
+// the cache) of one row r and
 // one key/value head g; the group's G query heads are the 32 MFMA columns
 // (G <= 8 valid), so the keys and values of the head are read once for the
 // whole group.  The range is cut into tiles (dec_tile_keys keys); wave w takes
@@ -37,7 +38,6 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
   constexpr int NKB = DH / 16;                 // 16-wide K steps of q.k
   constexpr int NDS = DH / 32;                 // output subtiles along dh
   constexpr int NPB = TK / 16;                 // 16-key P.V steps
-  constexpr int SPLIT = dec_split_keys(DH);
   auto& red_m = sm.red_m;
   auto& red_l = sm.red_l;
   auto& red_o = sm.red_o;
@@ -49,8 +49,11 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
   const DecItem it = a.items[item];
   const int t = it.t, n_keys = it.n_keys, split = it.split, n_split = it.n_split;
   const int G = a.hq / a.hkv;
-  const int k_begin = split * SPLIT;
-  const int n_tiles = (min(n_keys - k_begin, SPLIT) + TK - 1) / TK;
+  const int k_begin = split * a.unit_keys;
+  const int n_tiles = (min(n_keys - k_begin, a.unit_keys) + TK - 1) / TK;
+  // The range lies in one page (of a slot or the packed buffer): its first
+  // key sits at key0 = k_begin rounded down to the page size.
+  const int key0 = k_begin - k_begin % a.page_keys;
   const int my_tiles = n_tiles > wave ? (n_tiles - wave + 3) / 4 : 0;
   const int qh = min(fr, G - 1);  // query head of this lane's column (padding lanes repeat the last)
   const int64_t kbase = it.kbase + int64_t(g) * a.kv_head_stride;
@@ -72,11 +75,11 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
 
   // K rows (A operand of S^T = K Q^T, rows permuted by perm32) and V^T rows
   // (A operand of O^T = V^T P^T) of tile `ti` of the range, through buffer
-  // resources based at this row's slot and head: per-lane offsets are fixed,
-  // the tile moves the scalar offset.  A tile is one 32-key value tile of the
-  // cache, and its key rows are contiguous too.  Keys past the last one stay
-  // inside the slot (ranges are whole tiles of a slot whose length is a
-  // multiple of 64); their scores are masked below.
+  // resources based at the range's page and head: per-lane offsets are
+  // fixed, the tile moves the scalar offset.  A tile is one 32-key value tile
+  // of the cache, and its key rows are contiguous too.  Keys past the last
+  // one stay inside the page (ranges are whole tiles of a page whose length
+  // is a multiple of 64); their scores are masked below.
   static_assert(TK == kv_tile_keys, "a tile is one value tile of the cache");
   const __amdgpu_buffer_rsrc_t kres =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.kstore + kbase), 0, 0x7ffffff0, 0x00020000);
@@ -90,7 +93,7 @@ __device__ __forceinline__ void decode_attn_unit(const DecodeAttnArgs& a, int it
     u32x4 v[NDS][NPB];
   };
   auto load_tile = [&](int ti, Tile& tl) {
-    const int kv0 = k_begin + ti * TK;
+    const int kv0 = k_begin + ti * TK - key0;  // key index inside the page
 #pragma unroll
     for (int st = 0; st < NST; ++st) {
       const uint32_t so = uint32_t((kv0 + 32 * st) * DH * 2);

@@ -80,8 +80,9 @@ struct AttnArgs {
   const int32_t* seq_start; // [B] first packed row
   const int32_t* seq_len;   // [B] query rows
   const int32_t* seq_ctx;   // [B] cached rows before the chunk
-  const int64_t* seq_kbase; // [B] element offset of key position 0 (head 0)
-  const int64_t* seq_vbase; // [B] element offset of value position 0 (head 0, dim 0), tile aligned
+  const int32_t* seq_page0; // [B] index of the sequence's first page in page_base
+  const int64_t* page_base; // element offset of a page's position 0 (head 0, dim 0); keys and values alike
+  int page_keys;            // positions per page, a multiple of 64 (one key tile never straddles pages)
   int64_t kv_head_stride;
   int hq, hkv, dh;
   float scale_log2;         // log2(e) / sqrt(dh)
@@ -90,15 +91,16 @@ struct AttnArgs {
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 
 // Single-row (decode) attention: one block per (work item, key/value head);
-// a work item is one key range (dec_split_keys keys) of one row and carries
-// everything the block needs, so the K/V loads follow a single record load.
+// a work item is one key range (unit_keys keys, inside one page) of one row
+// and carries everything the block needs, so the K/V loads follow a single
+// record load.
 struct DecItem {
   int32_t t;        // packed row of the query
   int32_t n_keys;   // keys the row attends to (cached prefix + itself)
-  int32_t split;    // key range split * dec_split_keys ..
+  int32_t split;    // key range split * unit_keys ..
   int32_t n_split;  // splits of this row (its items are consecutive)
-  int64_t kbase;    // element offset of key position 0, head 0
-  int64_t vbase;    // element offset of value position 0, head 0, dim 0
+  int64_t kbase;    // element offset of position 0 (head 0) of the page holding the range
+  int64_t vbase;    // the same for values (dim 0)
 };
 static_assert(sizeof(DecItem) == 32, "decode item record");
 
@@ -113,6 +115,8 @@ struct DecodeAttnArgs {
   float* part;              // [n_items][hkv][dec_part_floats] partial states of split rows
   int32_t* counters;        // [n_items * hkv] arrival counters (first item of a row), zero on entry and exit
   int64_t kv_head_stride;
+  int page_keys;            // positions per page (the key range's page starts at split * unit_keys rounded down)
+  int unit_keys;            // keys per work item: divides dec_split_keys(dh), and page_keys on a paged cache
   int hq, hkv, dh;
   float scale_log2;
 };

@@ -119,18 +119,32 @@ static SkinnyNeeds skinny_needs(const hs_layer_cfg& c, int32_t T) {
   return n;
 }
 
-// Upper bound on decode work items: every single-row sequence split by the
-// longest possible key range.
-static int64_t max_dec_items(int32_t T, int32_t B, int32_t max_pos, int dh) {
-  return int64_t(std::min(T, B)) * dec_splits(max_pos, dh);
+int32_t dec_unit_keys(int dh, int32_t page_keys) {
+  const int32_t split = dec_split_keys(dh);
+  return page_keys > 0 ? std::gcd(split, page_keys) : split;
 }
 
-static size_t meta_bytes(int32_t T, int32_t B, int64_t att, int32_t counters, int64_t dec_items, int64_t dec_count) {
+static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Upper bound on decode work items: every single-row sequence split by the
+// longest possible key range.
+static int64_t max_dec_items(int32_t T, int32_t B, int32_t max_pos, int32_t unit) {
+  return int64_t(std::min(T, B)) * ceil_div(max_pos, unit);
+}
+
+// Upper bound on listed pages: one per sequence without a table, else every
+// page up to max_pos for every sequence.
+static int64_t max_pages(int32_t B, int32_t max_pos, int32_t page_keys) {
+  return page_keys > 0 ? int64_t(B) * ceil_div(max_pos, page_keys) : int64_t(B);
+}
+
+static size_t meta_bytes(int32_t T, int32_t B, int64_t pages, int64_t att, int32_t counters, int64_t dec_items,
+                         int64_t dec_count) {
   size_t s = 0;
   s += align_up(size_t(T) * 4, 16);       // pos
   s += align_up(size_t(T) * 8, 16) * 2;   // k_off, v_off
-  s += align_up(size_t(B) * 4, 16) * 3;   // seq_start, seq_len, seq_ctx
-  s += align_up(size_t(B) * 8, 16) * 2;   // seq_kbase, seq_vbase
+  s += align_up(size_t(B) * 4, 16) * 4;   // seq_start, seq_len, seq_ctx, seq_page0
+  s += align_up(size_t(pages) * 8, 16);   // page_base
   s += align_up(size_t(att) * 8, 16);     // att items
   s += align_up(size_t(B) * 16, 16);      // single-row (decode) rows
   s += align_up(size_t(counters) * 4, 16); // split-K counters
@@ -139,7 +153,7 @@ static size_t meta_bytes(int32_t T, int32_t B, int64_t att, int32_t counters, in
   return align_up(s, kAlign);
 }
 
-WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos) {
+WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos, int32_t page_keys) {
   WsLayout w{};
   const size_t d = c.hidden, hq = c.n_q_heads, hkv = c.n_kv_heads, dh = c.head_dim, f = c.ffn;
   size_t p = 0;
@@ -149,8 +163,9 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
     return at;
   };
   const SkinnyNeeds sk = skinny_needs(c, T);
-  const int64_t dec_items = max_dec_items(T, B, max_pos, c.head_dim);
-  w.meta_bytes = meta_bytes(T, B, max_att_items(T, B), sk.counters, dec_items, dec_items * c.n_kv_heads);
+  const int64_t dec_items = max_dec_items(T, B, max_pos, dec_unit_keys(c.head_dim, page_keys));
+  w.meta_bytes = meta_bytes(T, B, max_pages(B, max_pos, page_keys), max_att_items(T, B), sk.counters, dec_items,
+                            dec_items * c.n_kv_heads);
   w.meta = take(w.meta_bytes);
   // GEMM inputs of decode-sized batches are k-group-major over padded rows.
   const size_t act_rows = T <= kSkinnyMaxRows ? size_t(skinny_k8_rows(T)) : size_t(T);
@@ -175,6 +190,41 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos)
   w.dec_part = take(w.dec_part_bytes);
   w.total = p;
   return w;
+}
+
+hs_status check_block_table(const int32_t* table, int32_t pps, int32_t n_slots, int32_t page_keys,
+                            const int32_t* off, const int32_t* ctx, int32_t B) {
+  if (!table) return fail(HS_ERR_INVALID_ARG, "block table is null");
+  if (pps < 1) return fail(HS_ERR_INVALID_ARG, "pages_per_seq %d must be >= 1", pps);
+  if (n_slots < 1) return fail(HS_ERR_INVALID_ARG, "the cache has %d slots", n_slots);
+  if (page_keys < 64 || page_keys % 64 != 0)
+    return fail(HS_ERR_INVALID_ARG, "page size %d must be a positive multiple of 64", page_keys);
+  // writer[s]: the sequence that writes slot s in this call (-1: none);
+  // reader[s]: a sequence that reaches slot s (-1: none yet), -2: several.
+  std::vector<int32_t> writer(size_t(n_slots), -1), reader(size_t(n_slots), -1);
+  std::vector<int32_t> seen(size_t(n_slots), -1);
+  for (int32_t b = 0; b < B; ++b) {
+    const int64_t cx = ctx ? ctx[b] : 0, end = cx + (off[b + 1] - off[b]);
+    const int64_t n = ceil_div(end, page_keys);
+    if (n > pps)
+      return fail(HS_ERR_INVALID_ARG, "sequence %d reaches position %lld, beyond its %d pages of %d", b,
+                  (long long)(end - 1), pps, page_keys);
+    for (int64_t j = 0; j < n; ++j) {
+      const int32_t s = table[int64_t(b) * pps + j];
+      if (s < 0 || s >= n_slots)
+        return fail(HS_ERR_INVALID_ARG, "block_table[%d][%lld] = %d outside [0, %d)", b, (long long)j, s, n_slots);
+      if (seen[s] == b)
+        return fail(HS_ERR_INVALID_ARG, "sequence %d lists slot %d twice", b, s);
+      seen[s] = b;
+      reader[s] = (reader[s] == -1 || reader[s] == b) ? b : -2;
+      if (j >= cx / page_keys && end > cx) writer[s] = b;  // page j receives rows cx .. end - 1
+    }
+  }
+  for (int32_t s = 0; s < n_slots; ++s)
+    if (writer[s] >= 0 && reader[s] != writer[s])
+      return fail(HS_ERR_INVALID_ARG, "slot %d receives rows of sequence %d but other sequences reach it too", s,
+                  writer[s]);
+  return HS_OK;
 }
 
 hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* ctx, int32_t B,
@@ -221,16 +271,27 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   P.seq_start = take(size_t(B) * 4);
   P.seq_len = take(size_t(B) * 4);
   P.seq_ctx = take(size_t(B) * 4);
-  P.seq_kbase = take(size_t(B) * 8);
-  P.seq_vbase = take(size_t(B) * 8);
   P.att_items = take(size_t(P.n_att_items) * 8);
   P.dec_rows = take(size_t(P.n_dec_rows) * 16);
   P.n_counters = skinny_needs(c, int32_t(T)).counters;
   P.counters = take(size_t(P.n_counters) * 4);
+  // Pages: a slot, or the packed buffer, is one page per sequence; with a
+  // block table every page a sequence reaches is listed.
+  const bool paged = kv.cache && kv.table;
+  const int64_t slot_ctx = kv.cache ? kv.max_ctx : kv.packed_ctx;
+  P.page_keys = int32_t(slot_ctx);
+  P.unit_keys = dec_unit_keys(int(dh), paged ? kv.max_ctx : 0);
+  P.n_pages = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    const int64_t end = (ctx ? ctx[b] : 0) + (off[b + 1] - off[b]);
+    P.n_pages += paged ? int32_t(ceil_div(end, slot_ctx)) : 1;
+  }
+  P.seq_page0 = take(size_t(B) * 4);
+  P.page_base = take(size_t(P.n_pages) * 8);
   std::vector<int32_t> dec_nsplit(dec_seq.size());
   P.n_dec_items = 0;
   for (size_t r = 0; r < dec_seq.size(); ++r) {
-    dec_nsplit[r] = dec_splits((ctx ? ctx[dec_seq[r]] : 0) + 1, int(dh));
+    dec_nsplit[r] = int32_t(ceil_div((ctx ? ctx[dec_seq[r]] : 0) + 1, P.unit_keys));
     P.n_dec_items += dec_nsplit[r];
   }
   P.dec_items = take(size_t(P.n_dec_items) * 32);
@@ -240,30 +301,39 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   auto i32 = [&](size_t at) { return reinterpret_cast<int32_t*>(P.image.data() + at); };
   auto i64 = [&](size_t at) { return reinterpret_cast<int64_t*>(P.image.data() + at); };
 
-  // Cache: slot b holds hkv heads of max_ctx positions.  Packed (no cache):
-  // one slot of packed_ctx positions in which sequence b starts at the
-  // 64-aligned position base_b, so its key tiles line up with the value
-  // tiles.  Position p of a sequence: key element (base + p) * dh of head 0,
-  // value element ((base + p) / 32) * 32 dh + (base + p) % 32.
-  const int64_t slot_ctx = kv.cache ? kv.max_ctx : kv.packed_ctx;
+  // A page (a cache slot) holds hkv heads of slot_ctx positions.  Without a
+  // table sequence b has one page: slot b, or, packed (no cache), the
+  // positions from the 64-aligned base_b of one buffer of packed_ctx
+  // positions, so its key tiles line up with the value tiles.  Position p of
+  // a sequence lies in its page p / slot_ctx at i = p % slot_ctx: key element
+  // base + i * dh of head 0, value element base + (i / 32) * 32 dh + i % 32.
   P.kv_head_stride = slot_ctx * dh;
-  const int64_t slot = hkv * slot_ctx * dh;  // elements per cache slot (K and V alike)
+  const int64_t slot = hkv * slot_ctx * dh;  // elements per page (K and V alike)
   constexpr int64_t VT = kv_tile_keys;
   int64_t packed_base = 0;
+  int32_t page = 0;
   for (int32_t b = 0; b < B; ++b) {
     const int32_t cx = ctx ? ctx[b] : 0;
     const int32_t len = off[b + 1] - off[b];
     i32(P.seq_start)[b] = off[b];
     i32(P.seq_len)[b] = len;
     i32(P.seq_ctx)[b] = cx;
-    const int64_t base = kv.cache ? int64_t(b) * slot : packed_base * dh;  // element of position 0, head 0
-    i64(P.seq_kbase)[b] = base;
-    i64(P.seq_vbase)[b] = base;
+    i32(P.seq_page0)[b] = page;
+    int64_t* pages = i64(P.page_base) + page;
+    if (paged) {
+      const int32_t n = int32_t(ceil_div(int64_t(cx) + len, slot_ctx));
+      for (int32_t j = 0; j < n; ++j) pages[j] = int64_t(kv.table[int64_t(b) * kv.pages_per_seq + j]) * slot;
+      page += n;
+    } else {
+      pages[0] = kv.cache ? int64_t(b) * slot : packed_base * dh;
+      page += 1;
+    }
     for (int32_t t = off[b]; t < off[b + 1]; ++t) {
       const int64_t pos = cx + (t - off[b]);
+      const int64_t base = pages[pos / slot_ctx], i = pos % slot_ctx;
       i32(P.pos)[t] = int32_t(pos);
-      i64(P.k_off)[t] = base + pos * dh;
-      i64(P.v_off)[t] = base + (pos / VT) * VT * dh + pos % VT;
+      i64(P.k_off)[t] = base + i * dh;
+      i64(P.v_off)[t] = base + (i / VT) * VT * dh + i % VT;
     }
     if (!kv.cache) packed_base += int64_t(align_up(size_t(len), 64));
   }
@@ -283,14 +353,16 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
     row[2] = 0;
     row[3] = 0;
     for (int32_t sp = 0; sp < dec_nsplit[r]; ++sp, ++item) {
-      // Record layout: int32 t, n_keys, split, n_split; int64 K base, V base.
+      // Record layout: int32 t, n_keys, split, n_split; int64 K base, V base:
+      // the page holding the split's keys (a unit never straddles pages).
       int32_t* it = i32(P.dec_items + size_t(item) * 32);
       it[0] = off[b];
       it[1] = (ctx ? ctx[b] : 0) + 1;
       it[2] = sp;
       it[3] = dec_nsplit[r];
-      i64(P.dec_items + size_t(item) * 32 + 16)[0] = i64(P.seq_kbase)[b];
-      i64(P.dec_items + size_t(item) * 32 + 16)[1] = i64(P.seq_vbase)[b];
+      const int64_t base = i64(P.page_base)[i32(P.seq_page0)[b] + int64_t(sp) * P.unit_keys / slot_ctx];
+      i64(P.dec_items + size_t(item) * 32 + 16)[0] = base;
+      i64(P.dec_items + size_t(item) * 32 + 16)[1] = base;
     }
   }
   return HS_OK;
@@ -388,6 +460,19 @@ hs_status hs_workspace_size(const hs_layer_cfg* cfg, int32_t max_tokens, int32_t
   if (max_tokens < 1 || max_seqs < 1 || max_pos < 1)
     return hs::fail(HS_ERR_INVALID_ARG, "sizes must be >= 1");
   *bytes = hs::ws_layout(*cfg, max_tokens, max_seqs, max_pos).total;
+  return HS_OK;
+}
+
+hs_status hs_workspace_size_paged(const hs_layer_cfg* cfg, int32_t max_tokens, int32_t max_seqs, int32_t max_pos,
+                                  int32_t page_positions, size_t* bytes) {
+  hs_status st = hs::validate_cfg(cfg);
+  if (st != HS_OK) return st;
+  if (!bytes) return hs::fail(HS_ERR_INVALID_ARG, "bytes output is null");
+  if (max_tokens < 1 || max_seqs < 1 || max_pos < 1)
+    return hs::fail(HS_ERR_INVALID_ARG, "sizes must be >= 1");
+  if (page_positions < 0 || page_positions % 64 != 0)
+    return hs::fail(HS_ERR_INVALID_ARG, "page size %d must be 0 or a positive multiple of 64", page_positions);
+  *bytes = hs::ws_layout(*cfg, max_tokens, max_seqs, max_pos, page_positions).total;
   return HS_OK;
 }
 

@@ -54,7 +54,13 @@ struct WsLayout {
 // Upper bounds used for sizing: T rows, B sequences, positions < max_pos.
 int64_t max_att_items(int32_t T, int32_t B);
 
-WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos);
+// page_keys: positions per page of a paged cache, 0 without a block table.
+WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos, int32_t page_keys = 0);
+
+// Keys per single-row attention work unit: the head size's split, cut down
+// to a divisor of the page size on a paged cache so that no unit straddles
+// two pages.
+int32_t dec_unit_keys(int dh, int32_t page_keys);
 
 // Metadata of one call, laid out as one host image mirrored in the workspace.
 struct Plan {
@@ -62,7 +68,12 @@ struct Plan {
   std::vector<uint8_t> image;
   // byte offsets inside image
   size_t pos = 0, k_off = 0, v_off = 0;
-  size_t seq_start = 0, seq_len = 0, seq_ctx = 0, seq_kbase = 0, seq_vbase = 0;
+  size_t seq_start = 0, seq_len = 0, seq_ctx = 0;
+  size_t seq_page0 = 0;  // [B] int32: index of the sequence's first page in page_base
+  size_t page_base = 0;  // [n_pages] int64: element offset of a page's position 0, head 0
+  int32_t n_pages = 0;
+  int32_t page_keys = 0;  // positions per page (a slot, or the packed buffer, is one page)
+  int32_t unit_keys = 0;  // keys per single-row attention work unit
   size_t att_items = 0, dec_rows = 0;
   size_t counters = 0;  // split-K arrival counters of the skinny GEMM, zero in the image
   size_t dec_items = 0;  // [n_dec_items] 32-byte records (row, keys, split, splits, K base, V base)
@@ -71,12 +82,21 @@ struct Plan {
   int64_t kv_head_stride = 0;
 };
 
-// Key/value placement: packed (no cache, rows in the workspace) or cache slots.
+// Key/value placement: packed (no cache, rows in the workspace), cache slots
+// (sequence b in slot b) or pages named by a block table.
 struct KvPlacement {
   bool cache = false;
-  int32_t max_ctx = 0;
+  int32_t max_ctx = 0;             // positions per slot (per page with a table)
   int64_t packed_ctx = 0;
+  const int32_t* table = nullptr;  // host [B][pages_per_seq] slot indices, or null
+  int32_t pages_per_seq = 0;
 };
+
+// Checks a block table against a batch: every page a sequence reaches names
+// a slot in [0, n_slots), no sequence lists a page twice among the pages it
+// reaches, and a page that receives new rows is reached by no other sequence.
+hs_status check_block_table(const int32_t* table, int32_t pages_per_seq, int32_t n_slots, int32_t page_keys,
+                            const int32_t* seq_offsets, const int32_t* ctx_lens, int32_t n_seqs);
 
 hs_status build_plan(const hs_layer_cfg& c, const int32_t* seq_offsets, const int32_t* ctx_lens,
                      int32_t n_seqs, const KvPlacement& kv, Plan* out);

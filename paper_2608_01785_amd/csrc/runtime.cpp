@@ -238,10 +238,18 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
       if (!kv->k[l] || !kv->v[l]) return hs::fail(HS_ERR_INVALID_ARG, "cache of layer %d is null", l);
     if (kv->max_ctx < 64 || kv->max_ctx % 64 != 0)
       return hs::fail(HS_ERR_INVALID_ARG, "max_ctx %d must be a positive multiple of 64", kv->max_ctx);
-    if (n_seqs > kv->n_slots)
-      return hs::fail(HS_ERR_INVALID_ARG, "%d sequences but only %d cache slots", n_seqs, kv->n_slots);
-    if (max_pos > kv->max_ctx)
-      return hs::fail(HS_ERR_INVALID_ARG, "position %d exceeds max_ctx %d", max_pos - 1, kv->max_ctx);
+    if (kv->block_table) {
+      st = hs::check_block_table(kv->block_table, kv->pages_per_seq, kv->n_slots, kv->max_ctx, seq_offsets,
+                                 ctx_lens, n_seqs);
+      if (st != HS_OK) return st;
+      place.table = kv->block_table;
+      place.pages_per_seq = kv->pages_per_seq;
+    } else {
+      if (n_seqs > kv->n_slots)
+        return hs::fail(HS_ERR_INVALID_ARG, "%d sequences but only %d cache slots", n_seqs, kv->n_slots);
+      if (max_pos > kv->max_ctx)
+        return hs::fail(HS_ERR_INVALID_ARG, "position %d exceeds max_ctx %d", max_pos - 1, kv->max_ctx);
+    }
     place.cache = true;
     place.max_ctx = kv->max_ctx;
   } else if (ctx_lens) {
@@ -254,7 +262,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
   st = resolve_stream(ctx, budget, role, stream, &s);
   if (st != HS_OK) return st;
   if (!ws) return hs::fail(HS_ERR_WORKSPACE, "workspace is null");
-  const hs::WsLayout lay = hs::ws_layout(*cfg, T, n_seqs, max_pos);
+  const hs::WsLayout lay = hs::ws_layout(*cfg, T, n_seqs, max_pos, place.table ? place.max_ctx : 0);
   if (ws_bytes < lay.total)
     return hs::fail(HS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, lay.total);
   place.packed_ctx = lay.packed_ctx;
@@ -347,8 +355,9 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     at_args.seq_start = reinterpret_cast<const int32_t*>(meta + plan.seq_start);
     at_args.seq_len = reinterpret_cast<const int32_t*>(meta + plan.seq_len);
     at_args.seq_ctx = reinterpret_cast<const int32_t*>(meta + plan.seq_ctx);
-    at_args.seq_kbase = reinterpret_cast<const int64_t*>(meta + plan.seq_kbase);
-    at_args.seq_vbase = reinterpret_cast<const int64_t*>(meta + plan.seq_vbase);
+    at_args.seq_page0 = reinterpret_cast<const int32_t*>(meta + plan.seq_page0);
+    at_args.page_base = reinterpret_cast<const int64_t*>(meta + plan.page_base);
+    at_args.page_keys = plan.page_keys;
     at_args.kv_head_stride = plan.kv_head_stride;
     at_args.hq = hq;
     at_args.hkv = hkv;
@@ -367,6 +376,8 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     da.part = lay.dec_part_bytes ? at<float>(ws, lay.dec_part) : nullptr;
     da.counters = reinterpret_cast<int32_t*>(meta + plan.dec_count);
     da.kv_head_stride = plan.kv_head_stride;
+    da.page_keys = plan.page_keys;
+    da.unit_keys = plan.unit_keys;
     da.hq = hq;
     da.hkv = hkv;
     da.dh = dh;

@@ -110,3 +110,39 @@ class DeviceCache:
         v_all = self.v[layer][slot].transpose(2, 3).reshape(self.hkv, self.max_ctx, self.dh)
         v = f16_bits_of(v_all[:, start:stop].permute(1, 0, 2))
         return k, v
+
+
+class PagedCache(DeviceCache):
+    """A pool of n_pages pages of page_size positions per layer, plus a block table.
+
+    Sequence b's position p lives in page table[b, p // page_size] at position
+    p % page_size; a page is a slot of the DeviceCache layout.
+    """
+
+    def __init__(self, n_layers: int, n_pages: int, page_size: int, n_kv_heads: int, head_dim: int,
+                 table: np.ndarray, device="cuda", fill: Optional[float] = None):
+        super().__init__(n_layers, n_pages, page_size, n_kv_heads, head_dim, device, fill)
+        self.page_size = page_size
+        self.table = np.ascontiguousarray(table, dtype=np.int32)
+
+    def as_arg(self):
+        return (self.k, self.v, self.n_slots, self.max_ctx, self.table)
+
+    def load_prefix(self, layer: int, seq: int, k_bits: np.ndarray, v_bits: np.ndarray) -> None:
+        """Place logical [n, Hkv, dh] rows at positions 0..n-1 of sequence `seq`."""
+        P = self.page_size
+        for j in range(0, k_bits.shape[0], P):
+            super().load_prefix(layer, int(self.table[seq, j // P]), k_bits[j:j + P], v_bits[j:j + P])
+
+    def rows(self, layer: int, seq: int, start: int, stop: int):
+        """Logical [stop - start, Hkv, dh] K and V rows of sequence `seq` as fp16 bits on the host."""
+        P, ks, vs = self.page_size, [], []
+        p = start
+        while p < stop:
+            j, lo = divmod(p, P)
+            hi = min(stop - j * P, P)
+            k, v = super().rows(layer, int(self.table[seq, j]), lo, hi)
+            ks.append(k)
+            vs.append(v)
+            p = j * P + hi
+        return np.concatenate(ks), np.concatenate(vs)

@@ -147,14 +147,111 @@ def test_forward_validation_fails_before_any_gpu_work(b):
     assert st == b.HS_ERR_UNSUPPORTED
 
 
+def _fake_kv(b, n_slots, page, table=None, n_layers=1):
+    """A cache struct with fake (never dereferenced) layer pointers and an optional block table."""
+    from paper_2608_01785_amd import binding
+    return binding._kv_struct(([0x5000] * n_layers, [0x6000] * n_layers, n_slots, page, table))
+
+
+def test_paged_cache_validation_fails_before_any_gpu_work(b):
+    from paper_2608_01785_amd import workloads as W
+    c = W.TINY
+
+    def call(offsets, ctx_lens, n_slots, page, table):
+        kv = _fake_kv(b, n_slots, page, None if table is None else np.asarray(table, np.int32))
+        return _forward_null_ctx(b, c, offsets, ctx_lens=ctx_lens, kv=ctypes.byref(kv))
+
+    # Valid: two sequences share a read-only prefix page (slot 3) and write their own pages.
+    st, msg = call([0, 10, 30], [128, 200], 6, 128, [[3, 0, 5], [3, 1, 5]])
+    assert st == b.HS_ERR_INVALID_ARG and "context" in msg, msg
+    # The same batch without a table needs positions < max_ctx.
+    st, msg = call([0, 10, 30], [128, 200], 6, 128, None)
+    assert st == b.HS_ERR_INVALID_ARG and "exceeds max_ctx" in msg, msg
+    # Page size not a multiple of 64.
+    st, msg = call([0, 10], [0], 6, 96, [[0]])
+    assert st == b.HS_ERR_INVALID_ARG and "multiple of 64" in msg, msg
+    # Slot index outside the pool.
+    st, msg = call([0, 10], [100], 2, 64, [[0, 2]])
+    assert st == b.HS_ERR_INVALID_ARG and "outside" in msg, msg
+    # Positions beyond the sequence's pages.
+    st, msg = call([0, 10], [120], 6, 64, [[0, 1]])
+    assert st == b.HS_ERR_INVALID_ARG and "beyond" in msg, msg
+    # One sequence listing a slot twice.
+    st, msg = call([0, 10], [120], 6, 64, [[4, 4, 1]])
+    assert st == b.HS_ERR_INVALID_ARG and "twice" in msg, msg
+    # A page receiving rows of one sequence and reached by another.
+    st, msg = call([0, 10, 11], [60, 70], 6, 64, [[0, 1], [0, 1]])
+    assert st == b.HS_ERR_INVALID_ARG and "other sequences" in msg, msg
+    # Entries past the pages a sequence reaches are not read (-1 there is fine).
+    st, msg = call([0, 10], [0], 6, 64, [[2, -1, -1]])
+    assert st == b.HS_ERR_INVALID_ARG and "context" in msg, msg
+
+
+def test_paged_workspace_size(b):
+    from paper_2608_01785_amd import workloads as W
+    c = W.TALKER
+    plain = b.hs_workspace_size(c, 128, 128, 4096)
+    assert b.hs_workspace_size_paged(c, 128, 128, 4096, 0) == plain
+    assert b.hs_workspace_size_paged(c, 128, 128, 4096, 1024) >= plain
+    # Smaller pages cut single-row attention into more work units.
+    assert b.hs_workspace_size_paged(c, 128, 128, 4096, 64) > b.hs_workspace_size_paged(c, 128, 128, 4096, 1024)
+    for bad in (-64, 100):
+        with pytest.raises(b.HorizonError) as e:
+            b.hs_workspace_size_paged(c, 128, 128, 4096, bad)
+        assert e.value.status == b.HS_ERR_INVALID_ARG
+
+
 def test_host_planner_under_sanitizers(tmp_path):
     """Build the host-only planner and controller with g++ and ASan/UBSan and drive their entry points."""
     gxx = "g++"
     drv = tmp_path / "drv.cpp"
     drv.write_text(r'''
 #include "horizon.h"
+#include "plan.h"
+#include "decode_policy.h"
 #include <stdio.h>
 #include <vector>
+// A paged plan: every row's key/value offset and every single-row unit's page
+// base follow the block table, and every unit's keys stay inside its page.
+static int paged_plan_check() {
+  hs_layer_cfg c = {256, 4, 2, 64, 1024, 1e-6f, 1e4f};
+  const int P = 64, pps = 40, n_slots = 200, dh = 64, hkv = 2;
+  int off[] = {0, 1, 2, 150, 151};
+  int ctx[] = {0, 1999, 100, 64};
+  std::vector<int> table(4 * pps, -1);
+  int next = 0;
+  for (int b = 0; b < 4; ++b) {
+    const int end = ctx[b] + off[b + 1] - off[b];
+    for (int j = 0; j * P < end; ++j) table[b * pps + j] = (next++ * 7) % n_slots;
+  }
+  if (hs::check_block_table(table.data(), pps, n_slots, P, off, ctx, 4) != HS_OK) return 1;
+  hs::KvPlacement kv;
+  kv.cache = true; kv.max_ctx = P; kv.table = table.data(); kv.pages_per_seq = pps;
+  hs::Plan plan;
+  if (hs::build_plan(c, off, ctx, 4, kv, &plan) != HS_OK) return 2;
+  const int64_t slot = int64_t(hkv) * P * dh;
+  const int64_t* koff = reinterpret_cast<const int64_t*>(plan.image.data() + plan.k_off);
+  const int64_t* voff = reinterpret_cast<const int64_t*>(plan.image.data() + plan.v_off);
+  for (int b = 0; b < 4; ++b)
+    for (int t = off[b]; t < off[b + 1]; ++t) {
+      const int p = ctx[b] + t - off[b], s = table[b * pps + p / P], i = p % P;
+      if (koff[t] != s * slot + int64_t(i) * dh) return 3;
+      if (voff[t] != s * slot + int64_t(i / 32) * 32 * dh + i % 32) return 4;
+    }
+  if (plan.unit_keys != 64 || plan.page_keys != P) return 5;
+  for (int it = 0; it < plan.n_dec_items; ++it) {
+    const int32_t* r = reinterpret_cast<const int32_t*>(plan.image.data() + plan.dec_items + size_t(it) * 32);
+    const int64_t base = *reinterpret_cast<const int64_t*>(plan.image.data() + plan.dec_items + size_t(it) * 32 + 16);
+    int b = 0;
+    while (off[b] != r[0]) ++b;
+    const int k_begin = r[2] * plan.unit_keys;
+    if (k_begin >= r[1] || base != table[b * pps + k_begin / P] * slot) return 6;
+    if (k_begin % P + plan.unit_keys > P) return 7;  // the unit stays in its page
+  }
+  if (hs::dec_unit_keys(128, 1024) != 512 || hs::dec_unit_keys(64, 192) != 64 || hs::dec_unit_keys(64, 0) != 1024)
+    return 8;
+  return 0;
+}
 int main() {
   hs_topology t;
   if (hs_default_topology(256, 8, &t) != HS_OK) return 1;
@@ -168,6 +265,8 @@ int main() {
   hs_layer_cfg c = {3584, 28, 4, 128, 18944, 1e-6f, 1e4f};
   size_t n = 0;
   if (hs_workspace_size(&c, 10515, 8, 2048, &n) != HS_OK || n == 0) return 6;
+  size_t np = 0;
+  if (hs_workspace_size_paged(&c, 10515, 8, 2048, 64, &np) != HS_OK || np < n) return 10;
   int ladder[] = {64, 96, 128, 160, 192};
   hs_controller_cfg cc = {256, 256, ladder, 5, 0.4, 0.8, 1};
   hs_controller* ctrl = nullptr;
@@ -179,6 +278,7 @@ int main() {
   hs_controller_destroy(ctrl);
   cc.n_ladder = 0;
   if (hs_controller_create(&cc, &ctrl) != HS_ERR_INVALID_ARG) return 9;
+  if (paged_plan_check() != 0) return 11;
   printf("ok %zu\n", n);
   return 0;
 }
