@@ -349,6 +349,65 @@ hs_status hs_controller_destroy(hs_controller* ctrl);
  * it, or the reading, is unavailable. */
 hs_status hs_pressure_sample(int32_t device, double* activity);
 
+/* ------------------------------------------------------------------------
+ * Temporal scheduler: shared-stage path rotation (§4.2 "Remaining-slack
+ * ratio"; §4.3 "Path rotation", "Slack guard", "Adaptive rotation ratio",
+ * "Long-path admission cap"; Algorithm 1, steps 1 and 2).  Host only.
+ *
+ * Each call is one scheduling step k (counted from 0 per scheduler).  For
+ * every request of the queue:
+ *   u_i = (deadline - now) / remaining;  protected when u_i < u_guard.
+ * N = round(n_min + f (n_max - n_min)), halves upward, where f is the
+ * protected share of the waiting short-path prefills (0 when none wait).
+ * The step is a short-path phase when k mod (N + m) < N, else a long-path
+ * phase.  visible[i] = 1 for decode continuations, protected requests and
+ * prefills of the phase's path; other prefills get 0 for this step only.
+ * Then, if long_cap >= 0 and more than long_cap ordinary (unprotected)
+ * long-path prefills are visible, only the long_cap with the earliest
+ * deadlines stay visible (ties: lower index).  The caller batches from the
+ * visible requests; nothing of the queue is stored or reordered. */
+enum { HS_PATH_SHORT = 0, HS_PATH_LONG = 1 };
+enum { HS_WORK_PREFILL = 0, HS_WORK_DECODE = 1 };
+
+typedef struct hs_temporal_cfg {
+  int32_t n_min, n_max; /* short-path phases per cycle, 1 <= n_min <= n_max ([2, 8] in §4.3) */
+  int32_t m;            /* long-path phases per cycle, >= 1 (2 in §4.3) */
+  double u_guard;       /* slack guard, > 0 */
+  int32_t long_cap;     /* most ordinary long-path prefills per view; < 0: no cap */
+} hs_temporal_cfg;
+
+typedef struct hs_request_view {
+  int32_t path;      /* HS_PATH_SHORT: ends after the shared stage; HS_PATH_LONG: continues downstream */
+  int32_t work;      /* HS_WORK_PREFILL: waiting for its prefill; HS_WORK_DECODE: a decode continuation */
+  double deadline;   /* first-response deadline d_i = a_i + Delta_c, finite */
+  double remaining;  /* estimated remaining time to the first response, > 0, same unit */
+} hs_request_view;
+
+typedef struct hs_temporal_step_info {
+  int64_t step;        /* k of this call */
+  int32_t n;           /* N used by this step */
+  int32_t phase;       /* HS_PATH_* of this step */
+  int32_t n_protected; /* requests with u_i < u_guard */
+  int32_t n_hidden;    /* prefills hidden by the phase */
+  int32_t n_capped;    /* long-path prefills hidden by the cap */
+} hs_temporal_step_info;
+
+typedef struct hs_temporal hs_temporal;
+
+/* Errors: HS_ERR_INVALID_ARG for a null pointer, n_min < 1, n_min > n_max,
+ * m < 1 or u_guard not a positive finite number.  The scheduler copies the
+ * configuration; release it with hs_temporal_destroy. */
+hs_status hs_temporal_create(const hs_temporal_cfg* cfg, hs_temporal** out);
+
+/* reqs[n_reqs] and visible[n_reqs] are host arrays owned by the caller; info
+ * may be NULL.  Errors (HS_ERR_INVALID_ARG, nothing written and the step not
+ * counted): null pointers with n_reqs > 0, n_reqs < 0, a non-finite now or
+ * deadline, remaining <= 0, or an unknown path or work code. */
+hs_status hs_temporal_step(hs_temporal* s, double now, const hs_request_view* reqs, int32_t n_reqs,
+                           uint8_t* visible, hs_temporal_step_info* info);
+
+hs_status hs_temporal_destroy(hs_temporal* s);
+
 #ifdef __cplusplus
 }
 #endif

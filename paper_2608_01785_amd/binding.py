@@ -25,6 +25,7 @@ SYMBOLS = (
     "hs_context_destroy", "hs_workspace_size", "hs_workspace_size_paged", "hs_shared_stage_forward", "hs_downstream_decode_step",
     "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read", "hs_convert_weights_f16",
     "hs_controller_create", "hs_controller_step", "hs_controller_destroy", "hs_pressure_sample",
+    "hs_temporal_create", "hs_temporal_step", "hs_temporal_destroy",
 )
 HS_WEIGHTS_BF16, HS_WEIGHTS_F16 = 0, 1
 
@@ -66,6 +67,25 @@ class ControllerCfg(ctypes.Structure):
                 ("ladder", ctypes.POINTER(ctypes.c_int32)), ("n_ladder", ctypes.c_int32),
                 ("ewma_weight", ctypes.c_double), ("saturation", ctypes.c_double),
                 ("hysteresis_steps", ctypes.c_int32)]
+
+
+HS_PATH_SHORT, HS_PATH_LONG = 0, 1
+HS_WORK_PREFILL, HS_WORK_DECODE = 0, 1
+
+
+class TemporalCfg(ctypes.Structure):
+    _fields_ = [("n_min", ctypes.c_int32), ("n_max", ctypes.c_int32), ("m", ctypes.c_int32),
+                ("u_guard", ctypes.c_double), ("long_cap", ctypes.c_int32)]
+
+
+class RequestView(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_int32), ("work", ctypes.c_int32), ("deadline", ctypes.c_double),
+                ("remaining", ctypes.c_double)]
+
+
+class TemporalStepInfo(ctypes.Structure):
+    _fields_ = [("step", ctypes.c_int64), ("n", ctypes.c_int32), ("phase", ctypes.c_int32),
+                ("n_protected", ctypes.c_int32), ("n_hidden", ctypes.c_int32), ("n_capped", ctypes.c_int32)]
 
 
 class Split(ctypes.Structure):
@@ -117,6 +137,10 @@ def lib() -> ctypes.CDLL:
             "hs_controller_step": [vp, i32, ctypes.c_double, ctypes.POINTER(Split)],
             "hs_controller_destroy": [vp],
             "hs_pressure_sample": [i32, ctypes.POINTER(ctypes.c_double)],
+            "hs_temporal_create": [ctypes.POINTER(TemporalCfg), ctypes.POINTER(vp)],
+            "hs_temporal_step": [vp, ctypes.c_double, ctypes.POINTER(RequestView), i32,
+                                 ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(TemporalStepInfo)],
+            "hs_temporal_destroy": [vp],
         }
         for name, args in sigs.items():
             fn = getattr(L, name)
@@ -232,6 +256,38 @@ def hs_controller_step(ctrl: Controller, downstream_active: bool, sample: float)
     out = Split()
     _check(lib().hs_controller_step(ctrl.handle, 1 if downstream_active else 0, float(sample), ctypes.byref(out)))
     return out
+
+
+class Temporal:
+    """Owns an hs_temporal handle (shared-stage path rotation)."""
+
+    def __init__(self, n_min: int = 2, n_max: int = 8, m: int = 2, u_guard: float = 1.0, long_cap: int = -1):
+        cfg = TemporalCfg(n_min, n_max, m, u_guard, long_cap)
+        h = ctypes.c_void_p()
+        _check(lib().hs_temporal_create(ctypes.byref(cfg), ctypes.byref(h)))
+        self.handle = h
+
+    def close(self):
+        if self.handle:
+            lib().hs_temporal_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):  # pragma: no cover
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def hs_temporal_step(sched: Temporal, now: float, requests) -> Tuple[np.ndarray, TemporalStepInfo]:
+    """requests: sequence of (path, work, deadline, remaining); returns (visible bool array, step info)."""
+    n = len(requests)
+    arr = (RequestView * max(n, 1))(*[RequestView(int(p), int(w), float(d), float(r)) for p, w, d, r in requests])
+    vis = np.zeros(max(n, 1), np.uint8)
+    info = TemporalStepInfo()
+    _check(lib().hs_temporal_step(sched.handle, float(now), arr, n, vis.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)),
+                                  ctypes.byref(info)))
+    return vis[:n].astype(bool), info
 
 
 def hs_pressure_sample(device: int = 0) -> float:

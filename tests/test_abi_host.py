@@ -202,7 +202,7 @@ def test_paged_workspace_size(b):
 
 
 def test_host_planner_under_sanitizers(tmp_path):
-    """Build the host-only planner and controller with g++ and ASan/UBSan and drive their entry points."""
+    """Build the host-only planner, controller and temporal scheduler with g++ and ASan/UBSan and drive them."""
     gxx = "g++"
     drv = tmp_path / "drv.cpp"
     drv.write_text(r'''
@@ -279,12 +279,25 @@ int main() {
   cc.n_ladder = 0;
   if (hs_controller_create(&cc, &ctrl) != HS_ERR_INVALID_ARG) return 9;
   if (paged_plan_check() != 0) return 11;
+  hs_temporal_cfg tc = {2, 8, 2, 1.0, 3};
+  hs_temporal* ts = nullptr;
+  if (hs_temporal_create(&tc, &ts) != HS_OK) return 12;
+  std::vector<hs_request_view> rq(40);
+  std::vector<uint8_t> vis(40);
+  hs_temporal_step_info ti;
+  for (int k = 0; k < 500; ++k) {
+    for (int i = 0; i < 40; ++i) rq[i] = {i % 2, (i % 7) == 0, double(i % 11) + 0.25 * k, 1.0 + (i % 3)};
+    if (hs_temporal_step(ts, 0.5 * k, rq.data(), 40 - k % 40, vis.data(), &ti) != HS_OK || ti.step != k) return 13;
+  }
+  rq[0].remaining = 0.0;
+  if (hs_temporal_step(ts, 0.0, rq.data(), 1, vis.data(), &ti) != HS_ERR_INVALID_ARG) return 14;
+  hs_temporal_destroy(ts);
   printf("ok %zu\n", n);
   return 0;
 }
 ''')
     exe = tmp_path / "drv"
-    srcs = [os.path.join(ROOT, "paper_2608_01785_amd", "csrc", f) for f in ("plan.cpp", "controller.cpp")]
+    srcs = [os.path.join(ROOT, "paper_2608_01785_amd", "csrc", f) for f in ("plan.cpp", "controller.cpp", "temporal.cpp")]
     cmd = [gxx, "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
            f"-I{os.path.join(ROOT, 'include')}", f"-I{os.path.join(ROOT, 'paper_2608_01785_amd', 'csrc')}",
            str(drv), *srcs, "-o", str(exe), "-ldl"]
