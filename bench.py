@@ -13,6 +13,7 @@ same workload (rank 0, N = 1 only).
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import gc
 import json
 import os
@@ -215,6 +216,12 @@ def main():
     if not args.no_controller:
         controller = controller_measure(torch, binding, ctx, [b for b in ladder if b < N_CUS], dev)
 
+    # ---------------------------------------------------------------- serving-loop model on measured times
+    policy = None
+    if corun is not None and "unmasked" in corun:
+        gc.collect()
+        policy = policy_model(W, shape, batch, per_budget, corun)
+
     # ---------------------------------------------------------------- CPU reference sample
     cpu = None
     if not args.no_cpu_baseline:
@@ -248,6 +255,7 @@ def main():
         "mixed_corun": mixed,
         "decode_tpot_vs_cus": tpot,
         "controller": controller,
+        "policy_model": policy,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
@@ -277,14 +285,40 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
     s_sh = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_SHARED))
     s_dn = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_DOWN))
 
-    def decode(n):
+    def decode(n, cus=128, stream=None, rec=None):
+        rec = s_dn if rec is None else rec
         ev = []
         for _ in range(n):
-            binding.hs_downstream_decode_step(ctx, ts_shape, tl, xt, yt, cache.as_arg(), kv_lens, 128, None, wst)
+            binding.hs_downstream_decode_step(ctx, ts_shape, tl, xt, yt, cache.as_arg(), kv_lens, cus, stream, wst)
             e = torch.cuda.Event(enable_timing=True)
-            e.record(s_dn)
+            e.record(rec)
             ev.append(e)
         return ev
+
+    def corun_window(prefill_stream, prefill_cus, dec_cus, dec_stream, dec_rec):
+        """Prefill forward with decode steps looping beside it: (window ms, decode ms per step, steps)."""
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        start.record(prefill_stream)
+        dec_rec.wait_event(start)
+        binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, None, None, prefill_cus, None, ws)
+        p_end = torch.cuda.Event(enable_timing=True)
+        p_end.record(prefill_stream)
+        dec_ev = []
+        while True:
+            dec_ev += decode(1, dec_cus, dec_stream, dec_rec)
+            if p_end.query():
+                break
+            if len(dec_ev) > 4:
+                dec_ev[-4].synchronize()
+            if len(dec_ev) > 2000:
+                break
+        torch.cuda.synchronize()
+        window = start.elapsed_time(p_end)
+        done = [start.elapsed_time(e) for e in dec_ev]
+        n_in = sum(1 for t in done if t <= window)
+        t_last = max([t for t in done if t <= window], default=0.0)
+        return window, (t_last / n_in if n_in else float("nan")), n_in
 
     # Solo decode on its 128 CUs.
     torch.cuda.synchronize()
@@ -372,6 +406,44 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
     }
     log(f"[bench] co-run: prefill {window:.2f} ms (solo {prefill_solo:.2f}), decode {dec_ms:.3f} ms/step "
         f"(solo {solo_ms:.3f}), {n_in} steps in window")
+
+    # Talker step time against its CU count (the complement of each ladder level).
+    sweep = {}
+    for c in (64, 128, 160, 192, 224, 240):
+        sc = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, N_CUS - c, binding.HS_ROLE_DOWN))
+        decode(3, c, None, sc)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e0.record(sc)
+        ev = decode(10, c, None, sc)
+        torch.cuda.synchronize()
+        sweep[c] = round(e0.elapsed_time(ev[-1]) / 10, 4)
+    res["decode_ms_vs_cus"] = sweep
+    log("[bench] talker step vs CUs: " + ", ".join(f"{c}: {v:.3f} ms" for c, v in sweep.items()))
+
+    # No spatial control: both stages on the whole chip (no CU masks), time-sharing it.
+    full = torch.cuda.Stream()
+    s_full = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 256, binding.HS_ROLE_SHARED))
+    decode(3, 256, full.cuda_stream, full)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e0.record(full)
+    ev = decode(20, 256, full.cuda_stream, full)
+    torch.cuda.synchronize()
+    full_solo = e0.elapsed_time(ev[-1]) / 20
+    p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    p0.record(s_full)
+    binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, None, None, 256, None, ws)
+    p1.record(s_full)
+    torch.cuda.synchronize()
+    prefill_full_solo = p0.elapsed_time(p1)
+    w_un, d_un, n_un = corun_window(s_full, 256, 256, full.cuda_stream, full)
+    res["unmasked"] = {"prefill_ms": round(w_un, 3), "prefill_solo_ms": round(prefill_full_solo, 3),
+                       "decode_ms_per_step": round(d_un, 4) if n_un else None,
+                       "decode_solo_ms_per_step": round(full_solo, 4),
+                       "decode_steps_in_window": n_un}
+    log(f"[bench] unmasked co-run: prefill {w_un:.2f} ms (solo {prefill_full_solo:.2f}), decode {d_un:.3f} ms/step "
+        f"(solo {full_solo:.3f}), {n_un} steps in window")
     return res
 
 
@@ -543,6 +615,46 @@ def thinker_decode_sweep(torch, binding, W, ctx, shape, wdev, n_layers, dev, bat
         return out
     finally:
         torch.cuda.synchronize()
+
+
+def policy_model(W, shape, batch, per_budget, corun):
+    """Algorithm 1's loop in the discrete-event model, with the times measured above (model output)."""
+    from paper_2608_01785_amd import sim
+    T = batch.n_tokens
+    ts = W.TALKER
+    weights = 16 * ts.params_per_layer * 2
+    un = corun["unmasked"]
+    t = sim.Timing(
+        prefill_ms_per_token={int(b): v["ms_per_step"] / T for b, v in per_budget.items()},
+        decode_ms_per_step={int(c): v for c, v in corun["decode_ms_vs_cus"].items()},
+        decode_batch=32, weight_share=weights / corun["decode_bytes_per_step"],
+        masked_prefill_factor=corun["prefill_ms"] / corun["prefill_solo_ms"],
+        masked_decode_factor=corun["decode_ms_per_step"] / corun["decode_solo_ms_per_step"],
+        unmasked_prefill_factor=un["prefill_ms"] / un["prefill_solo_ms"],
+        # No step finished beside an unmasked prefill: the downstream stalls (a factor of 1e9).
+        unmasked_decode_factor=(un["decode_ms_per_step"] / un["decode_solo_ms_per_step"]
+                                if un["decode_steps_in_window"] else 1e9),
+        decode_full_ms=un["decode_solo_ms_per_step"],
+        hbm_share=corun["decode_hbm_frac_cu_scaled"] * corun["down_cus"] / N_CUS)
+    per_req_ms = 1152 * t.prefill_ms_per_token[N_CUS]  # mean prompt of U[256, 2048]
+    capacity = 1000.0 / per_req_ms
+    out = {"note": "model output on measured kernel times, not a measurement", "timing": dataclasses.asdict(t),
+           "capacity_req_s": round(capacity, 1), "loads": []}
+    # Calibration (§4.2): the shared stage's decode TPOT keeps improving up to the whole chip, so
+    # S_cap is the top ladder level below S_aggr; B_sat is the downstream's measured HBM share,
+    # so its usual pressure maps to S_cap and a lighter downstream batch cedes CUs to it.
+    ccfg = dict(total_cus=N_CUS, aggressive_cus=N_CUS, ladder=[128, 160, 192, 224], ewma_weight=0.4,
+                saturation=t.hbm_share, hysteresis_steps=1)
+    out["controller_cfg"] = ccfg
+    out["temporal_cfg"] = dict(n_min=2, n_max=8, m=2, u_guard=1.0, long_cap=4)
+    for load in (0.5, 0.8, 0.95):
+        w = sim.Workload(n_requests=400, rate_per_s=load * capacity)
+        res = [sim.simulate(p, t, w, out["temporal_cfg"], ccfg) for p in ("baseline", "temporal", "spatial", "joint")]
+        out["loads"].append({"load": load, "rate_req_s": round(w.rate_per_s, 1), "policies": res})
+        log(f"[bench] policy model at {load:.0%} of shared-stage capacity: " + "; ".join(
+            f"{r['policy']} short {r['short']['slo_attainment']:.3f} long {r['long']['slo_attainment']:.3f}"
+            for r in res))
+    return out
 
 
 def controller_measure(torch, binding, ctx, ladder, dev):
