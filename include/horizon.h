@@ -65,6 +65,14 @@ typedef struct hs_layer_cfg {
   int32_t ffn;
   float rms_eps;   /* RMSNorm epsilon, inside the square root */
   float rope_base; /* RoPE base; pair (j, j + dh/2) turns by pos * base^(-2j/dh) */
+  /* Multimodal RoPE: rotary pairs j < dh/2 split into temporal, height and
+   * width sections of these many pairs (in that order); pair j turns by the
+   * position component of its section.  All zero: one position per row (the
+   * plain RoPE above).  Otherwise each is a multiple of 4 and they sum to
+   * dh/2.  The paper does not define the multimodal positions; this is the
+   * sectioned form models of the Qwen2-VL family use for image and video
+   * rows. */
+  int32_t mrope_sections[3];
 } hs_layer_cfg;
 
 /* Storage format of the four projection matrices of a layer. */
@@ -232,6 +240,21 @@ hs_status hs_shared_stage_forward(hs_context* ctx, const hs_layer_cfg* cfg,
                                   const int32_t* ctx_lens, int32_t n_seqs, const hs_kv_cache* kv,
                                   int32_t cu_budget, void* stream, void* workspace,
                                   size_t ws_bytes);
+
+/* The same with multimodal RoPE positions (cfg->mrope_sections non-zero):
+ * positions3 is a host array [3][T] giving, for every packed row, its
+ * temporal, height and width position (image or video rows take their patch
+ * grid coordinates, text rows three equal positions).  Each must be in
+ * [0, P), P the largest ctx_lens[b] + row + 1 of the batch.  Cache
+ * placement and causal masking still follow the row order; only the RoPE
+ * angles change.  Errors as hs_shared_stage_forward, plus HS_ERR_INVALID_ARG
+ * for null positions3, zero mrope_sections or a position outside [0, P). */
+hs_status hs_shared_stage_forward_mrope(hs_context* ctx, const hs_layer_cfg* cfg,
+                                        const hs_layer_weights* w, int32_t n_layers, const void* x_in,
+                                        void* x_out, const int32_t* seq_offsets,
+                                        const int32_t* ctx_lens, int32_t n_seqs, const hs_kv_cache* kv,
+                                        const int32_t* positions3, int32_t cu_budget, void* stream,
+                                        void* workspace, size_t ws_bytes);
 
 /* Downstream decode step (§2.1: decode re-reads weights and the cache):
  * one new row per sequence through n_layers layers.

@@ -16,7 +16,12 @@ standard pre-norm decoder layer, with these readings of unstated details:
   rows per head; query head ``h`` reads key/value head ``h // (Hq / Hkv)``.
 * RoPE rotates the pairs (j, j + dh/2), j < dh/2, by ``pos * base^(-2j/dh)``;
   positions restart at 0 per sequence and are offset by the cached prefix
-  length.  Image/video-patch rows use the same 1-D positions as text rows.
+  length.  Image/video-patch rows use the same 1-D positions as text rows,
+  unless multimodal positions are given: then every row has a temporal,
+  height and width position, the pairs are split into consecutive sections
+  of ``cfg.mrope_sections`` pairs, and pair j turns by its section's
+  component (the sectioned multimodal RoPE of the Qwen2-VL family; the paper
+  does not define one).
 * Attention scale ``1/sqrt(dh)``; causal alignment is bottom-right: row ``i``
   of a chunk behind ``c`` cached rows sees keys ``0 .. c + i``; sequences never
   see each other.
@@ -47,12 +52,26 @@ def rope_angles(pos: np.ndarray, head_dim: int, base: float) -> np.ndarray:
     return np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]
 
 
-def rope(x: np.ndarray, pos: np.ndarray, base: float) -> np.ndarray:
-    """Rotate-half RoPE on x[T, H, dh]: (a, b) -> (a cos - b sin, b cos + a sin)."""
+def rope_angles_sectioned(pos3: np.ndarray, head_dim: int, base: float, sections) -> np.ndarray:
+    """theta[t, j] = pos3[c(j), t] * base^(-2j/dh), c(j) the section (0, 1, 2) holding pair j."""
+    j = np.arange(head_dim // 2, dtype=np.float64)
+    inv_freq = np.power(float(base), -2.0 * j / head_dim)
+    comp = np.repeat(np.arange(3), [int(n) for n in sections])       # [dh/2]
+    p = np.asarray(pos3, dtype=np.float64)[comp, :].T                # [T, dh/2]
+    return p * inv_freq[None, :]
+
+
+def rope(x: np.ndarray, pos: np.ndarray, base: float, sections=None) -> np.ndarray:
+    """Rotate-half RoPE on x[T, H, dh]: (a, b) -> (a cos - b sin, b cos + a sin).
+
+    pos is [T], or [3, T] with ``sections`` (pairs per temporal / height / width section)."""
     x = np.asarray(x, dtype=np.float64)
     dh = x.shape[-1]
     half = dh // 2
-    th = rope_angles(pos, dh, base)[:, None, :]          # [T, 1, dh/2]
+    if sections is not None:
+        th = rope_angles_sectioned(pos, dh, base, sections)[:, None, :]
+    else:
+        th = rope_angles(pos, dh, base)[:, None, :]      # [T, 1, dh/2]
     c, s = np.cos(th), np.sin(th)
     a, b = x[..., :half], x[..., half:]
     return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
@@ -96,7 +115,8 @@ def layer_forward(x: np.ndarray, w: Dict[str, np.ndarray], cfg, seq_offsets: Seq
                   ctx_lens: Optional[Sequence[int]] = None,
                   prefix_k: Optional[List[np.ndarray]] = None,
                   prefix_v: Optional[List[np.ndarray]] = None,
-                  seqs: Optional[Sequence[int]] = None) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+                  seqs: Optional[Sequence[int]] = None,
+                  positions3: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     """One pre-norm decoder layer over a packed ragged batch.
 
     x: [T, d] float64; w: float64 weights ('ln1', 'w_qkv', 'w_o', 'ln2',
@@ -104,7 +124,8 @@ def layer_forward(x: np.ndarray, w: Dict[str, np.ndarray], cfg, seq_offsets: Seq
     sequence (None = no prefix); prefix_k/v: per sequence [ctx_b, Hkv, dh].
     ``seqs`` restricts the attention to those sequences (their rows of the
     output are exact; other rows keep only the row-local parts and must not
-    be read).  Returns (y [T, d], k_new [T, Hkv, dh], v_new [T, Hkv, dh]).
+    be read).  ``positions3`` [3, T], if given, are the rows' multimodal RoPE positions
+    (``cfg.mrope_sections`` splits the pairs).  Returns (y [T, d], k_new [T, Hkv, dh], v_new [T, Hkv, dh]).
     """
     x = np.asarray(x, dtype=np.float64)
     T, d = x.shape
@@ -124,8 +145,12 @@ def layer_forward(x: np.ndarray, w: Dict[str, np.ndarray], cfg, seq_offsets: Seq
     q = qkv[:, : hq * dh].reshape(T, hq, dh)
     k = qkv[:, hq * dh: (hq + hkv) * dh].reshape(T, hkv, dh)
     v = qkv[:, (hq + hkv) * dh:].reshape(T, hkv, dh)
-    q = rope(q, pos, cfg.rope_base)
-    k = rope(k, pos, cfg.rope_base)
+    if positions3 is not None:
+        q = rope(q, positions3, cfg.rope_base, cfg.mrope_sections)
+        k = rope(k, positions3, cfg.rope_base, cfg.mrope_sections)
+    else:
+        q = rope(q, pos, cfg.rope_base)
+        k = rope(k, pos, cfg.rope_base)
 
     o = np.zeros((T, hq, dh), dtype=np.float64)
     for b in (range(B) if seqs is None else seqs):
@@ -149,7 +174,7 @@ def layer_forward(x: np.ndarray, w: Dict[str, np.ndarray], cfg, seq_offsets: Seq
 
 
 def stack_forward(x: np.ndarray, layers: List[Dict[str, np.ndarray]], cfg, seq_offsets,
-                  ctx_lens=None, prefix_k=None, prefix_v=None, seqs=None):
+                  ctx_lens=None, prefix_k=None, prefix_v=None, seqs=None, positions3=None):
     """Layers applied in order; the output is the residual stream (no final norm).
 
     prefix_k/v, if given, are per layer lists of per-sequence prefixes.
@@ -159,7 +184,7 @@ def stack_forward(x: np.ndarray, layers: List[Dict[str, np.ndarray]], cfg, seq_o
     for li, w in enumerate(layers):
         pk = None if prefix_k is None else prefix_k[li]
         pv = None if prefix_v is None else prefix_v[li]
-        x, k, v = layer_forward(x, w, cfg, seq_offsets, ctx_lens, pk, pv, seqs)
+        x, k, v = layer_forward(x, w, cfg, seq_offsets, ctx_lens, pk, pv, seqs, positions3)
         kv.append((k, v))
     return x, kv
 

@@ -22,7 +22,8 @@ HS_ROLE_SHARED, HS_ROLE_DOWN = 0, 1
 SYMBOLS = (
     "hs_status_string", "hs_last_error", "hs_default_topology", "hs_cu_partition", "hs_plan_metadata",
     "hs_context_create", "hs_context_topology", "hs_context_stream", "hs_context_masks",
-    "hs_context_destroy", "hs_workspace_size", "hs_workspace_size_paged", "hs_shared_stage_forward", "hs_downstream_decode_step",
+    "hs_context_destroy", "hs_workspace_size", "hs_workspace_size_paged", "hs_shared_stage_forward",
+    "hs_shared_stage_forward_mrope", "hs_downstream_decode_step",
     "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read", "hs_convert_weights_f16",
     "hs_controller_create", "hs_controller_step", "hs_controller_destroy", "hs_pressure_sample",
     "hs_temporal_create", "hs_temporal_step", "hs_temporal_destroy",
@@ -36,11 +37,13 @@ KERNEL_KINDS = {"rmsnorm": 0, "qkv": 1, "attention": 2, "decode_attn": 3, "o_pro
 class LayerCfg(ctypes.Structure):
     _fields_ = [("hidden", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32), ("rms_eps", ctypes.c_float),
-                ("rope_base", ctypes.c_float)]
+                ("rope_base", ctypes.c_float), ("mrope_sections", ctypes.c_int32 * 3)]
 
     @classmethod
     def of(cls, s) -> "LayerCfg":
-        return cls(s.hidden, s.n_q_heads, s.n_kv_heads, s.head_dim, s.ffn, s.rms_eps, s.rope_base)
+        sec = tuple(getattr(s, "mrope_sections", (0, 0, 0)))
+        return cls(s.hidden, s.n_q_heads, s.n_kv_heads, s.head_dim, s.ffn, s.rms_eps, s.rope_base,
+                   (ctypes.c_int32 * 3)(*sec))
 
 
 MATRICES = ("w_qkv", "w_o", "w_gate_up", "w_down")
@@ -127,6 +130,9 @@ def lib() -> ctypes.CDLL:
                                         ctypes.POINTER(ctypes.c_size_t)],
             "hs_shared_stage_forward": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp, vp,
                                         i32p, i32p, i32, ctypes.POINTER(KvCache), i32, vp, vp, ctypes.c_size_t],
+            "hs_shared_stage_forward_mrope": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp,
+                                              vp, i32p, i32p, i32, ctypes.POINTER(KvCache), i32p, i32, vp, vp,
+                                              ctypes.c_size_t],
             "hs_downstream_decode_step": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp, vp,
                                           ctypes.POINTER(KvCache), i32p, i32, i32, vp, vp, ctypes.c_size_t],
             "hs_probe_hw_ids": [vp, vp, i32, vp],
@@ -393,6 +399,23 @@ def hs_shared_stage_forward(ctx: Context, cfg, weights, x_in, x_out, seq_offsets
         ctx.handle, ctypes.byref(LayerCfg.of(cfg)), warr, len(weights), _ptr(x_in), _ptr(x_out), off,
         _i32_array(ctx_lens), len(off) - 1, ctypes.byref(kvs) if kvs is not None else None, cu_budget,
         _ptr(stream), _ptr(workspace), ws_bytes))
+
+
+def hs_shared_stage_forward_mrope(ctx: Context, cfg, weights, x_in, x_out, seq_offsets, positions3, ctx_lens=None,
+                                  kv=None, cu_budget: int = 256, stream=None, workspace=None,
+                                  ws_bytes: Optional[int] = None) -> None:
+    """positions3: host int array [3, T] (temporal, height, width position of every packed row)."""
+    warr = _weights_array(weights)
+    off = _i32_array(seq_offsets)
+    kvs = _kv_struct(kv)
+    pos = np.ascontiguousarray(positions3, dtype=np.int32)
+    assert pos.ndim == 2 and pos.shape[0] == 3
+    if ws_bytes is None:
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().hs_shared_stage_forward_mrope(
+        ctx.handle, ctypes.byref(LayerCfg.of(cfg)), warr, len(weights), _ptr(x_in), _ptr(x_out), off,
+        _i32_array(ctx_lens), len(off) - 1, ctypes.byref(kvs) if kvs is not None else None,
+        pos.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), cu_budget, _ptr(stream), _ptr(workspace), ws_bytes))
 
 
 def hs_downstream_decode_step(ctx: Context, cfg, weights, x_in, x_out, kv, kv_lens, cu_budget: int,

@@ -334,8 +334,6 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
             store_h4(a.out + int64_t(m) * a.ldo + c_base + i * 32 + 8 * g, v[0], v[1], v[2], v[3]);
           }
       } else {  // EPI_QKV
-        const int p = a.pos[m];
-        const float2* rt = a.rope + int64_t(p) * (DH / 2);
 #pragma unroll
         for (int pr = 0; pr < 2; ++pr) {  // (lo subtile, hi subtile) pairs of the wave
           // DH 128: one head per wave, pairs (0, 2), (1, 3); d_lo = 32 pr + ...
@@ -347,6 +345,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const int d = dsub + 8 * g + 4 * fh;  // < DH / 2
+            // Pairs d .. d + 3 share one RoPE section (sections are multiples of 4 pairs).
+            const float2* rt = a.rope + int64_t(rope_pos(a, m, d)) * (DH / 2);
             float lo[4], hi[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {

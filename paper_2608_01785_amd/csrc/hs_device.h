@@ -191,6 +191,13 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   return (bid % kNumXcd) * per + bid / kNumXcd;
 }
 
+// RoPE position of row m for rotary pair j (plain or sectioned multimodal).
+template <typename Args>
+__device__ __forceinline__ int rope_pos(const Args& a, int m, int j) {
+  const int c = int(j >= a.sec1) + int(j >= a.sec2);
+  return a.pos[c * a.pos_stride + m];
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

@@ -31,7 +31,9 @@ struct GemmArgs {
   uint16_t* q;            // [M, hq, dh] fp16
   uint16_t* kstore;       // keys: element k_off[m] + g * kv_head_stride + d
   uint16_t* vstore;       // values: element v_off[m] + g * kv_head_stride + d * kv_tile_keys
-  const int32_t* pos;     // [M] RoPE position of each row
+  const int32_t* pos;     // RoPE positions: component c of row m at pos[c * pos_stride + m]
+  int pos_stride;         // 0: one position per row
+  int sec1, sec2;         // rotary pair j uses component (j >= sec1) + (j >= sec2)
   const int64_t* k_off;   // [M]
   const int64_t* v_off;   // [M]
   int64_t kv_head_stride; // elements between the heads of one slot (max_ctx * dh)

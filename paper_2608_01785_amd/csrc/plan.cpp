@@ -62,6 +62,13 @@ hs_status validate_cfg(const hs_layer_cfg* c) {
     return fail(HS_ERR_UNSUPPORTED, "ffn %d must be a positive multiple of 128", c->ffn);
   if (!(c->rms_eps > 0.0f) || !(c->rope_base > 1.0f))
     return fail(HS_ERR_INVALID_ARG, "rms_eps must be > 0 and rope_base > 1");
+  const int32_t* sec = c->mrope_sections;
+  if (sec[0] || sec[1] || sec[2]) {
+    if (sec[0] < 0 || sec[1] < 0 || sec[2] < 0 || sec[0] % 4 || sec[1] % 4 || sec[2] % 4 ||
+        sec[0] + sec[1] + sec[2] != c->head_dim / 2)
+      return fail(HS_ERR_INVALID_ARG, "mrope_sections (%d, %d, %d) must be multiples of 4 summing to head_dim / 2",
+                  sec[0], sec[1], sec[2]);
+  }
   return HS_OK;
 }
 
@@ -142,6 +149,7 @@ static size_t meta_bytes(int32_t T, int32_t B, int64_t pages, int64_t att, int32
                          int64_t dec_count) {
   size_t s = 0;
   s += align_up(size_t(T) * 4, 16);       // pos
+  s += align_up(size_t(T) * 12, 16);      // pos3
   s += align_up(size_t(T) * 8, 16) * 2;   // k_off, v_off
   s += align_up(size_t(B) * 4, 16) * 4;   // seq_start, seq_len, seq_ctx, seq_page0
   s += align_up(size_t(pages) * 8, 16);   // page_base
@@ -228,7 +236,7 @@ hs_status check_block_table(const int32_t* table, int32_t pps, int32_t n_slots, 
 }
 
 hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* ctx, int32_t B,
-                     const KvPlacement& kv, Plan* out) {
+                     const KvPlacement& kv, Plan* out, const int32_t* positions3) {
   Plan& P = *out;
   hs_status st = validate_batch(off, ctx, B, &P.T, &P.max_pos);
   if (st != HS_OK) return st;
@@ -266,6 +274,7 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
     return at;
   };
   P.pos = take(size_t(T) * 4);
+  P.pos3 = positions3 ? take(size_t(T) * 12) : 0;
   P.k_off = take(size_t(T) * 8);
   P.v_off = take(size_t(T) * 8);
   P.seq_start = take(size_t(B) * 4);
@@ -299,6 +308,7 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   P.image.assign(align_up(p, kAlign), 0);
 
   auto i32 = [&](size_t at) { return reinterpret_cast<int32_t*>(P.image.data() + at); };
+  if (positions3) memcpy(P.image.data() + P.pos3, positions3, size_t(T) * 12);
   auto i64 = [&](size_t at) { return reinterpret_cast<int64_t*>(P.image.data() + at); };
 
   // A page (a cache slot) holds hkv heads of slot_ctx positions.  Without a

@@ -214,7 +214,7 @@ void use_norm(hs::GemmArgs& a, const float* sumsq, int parts, float eps) {
 hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w, int32_t n_layers,
                     const void* x_in, void* x_out, const int32_t* seq_offsets, const int32_t* ctx_lens,
                     int32_t n_seqs, const hs_kv_cache* kv, int32_t budget, int role, void* stream,
-                    void* ws, size_t ws_bytes) {
+                    void* ws, size_t ws_bytes, const int32_t* pos3 = nullptr) {
   hs::clear_error();
   hs_status st = hs::validate_cfg(cfg);
   if (st != HS_OK) return st;
@@ -267,7 +267,16 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     return hs::fail(HS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, lay.total);
   place.packed_ctx = lay.packed_ctx;
   hs::Plan plan;
-  st = hs::build_plan(*cfg, seq_offsets, ctx_lens, n_seqs, place, &plan);
+  if (pos3) {
+    const int32_t* sec = cfg->mrope_sections;
+    if (!(sec[0] || sec[1] || sec[2]))
+      return hs::fail(HS_ERR_INVALID_ARG, "multimodal positions need non-zero mrope_sections");
+    for (int64_t i = 0; i < 3 * int64_t(T); ++i)
+      if (pos3[i] < 0 || pos3[i] >= max_pos)
+        return hs::fail(HS_ERR_INVALID_ARG, "multimodal position %d (entry %lld) outside [0, %d)", pos3[i],
+                        (long long)i, max_pos);
+  }
+  st = hs::build_plan(*cfg, seq_offsets, ctx_lens, n_seqs, place, &plan, pos3);
   if (st != HS_OK) return st;
   if (plan.image.size() > lay.meta_bytes) return hs::fail(HS_ERR_INTERNAL, "metadata image exceeds its region");
 
@@ -331,7 +340,11 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     g.q = q_buf;
     g.kstore = kstore;
     g.vstore = vstore;
-    g.pos = d_pos;
+    // RoPE positions: the plain row positions, or the three multimodal components.
+    g.pos = pos3 ? reinterpret_cast<const int32_t*>(meta + plan.pos3) : d_pos;
+    g.pos_stride = pos3 ? T : 0;
+    g.sec1 = pos3 ? cfg->mrope_sections[0] : dh / 2;
+    g.sec2 = pos3 ? cfg->mrope_sections[0] + cfg->mrope_sections[1] : dh / 2;
     g.k_off = d_koff;
     g.v_off = d_voff;
     g.kv_head_stride = plan.kv_head_stride;
@@ -560,6 +573,19 @@ hs_status hs_shared_stage_forward(hs_context* ctx, const hs_layer_cfg* cfg, cons
                                   int32_t cu_budget, void* stream, void* workspace, size_t ws_bytes) {
   return run_stack(ctx, cfg, w, n_layers, x_in, x_out, seq_offsets, ctx_lens, n_seqs, kv, cu_budget,
                    HS_ROLE_SHARED, stream, workspace, ws_bytes);
+}
+
+hs_status hs_shared_stage_forward_mrope(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w,
+                                        int32_t n_layers, const void* x_in, void* x_out, const int32_t* seq_offsets,
+                                        const int32_t* ctx_lens, int32_t n_seqs, const hs_kv_cache* kv,
+                                        const int32_t* positions3, int32_t cu_budget, void* stream, void* workspace,
+                                        size_t ws_bytes) {
+  if (!positions3) {
+    hs::clear_error();
+    return hs::fail(HS_ERR_INVALID_ARG, "positions3 is null");
+  }
+  return run_stack(ctx, cfg, w, n_layers, x_in, x_out, seq_offsets, ctx_lens, n_seqs, kv, cu_budget,
+                   HS_ROLE_SHARED, stream, workspace, ws_bytes, positions3);
 }
 
 hs_status hs_downstream_decode_step(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w,

@@ -122,11 +122,9 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
         }
     }
   }
-  int qkv_pos = 0;
   int64_t qkv_koff = 0, qkv_voff = 0;
   if constexpr (EPI == EPI_QKV) {
     if (row_own) {
-      qkv_pos = a.pos[m_own];
       qkv_koff = a.k_off[m_own];
       qkv_voff = a.v_off[m_own];
     }
@@ -227,11 +225,14 @@ __device__ __forceinline__ void skinny_unit(const GemmArgs& a, int tile, int ks,
   float bias_pre[EPI == EPI_QKV ? 16 : 1];
   if constexpr (EPI == EPI_QKV) {
     if (row_own) {
-      const float2* rt = a.rope + int64_t(qkv_pos) * (DH / 2) + 16 * (tile % (DH / 32)) + 4 * fh;
 #pragma unroll
-      for (int g = 0; g < 2; ++g)
+      for (int g = 0; g < 2; ++g) {
+        // Pairs j .. j + 3 share one RoPE section (sections are multiples of 4 pairs).
+        const int j = 16 * (tile % (DH / 32)) + 8 * g + 4 * fh;
+        const float2* rt = a.rope + int64_t(rope_pos(a, m_own, j)) * (DH / 2) + j;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) rope_pre[4 * g + e] = rt[8 * g + e];
+        for (int e = 0; e < 4; ++e) rope_pre[4 * g + e] = rt[e];
+      }
     }
 #pragma unroll
     for (int r = 0; r < 16; ++r) bias_pre[r] = 0.0f;

@@ -81,6 +81,7 @@ class LayerShape:
     ffn: int
     rms_eps: float = 1e-6
     rope_base: float = 10000.0
+    mrope_sections: tuple = (0, 0, 0)   # temporal / height / width rotary pairs; zeros: plain RoPE
 
     @property
     def qkv_rows(self) -> int:
@@ -213,6 +214,27 @@ def thinker_batch(hidden: int = THINKER.hidden, n_requests: int = 8,
     lengths, n_img = draw_lengths(seeds["lengths"], n_requests, 256, 2048)
     off = _offsets(lengths)
     return PrefillBatch(lengths, off, None, n_img, token_rows(seeds["tokens"], int(off[-1]), hidden))
+
+
+def mrope_positions(lengths, n_img, ctx_lens=None, grid_w: int = 32) -> np.ndarray:
+    """Multimodal RoPE positions [3, T] of packed sequences whose first n_img[b] rows are
+    image patches: patch i sits at (t, h, w) = (s, s + i // grid_w, s + i % grid_w) with
+    s = ctx_lens[b]; the text rows after it continue from the largest position + 1 with three
+    equal components (the layout of the Qwen2-VL family)."""
+    lengths = [int(n) for n in lengths]
+    ctx = [0] * len(lengths) if ctx_lens is None else [int(c) for c in ctx_lens]
+    out = np.zeros((3, sum(lengths)), np.int32)
+    t0 = 0
+    for n, k, s in zip(lengths, [int(i) for i in n_img], ctx):
+        k = min(k, n)
+        i = np.arange(k)
+        out[0, t0:t0 + k] = s
+        out[1, t0:t0 + k] = s + i // grid_w
+        out[2, t0:t0 + k] = s + i % grid_w
+        nxt = s + (max((k - 1) // grid_w, min(k, grid_w) - 1) + 1 if k else 0)
+        out[:, t0 + k:t0 + n] = nxt + np.arange(n - k)
+        t0 += n
+    return out
 
 
 def random_batch(hidden: int, lengths, seed: int, ctx_lens=None) -> PrefillBatch:

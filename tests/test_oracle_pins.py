@@ -469,3 +469,56 @@ def test_tiny_workload_layer_is_finite_and_row_local_residual():
     for s in range(2):
         t = int(b.seq_offsets[s])
         assert np.all(np.isfinite(v[t]))
+
+
+# ----------------------------------------------------------------------------- multimodal RoPE
+
+def test_mrope_with_equal_components_is_plain_rope():
+    import dataclasses
+    c = dataclasses.replace(W.TINY, mrope_sections=(8, 12, 12))
+    w = weights_f64(W.make_weights(c, 1, 51))[0]
+    b = W.random_batch(c.hidden, [40, 7], seed=52, ctx_lens=[0, 0])
+    pos = np.concatenate([np.arange(40), np.arange(7)])
+    y0, k0, _ = L.layer_forward(f64(b.x), w, c, b.seq_offsets)
+    y1, k1, _ = L.layer_forward(f64(b.x), w, c, b.seq_offsets, positions3=np.stack([pos, pos, pos]))
+    np.testing.assert_array_equal(y0, y1)
+    np.testing.assert_array_equal(k0, k1)
+
+
+def test_mrope_scores_depend_only_on_per_section_offsets():
+    rng = np.random.default_rng(53)
+    sec, dh = (16, 24, 24), 128
+    q = rng.standard_normal((1, 1, dh))
+    k = rng.standard_normal((1, 1, dh))
+    pq, pk = np.array([[5], [9], [2]]), np.array([[1], [3], [7]])
+    for shift in ([0, 0, 0], [11, -2, 40], [100, 100, 3]):
+        s = np.array(shift)[:, None]
+        qa = L.rope(q, pq + s, 1e4, sec)
+        ka = L.rope(k, pk + s, 1e4, sec)
+        base = (L.rope(q, pq, 1e4, sec) * L.rope(k, pk, 1e4, sec)).sum()
+        assert abs((qa * ka).sum() - base) < 1e-9 * np.abs(q).sum() * np.abs(k).sum()
+
+
+def test_mrope_pair_turns_by_its_sections_component():
+    sec, dh, base = (4, 8, 4), 32, 1e4
+    for j, comp in ((2, 0), (5, 1), (13, 2)):
+        x = np.zeros((1, 1, dh))
+        x[0, 0, j] = 1.0                                  # (a, b) = (1, 0) in pair j
+        pos = np.zeros((3, 1))
+        pos[comp, 0] = 7.0
+        y = L.rope(x, pos, base, sec)
+        ang = 7.0 * base ** (-2.0 * j / dh)
+        assert y[0, 0, j] == pytest.approx(np.cos(ang), abs=1e-15)
+        assert y[0, 0, j + dh // 2] == pytest.approx(np.sin(ang), abs=1e-15)
+        pos_other = np.zeros((3, 1))
+        pos_other[(comp + 1) % 3, 0] = 7.0                # another component moves: no turn
+        y = L.rope(x, pos_other, base, sec)
+        assert y[0, 0, j] == 1.0 and y[0, 0, j + dh // 2] == 0.0
+
+
+def test_mrope_positions_layout():
+    p = W.mrope_positions([70, 5], [40, 0], [10, 3], grid_w=8)
+    assert p.shape == (3, 75)
+    assert list(p[:, 0]) == [10, 10, 10] and list(p[:, 9]) == [10, 11, 11]    # patch 9: row 1, col 1
+    assert list(p[:, 40]) == [18, 18, 18]                                     # text after a 5 x 8 grid
+    assert list(p[:, 70]) == [3, 3, 3] and p.max() < 80
