@@ -257,6 +257,15 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
       if (ctx_lens[b] != 0)
         return hs::fail(HS_ERR_INVALID_ARG, "ctx_lens[%d] = %d but no cache holds the prefix", b, ctx_lens[b]);
   }
+  if (pos3) {
+    const int32_t* sec = cfg->mrope_sections;
+    if (!(sec[0] || sec[1] || sec[2]))
+      return hs::fail(HS_ERR_INVALID_ARG, "multimodal positions need non-zero mrope_sections");
+    for (int64_t i = 0; i < 3 * int64_t(T); ++i)
+      if (pos3[i] < 0 || pos3[i] >= max_pos)
+        return hs::fail(HS_ERR_INVALID_ARG, "multimodal position %d (entry %lld) outside [0, %d)", pos3[i],
+                        (long long)i, max_pos);
+  }
   if (!ctx) return hs::fail(HS_ERR_INVALID_ARG, "context is null");
   hipStream_t s = nullptr;
   st = resolve_stream(ctx, budget, role, stream, &s);
@@ -267,15 +276,6 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     return hs::fail(HS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, lay.total);
   place.packed_ctx = lay.packed_ctx;
   hs::Plan plan;
-  if (pos3) {
-    const int32_t* sec = cfg->mrope_sections;
-    if (!(sec[0] || sec[1] || sec[2]))
-      return hs::fail(HS_ERR_INVALID_ARG, "multimodal positions need non-zero mrope_sections");
-    for (int64_t i = 0; i < 3 * int64_t(T); ++i)
-      if (pos3[i] < 0 || pos3[i] >= max_pos)
-        return hs::fail(HS_ERR_INVALID_ARG, "multimodal position %d (entry %lld) outside [0, %d)", pos3[i],
-                        (long long)i, max_pos);
-  }
   st = hs::build_plan(*cfg, seq_offsets, ctx_lens, n_seqs, place, &plan, pos3);
   if (st != HS_OK) return st;
   if (plan.image.size() > lay.meta_bytes) return hs::fail(HS_ERR_INTERNAL, "metadata image exceeds its region");

@@ -187,6 +187,39 @@ def test_paged_cache_validation_fails_before_any_gpu_work(b):
     assert st == b.HS_ERR_INVALID_ARG and "context" in msg, msg
 
 
+def test_mrope_validation_fails_before_any_gpu_work(b):
+    import dataclasses
+    from paper_2608_01785_amd import binding
+    from paper_2608_01785_amd import workloads as W
+
+    def call(cfg, offsets, pos3):
+        w = (binding.LayerWeights * 1)()
+        for name in ("ln1", "w_qkv", "w_o", "ln2", "w_gate_up", "w_down"):
+            setattr(w[0], name, 0x1000)
+        off = (ctypes.c_int32 * len(offsets))(*offsets)
+        p = None if pos3 is None else np.ascontiguousarray(pos3, np.int32)
+        st = b.lib().hs_shared_stage_forward_mrope(
+            None, ctypes.byref(binding.LayerCfg.of(cfg)), w, 1, 1 << 20, 2 << 20, off, None, len(offsets) - 1, None,
+            None if p is None else p.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), 256, None, 0x3000, 1 << 30)
+        return st, b.hs_last_error()
+
+    c = dataclasses.replace(W.TINY, mrope_sections=(8, 12, 12))
+    good = W.mrope_positions([10, 6], [4, 0])
+    st, msg = call(c, [0, 10, 16], good)
+    assert st == b.HS_ERR_INVALID_ARG and "context" in msg, msg          # every check passed
+    st, msg = call(c, [0, 10, 16], None)
+    assert st == b.HS_ERR_INVALID_ARG and "positions3" in msg, msg
+    st, msg = call(W.TINY, [0, 10, 16], good)
+    assert st == b.HS_ERR_INVALID_ARG and "mrope_sections" in msg, msg
+    bad = good.copy()
+    bad[1, 3] = 10                                                       # the largest row position is 9
+    st, msg = call(c, [0, 10, 16], bad)
+    assert st == b.HS_ERR_INVALID_ARG and "outside" in msg, msg
+    for sec in ((8, 12, 8), (6, 14, 12), (-4, 24, 12)):
+        st, msg = call(dataclasses.replace(W.TINY, mrope_sections=sec), [0, 10, 16], good)
+        assert st == b.HS_ERR_INVALID_ARG and "multiples of 4" in msg, msg
+
+
 def test_paged_workspace_size(b):
     from paper_2608_01785_amd import workloads as W
     c = W.TALKER
