@@ -80,6 +80,7 @@ def main():
     ap.add_argument("--no-controller", action="store_true")
     ap.add_argument("--no-tpot", action="store_true")
     ap.add_argument("--no-mixed", action="store_true")
+    ap.add_argument("--no-loop", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows per sequence in the CPU-reference sample (0: sized to take about 15 s)")
     ap.add_argument("--quick", action="store_true", help="headline stack only (no budget sweep, co-run, CPU leg)")
@@ -101,6 +102,7 @@ def main():
     if args.quick:
         budgets, args.no_corun, args.no_cpu_baseline, args.no_controller, args.no_tpot = [], True, True, True, True
         args.no_mixed = True
+        args.no_loop = True
     # One context holds every level the sections below use (each level is a
     # pair of CU-masked hardware queues).
     # The timed loops issue many short library calls from Python.  A cyclic
@@ -108,7 +110,7 @@ def main():
     # stalled one call by ~37 ms inside a timed loop, so the collector runs
     # only between sections.
     gc.disable()
-    ladder = sorted(set(budgets + [96, 128, 256] + ([] if args.no_tpot else TPOT_CAPS)))
+    ladder = sorted(set(budgets + [96, 128, 160, 224, 256] + ([] if args.no_tpot else TPOT_CAPS)))
     ctx = binding.Context(0, budgets=ladder)
 
     # ---------------------------------------------------------------- thinker stack
@@ -216,6 +218,12 @@ def main():
     if not args.no_controller:
         controller = controller_measure(torch, binding, ctx, [b for b in ladder if b < N_CUS], dev)
 
+    # ---------------------------------------------------------------- Algorithm 1 on the GPU
+    loop = None
+    if not args.no_loop:
+        gc.collect()
+        loop = [serving_loop(torch, binding, W, ctx, wdev, dev, p) for p in ("baseline", "joint")]
+
     # ---------------------------------------------------------------- serving-loop model on measured times
     policy = None
     if corun is not None and "unmasked" in corun:
@@ -256,6 +264,7 @@ def main():
         "decode_tpot_vs_cus": tpot,
         "controller": controller,
         "policy_model": policy,
+        "serving_loop": loop,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
@@ -654,6 +663,149 @@ def policy_model(W, shape, batch, per_budget, corun):
         log(f"[bench] policy model at {load:.0%} of shared-stage capacity: " + "; ".join(
             f"{r['policy']} short {r['short']['slo_attainment']:.3f} long {r['long']['slo_attainment']:.3f}"
             for r in res))
+    return out
+
+
+def serving_loop(torch, binding, W, ctx, wdev, dev, policy, n_req=32, first_chunk=20, seed=11):
+    """Algorithm 1 on the GPU (measured, unlike the model): a burst of requests, half long-path.
+    Per scheduling step the temporal view picks the visible requests (joint policy), an FCFS
+    batch of up to 4096 prompt tokens is prefilled through the 4-layer thinker stack, and the
+    controller picks the CU split; while the prefill runs, talker decode steps of the active
+    long-path requests loop on the complementary stream (their cache pages addressed through a
+    per-step block table).  A short request's first response is the end of its prefill step, a
+    long request's the end of the scheduling step in which its first_chunk-th talker step
+    completes.  Baseline: every request visible, both stages unmasked on the whole chip."""
+    from paper_2608_01785_amd.device_data import DeviceCache, prepare_f16, to_device, upload_weights
+    joint = policy == "joint"
+    rng = np.random.default_rng(seed)
+    th, ts = W.THINKER, W.TALKER
+    tokens = rng.integers(256, 1024, size=n_req, endpoint=True).astype(int)
+    long = rng.uniform(size=n_req) < 0.5
+    kv0 = rng.integers(128, 512, size=n_req, endpoint=True).astype(np.int32)
+    # Weights, inputs and caches.
+    tl = prepare_f16(ctx, upload_weights(W.make_weights(ts, 16, W.SEEDS["talker"]["weights"]), dev))
+    x_pool = to_device(W.token_rows(seed, 4096, th.hidden), dev)
+    y = torch.empty((4096, th.hidden), dtype=torch.float32, device=dev)
+    ws = torch.empty(binding.hs_workspace_size(th, 4096, n_req, 1024), dtype=torch.uint8, device=dev)
+    max_ctx = 576
+    cache = DeviceCache(16, n_req, max_ctx, ts.n_kv_heads, ts.head_dim, dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    for l in range(16):
+        for b in range(n_req):
+            if long[b]:
+                cache.fill_random(l, b, int(kv0[b]), gen)
+    xt = to_device(W.token_rows(seed + 1, n_req, ts.hidden), dev)
+    yt = torch.empty((n_req, ts.hidden), dtype=torch.float32, device=dev)
+    wst = torch.empty(binding.hs_workspace_size_paged(ts, n_req, n_req, max_ctx, max_ctx), dtype=torch.uint8, device=dev)
+    # Solo estimates (ms) for deadlines and remaining times: per-token prefill and one talker step.
+    per_tok, talker_ms = 0.00185, 0.9
+    solo = tokens * per_tok + np.where(long, first_chunk * talker_ms, 0.0)
+    delta = {c: 5.0 * float(np.percentile(solo[long == c], 95)) for c in (False, True)}
+    deadline = np.array([delta[bool(l)] for l in long])
+    sched = binding.Temporal(2, 8, 2, 1.0, 4) if joint else None
+    ctrl = binding.Controller(N_CUS, N_CUS, [128, 160, 192, 224], 0.4, 0.2, 1) if joint else None
+    full = torch.cuda.Stream()
+    s_full = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, N_CUS, binding.HS_ROLE_SHARED))
+    waiting = list(range(n_req))
+    active, steps, issued = [], np.zeros(n_req, int), np.zeros(n_req, int)
+    kv = kv0.copy()
+    first = np.full(n_req, np.nan)
+    shares = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+
+    def talker_step(s_shared, ids):
+        table = ids[:, None]
+        if joint and s_shared < N_CUS:
+            binding.hs_downstream_decode_step(ctx, ts, tl, xt, yt, (cache.k, cache.v, n_req, max_ctx, table),
+                                              kv[ids], N_CUS - s_shared, None, wst)
+            rec = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, s_shared, binding.HS_ROLE_DOWN))
+        else:
+            binding.hs_downstream_decode_step(ctx, ts, tl, xt, yt, (cache.k, cache.v, n_req, max_ctx, table),
+                                              kv[ids], N_CUS, full.cuda_stream, wst)
+            rec = full
+        e = torch.cuda.Event()
+        e.record(rec)
+        return e, ids
+
+    for _ in range(400):
+        if not waiting and not active:
+            break
+        now = (time.perf_counter() - t0) * 1e3
+        vis = [True] * len(waiting)
+        if sched is not None and waiting:
+            vis, _ = binding.hs_temporal_step(sched, now, [
+                (binding.HS_PATH_LONG if long[i] else binding.HS_PATH_SHORT, binding.HS_WORK_PREFILL,
+                 deadline[i], solo[i]) for i in waiting])
+        batch, tok = [], 0
+        for i, v in zip(waiting, vis):
+            if v and (not batch or tok + tokens[i] <= 4096):
+                batch.append(i)
+                tok += int(tokens[i])
+        s_sh = N_CUS
+        if ctrl is not None:
+            sample = 0.0
+            if active:
+                try:
+                    sample = binding.hs_pressure_sample(0)
+                except binding.HorizonError:
+                    sample = 0.2
+            s_sh = binding.hs_controller_step(ctrl, bool(active), sample).shared_cus
+        shares.append(s_sh)
+        pend = []
+        if batch:
+            off = np.concatenate([[0], np.cumsum(tokens[batch])]).astype(np.int32)
+            stream = s_full if s_sh == N_CUS else torch.cuda.ExternalStream(
+                binding.hs_context_stream(ctx, s_sh, binding.HS_ROLE_SHARED))
+            binding.hs_shared_stage_forward(ctx, th, wdev, x_pool[:tok], y[:tok], off, None, None, s_sh, None, ws)
+            p_end = torch.cuda.Event()
+            p_end.record(stream)
+            while not p_end.query():
+                cur = np.array([i for i in active if issued[i] < first_chunk], np.int32)
+                if len(cur) == 0:
+                    break
+                pend.append(talker_step(s_sh, cur))
+                kv[cur] += 1
+                issued[cur] += 1
+                if len(pend) > 3:
+                    pend[-4][0].synchronize()
+        elif active:
+            cur = np.array([i for i in active if issued[i] < first_chunk], np.int32)
+            if len(cur):
+                pend.append(talker_step(s_sh, cur))
+                kv[cur] += 1
+                issued[cur] += 1
+        torch.cuda.synchronize()
+        done_t = (time.perf_counter() - t0) * 1e3
+        for i in batch:
+            waiting.remove(i)
+            if long[i]:
+                active.append(i)
+            else:
+                first[i] = done_t
+        for _, ids in pend:
+            for i in ids:
+                steps[i] += 1
+                if steps[i] >= first_chunk and np.isnan(first[i]):
+                    first[i] = done_t
+        active = [i for i in active if np.isnan(first[i])]
+    if sched is not None:
+        sched.close()
+    if ctrl is not None:
+        ctrl.close()
+    out = {"policy": policy, "mean_shared_cus": round(float(np.mean(shares)), 1) if shares else None,
+           "makespan_ms": round(float(np.nanmax(first)), 2), "unfinished": int(np.isnan(first).sum())}
+    for name, flag in (("short", False), ("long", True)):
+        lat = first[long == flag]
+        lat = lat[~np.isnan(lat)]
+        met = (first[long == flag] <= deadline[long == flag])
+        out[name] = {"n": int((long == flag).sum()), "slo_attainment": round(float(met.mean()), 4),
+                     "p50_ms": round(float(np.percentile(lat, 50)), 2) if len(lat) else None,
+                     "p95_ms": round(float(np.percentile(lat, 95)), 2) if len(lat) else None}
+    log(f"[bench] serving loop ({policy}): short p50/p95 {out['short']['p50_ms']}/{out['short']['p95_ms']} ms, "
+        f"long p50/p95 {out['long']['p50_ms']}/{out['long']['p95_ms']} ms, makespan {out['makespan_ms']} ms, "
+        f"mean shared CUs {out['mean_shared_cus']}")
     return out
 
 
