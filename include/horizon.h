@@ -269,6 +269,18 @@ hs_status hs_shared_stage_forward_mrope(hs_context* ctx, const hs_layer_cfg* cfg
  *   DOWN role: stream NULL selects the context's DOWN stream for the ladder
  *   level whose SHARED budget is n_cus - cu_budget.
  * The library never changes kv_lens; the caller advances them. */
+/* The decode step with multimodal RoPE positions (cfg->mrope_sections
+ * non-zero): positions3 is a host array [3][batch] with the new rows'
+ * temporal, height and width positions, each in [0, max kv_lens + 1).  Cache
+ * placement and masking follow kv_lens.  Errors as for the decode step, plus
+ * HS_ERR_INVALID_ARG for null positions3, zero mrope_sections or a position
+ * out of range. */
+hs_status hs_downstream_decode_step_mrope(hs_context* ctx, const hs_layer_cfg* cfg,
+                                          const hs_layer_weights* w, int32_t n_layers, const void* x_in,
+                                          void* x_out, const hs_kv_cache* kv, const int32_t* kv_lens,
+                                          const int32_t* positions3, int32_t batch, int32_t cu_budget,
+                                          void* stream, void* workspace, size_t ws_bytes);
+
 hs_status hs_downstream_decode_step(hs_context* ctx, const hs_layer_cfg* cfg,
                                     const hs_layer_weights* w, int32_t n_layers,
                                     const void* x_in, void* x_out, const hs_kv_cache* kv,

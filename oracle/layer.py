@@ -189,14 +189,15 @@ def stack_forward(x: np.ndarray, layers: List[Dict[str, np.ndarray]], cfg, seq_o
     return x, kv
 
 
-def decode_step(x: np.ndarray, layers, cfg, kv_lens, cache_k, cache_v):
+def decode_step(x: np.ndarray, layers, cfg, kv_lens, cache_k, cache_v, positions3=None):
     """One decode step: every row is a one-row sequence behind kv_lens[b] cached rows.
 
     cache_k/v: per layer, per sequence [kv_len_b, Hkv, dh].  The new row sits
     at position kv_lens[b] and attends to kv_lens[b] + 1 keys.  Returns
-    (y [B, d], [(k_new [B, Hkv, dh], v_new) per layer]).
+    (y [B, d], [(k_new [B, Hkv, dh], v_new) per layer]).  positions3 [3, B]: the new rows'
+    multimodal RoPE positions (cfg.mrope_sections splits the pairs).
     """
     B = len(kv_lens)
     off = np.arange(B + 1)
-    return stack_forward(x, layers, cfg, off, kv_lens, cache_k, cache_v)
+    return stack_forward(x, layers, cfg, off, kv_lens, cache_k, cache_v, positions3=positions3)
 

@@ -23,7 +23,7 @@ SYMBOLS = (
     "hs_status_string", "hs_last_error", "hs_default_topology", "hs_cu_partition", "hs_plan_metadata",
     "hs_context_create", "hs_context_topology", "hs_context_stream", "hs_context_masks",
     "hs_context_destroy", "hs_workspace_size", "hs_workspace_size_paged", "hs_shared_stage_forward",
-    "hs_shared_stage_forward_mrope", "hs_downstream_decode_step",
+    "hs_shared_stage_forward_mrope", "hs_downstream_decode_step_mrope", "hs_downstream_decode_step",
     "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read", "hs_convert_weights_f16",
     "hs_controller_create", "hs_controller_step", "hs_controller_destroy", "hs_pressure_sample",
     "hs_temporal_create", "hs_temporal_step", "hs_temporal_destroy",
@@ -133,6 +133,9 @@ def lib() -> ctypes.CDLL:
             "hs_shared_stage_forward_mrope": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp,
                                               vp, i32p, i32p, i32, ctypes.POINTER(KvCache), i32p, i32, vp, vp,
                                               ctypes.c_size_t],
+            "hs_downstream_decode_step_mrope": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp,
+                                                vp, ctypes.POINTER(KvCache), i32p, i32p, i32, i32, vp, vp,
+                                                ctypes.c_size_t],
             "hs_downstream_decode_step": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp, vp,
                                           ctypes.POINTER(KvCache), i32p, i32, i32, vp, vp, ctypes.c_size_t],
             "hs_probe_hw_ids": [vp, vp, i32, vp],
@@ -416,6 +419,22 @@ def hs_shared_stage_forward_mrope(ctx: Context, cfg, weights, x_in, x_out, seq_o
         ctx.handle, ctypes.byref(LayerCfg.of(cfg)), warr, len(weights), _ptr(x_in), _ptr(x_out), off,
         _i32_array(ctx_lens), len(off) - 1, ctypes.byref(kvs) if kvs is not None else None,
         pos.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), cu_budget, _ptr(stream), _ptr(workspace), ws_bytes))
+
+
+def hs_downstream_decode_step_mrope(ctx: Context, cfg, weights, x_in, x_out, kv, kv_lens, positions3, cu_budget: int,
+                                    stream=None, workspace=None, ws_bytes: Optional[int] = None) -> None:
+    """positions3: host int array [3, batch] (the new rows' temporal, height and width positions)."""
+    warr = _weights_array(weights)
+    kvs = _kv_struct(kv)
+    lens = _i32_array(kv_lens)
+    pos = np.ascontiguousarray(positions3, dtype=np.int32)
+    assert pos.shape == (3, len(lens))
+    if ws_bytes is None:
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().hs_downstream_decode_step_mrope(
+        ctx.handle, ctypes.byref(LayerCfg.of(cfg)), warr, len(weights), _ptr(x_in), _ptr(x_out), ctypes.byref(kvs),
+        lens, pos.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), len(lens), cu_budget, _ptr(stream),
+        _ptr(workspace), ws_bytes))
 
 
 def hs_downstream_decode_step(ctx: Context, cfg, weights, x_in, x_out, kv, kv_lens, cu_budget: int,

@@ -602,6 +602,21 @@ hs_status hs_downstream_decode_step(hs_context* ctx, const hs_layer_cfg* cfg, co
                    HS_ROLE_DOWN, stream, workspace, ws_bytes);
 }
 
+hs_status hs_downstream_decode_step_mrope(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w,
+                                          int32_t n_layers, const void* x_in, void* x_out, const hs_kv_cache* kv,
+                                          const int32_t* kv_lens, const int32_t* positions3, int32_t batch,
+                                          int32_t cu_budget, void* stream, void* workspace, size_t ws_bytes) {
+  hs::clear_error();
+  if (!positions3) return hs::fail(HS_ERR_INVALID_ARG, "positions3 is null");
+  if (!kv) return hs::fail(HS_ERR_INVALID_ARG, "decode needs a key/value cache");
+  if (!kv_lens) return hs::fail(HS_ERR_INVALID_ARG, "kv_lens is null");
+  if (batch < 1) return hs::fail(HS_ERR_INVALID_ARG, "batch %d < 1", batch);
+  std::vector<int32_t> off(batch + 1);
+  for (int32_t b = 0; b <= batch; ++b) off[b] = b;
+  return run_stack(ctx, cfg, w, n_layers, x_in, x_out, off.data(), kv_lens, batch, kv, cu_budget, HS_ROLE_DOWN,
+                   stream, workspace, ws_bytes, positions3);
+}
+
 hs_status hs_convert_weights_f16(hs_context* ctx, const void* src, void* dst, int64_t rows, int64_t cols,
                                  void* stream) {
   hs::clear_error();

@@ -79,3 +79,43 @@ def test_prefill_with_mrope_positions(env, shape_name, lengths, n_img):
     binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, offsets, ctx_lens, cache.as_arg(), 128, None, ws)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(y_eq, y.cpu().numpy())
+
+
+def test_talker_decode_step_with_mrope_positions(env):
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    from paper_2608_01785_amd.device_data import DeviceCache, prepare_f16, to_device, upload_weights
+    shape = dataclasses.replace(W.TALKER, mrope_sections=SECTIONS[64])
+    n_layers, batch = 2, 24
+    rng = np.random.default_rng(111)
+    kv_lens = rng.integers(1, 400, size=batch).astype(np.int32)
+    # New rows of an audio-output stream: temporal position kv_len, height and width
+    # positions of a 2-D layout below it.
+    pos3 = np.stack([kv_lens, kv_lens // 2, kv_lens // 3]).astype(np.int32)
+    layers = W.make_weights(shape, n_layers, 112)
+    x = W.token_rows(113, batch, shape.hidden)
+    prefix = W.make_cache(shape, n_layers, kv_lens, seed=114)
+    cache = DeviceCache(n_layers, batch, 448, shape.n_kv_heads, shape.head_dim, fill=0.0)
+    for l in range(n_layers):
+        for b in range(batch):
+            cache.load_prefix(l, b, prefix.k[l][b], prefix.v[l][b])
+    log(f"[mrope decode] talker layers={n_layers} batch={batch}")
+    pk = [[h64(k) for k in prefix.k[l]] for l in range(n_layers)]
+    pv = [[h64(v) for v in prefix.v[l]] for l in range(n_layers)]
+    expect, kv_new = ref.decode_step(f64(x), weights_f64(layers), shape, kv_lens, pk, pv, positions3=pos3)
+    _, kv_plain = ref.decode_step(f64(x), weights_f64(layers), shape, kv_lens, pk, pv)
+    assert err_ratio(kv_plain[0][0], kv_new[0][0]) > 10 * TOL
+    ws = workspace(torch, shape, batch, batch, int(kv_lens.max()) + 1)
+    wdev = prepare_f16(ctx, upload_weights(layers))
+    xd = to_device(x)
+    y = torch.empty(xd.shape, dtype=torch.float32, device="cuda")
+    binding.hs_downstream_decode_step_mrope(ctx, shape, wdev, xd, y, cache.as_arg(), kv_lens, pos3, 128, None, ws)
+    torch.cuda.synchronize()
+    e = err_ratio(y.cpu().numpy(), expect)
+    log(f"  max err / rms = {e:.3e}")
+    assert e <= TOL
+    for l in range(n_layers):
+        for b in range(batch):
+            kb, vb = cache.rows(l, b, int(kv_lens[b]), int(kv_lens[b]) + 1)
+            assert err_ratio(h64(kb[0]), kv_new[l][0][b]) <= TOL
+            assert err_ratio(h64(vb[0]), kv_new[l][1][b]) <= TOL
