@@ -88,8 +88,8 @@ def main():
                     help="also run one device copy of this many MiB (counter calibration under a profiler)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build measures one GPU only; the hot path is a single-GPU "
-                                   "spatial-sharing design (run with --gpus 1)"}))
+        print(json.dumps({"error": "bench.py measures one GPU only: the path is a single-GPU spatial-sharing design "
+                                   "(run with --gpus 1)"}))
         sys.exit(2)
 
     import torch
@@ -810,7 +810,7 @@ def serving_loop(torch, binding, W, ctx, wdev, dev, policy, n_req=32, first_chun
 
 
 def controller_measure(torch, binding, ctx, ladder, dev):
-    """Costs of the spatial controller's control path on the GPU machine.
+    """Costs of the spatial controller's control path on the GPU.
 
     * switch_us: extra GPU-side delay when consecutive dependent launches move
       from the SHARED stream of one ladder level to that of another (an event
