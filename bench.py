@@ -666,15 +666,17 @@ def policy_model(W, shape, batch, per_budget, corun):
     return out
 
 
-def serving_loop(torch, binding, W, ctx, wdev, dev, policy, n_req=32, first_chunk=20, seed=11):
-    """Algorithm 1 on the GPU (measured, unlike the model): a burst of requests, half long-path.
+def serving_loop(torch, binding, W, ctx, wdev, dev, policy, n_req=48, first_chunk=20, seed=11, load=0.6):
+    """Algorithm 1 on the GPU (measured, unlike the model): a seeded Poisson stream of requests
+    at `load` times the shared stage's capacity, half long-path.
     Per scheduling step the temporal view picks the visible requests (joint policy), an FCFS
     batch of up to 4096 prompt tokens is prefilled through the 4-layer thinker stack, and the
     controller picks the CU split; while the prefill runs, talker decode steps of the active
     long-path requests loop on the complementary stream (their cache pages addressed through a
     per-step block table).  A short request's first response is the end of its prefill step, a
-    long request's the end of the scheduling step in which its first_chunk-th talker step
-    completes.  Baseline: every request visible, both stages unmasked on the whole chip."""
+    long request's the end of its first_chunk-th talker step (both from GPU events), each
+    measured from the request's arrival.  Baseline: every request visible, both stages unmasked
+    on the whole chip."""
     from paper_2608_01785_amd.device_data import DeviceCache, prepare_f16, to_device, upload_weights
     joint = policy == "joint"
     rng = np.random.default_rng(seed)
@@ -682,6 +684,8 @@ def serving_loop(torch, binding, W, ctx, wdev, dev, policy, n_req=32, first_chun
     tokens = rng.integers(256, 1024, size=n_req, endpoint=True).astype(int)
     long = rng.uniform(size=n_req) < 0.5
     kv0 = rng.integers(128, 512, size=n_req, endpoint=True).astype(np.int32)
+    per_tok, talker_ms = 0.00185, 0.9       # solo ms per prompt token at 256 CUs, talker step at 128
+    arrival = np.cumsum(rng.exponential(float(np.mean(tokens)) * per_tok / load, size=n_req))
     # Weights, inputs and caches.
     tl = prepare_f16(ctx, upload_weights(W.make_weights(ts, 16, W.SEEDS["talker"]["weights"]), dev))
     x_pool = to_device(W.token_rows(seed, 4096, th.hidden), dev)
@@ -699,20 +703,22 @@ def serving_loop(torch, binding, W, ctx, wdev, dev, policy, n_req=32, first_chun
     yt = torch.empty((n_req, ts.hidden), dtype=torch.float32, device=dev)
     wst = torch.empty(binding.hs_workspace_size_paged(ts, n_req, n_req, max_ctx, max_ctx), dtype=torch.uint8, device=dev)
     # Solo estimates (ms) for deadlines and remaining times: per-token prefill and one talker step.
-    per_tok, talker_ms = 0.00185, 0.9
     solo = tokens * per_tok + np.where(long, first_chunk * talker_ms, 0.0)
     delta = {c: 5.0 * float(np.percentile(solo[long == c], 95)) for c in (False, True)}
-    deadline = np.array([delta[bool(l)] for l in long])
+    deadline = arrival + np.array([delta[bool(l)] for l in long])
     sched = binding.Temporal(2, 8, 2, 1.0, 4) if joint else None
     ctrl = binding.Controller(N_CUS, N_CUS, [128, 160, 192, 224], 0.4, 0.2, 1) if joint else None
     full = torch.cuda.Stream()
     s_full = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, N_CUS, binding.HS_ROLE_SHARED))
-    waiting = list(range(n_req))
+    waiting, nxt = [], 0
     active, steps, issued = [], np.zeros(n_req, int), np.zeros(n_req, int)
     kv = kv0.copy()
     first = np.full(n_req, np.nan)
     shares = []
     torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    start.record(s_full)
+    full.wait_event(start)
     t0 = time.perf_counter()
 
     def talker_step(s_shared, ids):
@@ -725,14 +731,20 @@ def serving_loop(torch, binding, W, ctx, wdev, dev, policy, n_req=32, first_chun
             binding.hs_downstream_decode_step(ctx, ts, tl, xt, yt, (cache.k, cache.v, n_req, max_ctx, table),
                                               kv[ids], N_CUS, full.cuda_stream, wst)
             rec = full
-        e = torch.cuda.Event()
+        e = torch.cuda.Event(enable_timing=True)
         e.record(rec)
         return e, ids
 
-    for _ in range(400):
-        if not waiting and not active:
-            break
+    for _ in range(1000):
         now = (time.perf_counter() - t0) * 1e3
+        while nxt < n_req and arrival[nxt] <= now:
+            waiting.append(nxt)
+            nxt += 1
+        if not waiting and not active:
+            if nxt >= n_req:
+                break
+            time.sleep(max(0.0, (arrival[nxt] - now) / 1e3))
+            continue
         vis = [True] * len(waiting)
         if sched is not None and waiting:
             vis, _ = binding.hs_temporal_step(sched, now, [
@@ -759,7 +771,7 @@ def serving_loop(torch, binding, W, ctx, wdev, dev, policy, n_req=32, first_chun
             stream = s_full if s_sh == N_CUS else torch.cuda.ExternalStream(
                 binding.hs_context_stream(ctx, s_sh, binding.HS_ROLE_SHARED))
             binding.hs_shared_stage_forward(ctx, th, wdev, x_pool[:tok], y[:tok], off, None, None, s_sh, None, ws)
-            p_end = torch.cuda.Event()
+            p_end = torch.cuda.Event(enable_timing=True)
             p_end.record(stream)
             while not p_end.query():
                 cur = np.array([i for i in active if issued[i] < first_chunk], np.int32)
@@ -777,27 +789,28 @@ def serving_loop(torch, binding, W, ctx, wdev, dev, policy, n_req=32, first_chun
                 kv[cur] += 1
                 issued[cur] += 1
         torch.cuda.synchronize()
-        done_t = (time.perf_counter() - t0) * 1e3
         for i in batch:
             waiting.remove(i)
             if long[i]:
                 active.append(i)
             else:
-                first[i] = done_t
-        for _, ids in pend:
+                first[i] = start.elapsed_time(p_end)
+        for e, ids in pend:
             for i in ids:
                 steps[i] += 1
                 if steps[i] >= first_chunk and np.isnan(first[i]):
-                    first[i] = done_t
+                    first[i] = start.elapsed_time(e)
         active = [i for i in active if np.isnan(first[i])]
     if sched is not None:
         sched.close()
     if ctrl is not None:
         ctrl.close()
     out = {"policy": policy, "mean_shared_cus": round(float(np.mean(shares)), 1) if shares else None,
+           "n_requests": n_req, "load": load, "rate_req_s": round(1e3 * n_req / float(arrival[-1]), 1),
            "makespan_ms": round(float(np.nanmax(first)), 2), "unfinished": int(np.isnan(first).sum())}
+    resp = first - arrival
     for name, flag in (("short", False), ("long", True)):
-        lat = first[long == flag]
+        lat = resp[long == flag]
         lat = lat[~np.isnan(lat)]
         met = (first[long == flag] <= deadline[long == flag])
         out[name] = {"n": int((long == flag).sum()), "slo_attainment": round(float(met.mean()), 4),
