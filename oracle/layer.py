@@ -115,16 +115,13 @@ def layer_forward(x: np.ndarray, w: Dict[str, np.ndarray], cfg, seq_offsets: Seq
                   ctx_lens: Optional[Sequence[int]] = None,
                   prefix_k: Optional[List[np.ndarray]] = None,
                   prefix_v: Optional[List[np.ndarray]] = None,
-                  seqs: Optional[Sequence[int]] = None,
                   positions3: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     """One pre-norm decoder layer over a packed ragged batch.
 
     x: [T, d] float64; w: float64 weights ('ln1', 'w_qkv', 'w_o', 'ln2',
     'w_gate_up', 'w_down', optional 'b_qkv'); seq_offsets: [B+1]; ctx_lens: [B] cached rows per
     sequence (None = no prefix); prefix_k/v: per sequence [ctx_b, Hkv, dh].
-    ``seqs`` restricts the attention to those sequences (their rows of the
-    output are exact; other rows keep only the row-local parts and must not
-    be read).  ``positions3`` [3, T], if given, are the rows' multimodal RoPE positions
+    ``positions3`` [3, T], if given, are the rows' multimodal RoPE positions
     (``cfg.mrope_sections`` splits the pairs).  Returns (y [T, d], k_new [T, Hkv, dh], v_new [T, Hkv, dh]).
     """
     x = np.asarray(x, dtype=np.float64)
@@ -153,7 +150,7 @@ def layer_forward(x: np.ndarray, w: Dict[str, np.ndarray], cfg, seq_offsets: Seq
         k = rope(k, pos, cfg.rope_base)
 
     o = np.zeros((T, hq, dh), dtype=np.float64)
-    for b in (range(B) if seqs is None else seqs):
+    for b in range(B):
         lo, hi = off[b], off[b + 1]
         if hi == lo:
             continue
@@ -174,7 +171,7 @@ def layer_forward(x: np.ndarray, w: Dict[str, np.ndarray], cfg, seq_offsets: Seq
 
 
 def stack_forward(x: np.ndarray, layers: List[Dict[str, np.ndarray]], cfg, seq_offsets,
-                  ctx_lens=None, prefix_k=None, prefix_v=None, seqs=None, positions3=None):
+                  ctx_lens=None, prefix_k=None, prefix_v=None, positions3=None):
     """Layers applied in order; the output is the residual stream (no final norm).
 
     prefix_k/v, if given, are per layer lists of per-sequence prefixes.
@@ -184,7 +181,7 @@ def stack_forward(x: np.ndarray, layers: List[Dict[str, np.ndarray]], cfg, seq_o
     for li, w in enumerate(layers):
         pk = None if prefix_k is None else prefix_k[li]
         pv = None if prefix_v is None else prefix_v[li]
-        x, k, v = layer_forward(x, w, cfg, seq_offsets, ctx_lens, pk, pv, seqs, positions3)
+        x, k, v = layer_forward(x, w, cfg, seq_offsets, ctx_lens, pk, pv, positions3)
         kv.append((k, v))
     return x, kv
 

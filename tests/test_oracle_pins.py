@@ -293,6 +293,56 @@ def test_layer_with_prefix_matches_brute_force_loops():
     np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-11)
 
 
+def test_stack_chains_layers_like_brute_force_loops():
+    # Catches a stack that feeds the original x (or the previous layer's input)
+    # to every layer, reuses one layer's weights, or drops the last layer: the
+    # brute-force loops are applied layer after layer, each on the previous
+    # layer's output.
+    c = cfg(d=12, hq=4, hkv=2, dh=6, f=10)
+    rng = np.random.default_rng(21)
+    layers = [rand_weights(c, rng) for _ in range(3)]
+    off = [0, 3, 7]
+    x = rng.standard_normal((7, 12))
+    got, kv = L.stack_forward(x, layers, c, off)
+    ref = x
+    for w in layers:
+        ref = brute_force_layer(ref, w, c, off)
+    np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-10)
+    # Layers really differ: two layers are not one layer applied twice.
+    twice = brute_force_layer(brute_force_layer(x, layers[0], c, off), layers[0], c, off)
+    assert np.max(np.abs(L.stack_forward(x, layers[:2], c, off)[0] - twice)) > 1e-3
+    # Keys of layer 1 come from layer 0's output, not from x.
+    _, k1, _ = L.layer_forward(L.layer_forward(x, layers[0], c, off)[0], layers[1], c, off)
+    np.testing.assert_allclose(kv[1][0], k1, rtol=1e-12, atol=1e-12)
+
+
+def test_stack_with_per_layer_prefixes_matches_brute_force_loops():
+    # Each layer reads its own cached prefix: a stack that handed layer 0's
+    # prefix to every layer fails here.
+    c = cfg(d=8, hq=2, hkv=1, dh=4, f=6)
+    rng = np.random.default_rng(22)
+    layers = [rand_weights(c, rng) for _ in range(2)]
+    off, ctx = [0, 2, 5], [3, 1]
+    pk = [[rng.standard_normal((n, 1, 4)) for n in ctx] for _ in range(2)]
+    pv = [[rng.standard_normal((n, 1, 4)) for n in ctx] for _ in range(2)]
+    x = rng.standard_normal((5, 8))
+    got, _ = L.stack_forward(x, layers, c, off, ctx, pk, pv)
+    ref = x
+    for li, w in enumerate(layers):
+        ref = brute_force_layer(ref, w, c, off, ctx, pk[li], pv[li])
+    np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-10)
+    # The decode step is that stack over one-row sequences.
+    kv_lens = [4, 2]
+    dk = [[rng.standard_normal((n, 1, 4)) for n in kv_lens] for _ in range(2)]
+    dv = [[rng.standard_normal((n, 1, 4)) for n in kv_lens] for _ in range(2)]
+    xd = rng.standard_normal((2, 8))
+    yd, _ = L.decode_step(xd, layers, c, kv_lens, dk, dv)
+    ref = xd
+    for li, w in enumerate(layers):
+        ref = brute_force_layer(ref, w, c, [0, 1, 2], kv_lens, dk[li], dv[li])
+    np.testing.assert_allclose(yd, ref, rtol=1e-10, atol=1e-10)
+
+
 def test_residual_identity():
     c = cfg()
     rng = np.random.default_rng(9)
