@@ -412,7 +412,9 @@ def hs_shared_stage_forward_mrope(ctx: Context, cfg, weights, x_in, x_out, seq_o
     off = _i32_array(seq_offsets)
     kvs = _kv_struct(kv)
     pos = np.ascontiguousarray(positions3, dtype=np.int32)
-    assert pos.ndim == 2 and pos.shape[0] == 3
+    n_rows = int(off[len(off) - 1])
+    if pos.shape != (3, n_rows):
+        raise ValueError(f"positions3 has shape {pos.shape}, expected (3, {n_rows})")
     if ws_bytes is None:
         ws_bytes = workspace.numel() * workspace.element_size()
     _check(lib().hs_shared_stage_forward_mrope(
@@ -428,7 +430,8 @@ def hs_downstream_decode_step_mrope(ctx: Context, cfg, weights, x_in, x_out, kv,
     kvs = _kv_struct(kv)
     lens = _i32_array(kv_lens)
     pos = np.ascontiguousarray(positions3, dtype=np.int32)
-    assert pos.shape == (3, len(lens))
+    if pos.shape != (3, len(lens)):
+        raise ValueError(f"positions3 has shape {pos.shape}, expected (3, {len(lens)})")
     if ws_bytes is None:
         ws_bytes = workspace.numel() * workspace.element_size()
     _check(lib().hs_downstream_decode_step_mrope(

@@ -93,6 +93,30 @@ hs_status validate_batch(const int32_t* off, const int32_t* ctx, int32_t B, int3
   return HS_OK;
 }
 
+hs_status check_32bit_extents(const hs_layer_cfg& c, int32_t T, int32_t max_ctx) {
+  const int64_t limit = int64_t(1) << 32;  // exclusive: the resources' byte count is a uint32
+  const int64_t d = c.hidden, f = c.ffn, qd = int64_t(c.n_q_heads) * c.head_dim;
+  const int64_t qkv = int64_t(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  const struct {
+    const char* what;
+    int64_t bytes;
+  } ext[] = {
+      {"w_qkv", qkv * d * 2},          {"w_o", d * qd * 2},
+      {"w_gate_up", 2 * f * d * 2},    {"w_down", d * f * 2},
+      {"the hidden-wide activations", int64_t(T) * d * 2},
+      {"the attention output", int64_t(T) * qd * 2},
+      {"the SwiGLU output", int64_t(T) * f * 2},
+  };
+  for (const auto& e : ext)
+    if (e.bytes >= limit)
+      return fail(HS_ERR_UNSUPPORTED, "%s would take %lld bytes; the kernels address at most 2^32 - 1", e.what,
+                  (long long)e.bytes);
+  if (int64_t(max_ctx) * c.head_dim * 2 > 0x7ffffff0)
+    return fail(HS_ERR_UNSUPPORTED, "a cache page of %d positions exceeds the 2 GiB a single-row attention unit addresses",
+                max_ctx);
+  return HS_OK;
+}
+
 int64_t max_att_items(int32_t T, int32_t B) { return int64_t(T) / kAttnBlockQ + B + 1; }
 
 // Split-K scratch of the skinny GEMM over the four projections of a layer:

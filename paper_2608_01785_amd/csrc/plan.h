@@ -29,6 +29,13 @@ hs_status validate_cfg(const hs_layer_cfg* cfg);
 hs_status validate_batch(const int32_t* seq_offsets, const int32_t* ctx_lens, int32_t n_seqs,
                          int32_t* n_tokens, int32_t* max_pos);
 
+// The GEMMs address activations and weights through buffer resources whose
+// size and offsets are 32-bit byte counts, and single-row attention addresses
+// a cache page the same way within 2 GiB.  HS_ERR_UNSUPPORTED when a layer's
+// weight matrix, an activation matrix of T rows, or a cache page of max_ctx
+// positions (0: no cache) would not fit.
+hs_status check_32bit_extents(const hs_layer_cfg& cfg, int32_t n_tokens, int32_t max_ctx);
+
 // Byte offsets of every buffer inside the caller's workspace.
 struct WsLayout {
   size_t meta;        // metadata image (copied from the host each call)

@@ -230,6 +230,8 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
   int32_t T = 0, max_pos = 0;
   st = hs::validate_batch(seq_offsets, ctx_lens, n_seqs, &T, &max_pos);
   if (st != HS_OK) return st;
+  st = hs::check_32bit_extents(*cfg, T, kv ? kv->max_ctx : 0);
+  if (st != HS_OK) return st;
   hs::KvPlacement place;
   if (kv) {
     if (!ctx_lens) return hs::fail(HS_ERR_INVALID_ARG, "a key/value cache needs ctx_lens");

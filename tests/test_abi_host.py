@@ -147,6 +147,33 @@ def test_forward_validation_fails_before_any_gpu_work(b):
     assert st == b.HS_ERR_UNSUPPORTED
 
 
+def test_extents_beyond_32_bit_byte_offsets_are_rejected(b):
+    # The GEMMs' buffer resources count bytes in 32 bits: at FFN 18944 the
+    # SwiGLU output of 113,360 rows takes 2^32 bytes or more.  Such a batch
+    # must fail before any GPU work instead of reading zeros past the end.
+    from paper_2608_01785_amd import workloads as W
+    c = W.THINKER
+    assert 113360 * c.ffn * 2 >= 1 << 32 > 113359 * c.ffn * 2
+    st, msg = _forward_null_ctx(b, c, [0, 113360])
+    assert st == b.HS_ERR_UNSUPPORTED and "SwiGLU" in msg, msg
+    st, msg = _forward_null_ctx(b, c, [0, 60000, 113360])
+    assert st == b.HS_ERR_UNSUPPORTED, msg
+    st, msg = _forward_null_ctx(b, c, [0, 113359])
+    assert st == b.HS_ERR_INVALID_ARG and "context" in msg, msg           # every check passed
+    # A weight matrix of 2^32 bytes or more.
+    import dataclasses
+    big = dataclasses.replace(c, hidden=8192, ffn=131072)
+    st, msg = _forward_null_ctx(b, big, [0, 4])
+    assert st == b.HS_ERR_UNSUPPORTED and "w_gate_up" in msg, msg
+    # A cache page that single-row attention cannot address.
+    kv = _fake_kv(b, 1, 1 << 23)
+    st, msg = _forward_null_ctx(b, c, [0, 4], ctx_lens=[0], kv=ctypes.byref(kv))
+    assert st == b.HS_ERR_UNSUPPORTED and "page" in msg, msg
+    kv = _fake_kv(b, 1, 1 << 22)
+    st, msg = _forward_null_ctx(b, c, [0, 4], ctx_lens=[0], kv=ctypes.byref(kv))
+    assert st == b.HS_ERR_INVALID_ARG and "context" in msg, msg
+
+
 def _fake_kv(b, n_slots, page, table=None, n_layers=1):
     """A cache struct with fake (never dereferenced) layer pointers and an optional block table."""
     from paper_2608_01785_amd import binding
@@ -338,3 +365,20 @@ int main() {
     assert r.returncode == 0, r.stdout
     r = subprocess.run([str(exe)], stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     assert r.returncode == 0 and r.stdout.startswith("ok"), r.stdout
+
+
+def test_binding_rejects_positions3_of_the_wrong_length(b):
+    # The library reads 3 * T positions (T = the last offset); a shorter array
+    # would be read past its end on the host, so the binding refuses it before
+    # the call (no context or device memory is touched).
+    import dataclasses
+    from paper_2608_01785_amd import workloads as W
+    c = dataclasses.replace(W.TINY, mrope_sections=(8, 12, 12))
+    w = [{n: 0x1000 for n in ("ln1", "w_qkv", "w_o", "ln2", "w_gate_up", "w_down")}]
+    short = W.mrope_positions([10, 5], [4, 0])                  # T = 15, offsets say 16
+    with pytest.raises(ValueError, match="positions3"):
+        b.hs_shared_stage_forward_mrope(None, c, w, 1 << 20, 2 << 20, [0, 10, 16], short, workspace=0x3000,
+                                        ws_bytes=1 << 30)
+    with pytest.raises(ValueError, match="positions3"):
+        b.hs_downstream_decode_step_mrope(None, c, w, 1 << 20, 2 << 20, ([0x5000], [0x6000], 4, 64), [3, 4, 5],
+                                          np.zeros((3, 2), np.int32), 128, workspace=0x3000, ws_bytes=1 << 30)
