@@ -379,9 +379,13 @@ hs_status hs_controller_destroy(hs_controller* ctrl);
 
 /* Memory-system activity of a GPU in [0, 1]: the memory-controller (UMC)
  * activity that AMD SMI reports, the AMD counterpart of the NVML memory
- * activity the paper samples (§4.4, §5).  device is the index in AMD SMI's
- * enumeration.  The library is loaded on first use; HS_ERR_UNSUPPORTED when
- * it, or the reading, is unavailable. */
+ * activity the paper samples (§4.4, §5).  device is a HIP device index; the
+ * reading comes from the AMD SMI GPU at that device's PCI address (AMD SMI's
+ * own enumeration order is not used).  AMD SMI is loaded on first use.
+ * Errors: HS_ERR_INVALID_ARG for a null pointer or a device outside HIP's
+ * device count; HS_ERR_HIP if the PCI address cannot be read;
+ * HS_ERR_UNSUPPORTED when AMD SMI, a GPU at that address, or the reading is
+ * unavailable.  One reading takes on the order of 100 us (a driver query). */
 hs_status hs_pressure_sample(int32_t device, double* activity);
 
 /* ------------------------------------------------------------------------

@@ -20,7 +20,7 @@ LIB = os.path.join(PKG, "libhorizon.so")
 
 ARCH = "gfx950"
 HIP_SOURCES = ["gemm.hip", "gemm_skinny.hip", "attention.hip", "misc.hip"]
-HOST_SOURCES = ["plan.cpp", "runtime.cpp", "controller.cpp", "temporal.cpp"]
+HOST_SOURCES = ["plan.cpp", "runtime.cpp", "controller.cpp", "temporal.cpp", "pressure.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}"]
 # Keep the compiler from forming packed fp32 instructions.

@@ -1,6 +1,5 @@
 // Spatial controller: bandwidth-guided shared-stage CU cap (HorizonServe
-// §4.4, Eq. (1); Algorithm 1, steps 1 and 3) and the memory-pressure sample
-// it feeds on.  Host-only C++.
+// §4.4, Eq. (1); Algorithm 1, steps 1 and 3).  Host-only C++.
 //
 // Per scheduling step the caller passes the downstream activity A(t) and one
 // sample B(t) of memory-system activity.  The controller smooths the sample
@@ -10,12 +9,10 @@
 // away from the current one; with no downstream activity it returns the
 // aggressive cap.  The downstream stage gets S_tot - s_shared.  The chosen
 // counts are ladder levels of a context, so switching is the selection of a
-// pre-built stream pair (§5), not the creation of one.
-#include <dlfcn.h>
-
+// pre-built stream pair (§5), not the creation of one.  The sample itself
+// comes from pressure.cpp.
 #include <cmath>
 #include <cstdint>
-#include <mutex>
 #include <vector>
 
 #include "horizon.h"
@@ -40,44 +37,6 @@ int32_t snap_level(const std::vector<int32_t>& ladder, double x) {
   for (int32_t i = 0; i < int32_t(ladder.size()); ++i)
     if (std::fabs(ladder[i] - x) <= std::fabs(ladder[best] - x)) best = i;
   return best;
-}
-
-// ---------------------------------------------------------------------------
-// Memory-controller activity through the AMD SMI library, loaded on first use
-// so that the library does not depend on it at link time.
-
-struct AmdSmiStatics {
-  std::once_flag once;
-  bool ok = false;
-  std::vector<void*> gpus;  // processor handles in enumeration order
-  int (*get_activity)(void*, void*) = nullptr;
-};
-AmdSmiStatics g_smi;
-
-constexpr uint64_t kAmdSmiInitGpus = 1ull << 1;  // AMDSMI_INIT_AMD_GPUS
-
-void smi_load() {
-  void* h = dlopen("libamd_smi.so", RTLD_NOW | RTLD_LOCAL);
-  if (!h) h = dlopen("/opt/rocm/lib/libamd_smi.so", RTLD_NOW | RTLD_LOCAL);
-  if (!h) return;
-  auto init = reinterpret_cast<int (*)(uint64_t)>(dlsym(h, "amdsmi_init"));
-  auto sockets = reinterpret_cast<int (*)(uint32_t*, void**)>(dlsym(h, "amdsmi_get_socket_handles"));
-  auto procs = reinterpret_cast<int (*)(void*, uint32_t*, void**)>(dlsym(h, "amdsmi_get_processor_handles"));
-  g_smi.get_activity = reinterpret_cast<int (*)(void*, void*)>(dlsym(h, "amdsmi_get_gpu_activity"));
-  if (!init || !sockets || !procs || !g_smi.get_activity) return;
-  if (init(kAmdSmiInitGpus) != 0) return;
-  uint32_t n_sock = 0;
-  if (sockets(&n_sock, nullptr) != 0 || n_sock == 0) return;
-  std::vector<void*> socks(n_sock);
-  if (sockets(&n_sock, socks.data()) != 0) return;
-  for (uint32_t s = 0; s < n_sock; ++s) {
-    uint32_t n = 0;
-    if (procs(socks[s], &n, nullptr) != 0 || n == 0) continue;
-    std::vector<void*> p(n);
-    if (procs(socks[s], &n, p.data()) != 0) continue;
-    g_smi.gpus.insert(g_smi.gpus.end(), p.begin(), p.begin() + n);
-  }
-  g_smi.ok = !g_smi.gpus.empty();
 }
 
 }  // namespace
@@ -149,21 +108,6 @@ hs_status hs_controller_step(hs_controller* c, int32_t downstream_active, double
 
 hs_status hs_controller_destroy(hs_controller* c) {
   delete c;
-  return HS_OK;
-}
-
-hs_status hs_pressure_sample(int32_t device, double* activity) {
-  hs::clear_error();
-  if (!activity) return hs::fail(HS_ERR_INVALID_ARG, "output pointer is null");
-  std::call_once(g_smi.once, smi_load);
-  if (!g_smi.ok) return hs::fail(HS_ERR_UNSUPPORTED, "AMD SMI is not available");
-  if (device < 0 || device >= int32_t(g_smi.gpus.size()))
-    return hs::fail(HS_ERR_INVALID_ARG, "device %d outside the %zu GPUs AMD SMI lists", device, g_smi.gpus.size());
-  // amdsmi_engine_usage_t: gfx_activity, umc_activity, mm_activity (percent), reserved[13].
-  uint32_t usage[16] = {0};
-  if (g_smi.get_activity(g_smi.gpus[device], usage) != 0)
-    return hs::fail(HS_ERR_UNSUPPORTED, "AMD SMI could not read the activity of device %d", device);
-  *activity = double(usage[1]) / 100.0;
   return HS_OK;
 }
 

@@ -35,6 +35,45 @@ def test_pressure_sample_is_a_fraction():
     assert 0.0 <= v <= 1.0
 
 
+def test_pressure_rises_under_a_bandwidth_bound_load():
+    """The sample tracks this device's memory traffic: readings taken while a
+    stream of device-to-device copies (HBM-bound) runs on the device are higher
+    than readings of the idle device."""
+    import time
+    torch = require_gpu()
+    from paper_2608_01785_amd import binding
+    try:
+        binding.hs_pressure_sample(0)
+    except binding.HorizonError as e:
+        pytest.skip(f"AMD SMI memory activity unavailable on this box: {e}")
+    torch.cuda.synchronize()
+    time.sleep(0.3)
+    idle = []
+    for _ in range(20):
+        idle.append(binding.hs_pressure_sample(0))
+        time.sleep(0.005)
+    a = torch.empty(256 << 20, dtype=torch.float32, device="cuda")    # 1 GiB
+    b = torch.empty_like(a)
+    a.fill_(1.0)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    n_copies = 2000
+    e0.record()
+    for _ in range(n_copies):
+        b.copy_(a)
+    e1.record()
+    busy = []
+    while not e1.query():
+        busy.append(binding.hs_pressure_sample(0))
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    rate = n_copies * 2 * a.numel() * 4 / (ms / 1e3) / 1e12
+    log(f"[pressure] idle median {np.median(idle):.3f} (max {max(idle):.3f}); during {ms:.0f} ms of copies at "
+        f"{rate:.2f} TB/s: median {np.median(busy):.3f} over {len(busy)} samples")
+    assert len(busy) >= 20
+    assert np.median(busy) > np.median(idle) + 0.05
+
+
 def test_controller_drives_the_ladder_with_decode_running():
     torch = require_gpu()
     from paper_2608_01785_amd import binding

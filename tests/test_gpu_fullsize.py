@@ -1,13 +1,17 @@
 """GPU parity at the full workload sizes, in the launch configuration the
 benchmark times, through the C ABI.
 
-The float64 reference cannot run whole 4-layer, 10,515-row stacks in seconds,
-so these tests check outputs it can compute independently:
-* a whole request (sequences never see each other, so request 0 alone through
-  the reference equals its rows of the batched run);
-* the first rows of every request (causality: they depend on nothing later);
-* properties that hold at any size (bit-identical results across CU budgets,
-  concurrency with a co-running decode stage changes nothing).
+Every output row is compared element by element with the float64 reference:
+* the 4-layer thinker stack over all 10,515 rows (sequences never see each
+  other, so the reference runs request by request);
+* the 4096-wide mixed step (four 2048-row chunks behind up to 6,144 cached
+  rows, 64 decode rows) and its cache rows;
+* the talker step at batch 32 (128 CUs) and batch 128 (the 160-CU downstream
+  stream);
+* the thinker's decode rows behind 1-2k cached rows (seven query heads per
+  key/value head).
+Properties that hold at any size are checked as well: bit-identical results
+across CU budgets, and a co-running decode stage that changes nothing.
 """
 import numpy as np
 import pytest
@@ -55,7 +59,11 @@ def run_thinker(env, thinker, budget, stream=None):
     return y
 
 
-def test_thinker_stack_request_and_prefixes(env, thinker):
+def test_thinker_stack_every_row(env, thinker):
+    """All 10,515 rows of the 4-layer launch at 256 CUs against the reference,
+    element by element.  Sequences never see each other, so the reference runs
+    request by request; the longest request (1,901 rows, keys up to position
+    1,900) is one of them."""
     torch, _ = env
     layers, batch, _, _, _ = thinker
     log("[thinker] full stack at 256 CUs")
@@ -65,20 +73,16 @@ def test_thinker_stack_request_and_prefixes(env, thinker):
     assert np.all(np.isfinite(got))
     w64 = weights_f64(layers)
     off = batch.seq_offsets
-    # Whole request 0 (849 rows) through the reference on its own.
-    log("[thinker] reference on request 0")
-    exp0, _ = ref.stack_forward(f64(batch.x[off[0]:off[1]]), w64, W.THINKER, [0, off[1] - off[0]])
-    e = err_ratio(got[off[0]:off[1]], exp0)
-    log(f"  request 0: max err / rms = {e:.3e}")
-    assert e <= TOL
-    # First 24 rows of every request.
-    r = 24
-    xs = np.concatenate([batch.x[o:o + r] for o in off[:-1]])
-    exp, _ = ref.stack_forward(f64(xs), w64, W.THINKER, np.arange(batch.n_seqs + 1) * r)
-    gs = np.concatenate([got[o:o + r] for o in off[:-1]])
-    e = err_ratio(gs, exp)
-    log(f"  first {r} rows of all requests: max err / rms = {e:.3e}")
-    assert e <= TOL
+    assert int(np.max(np.diff(off))) == 1901
+    worst = 0.0
+    for b in range(batch.n_seqs):
+        lo, hi = int(off[b]), int(off[b + 1])
+        exp, _ = ref.stack_forward(f64(batch.x[lo:hi]), w64, W.THINKER, [0, hi - lo])
+        e = err_ratio(got[lo:hi], exp)
+        log(f"  request {b} ({hi - lo} rows): max err / rms = {e:.3e}")
+        assert e <= TOL, (b, e)
+        worst = max(worst, e)
+    log(f"  every row: worst max err / rms = {worst:.3e}")
 
 
 def test_thinker_budgets_bit_identical(env, thinker):
@@ -149,9 +153,11 @@ def test_talker_decode_step_full(env):
         assert err_ratio(vn, kv_new[l][1]) <= TOL
 
 
-def test_thinker_mixed_step_sampled(env):
+def test_thinker_mixed_step_every_row(env):
     """One layer at hidden 4096: four 2048-row chunks behind 0/2048/4096/6144 cached
-    rows and 64 single-row sequences behind 4096 cached rows, at 96 CUs."""
+    rows and 64 single-row sequences behind 4096 cached rows, at 96 CUs.  Every
+    row against the reference (the last chunk's rows sit at positions
+    6,144-8,191), and the new cache rows of every sequence."""
     torch, ctx = env
     from paper_2608_01785_amd import binding
     from paper_2608_01785_amd.device_data import DeviceCache, prepare_f16, to_device, upload_weights
@@ -175,18 +181,103 @@ def test_thinker_mixed_step_sampled(env):
     binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, ctx_lens, cache.as_arg(), 96, None, ws)
     torch.cuda.synchronize()
     got = y.cpu().numpy().astype(np.float64)
-    # Reference on sampled rows: first 16 rows of each chunk, and 8 decode rows.
     off = batch.seq_offsets
-    pick = [(b, 16) for b in range(4)] + [(b, 1) for b in range(4, B, 8)]
-    xs = np.concatenate([batch.x[off[b]:off[b] + n] for b, n in pick])
-    so = np.concatenate([[0], np.cumsum([n for _, n in pick])])
     w64 = weights_f64(layers)[0]
-    exp, _, _ = ref.layer_forward(f64(xs), w64, shape, so, [int(ctx_lens[b]) for b, _ in pick],
-                                  [h64(prefix.k[0][b]) for b, _ in pick], [h64(prefix.v[0][b]) for b, _ in pick])
-    gs = np.concatenate([got[off[b]:off[b] + n] for b, n in pick])
-    e = err_ratio(gs, exp)
-    log(f"  sampled rows: max err / rms = {e:.3e}")
+    log("[mixed] reference, every row")
+    exp, k_new, v_new = ref.layer_forward(f64(batch.x), w64, shape, off, [int(c) for c in ctx_lens],
+                                          [h64(k) for k in prefix.k[0]], [h64(v) for v in prefix.v[0]])
+    for b in range(4):
+        e = err_ratio(got[off[b]:off[b + 1]], exp[off[b]:off[b + 1]])
+        log(f"  chunk {b} (positions {ctx_lens[b]}..{ctx_lens[b] + lengths[b] - 1}): max err / rms = {e:.3e}")
+        assert e <= TOL, (b, e)
+    e = err_ratio(got[off[4]:], exp[off[4]:])
+    log(f"  64 decode rows: max err / rms = {e:.3e}")
     assert e <= TOL
+    # The new rows in the cache, at positions ctx .. ctx + len - 1 of each sequence.
+    kc = np.concatenate([h64(cache.rows(0, b, int(ctx_lens[b]), int(ctx_lens[b] + lengths[b]))[0]) for b in range(B)])
+    vc = np.concatenate([h64(cache.rows(0, b, int(ctx_lens[b]), int(ctx_lens[b] + lengths[b]))[1]) for b in range(B)])
+    assert err_ratio(kc, k_new) <= TOL
+    assert err_ratio(vc, v_new) <= TOL
+
+
+class _LazyLayers:
+    """Per-layer lists of float64 cache prefixes, converted when the reference reaches the layer
+    (a whole 16-layer cache in float64 would take tens of GB)."""
+
+    def __init__(self, per_layer):
+        self.per_layer = per_layer
+
+    def __getitem__(self, layer):
+        return [h64(a) for a in self.per_layer[layer]]
+
+
+def test_talker_batch128_on_the_160_cu_down_stream(env):
+    """The downstream-heavy talker: 16 layers, batch 128, cached lengths in
+    [128, 1024], on the DOWN stream of the 96-CU level (160 CUs)."""
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    shape, n_layers, batch = W.TALKER, 16, 128
+    log("[talker-128] 16 layers, batch 128, seeded cache")
+    layers, d, cache, wdev, x, ws = talker_setup(env, batch, W.SEEDS["talker_mixed"], n_layers)
+    assert int(d.kv_lens.sum()) == 75820 and int(d.kv_lens.max()) <= 1024
+    s_dn = binding.hs_context_stream(ctx, 96, binding.HS_ROLE_DOWN)
+    y = torch.empty(x.shape, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    binding.hs_downstream_decode_step(ctx, shape, wdev, x, y, cache.as_arg(), d.kv_lens, 160, s_dn, ws)
+    torch.cuda.synchronize()
+    log("[talker-128] reference")
+    expect, kv_new = ref.decode_step(f64(d.x), weights_f64(layers), shape, d.kv_lens,
+                                     _LazyLayers(d.cache.k), _LazyLayers(d.cache.v))
+    e = err_ratio(y.cpu().numpy(), expect)
+    log(f"  max err / rms = {e:.3e}")
+    assert e <= TOL
+    for l in (0, 8, 15):
+        kn = np.stack([h64(cache.rows(l, b, int(d.kv_lens[b]), int(d.kv_lens[b]) + 1)[0][0]) for b in range(batch)])
+        vn = np.stack([h64(cache.rows(l, b, int(d.kv_lens[b]), int(d.kv_lens[b]) + 1)[1][0]) for b in range(batch)])
+        assert err_ratio(kn, kv_new[l][0]) <= TOL
+        assert err_ratio(vn, kv_new[l][1]) <= TOL
+
+
+def test_thinker_decode_rows_behind_long_prefixes(env, thinker):
+    """The thinker stack's decode step (seven query heads per key/value head):
+    one row for each of 16 sequences behind 1,024-2,048 cached rows, the
+    workload of the decode-TPOT sweep, at caps 64/96/192/256.  Parity against
+    the reference, and the same bits at every cap."""
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    from paper_2608_01785_amd.device_data import DeviceCache, to_device
+    layers, _, wdev, _, _ = thinker
+    shape, n_layers, nb = W.THINKER, 4, 16
+    assert shape.n_q_heads // shape.n_kv_heads == 7
+    ctx_lens = np.random.default_rng(5001).integers(1024, 2048, size=nb, endpoint=True).astype(np.int32)
+    max_ctx = int(np.ceil((ctx_lens.max() + 1) / 64) * 64)
+    log(f"[thinker-decode] caches behind {ctx_lens.min()}-{ctx_lens.max()} rows")
+    pre = W.make_cache(shape, n_layers, ctx_lens, 5002)
+    xb = W.token_rows(5003, nb, shape.hidden)
+    outs = {}
+    for cap in (256, 192, 96, 64):
+        cache = DeviceCache(n_layers, nb, max_ctx, shape.n_kv_heads, shape.head_dim, fill=0.0)
+        for l in range(n_layers):
+            for b in range(nb):
+                cache.load_prefix(l, b, pre.k[l][b], pre.v[l][b])
+        x = to_device(xb)
+        y = torch.empty(x.shape, dtype=torch.float32, device="cuda")
+        ws = torch.empty(binding.hs_workspace_size(shape, nb, nb, max_ctx), dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+        log(f"[thinker-decode] cap {cap}")
+        binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, list(range(nb + 1)), ctx_lens, cache.as_arg(), cap,
+                                        None, ws)
+        torch.cuda.synchronize()
+        outs[cap] = (y.cpu().numpy(), cache.rows(3, nb - 1, int(ctx_lens[-1]), int(ctx_lens[-1]) + 1))
+        del cache
+    expect, kv_new = ref.decode_step(f64(xb), weights_f64(layers), shape, ctx_lens,
+                                     _LazyLayers(pre.k), _LazyLayers(pre.v))
+    e = err_ratio(outs[256][0], expect)
+    log(f"  max err / rms = {e:.3e}")
+    assert e <= TOL
+    assert err_ratio(h64(outs[256][1][0][0]), kv_new[3][0][nb - 1]) <= TOL
+    for cap in (192, 96, 64):
+        assert np.array_equal(outs[cap][0], outs[256][0]), f"cap {cap} differs from 256"
 
 
 def test_corun_changes_nothing(env, thinker):

@@ -263,15 +263,76 @@ def test_decode_rows_behind_long_prefixes(env):
         assert err_ratio(h64(vb), v_new[b:b + 1]) <= TOL
 
 
-def test_masks_hold_on_hardware(env):
+@pytest.fixture(scope="module")
+def hw_table(env):
+    """Measured topology: for every mask bit, the (XCD, shader engine, CU) that a
+    stream masked to that bit alone runs on (probe kernel, 64 work-groups)."""
+    import ctypes
     torch, ctx = env
     from paper_2608_01785_amd import binding
+    hip = ctypes.CDLL("libamdhip64.so.7")           # the runtime already loaded in this process
+    hip.hipExtStreamCreateWithCUMask.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32,
+                                                 ctypes.POINTER(ctypes.c_uint32)]
+    hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+    n = 64
+    out = torch.zeros(n * 4, dtype=torch.int32, device="cuda")
+    table = []
+    log("[topology] probing the 256 mask bits one at a time")
+    for i in range(256):
+        mask = (ctypes.c_uint32 * 8)()
+        mask[i // 32] = 1 << (i % 32)
+        s = ctypes.c_void_p()
+        assert hip.hipExtStreamCreateWithCUMask(ctypes.byref(s), 8, mask) == 0, i
+        try:
+            out.zero_()
+            torch.cuda.synchronize()
+            binding.hs_probe_hw_ids(ctx, s.value, n, out)
+            torch.cuda.synchronize()
+        finally:
+            hip.hipStreamDestroy(s)
+        ids = {(int(a), int(b_), int(c)) for a, b_, c, _ in out.view(n, 4).cpu().numpy()}
+        assert len(ids) == 1, (i, ids)                  # one bit, one CU
+        table.append(ids.pop())
+    return table
+
+
+def test_measured_topology_matches_the_default_xcd_mapping(hw_table):
+    """Every mask bit is a distinct CU; bit i sits on XCD i % 8 as the default
+    topology (and so the partition) assumes, and each XCD holds 32 bits."""
+    from paper_2608_01785_amd import binding
+    assert len(set(hw_table)) == 256
+    d = binding.hs_default_topology()
+    bad = [i for i in range(256) if hw_table[i][0] != d.xcc[i]]
+    assert not bad, f"bits on another XCD than the default topology says: {bad[:16]}"
+    per_xcd = np.bincount([t[0] for t in hw_table], minlength=8)
+    assert per_xcd.tolist() == [32] * 8
+    same = sum((hw_table[i][1], hw_table[i][2]) == (d.se[i], d.cu[i]) for i in range(256))
+    log(f"[topology] XCD of every bit as assumed; shader engine and CU as assumed for {same} of 256 bits")
+    # The partition from the measured table is balanced per XCD at every ladder budget.
+    t = binding.topology_from_lists([x for x, _, _ in hw_table], [s for _, s, _ in hw_table],
+                                    [c for _, _, c in hw_table], 8)
+    for c in (16, 64, 96, 128, 160, 192, 224):
+        sh, _ = binding.hs_cu_partition(t, c)
+        bits = [i for i in range(256) if (sh[i // 32] >> (i % 32)) & 1]
+        cnt = np.bincount([hw_table[i][0] for i in bits], minlength=8)
+        assert cnt.max() - cnt.min() <= 1 and cnt.sum() == c, (c, cnt)
+
+
+def test_masks_hold_on_hardware(env, hw_table):
+    """Waves of each ladder stream run only on the CUs its mask names (by the
+    measured table), the two sides are disjoint, and each side is balanced over
+    the eight XCDs."""
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    popc = lambda ws: sum(bin(w).count("1") for w in ws)
     for budget in (64, 128, 192):
         sh, dn = binding.hs_context_masks(ctx, budget)
-        popc = lambda ws: sum(bin(w).count("1") for w in ws)
         assert popc(sh) == budget and popc(dn) == 256 - budget
         seen = {}
-        for role in (binding.HS_ROLE_SHARED, binding.HS_ROLE_DOWN):
+        for role, words in ((binding.HS_ROLE_SHARED, sh), (binding.HS_ROLE_DOWN, dn)):
+            allowed = {hw_table[i] for i in range(256) if (words[i // 32] >> (i % 32)) & 1}
+            cnt = np.bincount([x for x, _, _ in allowed], minlength=8)
+            assert cnt.max() - cnt.min() <= 1, (budget, role, cnt)
             s = binding.hs_context_stream(ctx, budget, role)
             n = 4096
             out = torch.zeros(n * 4, dtype=torch.int32, device="cuda")
@@ -282,6 +343,7 @@ def test_masks_hold_on_hardware(env):
             ids = out.view(n, 4).cpu().numpy()
             seen[role] = {(int(a), int(b_), int(c)) for a, b_, c, _ in ids}
             log(f"  distinct CUs used: {len(seen[role])}")
+            assert seen[role] <= allowed, sorted(seen[role] - allowed)[:8]
         assert not (seen[0] & seen[1])
-        assert len(seen[0]) <= budget and len(seen[1]) <= 256 - budget
         assert len(seen[0]) >= 0.9 * budget  # 4096 blocks spread over (nearly) every CU of the mask
+
