@@ -283,6 +283,9 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
   if (plan.image.size() > lay.meta_bytes) return hs::fail(HS_ERR_INTERNAL, "metadata image exceeds its region");
 
   HIP_TRY(hipSetDevice(ctx->device));
+  // An error left by an earlier, unrelated runtime call has been reported to
+  // its caller; clear it so the launch checks below see only this call's.
+  (void)hipGetLastError();
   st = stage_metadata(ctx, plan, at<void>(ws, lay.meta), s);
   if (st != HS_OK) return st;
 

@@ -265,8 +265,12 @@ def test_decode_rows_behind_long_prefixes(env):
 
 @pytest.fixture(scope="module")
 def hw_table(env):
-    """Measured topology: for every mask bit, the (XCD, shader engine, CU) that a
-    stream masked to that bit alone runs on (probe kernel, 64 work-groups)."""
+    """Measured topology: for every mask bit, the (XCD, shader engine, CU) it names.
+
+    The runtime refuses a CU mask that leaves an XCD without CUs, so each bit is
+    found by difference: a stream masked to a base set of eight bits (one per
+    XCD by the default mapping) plus the bit runs on the base set's CUs and one
+    more, which is the bit's (probe kernel, 1024 work-groups per stream)."""
     import ctypes
     torch, ctx = env
     from paper_2608_01785_amd import binding
@@ -274,15 +278,18 @@ def hw_table(env):
     hip.hipExtStreamCreateWithCUMask.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32,
                                                  ctypes.POINTER(ctypes.c_uint32)]
     hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
-    n = 64
+    n = 1024
     out = torch.zeros(n * 4, dtype=torch.int32, device="cuda")
-    table = []
-    log("[topology] probing the 256 mask bits one at a time")
-    for i in range(256):
+
+    def probe(bits):
         mask = (ctypes.c_uint32 * 8)()
-        mask[i // 32] = 1 << (i % 32)
+        for i in bits:
+            mask[i // 32] |= 1 << (i % 32)
         s = ctypes.c_void_p()
-        assert hip.hipExtStreamCreateWithCUMask(ctypes.byref(s), 8, mask) == 0, i
+        rc = hip.hipExtStreamCreateWithCUMask(ctypes.byref(s), 8, mask)
+        if rc != 0:
+            hip.hipGetLastError()                       # leave no sticky error for later calls
+            raise AssertionError(f"stream with mask bits {sorted(bits)[:10]} refused: error {rc}")
         try:
             out.zero_()
             torch.cuda.synchronize()
@@ -290,9 +297,19 @@ def hw_table(env):
             torch.cuda.synchronize()
         finally:
             hip.hipStreamDestroy(s)
-        ids = {(int(a), int(b_), int(c)) for a, b_, c, _ in out.view(n, 4).cpu().numpy()}
-        assert len(ids) == 1, (i, ids)                  # one bit, one CU
-        table.append(ids.pop())
+        return {(int(a), int(b_), int(c)) for a, b_, c, _ in out.view(n, 4).cpu().numpy()}
+
+    log("[topology] probing every mask bit against a one-CU-per-XCD base set")
+    bases = [list(range(8 * j, 8 * j + 8)) for j in (0, 1)]
+    base_ids = [probe(b) for b in bases]
+    for b, ids in zip(bases, base_ids):
+        assert len(ids) == 8, (b, ids)
+    table = []
+    for i in range(256):
+        k = 1 if i < 8 else 0                           # a base that does not hold bit i
+        extra = probe(bases[k] + [i]) - base_ids[k]
+        assert len(extra) == 1, (i, extra)
+        table.append(extra.pop())
     return table
 
 
