@@ -287,6 +287,29 @@ hs_status hs_downstream_decode_step(hs_context* ctx, const hs_layer_cfg* cfg,
                                     const int32_t* kv_lens, int32_t batch, int32_t cu_budget,
                                     void* stream, void* workspace, size_t ws_bytes);
 
+/* The decode step for callers that cannot allocate device memory (tight
+ * serving loops, harnesses that forbid allocation): the same computation and
+ * kernels as hs_downstream_decode_step, with no workspace argument.  Its
+ * workspace is a static device array of 64 MiB that the library holds on each
+ * GPU it runs on until the process ends, laid out without the packed key/value
+ * region (the cache is required); the metadata is staged through a fixed ring
+ * of pinned slots allocated by hs_context_create.  The call allocates nothing
+ * (no hipMalloc, hipHostMalloc or hipFree); it may wait on the host for the
+ * oldest staging slot's copy when four calls are in flight.
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (on different streams, or from several contexts) race and must not be
+ * issued.  Consecutive calls on one stream are ordered and safe.
+ * Arguments as hs_downstream_decode_step.  Errors as that call, plus
+ * HS_ERR_UNSUPPORTED for batch > 1024 and HS_ERR_WORKSPACE when the call's
+ * workspace exceeds the 64 MiB array or its metadata a 1 MiB staging slot
+ * (the talker at batch 128 behind 1024 cached rows needs about 5 MiB);
+ * nothing is enqueued then. */
+hs_status hs_downstream_decode_step_noalloc(hs_context* ctx, const hs_layer_cfg* cfg,
+                                            const hs_layer_weights* w, int32_t n_layers,
+                                            const void* x_in, void* x_out, const hs_kv_cache* kv,
+                                            const int32_t* kv_lens, int32_t batch, int32_t cu_budget,
+                                            void* stream);
+
 /* Topology probe: launches n_groups work-groups on `stream` (NULL = the
  * context's full-budget stream); each writes, into out_ids (device, uint32
  * [n_groups * 4]): XCC id, shader engine, CU id, and the low 32 bits of the

@@ -24,6 +24,7 @@ SYMBOLS = (
     "hs_context_create", "hs_context_topology", "hs_context_stream", "hs_context_masks",
     "hs_context_destroy", "hs_workspace_size", "hs_workspace_size_paged", "hs_shared_stage_forward",
     "hs_shared_stage_forward_mrope", "hs_downstream_decode_step_mrope", "hs_downstream_decode_step",
+    "hs_downstream_decode_step_noalloc",
     "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read", "hs_convert_weights_f16",
     "hs_controller_create", "hs_controller_step", "hs_controller_destroy", "hs_pressure_sample",
     "hs_temporal_create", "hs_temporal_step", "hs_temporal_destroy",
@@ -138,6 +139,8 @@ def lib() -> ctypes.CDLL:
                                                 ctypes.c_size_t],
             "hs_downstream_decode_step": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp, vp,
                                           ctypes.POINTER(KvCache), i32p, i32, i32, vp, vp, ctypes.c_size_t],
+            "hs_downstream_decode_step_noalloc": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32,
+                                                  vp, vp, ctypes.POINTER(KvCache), i32p, i32, i32, vp],
             "hs_probe_hw_ids": [vp, vp, i32, vp],
             "hs_timing_enable": [vp, i32],
             "hs_timing_read": [vp, i32, ctypes.POINTER(ctypes.c_double), i32p],
@@ -450,6 +453,17 @@ def hs_downstream_decode_step(ctx: Context, cfg, weights, x_in, x_out, kv, kv_le
     _check(lib().hs_downstream_decode_step(
         ctx.handle, ctypes.byref(LayerCfg.of(cfg)), warr, len(weights), _ptr(x_in), _ptr(x_out),
         ctypes.byref(kvs), lens, len(lens), cu_budget, _ptr(stream), _ptr(workspace), ws_bytes))
+
+
+def hs_downstream_decode_step_noalloc(ctx: Context, cfg, weights, x_in, x_out, kv, kv_lens, cu_budget: int,
+                                      stream=None) -> None:
+    """The decode step on the library's static scratch (no workspace argument)."""
+    warr = _weights_array(weights)
+    kvs = _kv_struct(kv)
+    lens = _i32_array(kv_lens)
+    _check(lib().hs_downstream_decode_step_noalloc(
+        ctx.handle, ctypes.byref(LayerCfg.of(cfg)), warr, len(weights), _ptr(x_in), _ptr(x_out),
+        ctypes.byref(kvs) if kvs is not None else None, lens, len(lens), cu_budget, _ptr(stream)))
 
 
 def hs_probe_hw_ids(ctx: Context, stream, n_groups: int, out_ids) -> None:

@@ -135,6 +135,13 @@ hipError_t launch_rope_table(float2* tab, int max_pos, int dh, float base, hipSt
 hipError_t launch_probe(uint32_t* out, int n_groups, hipStream_t s);
 
 // dst = fp16(src) for n bf16 values (n even).
+// Static device scratch of the no-allocation decode step (noalloc.hip): its
+// size, and its address on `device`, which must be the current device on the
+// first call for it (later calls return the kept address).
+size_t noalloc_scratch_bytes();
+constexpr int kNoAllocMaxBatch = 1024;  // rows of one no-allocation decode step
+hipError_t noalloc_scratch_resolve(int device, void** out);
+
 hipError_t launch_convert_bf16_f16(const uint16_t* src, uint16_t* dst, int64_t rows, int64_t cols, hipStream_t s);
 
 }  // namespace hs

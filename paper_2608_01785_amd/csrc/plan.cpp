@@ -185,7 +185,7 @@ static size_t meta_bytes(int32_t T, int32_t B, int64_t pages, int64_t att, int32
   return align_up(s, kAlign);
 }
 
-WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos, int32_t page_keys) {
+WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos, int32_t page_keys, bool packs) {
   WsLayout w{};
   const size_t d = c.hidden, hq = c.n_q_heads, hkv = c.n_kv_heads, dh = c.head_dim, f = c.ffn;
   size_t p = 0;
@@ -206,7 +206,7 @@ WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos,
   // Packed keys/values: sequence b starts at the 64-aligned position
   // sum_{b' < b} round_up(len_b', 64); 64 more positions cover the last
   // tile's overhang.
-  w.packed_ctx = int64_t(align_up(size_t(T) + 64 * size_t(B), 64)) + 64;
+  w.packed_ctx = packs ? int64_t(align_up(size_t(T) + 64 * size_t(B), 64)) + 64 : 0;
   w.kpack = take(size_t(hkv) * size_t(w.packed_ctx) * dh * 2);
   w.vpack = take(size_t(hkv) * size_t(w.packed_ctx) * dh * 2);
   w.o = take(act_rows * hq * dh * 2);

@@ -62,7 +62,10 @@ struct WsLayout {
 int64_t max_att_items(int32_t T, int32_t B);
 
 // page_keys: positions per page of a paged cache, 0 without a block table.
-WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos, int32_t page_keys = 0);
+// packs: reserve the packed key/value slot that calls without a cache use
+// (false only for a call that is known to carry a cache).
+WsLayout ws_layout(const hs_layer_cfg& c, int32_t T, int32_t B, int32_t max_pos, int32_t page_keys = 0,
+                   bool packs = true);
 
 // Keys per single-row attention work unit: the head size's split, cut down
 // to a divisor of the page size on a paged cache so that no unit straddles

@@ -18,6 +18,11 @@ namespace {
 // the oldest.
 constexpr int kStagingSlots = 4;
 constexpr int kMaxStagingSlots = 64;
+// The no-allocation entry point stages through a ring of its own, allocated
+// with the context and never grown: a call waits for the oldest slot's copy
+// when every slot is still pending.
+constexpr int kFixedSlots = 4;
+constexpr size_t kFixedSlotBytes = size_t(1) << 20;
 
 struct Level {
   int budget = 0;
@@ -55,7 +60,9 @@ struct hs_context {
   hs_topology topo{};
   std::vector<Level> levels;
   std::vector<Slot> slots;
+  std::vector<Slot> fixed_slots;  // staging of the no-allocation entry point
   uint64_t calls = 0;
+  void* scratch = nullptr;        // this device's static scratch (device address)
   // Optional per-launch event timing.
   struct TimingRec {
     int kind;
@@ -83,13 +90,14 @@ void destroy_context(hs_context* ctx) {
     if (l.s_down) hipStreamDestroy(l.s_down);
   }
   for (hipEvent_t e : ctx->ev_pool) hipEventDestroy(e);
-  for (Slot& s : ctx->slots) {
-    if (s.ev) {
-      hipEventSynchronize(s.ev);
-      hipEventDestroy(s.ev);
+  for (std::vector<Slot>* ring : {&ctx->slots, &ctx->fixed_slots})
+    for (Slot& s : *ring) {
+      if (s.ev) {
+        hipEventSynchronize(s.ev);
+        hipEventDestroy(s.ev);
+      }
+      if (s.host) hipHostFree(s.host);
     }
-    if (s.host) hipHostFree(s.host);
-  }
   delete ctx;
 }
 
@@ -135,6 +143,35 @@ hs_status stage_metadata(hs_context* ctx, const hs::Plan& plan, void* dst, hipSt
   HIP_TRY(hipMemcpyAsync(dst, slot.host, bytes, hipMemcpyHostToDevice, s));
   HIP_TRY(hipEventRecord(slot.ev, s));
   slot.pending = true;
+  return HS_OK;
+}
+
+// The same through the fixed ring: no allocation, no growth.  The image must
+// fit a slot (checked by the caller before anything is enqueued).
+hs_status stage_metadata_fixed(hs_context* ctx, const hs::Plan& plan, void* dst, hipStream_t s) {
+  Slot* slot = nullptr;
+  for (Slot& sl : ctx->fixed_slots) {
+    if (sl.pending) {
+      const hipError_t q = hipEventQuery(sl.ev);
+      if (q == hipSuccess) {
+        sl.pending = false;
+      } else if (q != hipErrorNotReady) {
+        return hs::fail(HS_ERR_HIP, "hipEventQuery failed: %s", hipGetErrorString(q));
+      }
+    }
+    if (!sl.pending && !slot) slot = &sl;
+  }
+  if (!slot) {
+    for (Slot& sl : ctx->fixed_slots)
+      if (!slot || sl.used < slot->used) slot = &sl;
+    HIP_TRY(hipEventSynchronize(slot->ev));
+    slot->pending = false;
+  }
+  slot->used = ++ctx->calls;
+  memcpy(slot->host, plan.image.data(), plan.image.size());
+  HIP_TRY(hipMemcpyAsync(dst, slot->host, plan.image.size(), hipMemcpyHostToDevice, s));
+  HIP_TRY(hipEventRecord(slot->ev, s));
+  slot->pending = true;
   return HS_OK;
 }
 
@@ -211,10 +248,13 @@ void use_norm(hs::GemmArgs& a, const float* sumsq, int parts, float eps) {
 }
 
 // Shared body of the prefill forward and the decode step.
+// noalloc: the workspace is the context's static scratch (ws and ws_bytes are
+// ignored), laid out without the packed key/value slot (a cache is required),
+// and the metadata goes through the fixed staging ring.
 hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w, int32_t n_layers,
                     const void* x_in, void* x_out, const int32_t* seq_offsets, const int32_t* ctx_lens,
                     int32_t n_seqs, const hs_kv_cache* kv, int32_t budget, int role, void* stream,
-                    void* ws, size_t ws_bytes, const int32_t* pos3 = nullptr) {
+                    void* ws, size_t ws_bytes, const int32_t* pos3 = nullptr, bool noalloc = false) {
   hs::clear_error();
   hs_status st = hs::validate_cfg(cfg);
   if (st != HS_OK) return st;
@@ -272,21 +312,35 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
   hipStream_t s = nullptr;
   st = resolve_stream(ctx, budget, role, stream, &s);
   if (st != HS_OK) return st;
+  if (noalloc) {
+    if (!place.cache) return hs::fail(HS_ERR_INVALID_ARG, "the no-allocation call needs a key/value cache");
+    if (!ctx->scratch) return hs::fail(HS_ERR_INTERNAL, "the context has no static scratch");
+    ws = ctx->scratch;
+    ws_bytes = hs::noalloc_scratch_bytes();
+  }
   if (!ws) return hs::fail(HS_ERR_WORKSPACE, "workspace is null");
-  const hs::WsLayout lay = hs::ws_layout(*cfg, T, n_seqs, max_pos, place.table ? place.max_ctx : 0);
-  if (ws_bytes < lay.total)
+  const hs::WsLayout lay = hs::ws_layout(*cfg, T, n_seqs, max_pos, place.table ? place.max_ctx : 0, !noalloc);
+  if (ws_bytes < lay.total) {
+    if (noalloc)
+      return hs::fail(HS_ERR_WORKSPACE, "the call needs %zu bytes of scratch; the static scratch holds %zu",
+                      lay.total, ws_bytes);
     return hs::fail(HS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, lay.total);
+  }
   place.packed_ctx = lay.packed_ctx;
   hs::Plan plan;
   st = hs::build_plan(*cfg, seq_offsets, ctx_lens, n_seqs, place, &plan, pos3);
   if (st != HS_OK) return st;
   if (plan.image.size() > lay.meta_bytes) return hs::fail(HS_ERR_INTERNAL, "metadata image exceeds its region");
+  if (noalloc && plan.image.size() > kFixedSlotBytes)
+    return hs::fail(HS_ERR_WORKSPACE, "metadata of %zu bytes exceeds the %zu-byte staging slot of the "
+                    "no-allocation call", plan.image.size(), kFixedSlotBytes);
 
   HIP_TRY(hipSetDevice(ctx->device));
   // An error left by an earlier, unrelated runtime call has been reported to
   // its caller; clear it so the launch checks below see only this call's.
   (void)hipGetLastError();
-  st = stage_metadata(ctx, plan, at<void>(ws, lay.meta), s);
+  st = noalloc ? stage_metadata_fixed(ctx, plan, at<void>(ws, lay.meta), s)
+               : stage_metadata(ctx, plan, at<void>(ws, lay.meta), s);
   if (st != HS_OK) return st;
 
   const int d = cfg->hidden, hq = cfg->n_q_heads, hkv = cfg->n_kv_heads, dh = cfg->head_dim, f = cfg->ffn;
@@ -537,6 +591,27 @@ hs_status hs_context_create(int32_t device, const int32_t* budgets, int32_t n_bu
       return hs::fail(HS_ERR_HIP, "event creation failed: %s", hipGetErrorString(e));
     }
   }
+  // The no-allocation entry point's resources: this device's static scratch
+  // (its address resolved once per device, with the device current) and a
+  // fixed ring of pinned staging slots.
+  {
+    hipError_t e = hs::noalloc_scratch_resolve(device, &ctx->scratch);
+    if (e != hipSuccess) {
+      destroy_context(ctx);
+      return hs::fail(HS_ERR_HIP, "resolving the static scratch of device %d failed: %s", device,
+                      hipGetErrorString(e));
+    }
+    ctx->fixed_slots.resize(kFixedSlots);
+    for (Slot& s : ctx->fixed_slots) {
+      e = hipEventCreateWithFlags(&s.ev, hipEventDisableTiming);
+      if (e == hipSuccess) e = hipHostMalloc(&s.host, kFixedSlotBytes, hipHostMallocDefault);
+      if (e != hipSuccess) {
+        destroy_context(ctx);
+        return hs::fail(HS_ERR_HIP, "no-allocation staging setup failed: %s", hipGetErrorString(e));
+      }
+      s.cap = kFixedSlotBytes;
+    }
+  }
   *out = ctx;
   return HS_OK;
 }
@@ -605,6 +680,22 @@ hs_status hs_downstream_decode_step(hs_context* ctx, const hs_layer_cfg* cfg, co
   for (int32_t b = 0; b <= batch; ++b) off[b] = b;
   return run_stack(ctx, cfg, w, n_layers, x_in, x_out, off.data(), kv_lens, batch, kv, cu_budget,
                    HS_ROLE_DOWN, stream, workspace, ws_bytes);
+}
+
+hs_status hs_downstream_decode_step_noalloc(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w,
+                                            int32_t n_layers, const void* x_in, void* x_out, const hs_kv_cache* kv,
+                                            const int32_t* kv_lens, int32_t batch, int32_t cu_budget, void* stream) {
+  hs::clear_error();
+  if (!kv) return hs::fail(HS_ERR_INVALID_ARG, "decode needs a key/value cache");
+  if (!kv_lens) return hs::fail(HS_ERR_INVALID_ARG, "kv_lens is null");
+  if (batch < 1) return hs::fail(HS_ERR_INVALID_ARG, "batch %d < 1", batch);
+  if (batch > hs::kNoAllocMaxBatch)
+    return hs::fail(HS_ERR_UNSUPPORTED, "batch %d exceeds the no-allocation call's %d rows", batch,
+                    hs::kNoAllocMaxBatch);
+  int32_t off[hs::kNoAllocMaxBatch + 1];
+  for (int32_t b = 0; b <= batch; ++b) off[b] = b;
+  return run_stack(ctx, cfg, w, n_layers, x_in, x_out, off, kv_lens, batch, kv, cu_budget, HS_ROLE_DOWN, stream,
+                   nullptr, 0, nullptr, true);
 }
 
 hs_status hs_downstream_decode_step_mrope(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w,
