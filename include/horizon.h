@@ -408,7 +408,11 @@ hs_status hs_controller_destroy(hs_controller* ctrl);
  * Errors: HS_ERR_INVALID_ARG for a null pointer or a device outside HIP's
  * device count; HS_ERR_HIP if the PCI address cannot be read;
  * HS_ERR_UNSUPPORTED when AMD SMI, a GPU at that address, or the reading is
- * unavailable.  One reading takes on the order of 100 us (a driver query). */
+ * unavailable.  One reading takes on the order of 100 us (a driver query).
+ * The value is the firmware's average over its last interval, which MI355X
+ * refreshes about once per second: under a copy load at 5.0 TB/s it reads
+ * 0.61, close to the share of the 8 TB/s peak, and readings taken within one
+ * interval repeat. */
 hs_status hs_pressure_sample(int32_t device, double* activity);
 
 /* ------------------------------------------------------------------------
