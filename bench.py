@@ -28,6 +28,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16 = 2.5e15       # MI355X dense bf16/fp16 MFMA, FLOP/s, 256 CUs
 PEAK_HBM = 8.0e12        # bytes/s
 N_CUS = 256
+SPEC_MHZ = 2400.0        # clock of the published peak
 
 
 # HBM-side bytes per gate/up launch at 256 CUs from rocprofv3 FETCH_SIZE and
@@ -145,32 +146,56 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / k
 
+    def instrumented(budget, k):
+        """Per-kernel event times and sustained clocks over k more steps (outside the timed loops)."""
+        binding.hs_timing_enable(ctx, True)
+        run(budget, k)
+        kern = {n: binding.hs_timing_read(ctx, n) for n in binding.KERNEL_KINDS}
+        clk = {n: binding.hs_timing_read_clock(ctx, n)[0] for n in binding.KERNEL_KINDS}
+        binding.hs_timing_enable(ctx, False)
+        return ({n: (v[0] / v[1] if v[1] else 0.0) for n, v in kern.items()},
+                {n: round(v, 1) for n, v in clk.items() if v > 0})
+
     for _ in range(args.warmup):
         run(256, 1)
-    binding.hs_timing_enable(ctx, True)
+    # The headline loop runs without per-kernel events; a separate pass
+    # records them.
     ms = run(256, args.steps)
-    kern = {k: binding.hs_timing_read(ctx, k) for k in binding.KERNEL_KINDS}
-    binding.hs_timing_enable(ctx, False)
+    kernel_ms, clock_mhz = instrumented(256, max(2, args.steps // 2))
     tok_s = T / (ms / 1e3)
     log(f"[bench] thinker stack @256 CUs: {ms:.3f} ms/step, {tok_s:,.0f} tok/s, "
         f"{flops_step / (ms / 1e3) / 1e12:.1f} TFLOP/s")
-    kernel_ms = {k: (v[0] / v[1] if v[1] else 0.0) for k, v in kern.items()}
-    for k, v in kern.items():
-        if v[1]:
-            log(f"    {k:12s} {v[0] / v[1]:8.3f} ms avg over {v[1]} launches")
+    for k, v in kernel_ms.items():
+        if v:
+            log(f"    {k:12s} {v:8.3f} ms avg" + (f", clock {clock_mhz[k]:.0f} MHz" if k in clock_mhz else ""))
 
     # Dominant kernel: the gate/up projection (SwiGLU epilogue), ~58 % of the FLOPs.
     gu_flops = 2.0 * T * shape.hidden * 2 * shape.ffn
     gu_ms = kernel_ms["gate_up"]
     gu_bytes = 2 * (T * shape.hidden + 2 * shape.ffn * shape.hidden + T * shape.ffn)  # A, W, a (fp16)
     achieved = gu_flops / (gu_ms / 1e3) / 1e12
+    gu_mhz = clock_mhz.get("gate_up")
     roofline = {"bound": "mfma", "kernel": "gate_up_swiglu_gemm", "achieved": round(achieved, 1),
                 "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s", "frac": round(achieved / (PEAK_BF16 / 1e12), 4),
-                "traffic": gemm_traffic_bytes(), "algorithmic_bytes": gu_bytes, "avg_launch_ms": round(gu_ms, 4)}
+                "traffic": gemm_traffic_bytes(), "algorithmic_bytes": gu_bytes, "avg_launch_ms": round(gu_ms, 4),
+                # The same against the peak at the launch's measured sustained clock.
+                "clock_mhz": gu_mhz,
+                "frac_at_measured_clock": round(achieved / (PEAK_BF16 / 1e12 * gu_mhz / SPEC_MHZ), 4) if gu_mhz else None}
 
     run(256, 1, wbf16)
     ms_bf16w = run(256, max(2, args.steps // 2), wbf16)
     log(f"[bench] thinker stack @256 CUs with bf16 weights converted in the GEMM: {ms_bf16w:.3f} ms/step")
+
+    def budget_entry(b, mb, kms, clk):
+        """Stack rate at budget b, with the GEMMs' average clock (launch-time weighted) and the
+        fraction of the CU-scaled peak at that clock."""
+        gem = [k for k in ("qkv", "o_proj", "gate_up", "down") if k in clk and kms.get(k)]
+        mhz = sum(clk[k] * kms[k] for k in gem) / sum(kms[k] for k in gem) if gem else None
+        frac = flops_step / (mb / 1e3) / (PEAK_BF16 * b / N_CUS)
+        return {"ms_per_step": round(mb, 3), "tok_s": round(T / (mb / 1e3)), "mfma_frac_cu_scaled": round(frac, 4),
+                "gemm_clock_mhz": round(mhz, 1) if mhz else None,
+                "mfma_frac_cu_scaled_at_measured_clock": round(frac * SPEC_MHZ / mhz, 4) if mhz else None,
+                "kernel_ms": {k: round(v, 4) for k, v in kms.items() if v}}
 
     per_budget = {}
     for b in budgets:
@@ -178,11 +203,11 @@ def main():
             continue
         run(b, 1)
         mb = run(b, max(2, args.steps // 2))
-        per_budget[str(b)] = {"ms_per_step": round(mb, 3), "tok_s": round(T / (mb / 1e3)),
-                              "mfma_frac_cu_scaled": round(flops_step / (mb / 1e3) / (PEAK_BF16 * b / N_CUS), 4)}
-        log(f"[bench] thinker stack @{b} CUs: {mb:.3f} ms/step, {T / (mb / 1e3):,.0f} tok/s")
-    per_budget["256"] = {"ms_per_step": round(ms, 3), "tok_s": round(tok_s),
-                         "mfma_frac_cu_scaled": round(flops_step / (ms / 1e3) / PEAK_BF16, 4)}
+        kms, clk = instrumented(b, 1)
+        per_budget[str(b)] = budget_entry(b, mb, kms, clk)
+        log(f"[bench] thinker stack @{b} CUs: {mb:.3f} ms/step, {T / (mb / 1e3):,.0f} tok/s, "
+            f"GEMM clock {per_budget[str(b)]['gemm_clock_mhz']} MHz")
+    per_budget["256"] = budget_entry(256, ms, kernel_ms, clock_mhz)
 
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4
@@ -257,6 +282,7 @@ def main():
         "mfma_frac": round(flops_step / (ms / 1e3) / PEAK_BF16, 4),
         "roofline": roofline,
         "kernel_ms": {k: round(v, 4) for k, v in kernel_ms.items() if v},
+        "kernel_clock_mhz": clock_mhz,
         "ms_per_step_bf16_weights": round(ms_bf16w, 4),
         "budgets": per_budget,
         "corun": corun,
@@ -926,9 +952,53 @@ def cpu_baseline(W, layers, batch, shape, rows_per_seq, target_s=15.0):
         r = max(32, min(r, int(batch.lengths.min())))
     dt, rows = sample(r, len(layers))
     log(f"[bench] CPU reference: {rows} rows x {len(layers)} layers in {dt:.1f}s ({cores} threads)")
-    return {"value": round(rows / dt, 2), "unit": "tok/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"first {r} rows of each of the {batch.n_seqs} requests through all {len(layers)} layers "
-                      f"({rows} rows), float64 NumPy", "seconds": round(dt, 2)}
+    out = {"value": round(rows / dt, 2), "unit": "tok/s", "cores": int(cores), "kind": "oracle",
+           "sample": f"first {r} rows of each of the {batch.n_seqs} requests through all {len(layers)} layers "
+                     f"({rows} rows), float64 NumPy", "seconds": round(dt, 2)}
+    out.update(host_info())
+    out["talker_step"] = cpu_talker_step(W, ref)
+    return out
+
+
+def host_info():
+    """CPU model and the BLAS library NumPy runs on (as threadpoolctl reports it)."""
+    info = {"cpu_model": None, "blas": None}
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    info["cpu_model"] = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        libs = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if libs:
+            i = libs[0]
+            info["blas"] = f"{i.get('internal_api')} {i.get('version')} ({i.get('threading_layer')}, " \
+                           f"{i.get('num_threads')} threads)"
+    except Exception:
+        pass
+    return info
+
+
+def cpu_talker_step(W, ref, n_layers=4):
+    """The float64 reference of one talker decode step (batch 32, kv_len U[128, 1024]): the first
+    n_layers of the 16 (the seeded weights and cache of those layers), scaled to the whole step."""
+    ts, seeds = W.TALKER, W.SEEDS["talker"]
+    db = W.talker_batch(ts, n_layers, 32, seeds)
+    layers = W.make_weights(ts, n_layers, seeds["weights"])
+    w64 = [{k: W.bf16_to_f32(v).astype(np.float64) for k, v in lw.items()} for lw in layers]
+    ck = [[W.f16_to_f32(a).astype(np.float64) for a in per] for per in db.cache.k]
+    cv = [[W.f16_to_f32(a).astype(np.float64) for a in per] for per in db.cache.v]
+    x = W.bf16_to_f32(db.x).astype(np.float64)
+    t0 = time.time()
+    ref.decode_step(x, w64, ts, db.kv_lens, ck, cv)
+    dt = (time.time() - t0) * 16 / n_layers
+    log(f"[bench] CPU reference talker step: {dt * 1e3:.0f} ms per 16-layer step ({n_layers} layers timed)")
+    return {"ms_per_step": round(dt * 1e3, 1), "tok_s": round(32 / dt, 2),
+            "sample": f"layers 0-{n_layers - 1} of the 16-layer batch-32 step, scaled by 16/{n_layers}"}
 
 
 if __name__ == "__main__":

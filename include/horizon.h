@@ -348,6 +348,17 @@ enum {
 hs_status hs_timing_enable(hs_context* ctx, int32_t enable);
 hs_status hs_timing_read(hs_context* ctx, int32_t kernel_kind, double* total_ms, int32_t* n_launches);
 
+/* Sustained shader clock of the recorded launches of one kernel kind (the
+ * large GEMMs and multi-row attention; other kinds report 0 launches).
+ * While timing is enabled, the first lane of block 0 of each such launch
+ * reads the shader-clock counter (one count per core clock cycle) and the
+ * constant-rate counter at entry and exit; *mhz receives the ratio of the
+ * summed cycle counts to the summed constant-rate ticks, scaled by the
+ * device's constant clock rate.  The persistent GEMM's block 0 lives for the
+ * whole launch, so for it this is the launch's average clock.  Waits for the
+ * recorded launches; 0 MHz and 0 launches when none was recorded. */
+hs_status hs_timing_read_clock(hs_context* ctx, int32_t kernel_kind, double* mhz, int32_t* n_launches);
+
 /* ------------------------------------------------------------------------
  * Spatial controller: the bandwidth-guided shared-stage cap of §4.4
  * ("Bandwidth-pressure signal", "SM ladder", Eq. (1)) applied as in step 3 of

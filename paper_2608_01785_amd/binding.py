@@ -25,7 +25,7 @@ SYMBOLS = (
     "hs_context_destroy", "hs_workspace_size", "hs_workspace_size_paged", "hs_shared_stage_forward",
     "hs_shared_stage_forward_mrope", "hs_downstream_decode_step_mrope", "hs_downstream_decode_step",
     "hs_downstream_decode_step_noalloc",
-    "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read", "hs_convert_weights_f16",
+    "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read", "hs_timing_read_clock", "hs_convert_weights_f16",
     "hs_controller_create", "hs_controller_step", "hs_controller_destroy", "hs_pressure_sample",
     "hs_temporal_create", "hs_temporal_step", "hs_temporal_destroy",
 )
@@ -144,6 +144,7 @@ def lib() -> ctypes.CDLL:
             "hs_probe_hw_ids": [vp, vp, i32, vp],
             "hs_timing_enable": [vp, i32],
             "hs_timing_read": [vp, i32, ctypes.POINTER(ctypes.c_double), i32p],
+            "hs_timing_read_clock": [vp, i32, ctypes.POINTER(ctypes.c_double), i32p],
             "hs_convert_weights_f16": [vp, vp, vp, ctypes.c_int64, ctypes.c_int64, vp],
             "hs_controller_create": [ctypes.POINTER(ControllerCfg), ctypes.POINTER(vp)],
             "hs_controller_step": [vp, i32, ctypes.c_double, ctypes.POINTER(Split)],
@@ -472,6 +473,15 @@ def hs_probe_hw_ids(ctx: Context, stream, n_groups: int, out_ids) -> None:
 
 def hs_timing_enable(ctx: Context, enable: bool = True) -> None:
     _check(lib().hs_timing_enable(ctx.handle, 1 if enable else 0))
+
+
+def hs_timing_read_clock(ctx: Context, kind) -> Tuple[float, int]:
+    """(average shader clock in MHz, launches with clock records) of one kernel kind."""
+    k = KERNEL_KINDS[kind] if isinstance(kind, str) else int(kind)
+    mhz = ctypes.c_double(0)
+    n = ctypes.c_int32(0)
+    _check(lib().hs_timing_read_clock(ctx.handle, k, ctypes.byref(mhz), ctypes.byref(n)))
+    return float(mhz.value), int(n.value)
 
 
 def hs_timing_read(ctx: Context, kind) -> Tuple[float, int]:

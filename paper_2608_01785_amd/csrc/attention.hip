@@ -53,6 +53,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 31, fh = lane >> 5;
+  LaunchClock clk;
+  clk.begin(a.clock);
 
   // Units L = item * hq + head are ordered longest key range first, and the
   // Gq = hq / hkv consecutive units of a group share one key/value head.
@@ -252,6 +254,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
         store_h4(a.o + act_index(row0 + qw, head * DH + 32 * i + 8 * gq + 4 * fh, a.hq * DH, a.o_k8_rows),
                  o[i][4 * gq] * inv, o[i][4 * gq + 1] * inv, o[i][4 * gq + 2] * inv, o[i][4 * gq + 3] * inv);
   }
+  clk.end(a.clock);
 }
 
 // ----------------------------------------------------------------------------

@@ -88,6 +88,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  LaunchClock clk;
+  clk.begin(a.clock);
   const int wn = wave & 1;   // weight-row half of the tile (128 rows)
   const int wm = wave >> 1;  // activation-row quarter (64 rows; 32 in a half unit)
   const int fr = lane & 31;
@@ -393,6 +395,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     L = L_next;
     unit_coords(L, tile_m, tile_n, hm);
   }
+  clk.end(a.clock);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 

@@ -182,6 +182,30 @@ __device__ __forceinline__ void h2x_to_f(uint32_t u, float& lo, float& hi) {
   hi = h2f(uint16_t(u >> 16));
 }
 
+// Launch clock record (timing mode only): the first lane of block 0 reads the
+// shader-clock counter (s_memtime, counts core clock cycles) and the
+// constant-rate counter (s_memrealtime) at entry and exit and stores the four
+// values with one vector store, so the host can derive the sustained clock.
+struct LaunchClock {
+  uint64_t c0 = 0, w0 = 0;
+  __device__ __forceinline__ void begin(const uint64_t* out) {
+    if (out && blockIdx.x == 0 && threadIdx.x == 0) {
+      c0 = __builtin_amdgcn_s_memtime();
+      w0 = __builtin_amdgcn_s_memrealtime();
+    }
+  }
+  __device__ __forceinline__ void end(uint64_t* out) const {
+    if (out && blockIdx.x == 0 && threadIdx.x == 0) {
+      const uint64_t c1 = __builtin_amdgcn_s_memtime();
+      const uint64_t w1 = __builtin_amdgcn_s_memrealtime();
+      out[0] = c0;
+      out[1] = w0;
+      out[2] = c1;
+      out[3] = w1;
+    }
+  }
+};
+
 // Work-groups of a launch are handed to the 8 XCDs round-robin (block b runs
 // on XCD b % 8).  Remap so that each XCD processes a contiguous range of
 // logical work items, which then share operands in that XCD's L2.

@@ -61,6 +61,8 @@ struct GemmArgs {
   // Skinny GEMM only: A, out and scaled_out are k-group-major with this many
   // padded rows (skinny_k8_rows(M)); 0 = row-major.
   int k8_rows;
+  // Timing mode: four counters of the launch (see LaunchClock), or null.
+  uint64_t* clock;
 };
 
 // The large GEMM does not take the folded-RMSNorm fields (they must be null).
@@ -88,6 +90,7 @@ struct AttnArgs {
   int64_t kv_head_stride;
   int hq, hkv, dh;
   float scale_log2;         // log2(e) / sqrt(dh)
+  uint64_t* clock;          // timing mode: four counters of the launch (see LaunchClock), or null
 };
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);

@@ -69,6 +69,7 @@ struct hs_context {
     hipEvent_t a, b;
   };
   bool timing = false;
+  uint64_t* clock_buf = nullptr;  // device, four launch counters per record (see LaunchClock)
   std::vector<hipEvent_t> ev_pool;
   size_t ev_next = 0;
   std::vector<TimingRec> recs;
@@ -90,6 +91,7 @@ void destroy_context(hs_context* ctx) {
     if (l.s_down) hipStreamDestroy(l.s_down);
   }
   for (hipEvent_t e : ctx->ev_pool) hipEventDestroy(e);
+  if (ctx->clock_buf) hipFree(ctx->clock_buf);
   for (std::vector<Slot>* ring : {&ctx->slots, &ctx->fixed_slots})
     for (Slot& s : *ring) {
       if (s.ev) {
@@ -216,6 +218,13 @@ void timing_end(hs_context* ctx, hipStream_t s, int kind, hipEvent_t a, hipEvent
   if (!a) return;
   hipEventRecord(b, s);
   ctx->recs.push_back({kind, a, b});
+}
+
+// Clock counters of the launch the next TIMED record brackets (record i
+// owns counters 4i .. 4i + 3), or null when it will not be recorded.
+uint64_t* clock_slot(const hs_context* ctx) {
+  if (!ctx->timing || !ctx->clock_buf || ctx->ev_next + 2 > ctx->ev_pool.size()) return nullptr;
+  return ctx->clock_buf + 4 * (ctx->ev_next / 2);
 }
 
 #define TIMED(kind, expr)                              \
@@ -414,6 +423,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     g.dh = dh;
     g.k8_rows = k8;
     if (folded) use_norm(g, sumsq, norm_parts, cfg->rms_eps);
+    g.clock = clock_slot(ctx);
     TIMED(HS_KERNEL_QKV, gemm(hs::EPI_QKV, g, grid_cap, s));
 
     hs::AttnArgs at_args{};
@@ -435,6 +445,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     at_args.hkv = hkv;
     at_args.dh = dh;
     at_args.scale_log2 = scale_log2;
+    at_args.clock = clock_slot(ctx);
     if (plan.n_att_items > 0) TIMED(HS_KERNEL_ATTENTION, hs::launch_attention(at_args, s));
 
     hs::DecodeAttnArgs da{};
@@ -476,6 +487,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     const bool fold = hs::skinny_supported(hs::EPI_QKV, g) && hs::skinny_supported(hs::EPI_RESID, go) &&
                       norm_parts <= hs::kSkinnyMaxNormParts;
     if (fold) fold_norm(go, sumsq, n_buf, w[l].ln2);
+    go.clock = clock_slot(ctx);
     TIMED(HS_KERNEL_O_PROJ, gemm(hs::EPI_RESID, go, grid_cap, s));
     if (!fold)
       TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(nullptr, h_buf, static_cast<const uint16_t*>(w[l].ln2), n_buf, T,
@@ -495,6 +507,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     gu.ffn = f;
     gu.k8_rows = k8;
     if (fold) use_norm(gu, sumsq, norm_parts, cfg->rms_eps);
+    gu.clock = clock_slot(ctx);
     TIMED(HS_KERNEL_GATE_UP, gemm(hs::EPI_SWIGLU, gu, grid_cap, s));
 
     hs::GemmArgs gd{};
@@ -512,6 +525,7 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
     gd.k8_rows = k8;
     folded = fold && l + 1 < n_layers;
     if (folded) fold_norm(gd, sumsq, n_buf, w[l + 1].ln1);
+    gd.clock = clock_slot(ctx);
     TIMED(HS_KERNEL_DOWN, gemm(hs::EPI_RESID, gd, grid_cap, s));
     x_cur = nullptr;
     x_cur_f32 = x_next;
@@ -744,11 +758,40 @@ hs_status hs_timing_enable(hs_context* ctx, int32_t enable) {
       ctx->ev_pool.push_back(e);
     }
   }
+  if (enable && !ctx->clock_buf) HIP_TRY(hipMalloc(&ctx->clock_buf, kTimingPairs * 4 * sizeof(uint64_t)));
   // Finish outstanding records before their events can be recorded again.
   for (const auto& r : ctx->recs) HIP_TRY(hipEventSynchronize(r.b));
   ctx->recs.clear();
   ctx->ev_next = 0;
+  if (enable) HIP_TRY(hipMemset(ctx->clock_buf, 0, kTimingPairs * 4 * sizeof(uint64_t)));
   ctx->timing = enable != 0;
+  return HS_OK;
+}
+
+hs_status hs_timing_read_clock(hs_context* ctx, int32_t kind, double* mhz, int32_t* n_launches) {
+  hs::clear_error();
+  if (!ctx || !mhz || !n_launches) return hs::fail(HS_ERR_INVALID_ARG, "null argument");
+  if (kind < 0 || kind >= HS_KERNEL_KINDS) return hs::fail(HS_ERR_INVALID_ARG, "kernel kind %d", kind);
+  *mhz = 0.0;
+  *n_launches = 0;
+  if (!ctx->clock_buf || ctx->recs.empty()) return HS_OK;
+  HIP_TRY(hipSetDevice(ctx->device));
+  for (const auto& r : ctx->recs) HIP_TRY(hipEventSynchronize(r.b));
+  std::vector<uint64_t> c(4 * ctx->recs.size());
+  HIP_TRY(hipMemcpy(c.data(), ctx->clock_buf, c.size() * sizeof(uint64_t), hipMemcpyDeviceToHost));
+  int wall_khz = 0;
+  HIP_TRY(hipDeviceGetAttribute(&wall_khz, hipDeviceAttributeWallClockRate, ctx->device));
+  double cycles = 0.0, ticks = 0.0;
+  int32_t n = 0;
+  for (size_t i = 0; i < ctx->recs.size(); ++i) {
+    const uint64_t* v = &c[4 * i];
+    if (ctx->recs[i].kind != kind || v[3] <= v[1] || v[2] <= v[0]) continue;
+    cycles += double(v[2] - v[0]);
+    ticks += double(v[3] - v[1]);
+    ++n;
+  }
+  if (n && ticks > 0.0) *mhz = cycles / ticks * (double(wall_khz) / 1e3);
+  *n_launches = n;
   return HS_OK;
 }
 
