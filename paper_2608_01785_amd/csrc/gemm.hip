@@ -206,12 +206,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
 
   f32x16 acc[4][2];
   while (true) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    // Output rows of this lane: m0 + 32 j for j < nj.
+    const int nj = hm < 0 ? 2 : 1;
+    const int m0 = tile_m * BM + (hm < 0 ? wm * 64 : hm * 128 + wm * 32) + fr;
     const int L_next = L + G;
 
     auto mfma_half = [&](auto jt, const Frag& h) {
@@ -224,12 +221,58 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
       }
     };
 
+    // Accumulator start values for a unit with JT activation subtiles per
+    // wave (the rows a half unit does not own stay constant zeros).
+    auto init_acc = [&](auto jt) {
+      constexpr int JT = decltype(jt)::value;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+      if constexpr (EPI == EPI_RESID) {
+        // The accumulators start from the residual, so the epilogue is plain
+        // stores: these loads overlap the previous unit's stores and this
+        // unit's first stages instead of stalling a separate epilogue pass.
+        // Rows past M (never stored) read the last valid row instead.
+        const int n_base = tile_n * BN + wn * 128 + 4 * fh;
+        int64_t roff[JT];
+#pragma unroll
+        for (int j = 0; j < JT; ++j) roff[j] = int64_t(min(m0 + j * 32, a.M - 1)) * a.ldo + n_base;
+        if (a.resid_f32) {
+#pragma unroll
+          for (int j = 0; j < JT; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+              for (int g4 = 0; g4 < 4; ++g4) {
+                const f32x4 v = *reinterpret_cast<const f32x4*>(a.resid_f32 + roff[j] + i * 32 + 8 * g4);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc[i][j][4 * g4 + e] = v[e];
+              }
+        } else {
+#pragma unroll
+          for (int j = 0; j < JT; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+              for (int g4 = 0; g4 < 4; ++g4) {
+                float r[4];
+                load_bf16x4(a.resid + roff[j] + i * 32 + 8 * g4, r);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc[i][j][4 * g4 + e] = r[e];
+              }
+        }
+      }
+    };
     // Stage s of the unit: buffer s % 2, register slot s % 4 (K % 128 == 0).
     auto k_loop = [&](auto jt) {
       constexpr int JT = decltype(jt)::value;
       constexpr int NM = 4 * JT;      // MFMAs per half stage
       constexpr int NR = 4 + JT;      // fragment reads per half stage
       Frag h0, h1;
+      init_acc(jt);
       read_frag(jt, 0, 0, h0);
       for (int kt = 0; kt < KT; kt += kUnroll) {
         const bool last = kt + kUnroll == KT;
@@ -295,14 +338,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
       k_loop(std::integral_constant<int, 1>{});
 
     // ---------------------------------------------------------------- epilogue
-    const int nj = hm < 0 ? 2 : 1;
-    const int m0 = tile_m * BM + (hm < 0 ? wm * 64 : hm * 128 + wm * 32) + fr;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int m = m0 + j * 32;
       if (j >= nj || m >= a.M) continue;
       if constexpr (EPI == EPI_RESID) {
-        // out (fp32) = resid (bf16 or fp32) + acc: the residual stream stays in fp32.
+        // out (fp32) = resid + products, the accumulators having started from
+        // the residual: the residual stream stays in fp32.
         const int n_base = tile_n * BN + wn * 128 + 4 * fh;
         float* orow = a.out_f32 + int64_t(m) * a.ldo;
 #pragma unroll
@@ -310,18 +352,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const int n = n_base + i * 32 + 8 * g;
-            f32x4 v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-            if (a.resid_f32) {
-              const f32x4 r = *reinterpret_cast<const f32x4*>(a.resid_f32 + int64_t(m) * a.ldo + n);
-              v += r;
-            } else {
-              float r[4];
-              load_bf16x4(a.resid + int64_t(m) * a.ldo + n, r);
-              v[0] += r[0];
-              v[1] += r[1];
-              v[2] += r[2];
-              v[3] += r[3];
-            }
+            const f32x4 v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
             *reinterpret_cast<f32x4*>(orow + n) = v;
           }
       } else if constexpr (EPI == EPI_SWIGLU) {
