@@ -146,6 +146,7 @@ typedef struct hs_topology {
 } hs_topology;
 
 typedef struct hs_context hs_context;
+typedef struct hs_decode_graph hs_decode_graph;
 
 enum { HS_ROLE_SHARED = 0, HS_ROLE_DOWN = 1 };
 
@@ -309,6 +310,51 @@ hs_status hs_downstream_decode_step_noalloc(hs_context* ctx, const hs_layer_cfg*
                                             const void* x_in, void* x_out, const hs_kv_cache* kv,
                                             const int32_t* kv_lens, int32_t batch, int32_t cu_budget,
                                             void* stream);
+
+/* The downstream decode step captured once and replayed per step (§2.1:
+ * decode re-runs the same layers for every new token, so the launch sequence
+ * of a step does not change while the batch does not).  A talker step is a
+ * chain of ~5 short launches per layer; replaying them from a HIP graph takes
+ * the host's launch work and most of the gaps between them off the step.
+ *
+ * hs_decode_graph_create captures the launches of hs_downstream_decode_step
+ * for fixed (cfg, weights, n_layers, x_in, x_out, cache, batch, cu_budget,
+ * stream, workspace): every pointer is bound at capture and must stay valid,
+ * and the caller refreshes the contents of x_in between launches and reads
+ * x_out after.  The metadata image has a fixed layout sized for the cache's
+ * capacity (positions below max_ctx, or below pages_per_seq * max_ctx with a
+ * block table), single-row attention is launched over that capacity and its
+ * blocks beyond the step's work exit, and the RoPE table for every such
+ * position is computed once (enqueued on the stream by this call).  The
+ * stream is resolved as hs_downstream_decode_step resolves it (NULL: the
+ * context's DOWN stream of that budget); a replay keeps the stream's CU
+ * mask (the graph's kernels run on the stream it is launched on).  The
+ * workspace (hs_workspace_size, or hs_workspace_size_paged with the page
+ * size, for batch rows, batch sequences and that position capacity) belongs
+ * to the graph until it is destroyed; no other call may use it.
+ * kv->block_table, if non-null, only marks the cache as paged (its contents
+ * are not read here); kv->k / kv->v arrays are copied.
+ *
+ * hs_decode_graph_launch stages the step's metadata from kv_lens (host,
+ * [batch], cached rows before the step, as hs_downstream_decode_step) and,
+ * for a paged cache, block_table (host, [batch][pages_per_seq], checked as
+ * that call checks it; NULL otherwise) into the graph's workspace with an
+ * ordinary copy on the stream, then launches the graph on the stream.  The
+ * copy is issued before the graph, outside it, so a replay never reads a
+ * staging buffer that a later launch reuses.  Outputs are bit-identical to
+ * hs_downstream_decode_step on the same inputs.  Errors: HS_ERR_INVALID_ARG
+ * (kv_lens outside the capacity, table errors), HS_ERR_HIP; nothing is
+ * enqueued on a validation error.
+ *
+ * hs_decode_graph_destroy waits for the graph's stream and frees the graph
+ * (NULL is a no-op).  A graph is not thread-safe, like its context, and must
+ * be destroyed before its context. */
+hs_status hs_decode_graph_create(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w,
+                                 int32_t n_layers, const void* x_in, void* x_out, const hs_kv_cache* kv,
+                                 int32_t batch, int32_t cu_budget, void* stream, void* workspace,
+                                 size_t ws_bytes, hs_decode_graph** out);
+hs_status hs_decode_graph_launch(hs_decode_graph* graph, const int32_t* kv_lens, const int32_t* block_table);
+hs_status hs_decode_graph_destroy(hs_decode_graph* graph);
 
 /* Topology probe: launches n_groups work-groups on `stream` (NULL = the
  * context's full-budget stream); each writes, into out_ids (device, uint32

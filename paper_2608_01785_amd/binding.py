@@ -24,7 +24,8 @@ SYMBOLS = (
     "hs_context_create", "hs_context_topology", "hs_context_stream", "hs_context_masks",
     "hs_context_destroy", "hs_workspace_size", "hs_workspace_size_paged", "hs_shared_stage_forward",
     "hs_shared_stage_forward_mrope", "hs_downstream_decode_step_mrope", "hs_downstream_decode_step",
-    "hs_downstream_decode_step_noalloc",
+    "hs_downstream_decode_step_noalloc", "hs_decode_graph_create", "hs_decode_graph_launch",
+    "hs_decode_graph_destroy",
     "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read", "hs_timing_read_clock", "hs_convert_weights_f16",
     "hs_controller_create", "hs_controller_step", "hs_controller_destroy", "hs_pressure_sample",
     "hs_temporal_create", "hs_temporal_step", "hs_temporal_destroy",
@@ -141,6 +142,11 @@ def lib() -> ctypes.CDLL:
                                           ctypes.POINTER(KvCache), i32p, i32, i32, vp, vp, ctypes.c_size_t],
             "hs_downstream_decode_step_noalloc": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32,
                                                   vp, vp, ctypes.POINTER(KvCache), i32p, i32, i32, vp],
+            "hs_decode_graph_create": [vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights), i32, vp, vp,
+                                       ctypes.POINTER(KvCache), i32, i32, vp, vp, ctypes.c_size_t,
+                                       ctypes.POINTER(vp)],
+            "hs_decode_graph_launch": [vp, i32p, i32p],
+            "hs_decode_graph_destroy": [vp],
             "hs_probe_hw_ids": [vp, vp, i32, vp],
             "hs_timing_enable": [vp, i32],
             "hs_timing_read": [vp, i32, ctypes.POINTER(ctypes.c_double), i32p],
@@ -465,6 +471,50 @@ def hs_downstream_decode_step_noalloc(ctx: Context, cfg, weights, x_in, x_out, k
     _check(lib().hs_downstream_decode_step_noalloc(
         ctx.handle, ctypes.byref(LayerCfg.of(cfg)), warr, len(weights), _ptr(x_in), _ptr(x_out),
         ctypes.byref(kvs) if kvs is not None else None, lens, len(lens), cu_budget, _ptr(stream)))
+
+
+class DecodeGraph:
+    """A captured decode step (hs_decode_graph_create); launch(kv_lens[, block_table]) replays it.
+
+    kv as for hs_downstream_decode_step; with a block table there (any contents of the right
+    shape [batch, pages_per_seq]) the graph addresses a paged cache and every launch takes
+    that step's table."""
+
+    def __init__(self, ctx: Context, cfg, weights, x_in, x_out, kv, batch: int, cu_budget: int,
+                 stream=None, workspace=None, ws_bytes: Optional[int] = None):
+        self.handle = None
+        self._ctx = ctx
+        warr = _weights_array(weights)
+        kvs = _kv_struct(kv)
+        if ws_bytes is None:
+            ws_bytes = workspace.numel() * workspace.element_size()
+        h = ctypes.c_void_p()
+        _check(lib().hs_decode_graph_create(
+            ctx.handle, ctypes.byref(LayerCfg.of(cfg)), warr, len(weights), _ptr(x_in), _ptr(x_out),
+            ctypes.byref(kvs), batch, cu_budget, _ptr(stream), _ptr(workspace), ws_bytes, ctypes.byref(h)))
+        self.handle = h
+        self.batch = batch
+
+    def launch(self, kv_lens, block_table=None) -> None:
+        lens = _i32_array(kv_lens)
+        assert len(lens) == self.batch, (len(lens), self.batch)
+        tp = None
+        if block_table is not None:
+            table = np.ascontiguousarray(block_table, dtype=np.int32)
+            assert table.ndim == 2 and table.shape[0] == self.batch
+            tp = table.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        _check(lib().hs_decode_graph_launch(self.handle, lens, tp))
+
+    def close(self) -> None:
+        if self.handle is not None:
+            _check(lib().hs_decode_graph_destroy(self.handle))
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def hs_probe_hw_ids(ctx: Context, stream, n_groups: int, out_ids) -> None:

@@ -263,7 +263,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
 template <int DH>
 __global__ __launch_bounds__(kThreads, 2) void decode_attn_kernel(DecodeAttnArgs a) {
   __shared__ decode::DecodeSmem<DH> sm;
-  decode::decode_attn_unit<DH>(a, blockIdx.x / a.hkv, blockIdx.x % a.hkv, sm);
+  const int item = blockIdx.x / a.hkv;
+  if (a.n_items_dev && item >= *a.n_items_dev) return;  // a grid sized for a fixed layout
+  decode::decode_attn_unit<DH>(a, item, blockIdx.x % a.hkv, sm);
 }
 
 }  // namespace

@@ -116,7 +116,8 @@ struct DecodeAttnArgs {
   uint16_t* o;               // [T, hq * dh], k-group-major when o_k8_rows > 0
   int o_k8_rows;
   const DecItem* items;
-  int n_items;
+  int n_items;              // work items the grid covers
+  const int32_t* n_items_dev;  // or null; else the call's items on the device (<= n_items), the rest exit
   float* part;              // [n_items][hkv][dec_part_floats] partial states of split rows
   int32_t* counters;        // [n_items * hkv] arrival counters (first item of a row), zero on entry and exit
   int64_t kv_head_stride;

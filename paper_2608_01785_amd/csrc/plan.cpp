@@ -182,6 +182,7 @@ static size_t meta_bytes(int32_t T, int32_t B, int64_t pages, int64_t att, int32
   s += align_up(size_t(counters) * 4, 16); // split-K counters
   s += align_up(size_t(dec_items) * 32, 16); // decode work items
   s += align_up(size_t(dec_count) * 4, 16);  // decode arrival counters
+  s += 16;                                   // decode work item count
   return align_up(s, kAlign);
 }
 
@@ -260,7 +261,7 @@ hs_status check_block_table(const int32_t* table, int32_t pps, int32_t n_slots, 
 }
 
 hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* ctx, int32_t B,
-                     const KvPlacement& kv, Plan* out, const int32_t* positions3) {
+                     const KvPlacement& kv, Plan* out, const int32_t* positions3, const PlanCapacity* cap) {
   Plan& P = *out;
   hs_status st = validate_batch(off, ctx, B, &P.T, &P.max_pos);
   if (st != HS_OK) return st;
@@ -304,8 +305,11 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   P.seq_start = take(size_t(B) * 4);
   P.seq_len = take(size_t(B) * 4);
   P.seq_ctx = take(size_t(B) * 4);
-  P.att_items = take(size_t(P.n_att_items) * 8);
-  P.dec_rows = take(size_t(P.n_dec_rows) * 16);
+  if (cap && P.max_pos > cap->max_pos)
+    return fail(HS_ERR_INVALID_ARG, "position %d beyond the %d positions the fixed layout holds", P.max_pos - 1,
+                cap->max_pos);
+  P.att_items = take(size_t(cap ? max_att_items(int32_t(T), B) : P.n_att_items) * 8);
+  P.dec_rows = take(size_t(cap ? B : P.n_dec_rows) * 16);
   P.n_counters = skinny_needs(c, int32_t(T)).counters;
   P.counters = take(size_t(P.n_counters) * 4);
   // Pages: a slot, or the packed buffer, is one page per sequence; with a
@@ -320,15 +324,18 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
     P.n_pages += paged ? int32_t(ceil_div(end, slot_ctx)) : 1;
   }
   P.seq_page0 = take(size_t(B) * 4);
-  P.page_base = take(size_t(P.n_pages) * 8);
+  P.page_base = take(size_t(cap ? max_pages(B, cap->max_pos, cap->page_keys) : P.n_pages) * 8);
   std::vector<int32_t> dec_nsplit(dec_seq.size());
   P.n_dec_items = 0;
   for (size_t r = 0; r < dec_seq.size(); ++r) {
     dec_nsplit[r] = int32_t(ceil_div((ctx ? ctx[dec_seq[r]] : 0) + 1, P.unit_keys));
     P.n_dec_items += dec_nsplit[r];
   }
-  P.dec_items = take(size_t(P.n_dec_items) * 32);
-  P.dec_count = take(size_t(P.n_dec_items) * hkv * 4);
+  P.cap_dec_items = cap ? max_dec_items(int32_t(T), B, cap->max_pos, P.unit_keys) : P.n_dec_items;
+  if (P.n_dec_items > P.cap_dec_items) return fail(HS_ERR_INTERNAL, "decode work exceeds the fixed layout");
+  P.dec_items = take(size_t(P.cap_dec_items) * 32);
+  P.dec_count = take(size_t(P.cap_dec_items) * hkv * 4);
+  P.dec_n = take(4);
   P.image.assign(align_up(p, kAlign), 0);
 
   auto i32 = [&](size_t at) { return reinterpret_cast<int32_t*>(P.image.data() + at); };
@@ -378,6 +385,7 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
     i32(P.att_items)[2 * i] = att[i].b;
     i32(P.att_items)[2 * i + 1] = att[i].q0;
   }
+  i32(P.dec_n)[0] = P.n_dec_items;
   int32_t item = 0;
   for (int32_t r = 0; r < P.n_dec_rows; ++r) {
     const int32_t b = dec_seq[r];

@@ -90,7 +90,19 @@ struct Plan {
   size_t dec_items = 0;  // [n_dec_items] 32-byte records (row, keys, split, splits, K base, V base)
   size_t dec_count = 0;  // [n_dec_items * hkv] arrival counters, zero in the image
   int32_t n_att_items = 0, n_dec_rows = 0, n_counters = 0, n_dec_items = 0;
+  size_t dec_n = 0;      // int32: n_dec_items, for kernels launched with a grid for the capacity
+  int64_t cap_dec_items = 0;  // decode work items the layout holds (== n_dec_items unless fixed)
   int64_t kv_head_stride = 0;
+};
+
+// A fixed layout: every region of the image sized for the largest batch of
+// this shape whose positions stay below max_pos (the bounds the workspace
+// layout reserves), so that region offsets, the image size and the single-row
+// attention grid do not depend on the call's lengths.  Kernels replayed from
+// a captured graph read the call's metadata from such an image.
+struct PlanCapacity {
+  int32_t max_pos = 0;
+  int32_t page_keys = 0;  // positions per page of a paged cache, 0 without a block table
 };
 
 // Key/value placement: packed (no cache, rows in the workspace), cache slots
@@ -110,6 +122,7 @@ hs_status check_block_table(const int32_t* table, int32_t pages_per_seq, int32_t
                             const int32_t* seq_offsets, const int32_t* ctx_lens, int32_t n_seqs);
 
 hs_status build_plan(const hs_layer_cfg& c, const int32_t* seq_offsets, const int32_t* ctx_lens,
-                     int32_t n_seqs, const KvPlacement& kv, Plan* out, const int32_t* positions3 = nullptr);
+                     int32_t n_seqs, const KvPlacement& kv, Plan* out, const int32_t* positions3 = nullptr,
+                     const PlanCapacity* cap = nullptr);
 
 }  // namespace hs

@@ -75,6 +75,25 @@ struct hs_context {
   std::vector<TimingRec> recs;
 };
 
+// A captured decode step (see hs_decode_graph_create).
+struct hs_decode_graph {
+  hs_context* ctx = nullptr;
+  hs_layer_cfg cfg{};
+  std::vector<hs_layer_weights> w;
+  std::vector<void*> k, v;  // copies of the caller's per-layer cache pointer arrays
+  hs_kv_cache kv{};
+  int32_t n_layers = 0, batch = 0, budget = 0;
+  const void* x_in = nullptr;
+  void* x_out = nullptr;
+  void* ws = nullptr;
+  hs::WsLayout lay{};
+  hs::PlanCapacity cap{};
+  bool paged = false;
+  size_t image_bytes = 0;   // the fixed layout's image size (every launch's plan has it)
+  hipStream_t stream = nullptr;
+  hipGraphExec_t exec = nullptr;
+};
+
 namespace {
 
 const Level* find_level(const hs_context* ctx, int budget) {
@@ -256,6 +275,216 @@ void use_norm(hs::GemmArgs& a, const float* sumsq, int parts, float eps) {
   a.eps = eps;
 }
 
+// The kernel launches of one call (everything after the metadata copy and
+// the RoPE table): the layer loop of the shared-stage forward and the decode
+// step.  With L.fixed the plan has a fixed layout and single-row attention is
+// launched over the layout's capacity, reading the call's work item count from
+// the metadata image, so the launches can be captured once and replayed.
+struct LaunchSet {
+  const hs_layer_cfg* cfg;
+  const hs_layer_weights* w;
+  int32_t n_layers;
+  const void* x_in;
+  void* x_out;
+  const hs_kv_cache* kv;
+  bool cache;
+  void* ws;
+  hs::WsLayout lay;
+  const hs::Plan* plan_ptr;
+  int32_t budget;
+  bool pos3;
+  bool fixed;
+};
+
+hs_status launch_layers(hs_context* ctx, const LaunchSet& L, hipStream_t s) {
+  const hs_layer_cfg* cfg = L.cfg;
+  const hs_layer_weights* w = L.w;
+  const int32_t n_layers = L.n_layers;
+  const hs::Plan& plan = *L.plan_ptr;
+  const hs::WsLayout& lay = L.lay;
+  void* ws = L.ws;
+  const hs_kv_cache* kv = L.kv;
+  const int32_t T = plan.T, budget = L.budget;
+  const int d = cfg->hidden, hq = cfg->n_q_heads, hkv = cfg->n_kv_heads, dh = cfg->head_dim, f = cfg->ffn;
+  uint8_t* meta = at<uint8_t>(ws, lay.meta);
+  const int32_t* d_pos = reinterpret_cast<const int32_t*>(meta + plan.pos);
+  const int64_t* d_koff = reinterpret_cast<const int64_t*>(meta + plan.k_off);
+  const int64_t* d_voff = reinterpret_cast<const int64_t*>(meta + plan.v_off);
+  float2* rope = at<float2>(ws, lay.rope);
+  uint16_t* n_buf = at<uint16_t>(ws, lay.n);
+  uint16_t* q_buf = at<uint16_t>(ws, lay.q);
+  uint16_t* o_buf = at<uint16_t>(ws, lay.o);
+  float* h_buf = at<float>(ws, lay.h);
+  uint16_t* a_buf = at<uint16_t>(ws, lay.a);
+  float* xtmp = at<float>(ws, lay.xtmp);
+  float* sk_part = lay.part_bytes ? at<float>(ws, lay.part) : nullptr;
+  int32_t* sk_count = plan.n_counters ? reinterpret_cast<int32_t*>(meta + plan.counters) : nullptr;
+  // Decode-sized layers (every GEMM on the skinny path) fold RMSNorm into the
+  // GEMMs around it after layer 0's: each residual GEMM writes its output
+  // times the next norm's gain (fp16, into n_buf) and per-row partial sums of
+  // squares over its 32-column strips; the next projection scales its rows by
+  // rsqrt(mean square + eps).  Larger batches keep the norm kernel.
+  float* sumsq = at<float>(ws, lay.sumsq);
+  const int norm_parts = d / 32;
+  bool folded = false;  // n_buf holds x * gain, sumsq its partial sums
+  // Decode-sized batches keep the GEMM inputs (normed rows, attention output,
+  // SwiGLU output) k-group-major, the skinny GEMM's operand layout.
+  const int k8 = T <= hs::kSkinnyMaxRows ? hs::skinny_k8_rows(T) : 0;
+
+  const int grid_cap = budget;  // persistent GEMM: one block per CU of the budget
+  const float scale_log2 = 1.4426950408889634f / sqrtf(float(dh));
+  // The residual stream is bf16 only at the input; every layer writes fp32.
+  const uint16_t* x_cur = static_cast<const uint16_t*>(L.x_in);
+  const float* x_cur_f32 = nullptr;
+  for (int l = 0; l < n_layers; ++l) {
+    // The last layer writes x_out; earlier layers alternate so that no layer
+    // reads and writes the same buffer.
+    const int remaining = n_layers - 1 - l;
+    float* x_next = (remaining % 2 == 0) ? static_cast<float*>(L.x_out) : xtmp;
+    uint16_t* kstore = L.cache ? static_cast<uint16_t*>(kv->k[l]) : at<uint16_t>(ws, lay.kpack);
+    uint16_t* vstore = L.cache ? static_cast<uint16_t*>(kv->v[l]) : at<uint16_t>(ws, lay.vpack);
+
+    if (!folded)
+      TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(x_cur, x_cur_f32, static_cast<const uint16_t*>(w[l].ln1), n_buf,
+                                                  T, d, cfg->rms_eps, k8, 4 * budget, s));
+    hs::GemmArgs g{};
+    g.part = sk_part;
+    g.counters = sk_count;
+    g.A = n_buf;
+    g.W = static_cast<const uint16_t*>(w[l].w_qkv);
+    g.w_f16 = w[l].format == HS_WEIGHTS_F16;
+    g.M = T;
+    g.K = d;
+    g.n_tiles_n = (hq + 2 * hkv) * dh / 256;
+    g.q = q_buf;
+    g.kstore = kstore;
+    g.vstore = vstore;
+    // RoPE positions: the plain row positions, or the three multimodal components.
+    g.pos = L.pos3 ? reinterpret_cast<const int32_t*>(meta + plan.pos3) : d_pos;
+    g.pos_stride = L.pos3 ? T : 0;
+    g.sec1 = L.pos3 ? cfg->mrope_sections[0] : dh / 2;
+    g.sec2 = L.pos3 ? cfg->mrope_sections[0] + cfg->mrope_sections[1] : dh / 2;
+    g.k_off = d_koff;
+    g.v_off = d_voff;
+    g.kv_head_stride = plan.kv_head_stride;
+    g.rope = rope;
+    g.bias = static_cast<const uint16_t*>(w[l].b_qkv);
+    g.hq = hq;
+    g.hkv = hkv;
+    g.dh = dh;
+    g.k8_rows = k8;
+    if (folded) use_norm(g, sumsq, norm_parts, cfg->rms_eps);
+    g.clock = clock_slot(ctx);
+    TIMED(HS_KERNEL_QKV, gemm(hs::EPI_QKV, g, grid_cap, s));
+
+    hs::AttnArgs at_args{};
+    at_args.q = q_buf;
+    at_args.kstore = kstore;
+    at_args.vstore = vstore;
+    at_args.o = o_buf;
+    at_args.o_k8_rows = k8;
+    at_args.items = reinterpret_cast<const int32_t*>(meta + plan.att_items);
+    at_args.n_items = plan.n_att_items;
+    at_args.seq_start = reinterpret_cast<const int32_t*>(meta + plan.seq_start);
+    at_args.seq_len = reinterpret_cast<const int32_t*>(meta + plan.seq_len);
+    at_args.seq_ctx = reinterpret_cast<const int32_t*>(meta + plan.seq_ctx);
+    at_args.seq_page0 = reinterpret_cast<const int32_t*>(meta + plan.seq_page0);
+    at_args.page_base = reinterpret_cast<const int64_t*>(meta + plan.page_base);
+    at_args.page_keys = plan.page_keys;
+    at_args.kv_head_stride = plan.kv_head_stride;
+    at_args.hq = hq;
+    at_args.hkv = hkv;
+    at_args.dh = dh;
+    at_args.scale_log2 = scale_log2;
+    at_args.clock = clock_slot(ctx);
+    if (plan.n_att_items > 0) TIMED(HS_KERNEL_ATTENTION, hs::launch_attention(at_args, s));
+
+    hs::DecodeAttnArgs da{};
+    da.q = q_buf;
+    da.kstore = kstore;
+    da.vstore = vstore;
+    da.o = o_buf;
+    da.o_k8_rows = k8;
+    da.items = reinterpret_cast<const hs::DecItem*>(meta + plan.dec_items);
+    da.n_items = L.fixed ? int(plan.cap_dec_items) : plan.n_dec_items;
+    da.n_items_dev = L.fixed ? reinterpret_cast<const int32_t*>(meta + plan.dec_n) : nullptr;
+    da.part = lay.dec_part_bytes ? at<float>(ws, lay.dec_part) : nullptr;
+    da.counters = reinterpret_cast<int32_t*>(meta + plan.dec_count);
+    da.kv_head_stride = plan.kv_head_stride;
+    da.page_keys = plan.page_keys;
+    da.unit_keys = plan.unit_keys;
+    da.hq = hq;
+    da.hkv = hkv;
+    da.dh = dh;
+    da.scale_log2 = scale_log2;
+    if (plan.n_dec_rows > 0 || L.fixed) TIMED(HS_KERNEL_DECODE_ATTN, hs::launch_decode_attention(da, s));
+
+    hs::GemmArgs go{};
+    go.part = sk_part;
+    go.counters = sk_count;
+    go.A = o_buf;
+    go.W = static_cast<const uint16_t*>(w[l].w_o);
+    go.w_f16 = w[l].format == HS_WEIGHTS_F16;
+    go.M = T;
+    go.K = hq * dh;
+    go.n_tiles_n = d / 256;
+    go.out_f32 = h_buf;
+    go.ldo = d;
+    go.resid = x_cur;
+    go.resid_f32 = x_cur_f32;
+    go.k8_rows = k8;
+    // Fold when every GEMM of the layer takes the skinny path (gate/up and
+    // down share M, and their K are multiples of 64) and a consumer can
+    // prefetch a row's partial sums.
+    const bool fold = hs::skinny_supported(hs::EPI_QKV, g) && hs::skinny_supported(hs::EPI_RESID, go) &&
+                      norm_parts <= hs::kSkinnyMaxNormParts;
+    if (fold) fold_norm(go, sumsq, n_buf, w[l].ln2);
+    go.clock = clock_slot(ctx);
+    TIMED(HS_KERNEL_O_PROJ, gemm(hs::EPI_RESID, go, grid_cap, s));
+    if (!fold)
+      TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(nullptr, h_buf, static_cast<const uint16_t*>(w[l].ln2), n_buf, T,
+                                                  d, cfg->rms_eps, k8, 4 * budget, s));
+
+    hs::GemmArgs gu{};
+    gu.part = sk_part;
+    gu.counters = sk_count;
+    gu.A = n_buf;
+    gu.W = static_cast<const uint16_t*>(w[l].w_gate_up);
+    gu.w_f16 = w[l].format == HS_WEIGHTS_F16;
+    gu.M = T;
+    gu.K = d;
+    gu.n_tiles_n = f / 128;
+    gu.out = a_buf;
+    gu.ldo = f;
+    gu.ffn = f;
+    gu.k8_rows = k8;
+    if (fold) use_norm(gu, sumsq, norm_parts, cfg->rms_eps);
+    gu.clock = clock_slot(ctx);
+    TIMED(HS_KERNEL_GATE_UP, gemm(hs::EPI_SWIGLU, gu, grid_cap, s));
+
+    hs::GemmArgs gd{};
+    gd.part = sk_part;
+    gd.counters = sk_count;
+    gd.A = a_buf;
+    gd.W = static_cast<const uint16_t*>(w[l].w_down);
+    gd.w_f16 = w[l].format == HS_WEIGHTS_F16;
+    gd.M = T;
+    gd.K = f;
+    gd.n_tiles_n = d / 256;
+    gd.out_f32 = x_next;
+    gd.ldo = d;
+    gd.resid_f32 = h_buf;
+    gd.k8_rows = k8;
+    folded = fold && l + 1 < n_layers;
+    if (folded) fold_norm(gd, sumsq, n_buf, w[l + 1].ln1);
+    gd.clock = clock_slot(ctx);
+    TIMED(HS_KERNEL_DOWN, gemm(hs::EPI_RESID, gd, grid_cap, s));
+    x_cur = nullptr;
+    x_cur_f32 = x_next;
+  }
+  return HS_OK;
+}
+
 // Shared body of the prefill forward and the decode step.
 // noalloc: the workspace is the context's static scratch (ws and ws_bytes are
 // ignored), laid out without the packed key/value slot (a cache is required),
@@ -351,186 +580,10 @@ hs_status run_stack(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_wei
   st = noalloc ? stage_metadata_fixed(ctx, plan, at<void>(ws, lay.meta), s)
                : stage_metadata(ctx, plan, at<void>(ws, lay.meta), s);
   if (st != HS_OK) return st;
-
-  const int d = cfg->hidden, hq = cfg->n_q_heads, hkv = cfg->n_kv_heads, dh = cfg->head_dim, f = cfg->ffn;
-  uint8_t* meta = at<uint8_t>(ws, lay.meta);
-  const int32_t* d_pos = reinterpret_cast<const int32_t*>(meta + plan.pos);
-  const int64_t* d_koff = reinterpret_cast<const int64_t*>(meta + plan.k_off);
-  const int64_t* d_voff = reinterpret_cast<const int64_t*>(meta + plan.v_off);
-  float2* rope = at<float2>(ws, lay.rope);
-  uint16_t* n_buf = at<uint16_t>(ws, lay.n);
-  uint16_t* q_buf = at<uint16_t>(ws, lay.q);
-  uint16_t* o_buf = at<uint16_t>(ws, lay.o);
-  float* h_buf = at<float>(ws, lay.h);
-  uint16_t* a_buf = at<uint16_t>(ws, lay.a);
-  float* xtmp = at<float>(ws, lay.xtmp);
-  float* sk_part = lay.part_bytes ? at<float>(ws, lay.part) : nullptr;
-  int32_t* sk_count = plan.n_counters ? reinterpret_cast<int32_t*>(meta + plan.counters) : nullptr;
-  // Decode-sized layers (every GEMM on the skinny path) fold RMSNorm into the
-  // GEMMs around it after layer 0's: each residual GEMM writes its output
-  // times the next norm's gain (fp16, into n_buf) and per-row partial sums of
-  // squares over its 32-column strips; the next projection scales its rows by
-  // rsqrt(mean square + eps).  Larger batches keep the norm kernel.
-  float* sumsq = at<float>(ws, lay.sumsq);
-  const int norm_parts = d / 32;
-  bool folded = false;  // n_buf holds x * gain, sumsq its partial sums
-  // Decode-sized batches keep the GEMM inputs (normed rows, attention output,
-  // SwiGLU output) k-group-major, the skinny GEMM's operand layout.
-  const int k8 = T <= hs::kSkinnyMaxRows ? hs::skinny_k8_rows(T) : 0;
-
-  TIMED(HS_KERNEL_ROPE_TABLE, hs::launch_rope_table(rope, max_pos, dh, cfg->rope_base, s));
-
-  const int grid_cap = budget;  // persistent GEMM: one block per CU of the budget
-  const float scale_log2 = 1.4426950408889634f / sqrtf(float(dh));
-  // The residual stream is bf16 only at the input; every layer writes fp32.
-  const uint16_t* x_cur = static_cast<const uint16_t*>(x_in);
-  const float* x_cur_f32 = nullptr;
-  for (int l = 0; l < n_layers; ++l) {
-    // The last layer writes x_out; earlier layers alternate so that no layer
-    // reads and writes the same buffer.
-    const int remaining = n_layers - 1 - l;
-    float* x_next = (remaining % 2 == 0) ? static_cast<float*>(x_out) : xtmp;
-    uint16_t* kstore = place.cache ? static_cast<uint16_t*>(kv->k[l]) : at<uint16_t>(ws, lay.kpack);
-    uint16_t* vstore = place.cache ? static_cast<uint16_t*>(kv->v[l]) : at<uint16_t>(ws, lay.vpack);
-
-    if (!folded)
-      TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(x_cur, x_cur_f32, static_cast<const uint16_t*>(w[l].ln1), n_buf,
-                                                  T, d, cfg->rms_eps, k8, 4 * budget, s));
-    hs::GemmArgs g{};
-    g.part = sk_part;
-    g.counters = sk_count;
-    g.A = n_buf;
-    g.W = static_cast<const uint16_t*>(w[l].w_qkv);
-    g.w_f16 = w[l].format == HS_WEIGHTS_F16;
-    g.M = T;
-    g.K = d;
-    g.n_tiles_n = (hq + 2 * hkv) * dh / 256;
-    g.q = q_buf;
-    g.kstore = kstore;
-    g.vstore = vstore;
-    // RoPE positions: the plain row positions, or the three multimodal components.
-    g.pos = pos3 ? reinterpret_cast<const int32_t*>(meta + plan.pos3) : d_pos;
-    g.pos_stride = pos3 ? T : 0;
-    g.sec1 = pos3 ? cfg->mrope_sections[0] : dh / 2;
-    g.sec2 = pos3 ? cfg->mrope_sections[0] + cfg->mrope_sections[1] : dh / 2;
-    g.k_off = d_koff;
-    g.v_off = d_voff;
-    g.kv_head_stride = plan.kv_head_stride;
-    g.rope = rope;
-    g.bias = static_cast<const uint16_t*>(w[l].b_qkv);
-    g.hq = hq;
-    g.hkv = hkv;
-    g.dh = dh;
-    g.k8_rows = k8;
-    if (folded) use_norm(g, sumsq, norm_parts, cfg->rms_eps);
-    g.clock = clock_slot(ctx);
-    TIMED(HS_KERNEL_QKV, gemm(hs::EPI_QKV, g, grid_cap, s));
-
-    hs::AttnArgs at_args{};
-    at_args.q = q_buf;
-    at_args.kstore = kstore;
-    at_args.vstore = vstore;
-    at_args.o = o_buf;
-    at_args.o_k8_rows = k8;
-    at_args.items = reinterpret_cast<const int32_t*>(meta + plan.att_items);
-    at_args.n_items = plan.n_att_items;
-    at_args.seq_start = reinterpret_cast<const int32_t*>(meta + plan.seq_start);
-    at_args.seq_len = reinterpret_cast<const int32_t*>(meta + plan.seq_len);
-    at_args.seq_ctx = reinterpret_cast<const int32_t*>(meta + plan.seq_ctx);
-    at_args.seq_page0 = reinterpret_cast<const int32_t*>(meta + plan.seq_page0);
-    at_args.page_base = reinterpret_cast<const int64_t*>(meta + plan.page_base);
-    at_args.page_keys = plan.page_keys;
-    at_args.kv_head_stride = plan.kv_head_stride;
-    at_args.hq = hq;
-    at_args.hkv = hkv;
-    at_args.dh = dh;
-    at_args.scale_log2 = scale_log2;
-    at_args.clock = clock_slot(ctx);
-    if (plan.n_att_items > 0) TIMED(HS_KERNEL_ATTENTION, hs::launch_attention(at_args, s));
-
-    hs::DecodeAttnArgs da{};
-    da.q = q_buf;
-    da.kstore = kstore;
-    da.vstore = vstore;
-    da.o = o_buf;
-    da.o_k8_rows = k8;
-    da.items = reinterpret_cast<const hs::DecItem*>(meta + plan.dec_items);
-    da.n_items = plan.n_dec_items;
-    da.part = lay.dec_part_bytes ? at<float>(ws, lay.dec_part) : nullptr;
-    da.counters = reinterpret_cast<int32_t*>(meta + plan.dec_count);
-    da.kv_head_stride = plan.kv_head_stride;
-    da.page_keys = plan.page_keys;
-    da.unit_keys = plan.unit_keys;
-    da.hq = hq;
-    da.hkv = hkv;
-    da.dh = dh;
-    da.scale_log2 = scale_log2;
-    if (plan.n_dec_rows > 0) TIMED(HS_KERNEL_DECODE_ATTN, hs::launch_decode_attention(da, s));
-
-    hs::GemmArgs go{};
-    go.part = sk_part;
-    go.counters = sk_count;
-    go.A = o_buf;
-    go.W = static_cast<const uint16_t*>(w[l].w_o);
-    go.w_f16 = w[l].format == HS_WEIGHTS_F16;
-    go.M = T;
-    go.K = hq * dh;
-    go.n_tiles_n = d / 256;
-    go.out_f32 = h_buf;
-    go.ldo = d;
-    go.resid = x_cur;
-    go.resid_f32 = x_cur_f32;
-    go.k8_rows = k8;
-    // Fold when every GEMM of the layer takes the skinny path (gate/up and
-    // down share M, and their K are multiples of 64) and a consumer can
-    // prefetch a row's partial sums.
-    const bool fold = hs::skinny_supported(hs::EPI_QKV, g) && hs::skinny_supported(hs::EPI_RESID, go) &&
-                      norm_parts <= hs::kSkinnyMaxNormParts;
-    if (fold) fold_norm(go, sumsq, n_buf, w[l].ln2);
-    go.clock = clock_slot(ctx);
-    TIMED(HS_KERNEL_O_PROJ, gemm(hs::EPI_RESID, go, grid_cap, s));
-    if (!fold)
-      TIMED(HS_KERNEL_RMSNORM, hs::launch_rmsnorm(nullptr, h_buf, static_cast<const uint16_t*>(w[l].ln2), n_buf, T,
-                                                  d, cfg->rms_eps, k8, 4 * budget, s));
-
-    hs::GemmArgs gu{};
-    gu.part = sk_part;
-    gu.counters = sk_count;
-    gu.A = n_buf;
-    gu.W = static_cast<const uint16_t*>(w[l].w_gate_up);
-    gu.w_f16 = w[l].format == HS_WEIGHTS_F16;
-    gu.M = T;
-    gu.K = d;
-    gu.n_tiles_n = f / 128;
-    gu.out = a_buf;
-    gu.ldo = f;
-    gu.ffn = f;
-    gu.k8_rows = k8;
-    if (fold) use_norm(gu, sumsq, norm_parts, cfg->rms_eps);
-    gu.clock = clock_slot(ctx);
-    TIMED(HS_KERNEL_GATE_UP, gemm(hs::EPI_SWIGLU, gu, grid_cap, s));
-
-    hs::GemmArgs gd{};
-    gd.part = sk_part;
-    gd.counters = sk_count;
-    gd.A = a_buf;
-    gd.W = static_cast<const uint16_t*>(w[l].w_down);
-    gd.w_f16 = w[l].format == HS_WEIGHTS_F16;
-    gd.M = T;
-    gd.K = f;
-    gd.n_tiles_n = d / 256;
-    gd.out_f32 = x_next;
-    gd.ldo = d;
-    gd.resid_f32 = h_buf;
-    gd.k8_rows = k8;
-    folded = fold && l + 1 < n_layers;
-    if (folded) fold_norm(gd, sumsq, n_buf, w[l + 1].ln1);
-    gd.clock = clock_slot(ctx);
-    TIMED(HS_KERNEL_DOWN, gemm(hs::EPI_RESID, gd, grid_cap, s));
-    x_cur = nullptr;
-    x_cur_f32 = x_next;
-  }
-  return HS_OK;
+  TIMED(HS_KERNEL_ROPE_TABLE,
+        hs::launch_rope_table(at<float2>(ws, lay.rope), max_pos, cfg->head_dim, cfg->rope_base, s));
+  LaunchSet L{cfg, w, n_layers, x_in, x_out, kv, place.cache, ws, lay, &plan, budget, pos3 != nullptr, false};
+  return launch_layers(ctx, L, s);
 }
 
 }  // namespace
@@ -710,6 +763,177 @@ hs_status hs_downstream_decode_step_noalloc(hs_context* ctx, const hs_layer_cfg*
   for (int32_t b = 0; b <= batch; ++b) off[b] = b;
   return run_stack(ctx, cfg, w, n_layers, x_in, x_out, off, kv_lens, batch, kv, cu_budget, HS_ROLE_DOWN, stream,
                    nullptr, 0, nullptr, true);
+}
+
+hs_status hs_decode_graph_create(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w,
+                                 int32_t n_layers, const void* x_in, void* x_out, const hs_kv_cache* kv,
+                                 int32_t batch, int32_t cu_budget, void* stream, void* workspace, size_t ws_bytes,
+                                 hs_decode_graph** out) {
+  hs::clear_error();
+  if (!out) return hs::fail(HS_ERR_INVALID_ARG, "output pointer is null");
+  *out = nullptr;
+  if (!ctx) return hs::fail(HS_ERR_INVALID_ARG, "context is null");
+  hs_status st = hs::validate_cfg(cfg);
+  if (st != HS_OK) return st;
+  if (!w || n_layers < 1) return hs::fail(HS_ERR_INVALID_ARG, "weights missing or n_layers %d < 1", n_layers);
+  for (int l = 0; l < n_layers; ++l) {
+    if (!w[l].ln1 || !w[l].w_qkv || !w[l].w_o || !w[l].ln2 || !w[l].w_gate_up || !w[l].w_down)
+      return hs::fail(HS_ERR_INVALID_ARG, "layer %d has a null weight pointer", l);
+    if (w[l].format != HS_WEIGHTS_BF16 && w[l].format != HS_WEIGHTS_F16)
+      return hs::fail(HS_ERR_INVALID_ARG, "layer %d has weight format %d", l, w[l].format);
+  }
+  if (!x_in || !x_out) return hs::fail(HS_ERR_INVALID_ARG, "x_in / x_out is null");
+  if (x_in == x_out) return hs::fail(HS_ERR_INVALID_ARG, "x_in and x_out must not alias");
+  if (batch < 1) return hs::fail(HS_ERR_INVALID_ARG, "batch %d < 1", batch);
+  if (!kv || !kv->k || !kv->v) return hs::fail(HS_ERR_INVALID_ARG, "decode needs a key/value cache");
+  for (int l = 0; l < n_layers; ++l)
+    if (!kv->k[l] || !kv->v[l]) return hs::fail(HS_ERR_INVALID_ARG, "cache of layer %d is null", l);
+  if (kv->max_ctx < 64 || kv->max_ctx % 64 != 0)
+    return hs::fail(HS_ERR_INVALID_ARG, "max_ctx %d must be a positive multiple of 64", kv->max_ctx);
+  if (kv->n_slots < 1) return hs::fail(HS_ERR_INVALID_ARG, "the cache has %d slots", kv->n_slots);
+  const bool paged = kv->block_table != nullptr;
+  if (paged && kv->pages_per_seq < 1)
+    return hs::fail(HS_ERR_INVALID_ARG, "pages_per_seq %d must be >= 1", kv->pages_per_seq);
+  if (!paged && batch > kv->n_slots)
+    return hs::fail(HS_ERR_INVALID_ARG, "batch %d but only %d cache slots", batch, kv->n_slots);
+  st = hs::check_32bit_extents(*cfg, batch, kv->max_ctx);
+  if (st != HS_OK) return st;
+  hs::PlanCapacity cap;
+  cap.page_keys = paged ? kv->max_ctx : 0;
+  const int64_t max_pos = paged ? int64_t(kv->pages_per_seq) * kv->max_ctx : int64_t(kv->max_ctx);
+  if (max_pos > (int64_t(1) << 30)) return hs::fail(HS_ERR_UNSUPPORTED, "%lld positions per sequence", (long long)max_pos);
+  cap.max_pos = int32_t(max_pos);
+  hipStream_t s = nullptr;
+  st = resolve_stream(ctx, cu_budget, HS_ROLE_DOWN, stream, &s);
+  if (st != HS_OK) return st;
+  if (!workspace) return hs::fail(HS_ERR_WORKSPACE, "workspace is null");
+  const hs::WsLayout lay = hs::ws_layout(*cfg, batch, batch, cap.max_pos, cap.page_keys, false);
+  if (ws_bytes < lay.total) return hs::fail(HS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, lay.total);
+
+  // The launches are captured from a plan of empty caches in the fixed
+  // layout: its offsets, and so every kernel argument, are those of any
+  // later call; the contents are staged per launch.
+  std::vector<int32_t> off(batch + 1), zero(batch, 0), table;
+  for (int32_t b = 0; b <= batch; ++b) off[b] = b;
+  hs::KvPlacement place;
+  place.cache = true;
+  place.max_ctx = kv->max_ctx;
+  if (paged) {
+    table.assign(size_t(batch) * kv->pages_per_seq, 0);
+    place.table = table.data();
+    place.pages_per_seq = kv->pages_per_seq;
+  }
+  hs::Plan plan;
+  st = hs::build_plan(*cfg, off.data(), zero.data(), batch, place, &plan, nullptr, &cap);
+  if (st != HS_OK) return st;
+  if (plan.image.size() > lay.meta_bytes) return hs::fail(HS_ERR_INTERNAL, "metadata image exceeds its region");
+
+  hs_decode_graph* g = new hs_decode_graph();
+  g->ctx = ctx;
+  g->cfg = *cfg;
+  g->w.assign(w, w + n_layers);
+  g->k.assign(kv->k, kv->k + n_layers);
+  g->v.assign(kv->v, kv->v + n_layers);
+  g->kv = *kv;
+  g->kv.k = g->k.data();
+  g->kv.v = g->v.data();
+  g->kv.block_table = nullptr;
+  g->n_layers = n_layers;
+  g->batch = batch;
+  g->budget = cu_budget;
+  g->x_in = x_in;
+  g->x_out = x_out;
+  g->ws = workspace;
+  g->lay = lay;
+  g->cap = cap;
+  g->paged = paged;
+  g->image_bytes = plan.image.size();
+  g->stream = s;
+
+  auto fail_hip = [&](const char* what, hipError_t e) {
+    delete g;
+    return hs::fail(HS_ERR_HIP, "%s failed: %s", what, hipGetErrorString(e));
+  };
+  hipError_t e = hipSetDevice(ctx->device);
+  if (e != hipSuccess) return fail_hip("hipSetDevice", e);
+  (void)hipGetLastError();
+  // The RoPE table for every position the layout holds, once, on the stream.
+  e = hs::launch_rope_table(at<float2>(workspace, lay.rope), cap.max_pos, cfg->head_dim, cfg->rope_base, s);
+  if (e != hipSuccess) return fail_hip("the RoPE table launch", e);
+  const bool timing = ctx->timing;
+  ctx->timing = false;  // no event records inside the capture
+  e = hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) {
+    ctx->timing = timing;
+    return fail_hip("hipStreamBeginCapture", e);
+  }
+  LaunchSet L{&g->cfg, g->w.data(), n_layers, x_in, x_out, &g->kv, true, workspace, lay, &plan, cu_budget, false, true};
+  st = launch_layers(ctx, L, s);
+  hipGraph_t graph = nullptr;
+  e = hipStreamEndCapture(s, &graph);
+  ctx->timing = timing;
+  if (st != HS_OK) {
+    if (graph) hipGraphDestroy(graph);
+    delete g;
+    return st;
+  }
+  if (e != hipSuccess) {
+    if (graph) hipGraphDestroy(graph);
+    return fail_hip("hipStreamEndCapture", e);
+  }
+  e = hipGraphInstantiate(&g->exec, graph, nullptr, nullptr, 0);
+  hipGraphDestroy(graph);
+  if (e != hipSuccess) return fail_hip("hipGraphInstantiate", e);
+  *out = g;
+  return HS_OK;
+}
+
+hs_status hs_decode_graph_launch(hs_decode_graph* g, const int32_t* kv_lens, const int32_t* block_table) {
+  hs::clear_error();
+  if (!g) return hs::fail(HS_ERR_INVALID_ARG, "graph is null");
+  if (!kv_lens) return hs::fail(HS_ERR_INVALID_ARG, "kv_lens is null");
+  if (g->paged != (block_table != nullptr))
+    return hs::fail(HS_ERR_INVALID_ARG, g->paged ? "the graph was captured for a paged cache: block_table is required"
+                                                 : "the graph was captured for cache slots: block_table must be null");
+  std::vector<int32_t> off(g->batch + 1);
+  for (int32_t b = 0; b <= g->batch; ++b) off[b] = b;
+  for (int32_t b = 0; b < g->batch; ++b)
+    if (kv_lens[b] < 0 || int64_t(kv_lens[b]) + 1 > g->cap.max_pos)
+      return hs::fail(HS_ERR_INVALID_ARG, "kv_lens[%d] = %d: the new row must sit below position %d", b, kv_lens[b],
+                      g->cap.max_pos);
+  hs::KvPlacement place;
+  place.cache = true;
+  place.max_ctx = g->kv.max_ctx;
+  if (g->paged) {
+    hs_status st = hs::check_block_table(block_table, g->kv.pages_per_seq, g->kv.n_slots, g->kv.max_ctx,
+                                         off.data(), kv_lens, g->batch);
+    if (st != HS_OK) return st;
+    place.table = block_table;
+    place.pages_per_seq = g->kv.pages_per_seq;
+  }
+  hs::Plan plan;
+  hs_status st = hs::build_plan(g->cfg, off.data(), kv_lens, g->batch, place, &plan, nullptr, &g->cap);
+  if (st != HS_OK) return st;
+  if (plan.image.size() != g->image_bytes) return hs::fail(HS_ERR_INTERNAL, "metadata layout changed since capture");
+  hs_context* ctx = g->ctx;
+  HIP_TRY(hipSetDevice(ctx->device));
+  (void)hipGetLastError();
+  st = stage_metadata(ctx, plan, at<void>(g->ws, g->lay.meta), g->stream);
+  if (st != HS_OK) return st;
+  HIP_TRY(hipGraphLaunch(g->exec, g->stream));
+  return HS_OK;
+}
+
+hs_status hs_decode_graph_destroy(hs_decode_graph* g) {
+  hs::clear_error();
+  if (!g) return HS_OK;
+  if (g->exec) {
+    hipSetDevice(g->ctx->device);
+    hipStreamSynchronize(g->stream);
+    hipGraphExecDestroy(g->exec);
+  }
+  delete g;
+  return HS_OK;
 }
 
 hs_status hs_downstream_decode_step_mrope(hs_context* ctx, const hs_layer_cfg* cfg, const hs_layer_weights* w,

@@ -364,3 +364,33 @@ def test_masks_hold_on_hardware(env, hw_table):
         assert not (seen[0] & seen[1])
         assert len(seen[0]) >= 0.9 * budget  # 4096 blocks spread over (nearly) every CU of the mask
 
+
+
+def test_graph_replay_keeps_the_stream_mask(env, hw_table):
+    """Kernels replayed from a captured graph run on the CUs of the stream the
+    graph is launched on: a probe captured once and replayed on each side of a
+    ladder level stays inside that side's mask."""
+    torch, ctx = env
+    from paper_2608_01785_amd import binding
+    n = 4096
+    out = torch.zeros(n * 4, dtype=torch.int32, device="cuda")
+    sh, dn = binding.hs_context_masks(ctx, 128)
+    for role, words in ((binding.HS_ROLE_SHARED, sh), (binding.HS_ROLE_DOWN, dn)):
+        allowed = {hw_table[i] for i in range(256) if (words[i // 32] >> (i % 32)) & 1}
+        s = binding.hs_context_stream(ctx, 128, role)
+        ext = torch.cuda.ExternalStream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=ext):
+            binding.hs_probe_hw_ids(ctx, s, n, out)
+        out.zero_()
+        torch.cuda.synchronize()
+        log(f"[graph probe] role {role}")
+        with torch.cuda.stream(ext):
+            g.replay()
+        torch.cuda.synchronize()
+        seen = {(int(a), int(b_), int(c)) for a, b_, c, _ in out.view(n, 4).cpu().numpy()}
+        log(f"  distinct CUs used by the replay: {len(seen)}")
+        assert seen <= allowed, sorted(seen - allowed)[:8]
+        assert len(seen) >= 0.9 * 128
+        del g
