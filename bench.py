@@ -320,11 +320,19 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
     s_sh = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_SHARED))
     s_dn = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_DOWN))
 
-    def decode(n, cus=128, stream=None, rec=None):
+    # The same step captured once and replayed (the serving path for a fixed batch).
+    wsg = torch.empty(binding.hs_workspace_size(ts_shape, bt, bt, max_ctx), dtype=torch.uint8, device=dev)
+    tgraph = binding.DecodeGraph(ctx, ts_shape, tl, xt, yt, cache.as_arg(), bt, 128, None, wsg)
+
+    def decode(n, cus=128, stream=None, rec=None, graph=False):
         rec = s_dn if rec is None else rec
         ev = []
         for _ in range(n):
-            binding.hs_downstream_decode_step(ctx, ts_shape, tl, xt, yt, cache.as_arg(), kv_lens, cus, stream, wst)
+            if graph:
+                tgraph.launch(kv_lens)
+            else:
+                binding.hs_downstream_decode_step(ctx, ts_shape, tl, xt, yt, cache.as_arg(), kv_lens, cus, stream,
+                                                  wst)
             e = torch.cuda.Event(enable_timing=True)
             e.record(rec)
             ev.append(e)
@@ -355,15 +363,22 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
         t_last = max([t for t in done if t <= window], default=0.0)
         return window, (t_last / n_in if n_in else float("nan")), n_in
 
-    # Solo decode on its 128 CUs.
-    torch.cuda.synchronize()
-    decode(3)
-    torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e0.record(s_dn)
-    ev = decode(20)
-    torch.cuda.synchronize()
-    solo_ms = e0.elapsed_time(ev[-1]) / 20
+    # Solo decode on its 128 CUs: replayed graph, and eager launches.
+    def solo(graph):
+        """(GPU ms per step, host ms per issued step) over 20 back-to-back steps."""
+        torch.cuda.synchronize()
+        decode(3, graph=graph)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e0.record(s_dn)
+        t0 = time.perf_counter()
+        ev = decode(20, graph=graph)
+        host = (time.perf_counter() - t0) * 1e3 / 20
+        torch.cuda.synchronize()
+        return e0.elapsed_time(ev[-1]) / 20, host
+
+    solo_eager_ms, host_eager_ms = solo(False)
+    solo_ms, host_graph_ms = solo(True)
 
     # Per-kernel averages of the solo decode step (events on the decode stream).
     binding.hs_timing_enable(ctx, True)
@@ -399,28 +414,33 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
     prefill_solo = p0.elapsed_time(p1)
 
     # Co-run: both streams start after a common point.
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    start.record(s_sh)
-    s_dn.wait_event(start)
-    binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, None, None, 128, None, ws)
-    p_end = torch.cuda.Event(enable_timing=True)
-    p_end.record(s_sh)
-    dec_ev = []
-    while True:
-        dec_ev += decode(1)
-        if p_end.query():
-            break
-        if len(dec_ev) > 4:
-            dec_ev[-4].synchronize()
-        if len(dec_ev) > 2000:
-            break
-    torch.cuda.synchronize()
-    window = start.elapsed_time(p_end)
-    done = [start.elapsed_time(e) for e in dec_ev]
-    n_in = sum(1 for t in done if t <= window)
-    t_last = max([t for t in done if t <= window], default=0.0)
-    dec_ms = t_last / n_in if n_in else float("nan")
+    def corun(graph):
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        start.record(s_sh)
+        s_dn.wait_event(start)
+        binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, None, None, 128, None, ws)
+        p_end = torch.cuda.Event(enable_timing=True)
+        p_end.record(s_sh)
+        dec_ev = []
+        while True:
+            dec_ev += decode(1, graph=graph)
+            if p_end.query():
+                break
+            if len(dec_ev) > 4:
+                dec_ev[-4].synchronize()
+            if len(dec_ev) > 2000:
+                break
+        torch.cuda.synchronize()
+        window = start.elapsed_time(p_end)
+        done = [start.elapsed_time(e) for e in dec_ev]
+        n_in = sum(1 for t in done if t <= window)
+        t_last = max([t for t in done if t <= window], default=0.0)
+        return window, (t_last / n_in if n_in else float("nan")), n_in
+
+    window_e, dec_eager_ms, n_in_e = corun(False)
+    window, dec_ms, n_in = corun(True)
+    tgraph.close()
     T = batch.n_tokens
     res = {
         "shared_cus": 128, "down_cus": 128,
@@ -431,6 +451,10 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
         "decode_ms_per_step": round(dec_ms, 4),
         "decode_tok_s": round(32 / (dec_ms / 1e3)) if n_in else None,
         "decode_hbm_frac_cu_scaled": round(step_bytes / (dec_ms / 1e3) / (PEAK_HBM * 128 / N_CUS), 4) if n_in else None,
+        "decode_path": "captured decode step replayed per step (hs_decode_graph_launch)",
+        "decode_eager_ms_per_step": round(dec_eager_ms, 4), "prefill_ms_with_eager_decode": round(window_e, 3),
+        "decode_eager_solo_ms_per_step": round(solo_eager_ms, 4),
+        "decode_host_ms_per_step": {"graph": round(host_graph_ms, 4), "eager": round(host_eager_ms, 4)},
         "decode_solo_ms_per_step": round(solo_ms, 4),
         "decode_solo_tok_s": round(32 / (solo_ms / 1e3)),
         "decode_solo_hbm_frac_cu_scaled": round(step_bytes / (solo_ms / 1e3) / (PEAK_HBM * 128 / N_CUS), 4),
@@ -440,7 +464,8 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
         "talker": "16 layers, hidden 1024, 16/16 heads, dh 64, ffn 4096, batch 32, kv_len U[128,1024] (sum 17437)",
     }
     log(f"[bench] co-run: prefill {window:.2f} ms (solo {prefill_solo:.2f}), decode {dec_ms:.3f} ms/step "
-        f"(solo {solo_ms:.3f}), {n_in} steps in window")
+        f"(solo {solo_ms:.3f}), {n_in} steps in window; eager decode steps: {dec_eager_ms:.3f} ms/step "
+        f"(solo {solo_eager_ms:.3f}); host time per step: graph {host_graph_ms:.3f} ms, eager {host_eager_ms:.3f} ms")
 
     # Talker step time against its CU count (the complement of each ladder level).
     sweep = {}
@@ -526,10 +551,17 @@ def corun_mixed(torch, binding, W, ctx, dev, steps=4):
             binding.hs_shared_stage_forward(ctx, shape, wth, x, y, batch.seq_offsets, ctx_lens, cache.as_arg(), 96,
                                             None, ws)
 
-    def talker(n):
+    wsg = torch.empty(binding.hs_workspace_size(ts_shape, bt, bt, max_ctx), dtype=torch.uint8, device=dev)
+    tgraph = binding.DecodeGraph(ctx, ts_shape, tl, xt, yt, tcache.as_arg(), bt, 160, None, wsg)
+
+    def talker(n, graph=True):
         ev = []
         for _ in range(n):
-            binding.hs_downstream_decode_step(ctx, ts_shape, tl, xt, yt, tcache.as_arg(), kv_lens, 160, None, wst)
+            if graph:
+                tgraph.launch(kv_lens)
+            else:
+                binding.hs_downstream_decode_step(ctx, ts_shape, tl, xt, yt, tcache.as_arg(), kv_lens, 160, None,
+                                                  wst)
             e = torch.cuda.Event(enable_timing=True)
             e.record(s_dn)
             ev.append(e)
@@ -544,6 +576,12 @@ def corun_mixed(torch, binding, W, ctx, dev, steps=4):
     e1.record(s_sh)
     torch.cuda.synchronize()
     th_solo = e0.elapsed_time(e1) / steps
+    talker(2, graph=False)
+    torch.cuda.synchronize()
+    e0.record(s_dn)
+    ev = talker(10, graph=False)
+    torch.cuda.synchronize()
+    tk_solo_eager = e0.elapsed_time(ev[-1]) / 10
     talker(2)
     torch.cuda.synchronize()
     e0.record(s_dn)
@@ -586,9 +624,12 @@ def corun_mixed(torch, binding, W, ctx, dev, steps=4):
         "talker_hbm_frac_cu_scaled": round(t_bytes / (tk_ms / 1e3) / (PEAK_HBM * 160 / N_CUS), 4) if n_in else None,
         "talker_solo_hbm_frac_cu_scaled": round(t_bytes / (tk_solo / 1e3) / (PEAK_HBM * 160 / N_CUS), 4),
         "talker_steps_in_window": n_in, "thinker_flops": th_flops, "talker_bytes_per_step": int(t_bytes),
+        "talker_path": "captured decode step replayed per step",
+        "talker_eager_solo_ms_per_step": round(tk_solo_eager, 4),
     }
     log(f"[bench] mixed co-run: thinker {th_ms:.3f} ms/step (solo {th_solo:.3f}), talker {tk_ms:.3f} ms/step "
-        f"(solo {tk_solo:.3f}), {n_in} talker steps in window")
+        f"(solo {tk_solo:.3f}, eager solo {tk_solo_eager:.3f}), {n_in} talker steps in window")
+    tgraph.close()
     del wth, tl, cache, tcache
     return res
 
