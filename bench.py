@@ -111,7 +111,8 @@ def main():
     # stalled one call by ~37 ms inside a timed loop, so the collector runs
     # only between sections.
     gc.disable()
-    ladder = sorted(set(budgets + [96, 128, 160, 224, 256] + ([] if args.no_tpot else TPOT_CAPS)))
+    ladder = sorted(set(budgets + [96, 128, 160, 224, 256] + ([] if args.no_tpot else TPOT_CAPS)
+                        + ([] if args.no_corun else [N_CUS - c for c in DOWN_SWEEP])))
     ctx = binding.Context(0, budgets=ladder)
 
     # ---------------------------------------------------------------- thinker stack
@@ -247,7 +248,14 @@ def main():
     loop = None
     if not args.no_loop:
         gc.collect()
-        loop = [serving_loop(torch, binding, W, ctx, wdev, dev, p) for p in ("baseline", "joint")]
+        # B_sat: the talker's traffic share where its step stops improving with more CUs
+        # (the largest share over the complement sweep).
+        b_sat = 0.25
+        if corun is not None:
+            tb = corun["decode_bytes_per_step"]
+            b_sat = round(max(tb / (ms_ / 1e3) / PEAK_HBM for ms_ in corun["decode_ms_vs_cus"].values()), 4)
+        loop = [serving_loop(torch, binding, W, ctx, wdev, dev, p, saturation=b_sat, short_budget=sb)
+                for p, sb in (("baseline", 0), ("joint", 0), ("joint", 1024))]
 
     # ---------------------------------------------------------------- serving-loop model on measured times
     policy = None
@@ -469,7 +477,7 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
 
     # Talker step time against its CU count (the complement of each ladder level).
     sweep = {}
-    for c in (64, 128, 160, 192, 224, 240):
+    for c in DOWN_SWEEP:
         sc = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, N_CUS - c, binding.HS_ROLE_DOWN))
         decode(3, c, None, sc)
         torch.cuda.synchronize()
@@ -504,6 +512,39 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
                        "decode_steps_in_window": n_un}
     log(f"[bench] unmasked co-run: prefill {w_un:.2f} ms (solo {prefill_full_solo:.2f}), decode {d_un:.3f} ms/step "
         f"(solo {full_solo:.3f}), {n_un} steps in window")
+
+    # Pressure calibration: talker-only loops held for ~1.3 s (past one refresh of the
+    # memory-controller activity) at 64 / 128 / 256 CUs, with the AMD SMI reading polled
+    # meanwhile, against the loop's event-timed traffic share of the 8 TB/s peak.
+    calib = {}
+    for c in (64, 128, 256):
+        if c == N_CUS:
+            st, rec_s = full.cuda_stream, full
+        else:
+            rec_s = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, N_CUS - c, binding.HS_ROLE_DOWN))
+            st = None
+        decode(2, c, st, rec_s)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e0.record(rec_s)
+        t_end, polls, evs = time.perf_counter() + 1.3, [], []
+        while time.perf_counter() < t_end:
+            evs += decode(8, c, st, rec_s)
+            try:
+                polls.append(binding.hs_pressure_sample(0))
+            except binding.HorizonError:
+                pass
+            while len(evs) > 16 and not evs[-16].query():
+                time.sleep(0.0005)
+        torch.cuda.synchronize()
+        ms_ = e0.elapsed_time(evs[-1])
+        share = len(evs) * step_bytes / (ms_ / 1e3) / PEAK_HBM
+        calib[c] = {"steps": len(evs), "ms_per_step": round(ms_ / len(evs), 4), "traffic_share": round(share, 4),
+                    "umc_readings": sorted(set(round(v, 3) for v in polls)),
+                    "umc_max": round(max(polls), 3) if polls else None}
+        log(f"[bench] pressure calibration @{c} CUs: traffic share {share:.3f} of 8 TB/s, AMD SMI memory activity "
+            f"{calib[c]['umc_readings']}")
+    res["pressure_calibration"] = calib
     return res
 
 
@@ -635,6 +676,7 @@ def corun_mixed(torch, binding, W, ctx, dev, steps=4):
 
 
 TPOT_CAPS = [16, 32, 48, 64, 96, 128, 192, 256]
+DOWN_SWEEP = (64, 128, 160, 192, 224, 240)   # talker CU counts of the co-run sweep
 
 
 def thinker_decode_sweep(torch, binding, W, ctx, shape, wdev, n_layers, dev, batch=16):
@@ -733,159 +775,39 @@ def policy_model(W, shape, batch, per_budget, corun):
     return out
 
 
-def serving_loop(torch, binding, W, ctx, wdev, dev, policy, n_req=48, first_chunk=20, seed=11, load=0.6):
-    """Algorithm 1 on the GPU (measured, unlike the model): a seeded Poisson stream of requests
-    at `load` times the shared stage's capacity, half long-path.
-    Per scheduling step the temporal view picks the visible requests (joint policy), an FCFS
-    batch of up to 4096 prompt tokens is prefilled through the 4-layer thinker stack, and the
-    controller picks the CU split; while the prefill runs, talker decode steps of the active
-    long-path requests loop on the complementary stream (their cache pages addressed through a
-    per-step block table).  A short request's first response is the end of its prefill step, a
-    long request's the end of its first_chunk-th talker step (both from GPU events), each
-    measured from the request's arrival.  Baseline: every request visible, both stages unmasked
-    on the whole chip."""
-    from paper_2608_01785_amd.device_data import DeviceCache, prepare_f16, to_device, upload_weights
-    joint = policy == "joint"
-    rng = np.random.default_rng(seed)
+def serving_loop(torch, binding, W, ctx, wdev, dev, policy, n_req=48, first_chunk=20, seed=11, load=0.6,
+                 saturation=0.25, short_budget=0):
+    """Algorithm 1 on the GPU (measured, unlike the model; the loop is
+    paper_2608_01785_amd.serving.Algorithm1): a seeded Poisson stream of requests at `load`
+    times the shared stage's capacity, half long-path, prompts of 256-1024 rows through the
+    4-layer thinker stack, long-path requests decoding talker steps (16 layers, 128-512 cached
+    rows, paged cache) on the complementary stream.  Baseline: every request visible, both
+    stages unmasked on the whole chip.  The pressure signal is the talker's event-timed
+    traffic share; B_sat = `saturation`."""
+    from paper_2608_01785_amd import serving
+    from paper_2608_01785_amd.device_data import prepare_f16, to_device, upload_weights
     th, ts = W.THINKER, W.TALKER
-    tokens = rng.integers(256, 1024, size=n_req, endpoint=True).astype(int)
-    long = rng.uniform(size=n_req) < 0.5
-    kv0 = rng.integers(128, 512, size=n_req, endpoint=True).astype(np.int32)
     per_tok, talker_ms = 0.00185, 0.9       # solo ms per prompt token at 256 CUs, talker step at 128
-    arrival = np.cumsum(rng.exponential(float(np.mean(tokens)) * per_tok / load, size=n_req))
-    # Weights, inputs and caches.
+    cfg = serving.LoopConfig(policy=policy, token_budget=4096, short_budget=short_budget, first_chunk=first_chunk,
+                             saturation=saturation)
+    reqs = serving.make_requests(n_req, seed, load, per_tok, talker_ms, first_chunk)
     tl = prepare_f16(ctx, upload_weights(W.make_weights(ts, 16, W.SEEDS["talker"]["weights"]), dev))
     x_pool = to_device(W.token_rows(seed, 4096, th.hidden), dev)
-    y = torch.empty((4096, th.hidden), dtype=torch.float32, device=dev)
-    ws = torch.empty(binding.hs_workspace_size(th, 4096, n_req, 1024), dtype=torch.uint8, device=dev)
-    max_ctx = 576
-    cache = DeviceCache(16, n_req, max_ctx, ts.n_kv_heads, ts.head_dim, dev)
-    gen = torch.Generator(device=dev)
-    gen.manual_seed(seed)
-    for l in range(16):
-        for b in range(n_req):
-            if long[b]:
-                cache.fill_random(l, b, int(kv0[b]), gen)
     xt = to_device(W.token_rows(seed + 1, n_req, ts.hidden), dev)
-    yt = torch.empty((n_req, ts.hidden), dtype=torch.float32, device=dev)
-    wst = torch.empty(binding.hs_workspace_size_paged(ts, n_req, n_req, max_ctx, max_ctx), dtype=torch.uint8, device=dev)
-    # Solo estimates (ms) for deadlines and remaining times: per-token prefill and one talker step.
-    solo = tokens * per_tok + np.where(long, first_chunk * talker_ms, 0.0)
-    delta = {c: 5.0 * float(np.percentile(solo[long == c], 95)) for c in (False, True)}
-    deadline = arrival + np.array([delta[bool(l)] for l in long])
-    sched = binding.Temporal(2, 8, 2, 1.0, 4) if joint else None
-    ctrl = binding.Controller(N_CUS, N_CUS, [128, 160, 192, 224], 0.4, 0.2, 1) if joint else None
-    full = torch.cuda.Stream()
-    s_full = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, N_CUS, binding.HS_ROLE_SHARED))
-    waiting, nxt = [], 0
-    active, steps, issued = [], np.zeros(n_req, int), np.zeros(n_req, int)
-    kv = kv0.copy()
-    first = np.full(n_req, np.nan)
-    shares = []
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    start.record(s_full)
-    full.wait_event(start)
-    t0 = time.perf_counter()
-
-    def talker_step(s_shared, ids):
-        table = ids[:, None]
-        if joint and s_shared < N_CUS:
-            binding.hs_downstream_decode_step(ctx, ts, tl, xt, yt, (cache.k, cache.v, n_req, max_ctx, table),
-                                              kv[ids], N_CUS - s_shared, None, wst)
-            rec = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, s_shared, binding.HS_ROLE_DOWN))
-        else:
-            binding.hs_downstream_decode_step(ctx, ts, tl, xt, yt, (cache.k, cache.v, n_req, max_ctx, table),
-                                              kv[ids], N_CUS, full.cuda_stream, wst)
-            rec = full
-        e = torch.cuda.Event(enable_timing=True)
-        e.record(rec)
-        return e, ids
-
-    for _ in range(1000):
-        now = (time.perf_counter() - t0) * 1e3
-        while nxt < n_req and arrival[nxt] <= now:
-            waiting.append(nxt)
-            nxt += 1
-        if not waiting and not active:
-            if nxt >= n_req:
-                break
-            time.sleep(max(0.0, (arrival[nxt] - now) / 1e3))
-            continue
-        vis = [True] * len(waiting)
-        if sched is not None and waiting:
-            vis, _ = binding.hs_temporal_step(sched, now, [
-                (binding.HS_PATH_LONG if long[i] else binding.HS_PATH_SHORT, binding.HS_WORK_PREFILL,
-                 deadline[i], solo[i]) for i in waiting])
-        batch, tok = [], 0
-        for i, v in zip(waiting, vis):
-            if v and (not batch or tok + tokens[i] <= 4096):
-                batch.append(i)
-                tok += int(tokens[i])
-        s_sh = N_CUS
-        if ctrl is not None:
-            sample = 0.0
-            if active:
-                try:
-                    sample = binding.hs_pressure_sample(0)
-                except binding.HorizonError:
-                    sample = 0.2
-            s_sh = binding.hs_controller_step(ctrl, bool(active), sample).shared_cus
-        shares.append(s_sh)
-        pend = []
-        if batch:
-            off = np.concatenate([[0], np.cumsum(tokens[batch])]).astype(np.int32)
-            stream = s_full if s_sh == N_CUS else torch.cuda.ExternalStream(
-                binding.hs_context_stream(ctx, s_sh, binding.HS_ROLE_SHARED))
-            binding.hs_shared_stage_forward(ctx, th, wdev, x_pool[:tok], y[:tok], off, None, None, s_sh, None, ws)
-            p_end = torch.cuda.Event(enable_timing=True)
-            p_end.record(stream)
-            while not p_end.query():
-                cur = np.array([i for i in active if issued[i] < first_chunk], np.int32)
-                if len(cur) == 0:
-                    break
-                pend.append(talker_step(s_sh, cur))
-                kv[cur] += 1
-                issued[cur] += 1
-                if len(pend) > 3:
-                    pend[-4][0].synchronize()
-        elif active:
-            cur = np.array([i for i in active if issued[i] < first_chunk], np.int32)
-            if len(cur):
-                pend.append(talker_step(s_sh, cur))
-                kv[cur] += 1
-                issued[cur] += 1
-        torch.cuda.synchronize()
-        for i in batch:
-            waiting.remove(i)
-            if long[i]:
-                active.append(i)
-            else:
-                first[i] = start.elapsed_time(p_end)
-        for e, ids in pend:
-            for i in ids:
-                steps[i] += 1
-                if steps[i] >= first_chunk and np.isnan(first[i]):
-                    first[i] = start.elapsed_time(e)
-        active = [i for i in active if np.isnan(first[i])]
-    if sched is not None:
-        sched.close()
-    if ctrl is not None:
-        ctrl.close()
-    out = {"policy": policy, "mean_shared_cus": round(float(np.mean(shares)), 1) if shares else None,
-           "n_requests": n_req, "load": load, "rate_req_s": round(1e3 * n_req / float(arrival[-1]), 1),
-           "makespan_ms": round(float(np.nanmax(first)), 2), "unfinished": int(np.isnan(first).sum())}
-    resp = first - arrival
-    for name, flag in (("short", False), ("long", True)):
-        lat = resp[long == flag]
-        lat = lat[~np.isnan(lat)]
-        met = (first[long == flag] <= deadline[long == flag])
-        out[name] = {"n": int((long == flag).sum()), "slo_attainment": round(float(met.mean()), 4),
-                     "p50_ms": round(float(np.percentile(lat, 50)), 2) if len(lat) else None,
-                     "p95_ms": round(float(np.percentile(lat, 95)), 2) if len(lat) else None}
-    log(f"[bench] serving loop ({policy}): short p50/p95 {out['short']['p50_ms']}/{out['short']['p95_ms']} ms, "
-        f"long p50/p95 {out['long']['p50_ms']}/{out['long']['p95_ms']} ms, makespan {out['makespan_ms']} ms, "
-        f"mean shared CUs {out['mean_shared_cus']}")
+    loop = serving.Algorithm1(ctx, (th, wdev, 4), (ts, tl, 16), reqs, x_pool, cfg, max_ctx=576, x_talker=xt,
+                              device=dev)
+    try:
+        out = loop.run()
+    finally:
+        loop.close()
+    out["load"] = load
+    out["rate_req_s"] = round(1e3 * n_req / reqs[-1].arrival, 1)
+    out["saturation"] = saturation
+    out["short_budget"] = short_budget or cfg.token_budget
+    log(f"[bench] serving loop ({policy}, short budget {out['short_budget']}, B_sat {saturation:.3f}): short p50/p95 "
+        f"{out['short']['p50_ms']}/{out['short']['p95_ms']} ms (SLO {out['short']['slo_attainment']}), long p50/p95 "
+        f"{out['long']['p50_ms']}/{out['long']['p95_ms']} ms (SLO {out['long']['slo_attainment']}), makespan "
+        f"{out['makespan_ms']} ms, mean shared CUs {out['mean_shared_cus']}")
     return out
 
 
