@@ -301,3 +301,58 @@ def thinker_mixed_layout(n_chunks: int = 4, chunk: int = 2048, n_decode: int = 6
     lengths = [chunk] * n_chunks + [1] * n_decode
     ctx = [chunk * i for i in range(n_chunks)] + [decode_ctx] * n_decode
     return np.asarray(lengths, np.int32), np.asarray(ctx, np.int32)
+
+
+# ----------------------------------------------------------------------------
+# Diffusion-transformer (DiT) denoising step: the image / audio generator
+# downstream stage
+# ----------------------------------------------------------------------------
+
+
+@dataclasses.dataclass(frozen=True)
+class DitShape:
+    hidden: int
+    n_heads: int
+    head_dim: int
+    mlp: int
+    ln_eps: float = 1e-6
+
+    @property
+    def params_per_layer(self) -> int:
+        d, m = self.hidden, self.mlp
+        return 6 * d * d + 3 * d * d + d * d + 2 * m * d
+
+
+DIT_TINY = DitShape(256, 4, 64, 1024)
+DIT = DitShape(1024, 16, 64, 4096)
+
+DIT_WEIGHT_NAMES = ("w_ada", "b_ada", "w_qkv", "b_qkv", "w_o", "b_o", "w_fc1", "b_fc1", "w_fc2", "b_fc2")
+
+SEEDS["dit"] = dict(weights=1005, tokens=2005, lengths=3005, cond=4005)
+
+
+def dit_weight_shapes(s: DitShape) -> Dict[str, tuple]:
+    d, m = s.hidden, s.mlp
+    return {"w_ada": (6 * d, d), "b_ada": (6 * d,), "w_qkv": (3 * d, d), "b_qkv": (3 * d,),
+            "w_o": (d, d), "b_o": (d,), "w_fc1": (m, d), "b_fc1": (m,), "w_fc2": (d, m), "b_fc2": (d,)}
+
+
+def make_dit_weights(s: DitShape, n_layers: int, seed: int, std: float = 0.02) -> List[Dict[str, np.ndarray]]:
+    """Per-layer dict of bf16 bits, drawn layer by layer in DIT_WEIGHT_NAMES order, all N(0, std)."""
+    rng = np.random.default_rng(seed)
+    shapes = dit_weight_shapes(s)
+    layers = []
+    for _ in range(n_layers):
+        lw = {}
+        for name in DIT_WEIGHT_NAMES:
+            v = rng.standard_normal(shapes[name], dtype=np.float32)
+            v *= np.float32(std)
+            lw[name] = bf16_bits(v)
+            del v
+        layers.append(lw)
+    return layers
+
+
+def dit_cond(seed: int, n_seqs: int, hidden: int) -> np.ndarray:
+    """Per-sequence conditioning vectors, N(0, 1) float32 (the embedded timestep and class)."""
+    return np.random.default_rng(seed).standard_normal((n_seqs, hidden), dtype=np.float32)
