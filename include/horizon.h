@@ -356,6 +356,69 @@ hs_status hs_decode_graph_create(hs_context* ctx, const hs_layer_cfg* cfg, const
 hs_status hs_decode_graph_launch(hs_decode_graph* graph, const int32_t* kv_lens, const int32_t* block_table);
 hs_status hs_decode_graph_destroy(hs_decode_graph* graph);
 
+/* ------------------------------------------------------------------------
+ * Diffusion-transformer (DiT) denoising step: a second downstream workload.
+ * The paper names diffusion transformers among the output-side generators of
+ * omni models, a denoising loop distinct from autoregressive decode (§2.1,
+ * "Visual generators"), which an image-output request enters as its
+ * downstream stage (§2.2).  It gives no block formula; this is the
+ * adaLN-Zero block of the DiT design over a ragged batch of latent-token
+ * sequences, each with its own conditioning vector c_b:
+ *   (shift1, scale1, gate1, shift2, scale2, gate2) = chunk6(silu(c_b) W_ada^T + b_ada)
+ *   h = LN(x) (1 + scale1) + shift1;  x += gate1 * (MHSA(h) W_o^T + b_o)
+ *   h = LN(x) (1 + scale2) + shift2;  x += gate2 * (gelu_tanh(h W_1^T + b_1) W_2^T + b_2)
+ * LN without affine parameters, eps inside the root; attention bidirectional
+ * within each sequence (Hq = Hkv = n_heads, scale 1/sqrt(head_dim)); w_qkv
+ * rows [Q heads | K heads | V heads] with bias b_qkv; no rotary embedding.
+ * A step is the block stack; patch embedding, the final projection and the
+ * sampler's update are outside it. */
+typedef struct hs_dit_cfg {
+  int32_t hidden;     /* multiple of 256, at most 8192 */
+  int32_t n_heads;    /* n_heads * head_dim == hidden */
+  int32_t head_dim;   /* 64 or 128 */
+  int32_t mlp;        /* MLP width, multiple of 256 */
+  float ln_eps;       /* > 0 */
+} hs_dit_cfg;
+
+/* Device pointers, bf16 unless noted.  w_ada [6 hidden, hidden] and all
+ * biases are bf16 row-major; w_qkv [3 hidden, hidden], w_o [hidden, hidden],
+ * w_fc1 [mlp, hidden], w_fc2 [hidden, mlp] are bf16 row-major
+ * (format HS_WEIGHTS_BF16) or prepared by hs_convert_weights_f16
+ * (HS_WEIGHTS_F16). */
+typedef struct hs_dit_weights {
+  const void* w_ada;
+  const void* b_ada;
+  const void* w_qkv;
+  const void* b_qkv;
+  const void* w_o;
+  const void* b_o;
+  const void* w_fc1;
+  const void* b_fc1;
+  const void* w_fc2;
+  const void* b_fc2;
+  int32_t format;
+} hs_dit_weights;
+
+/* Workspace bytes of hs_dit_forward for up to max_tokens rows in max_seqs
+ * sequences. */
+hs_status hs_dit_workspace_size(const hs_dit_cfg* cfg, int32_t max_tokens, int32_t max_seqs, size_t* bytes);
+
+/* n_layers DiT blocks over a packed ragged batch, on the downstream side of a
+ * ladder level (cu_budget and stream as hs_downstream_decode_step).
+ *   x_in   bf16 [T, hidden] device, T = seq_offsets[n_seqs]; x_out fp32
+ *          [T, hidden] device (the residual stream is fp32 between blocks),
+ *          not overlapping x_in.
+ *   cond   fp32 [n_seqs, hidden] device: sequence b's conditioning vector.
+ *   seq_offsets host [n_seqs + 1], non-decreasing from 0 (empty sequences
+ *          allowed); copied before the call returns.
+ * MFMA operands are fp16 (activations rounded once per GEMM input) with fp32
+ * accumulation; LayerNorm statistics, the modulation and the residual
+ * branches are fp32.  Errors as hs_shared_stage_forward (validation enqueues
+ * nothing). */
+hs_status hs_dit_forward(hs_context* ctx, const hs_dit_cfg* cfg, const hs_dit_weights* w, int32_t n_layers,
+                         const void* x_in, void* x_out, const float* cond, const int32_t* seq_offsets,
+                         int32_t n_seqs, int32_t cu_budget, void* stream, void* workspace, size_t ws_bytes);
+
 /* Topology probe: launches n_groups work-groups on `stream` (NULL = the
  * context's full-budget stream); each writes, into out_ids (device, uint32
  * [n_groups * 4]): XCC id, shader engine, CU id, and the low 32 bits of the
@@ -388,7 +451,11 @@ enum {
   HS_KERNEL_GATE_UP = 5,      /* gate/up projection + SwiGLU */
   HS_KERNEL_DOWN = 6,         /* down projection + residual */
   HS_KERNEL_ROPE_TABLE = 7,
-  HS_KERNEL_KINDS = 8
+  HS_KERNEL_MODULATION = 8,   /* DiT: silu(c) and the per-layer adaLN modulation */
+  HS_KERNEL_LN_MOD = 9,       /* DiT: modulated LayerNorm */
+  HS_KERNEL_MLP_UP = 10,      /* DiT: first MLP projection + bias + GELU */
+  HS_KERNEL_MLP_DOWN = 11,    /* DiT: second MLP projection + bias + gated residual */
+  HS_KERNEL_KINDS = 12
 };
 
 hs_status hs_timing_enable(hs_context* ctx, int32_t enable);

@@ -25,7 +25,7 @@ SYMBOLS = (
     "hs_context_destroy", "hs_workspace_size", "hs_workspace_size_paged", "hs_shared_stage_forward",
     "hs_shared_stage_forward_mrope", "hs_downstream_decode_step_mrope", "hs_downstream_decode_step",
     "hs_downstream_decode_step_noalloc", "hs_decode_graph_create", "hs_decode_graph_launch",
-    "hs_decode_graph_destroy",
+    "hs_decode_graph_destroy", "hs_dit_workspace_size", "hs_dit_forward",
     "hs_probe_hw_ids", "hs_timing_enable", "hs_timing_read", "hs_timing_read_clock", "hs_convert_weights_f16",
     "hs_controller_create", "hs_controller_step", "hs_controller_destroy", "hs_pressure_sample",
     "hs_temporal_create", "hs_temporal_step", "hs_temporal_destroy",
@@ -33,7 +33,7 @@ SYMBOLS = (
 HS_WEIGHTS_BF16, HS_WEIGHTS_F16 = 0, 1
 
 KERNEL_KINDS = {"rmsnorm": 0, "qkv": 1, "attention": 2, "decode_attn": 3, "o_proj": 4, "gate_up": 5,
-                "down": 6, "rope_table": 7}
+                "down": 6, "rope_table": 7, "modulation": 8, "ln_mod": 9, "mlp_up": 10, "mlp_down": 11}
 
 
 class LayerCfg(ctypes.Structure):
@@ -49,6 +49,21 @@ class LayerCfg(ctypes.Structure):
 
 
 MATRICES = ("w_qkv", "w_o", "w_gate_up", "w_down")
+DIT_MATRICES = ("w_qkv", "w_o", "w_fc1", "w_fc2")   # the DiT projections fp16 preparation applies to
+DIT_FIELDS = ("w_ada", "b_ada", "w_qkv", "b_qkv", "w_o", "b_o", "w_fc1", "b_fc1", "w_fc2", "b_fc2")
+
+
+class DitCfg(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("mlp", ctypes.c_int32), ("ln_eps", ctypes.c_float)]
+
+    @classmethod
+    def of(cls, s) -> "DitCfg":
+        return cls(s.hidden, s.n_heads, s.head_dim, s.mlp, s.ln_eps)
+
+
+class DitWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in DIT_FIELDS] + [("format", ctypes.c_int32)]
 
 
 class LayerWeights(ctypes.Structure):
@@ -146,6 +161,9 @@ def lib() -> ctypes.CDLL:
                                        ctypes.POINTER(KvCache), i32, i32, vp, vp, ctypes.c_size_t,
                                        ctypes.POINTER(vp)],
             "hs_decode_graph_launch": [vp, i32p, i32p],
+            "hs_dit_workspace_size": [ctypes.POINTER(DitCfg), i32, i32, ctypes.POINTER(ctypes.c_size_t)],
+            "hs_dit_forward": [vp, ctypes.POINTER(DitCfg), ctypes.POINTER(DitWeights), i32, vp, vp, vp, i32p, i32,
+                               i32, vp, vp, ctypes.c_size_t],
             "hs_decode_graph_destroy": [vp],
             "hs_probe_hw_ids": [vp, vp, i32, vp],
             "hs_timing_enable": [vp, i32],
@@ -515,6 +533,33 @@ class DecodeGraph:
             self.close()
         except Exception:
             pass
+
+
+def hs_dit_workspace_size(cfg, max_tokens: int, max_seqs: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().hs_dit_workspace_size(ctypes.byref(DitCfg.of(cfg)), max_tokens, max_seqs, ctypes.byref(n)))
+    return int(n.value)
+
+
+def _dit_weights_array(weights):
+    arr = (DitWeights * len(weights))()
+    for i, w in enumerate(weights):
+        for name in DIT_FIELDS:
+            setattr(arr[i], name, _ptr(w[name]))
+        arr[i].format = int(w.get("format", HS_WEIGHTS_BF16))
+    return arr
+
+
+def hs_dit_forward(ctx: Context, cfg, weights, x_in, x_out, cond, seq_offsets, cu_budget: int, stream=None,
+                   workspace=None, ws_bytes: Optional[int] = None) -> None:
+    """DiT blocks over a packed ragged batch on the downstream side (cu_budget = its CUs)."""
+    warr = _dit_weights_array(weights)
+    off = _i32_array(seq_offsets)
+    if ws_bytes is None:
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().hs_dit_forward(ctx.handle, ctypes.byref(DitCfg.of(cfg)), warr, len(weights), _ptr(x_in),
+                                _ptr(x_out), _ptr(cond), off, len(off) - 1, cu_budget, _ptr(stream),
+                                _ptr(workspace), ws_bytes))
 
 
 def hs_probe_hw_ids(ctx: Context, stream, n_groups: int, out_ids) -> None:

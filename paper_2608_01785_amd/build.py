@@ -19,7 +19,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libhorizon.so")
 
 ARCH = "gfx950"
-HIP_SOURCES = ["gemm.hip", "gemm_skinny.hip", "attention.hip", "misc.hip", "noalloc.hip"]
+HIP_SOURCES = ["gemm.hip", "gemm_skinny.hip", "attention.hip", "misc.hip", "noalloc.hip", "dit.hip"]
 HOST_SOURCES = ["plan.cpp", "runtime.cpp", "controller.cpp", "temporal.cpp", "pressure.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}"]

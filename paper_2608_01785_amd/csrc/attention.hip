@@ -79,12 +79,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
   const int64_t head_off = int64_t(g) * a.kv_head_stride;
   const int kv_row_stride = DH;
 
-  const int n_keys = ctx + min(q0 + BQ, len);      // keys any query of the block may see
+  // Causal: row i sees keys 0 .. ctx + i.  Bidirectional: every row sees all
+  // ctx + len keys, which is the causal rule applied as if every row sat at
+  // the sequence's last position.
+  const bool bidir = a.bidirectional != 0;
+  const int n_keys = ctx + (bidir ? len : min(q0 + BQ, len));  // keys any query of the block may see
   const int n_tiles = (n_keys + BKV - 1) / BKV;
   const int qi = min(q0 + wave * 32 + fr, len - 1);  // clamped query row (tail lanes recompute the last row)
-  const int qpos = ctx + qi;
-  const int wave_last = ctx + min(q0 + wave * 32 + 31, len - 1);  // last key this wave needs
-  const int wave_first = ctx + min(q0 + wave * 32, len - 1);      // position of the wave's first row
+  const int qpos = bidir ? ctx + len - 1 : ctx + qi;
+  const int wave_last = bidir ? ctx + len - 1 : ctx + min(q0 + wave * 32 + 31, len - 1);  // last key needed
+  const int wave_first = bidir ? ctx + len - 1 : ctx + min(q0 + wave * 32, len - 1);  // first row's position
 
   // Query fragments: B operand of S^T = K Q^T, lane = query, k = head dimension.
   u32x4 qf[DH / 16];

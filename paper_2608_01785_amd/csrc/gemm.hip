@@ -355,6 +355,52 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
             const f32x4 v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
             *reinterpret_cast<f32x4*>(orow + n) = v;
           }
+      } else if constexpr (EPI == EPI_GATED) {
+        // out (fp32) = resid + gate_seq(m) * (products + bias): the adaLN-Zero residual branch.
+        const int n_base = tile_n * BN + wn * 128 + 4 * fh;
+        float* orow = a.out_f32 + int64_t(m) * a.ldo;
+        const float* grow = a.gate + int64_t(a.row_seq[m]) * a.gate_stride;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int n = n_base + i * 32 + 8 * g;
+            float b4[4], r4[4];
+            load_bf16x4(a.bias + n, b4);
+            if (a.resid_f32) {
+              const f32x4 r = *reinterpret_cast<const f32x4*>(a.resid_f32 + int64_t(m) * a.ldo + n);
+              r4[0] = r[0];
+              r4[1] = r[1];
+              r4[2] = r[2];
+              r4[3] = r[3];
+            } else {
+              load_bf16x4(a.resid + int64_t(m) * a.ldo + n, r4);
+            }
+            const f32x4 gt = *reinterpret_cast<const f32x4*>(grow + n);
+            f32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = r4[e] + gt[e] * (acc[i][j][4 * g + e] + b4[e]);
+            *reinterpret_cast<f32x4*>(orow + n) = v;
+          }
+      } else if constexpr (EPI == EPI_GELU) {
+        // out (fp16) = gelu_tanh(products + bias); 0.5 z (1 + tanh(u)) = z / (1 + exp(-2u)).
+        const int n_base = tile_n * BN + wn * 128 + 4 * fh;
+        uint16_t* orow = a.out + int64_t(m) * a.ldo;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int n = n_base + i * 32 + 8 * g;
+            float b4[4], v[4];
+            load_bf16x4(a.bias + n, b4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float z = acc[i][j][4 * g + e] + b4[e];
+              const float u = 0.7978845608028654f * (z + 0.044715f * z * z * z);
+              v[e] = z / (1.0f + __expf(-2.0f * u));
+            }
+            store_h4(orow + n, v[0], v[1], v[2], v[3]);
+          }
       } else if constexpr (EPI == EPI_SWIGLU) {
         const int c_base = tile_n * 128 + wn * 64 + 4 * fh;
 #pragma unroll
@@ -379,7 +425,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
           for (int g = 0; g < 4; ++g) {
             const int d = dsub + 8 * g + 4 * fh;  // < DH / 2
             // Pairs d .. d + 3 share one RoPE section (sections are multiples of 4 pairs).
-            const float2* rt = a.rope + int64_t(rope_pos(a, m, d)) * (DH / 2);
+            const float2* rt = a.rope ? a.rope + int64_t(rope_pos(a, m, d)) * (DH / 2) : nullptr;
             float lo[4], hi[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -398,11 +444,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
             }
             if (head < a.hq + a.hkv) {
               float rl[4], rh[4];
+              if (a.rope) {
 #pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const float2 cs = rt[d + e];
-                rl[e] = lo[e] * cs.x - hi[e] * cs.y;
-                rh[e] = hi[e] * cs.x + lo[e] * cs.y;
+                for (int e = 0; e < 4; ++e) {
+                  const float2 cs = rt[d + e];
+                  rl[e] = lo[e] * cs.x - hi[e] * cs.y;
+                  rh[e] = hi[e] * cs.x + lo[e] * cs.y;
+                }
+              } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  rl[e] = lo[e];
+                  rh[e] = hi[e];
+                }
               }
               uint16_t* dst = (head < a.hq)
                                   ? a.q + (int64_t(m) * a.hq + head) * DH
@@ -451,6 +505,8 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, int max_blocks, hipStream_t s
   switch (epi) {
     case EPI_RESID: return launch_one<EPI_RESID, 128>(a, max_blocks, s);
     case EPI_SWIGLU: return launch_one<EPI_SWIGLU, 128>(a, max_blocks, s);
+    case EPI_GATED: return launch_one<EPI_GATED, 128>(a, max_blocks, s);
+    case EPI_GELU: return launch_one<EPI_GELU, 128>(a, max_blocks, s);
     case EPI_QKV:
       return a.dh == 64 ? launch_one<EPI_QKV, 64>(a, max_blocks, s)
                         : launch_one<EPI_QKV, 128>(a, max_blocks, s);

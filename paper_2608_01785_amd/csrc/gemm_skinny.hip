@@ -41,6 +41,7 @@ hipError_t launch_ns(const GemmArgs& a_in, int strips, hipStream_t s) {
 
 bool skinny_supported(int epi, const GemmArgs& a) {
   if (a.M <= 0 || a.M > kSkinnyMaxRows || a.K % BK != 0) return false;
+  if (epi == EPI_GATED || epi == EPI_GELU || (epi == EPI_QKV && !a.rope)) return false;  // large GEMM only
   if (epi == EPI_QKV) return a.dh == 64 || a.dh == 128;
   return true;
 }

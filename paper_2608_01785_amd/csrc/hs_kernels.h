@@ -13,6 +13,8 @@ enum Epilogue : int {
   EPI_RESID = 1,   // out_f32 = resid + acc
   EPI_SWIGLU = 2,  // out = silu(gate) * up, gate/up rows gathered from [gate | up]
   EPI_QKV = 3,     // RoPE on Q and K heads, Q -> q buffer, K/V -> key/value store
+  EPI_GATED = 4,   // out_f32 = resid + gate[seq(m)] * (acc + bias)   (large GEMM only)
+  EPI_GELU = 5,    // out = gelu_tanh(acc + bias), fp16                  (large GEMM only)
 };
 
 struct GemmArgs {
@@ -37,8 +39,11 @@ struct GemmArgs {
   const int64_t* k_off;   // [M]
   const int64_t* v_off;   // [M]
   int64_t kv_head_stride; // elements between the heads of one slot (max_ctx * dh)
-  const float2* rope;     // [max_pos, dh / 2] (cos, sin)
-  const uint16_t* bias;   // QKV: bf16 [(hq + 2 hkv) * dh] added before RoPE, or null
+  const float2* rope;     // [max_pos, dh / 2] (cos, sin); null: no rotation (the large GEMM only)
+  const uint16_t* bias;   // QKV: bf16 [(hq + 2 hkv) * dh] added before RoPE, or null; GATED / GELU: bf16 [N]
+  const float* gate;      // GATED: row m scales by gate[row_seq[m] * gate_stride + n]
+  int gate_stride;
+  const int32_t* row_seq; // GATED: sequence of each row
   int hq, hkv, dh;
   // Skinny GEMM split along K: fp32 partial sums and one arrival counter per
   // weight strip (zero on entry, left at zero on exit).
@@ -90,6 +95,7 @@ struct AttnArgs {
   int64_t kv_head_stride;
   int hq, hkv, dh;
   float scale_log2;         // log2(e) / sqrt(dh)
+  int bidirectional;        // 0: causal (bottom-right); 1: every row sees every key of its sequence
   uint64_t* clock;          // timing mode: four counters of the launch (see LaunchClock), or null
 };
 
@@ -135,6 +141,18 @@ hipError_t launch_rmsnorm(const uint16_t* x, const float* x_f32, const uint16_t*
                           int d, float eps, int k8_rows, int max_blocks, hipStream_t s);
 
 hipError_t launch_rope_table(float2* tab, int max_pos, int dh, float base, hipStream_t s);
+
+// Diffusion-transformer pieces (dit.hip).  s = silu(c) for B x d conditioning
+// values (fp32); mod[b][j] = bias[j] + sum_k s[b][k] W[j][k] for the 6d
+// modulation rows of one layer (W bf16 [6d, d] row-major, bias bf16 [6d]).
+hipError_t launch_silu_rows(const float* c, float* s, int n, hipStream_t st);
+hipError_t launch_dit_modulation(const uint16_t* w, const uint16_t* bias, const float* s, float* mod, int n_seqs,
+                                 int d, hipStream_t st);
+// y[t] = fp16(LN(x[t]) * (1 + mod[b][scale_off + j]) + mod[b][shift_off + j]),
+// b = row_seq[t]; x bf16 (x_f32 null) or fp32; mod rows of 6d floats.
+hipError_t launch_ln_modulate(const uint16_t* x, const float* x_f32, const float* mod, const int32_t* row_seq,
+                              uint16_t* y, int rows, int d, float eps, int shift_off, int scale_off, int max_blocks,
+                              hipStream_t st);
 
 hipError_t launch_probe(uint32_t* out, int n_groups, hipStream_t s);
 

@@ -174,6 +174,7 @@ static size_t meta_bytes(int32_t T, int32_t B, int64_t pages, int64_t att, int32
   size_t s = 0;
   s += align_up(size_t(T) * 4, 16);       // pos
   s += align_up(size_t(T) * 12, 16);      // pos3
+  s += align_up(size_t(T) * 4, 16);       // row_seq
   s += align_up(size_t(T) * 8, 16) * 2;   // k_off, v_off
   s += align_up(size_t(B) * 4, 16) * 4;   // seq_start, seq_len, seq_ctx, seq_page0
   s += align_up(size_t(pages) * 8, 16);   // page_base
@@ -261,7 +262,8 @@ hs_status check_block_table(const int32_t* table, int32_t pps, int32_t n_slots, 
 }
 
 hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* ctx, int32_t B,
-                     const KvPlacement& kv, Plan* out, const int32_t* positions3, const PlanCapacity* cap) {
+                     const KvPlacement& kv, Plan* out, const int32_t* positions3, const PlanCapacity* cap,
+                     bool bidirectional) {
   Plan& P = *out;
   hs_status st = validate_batch(off, ctx, B, &P.T, &P.max_pos);
   if (st != HS_OK) return st;
@@ -281,7 +283,7 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
       dec_seq.push_back(b);
     } else {
       for (int32_t q0 = 0; q0 < len; q0 += kAttnBlockQ)
-        att.push_back({b, q0, cx + std::min(q0 + kAttnBlockQ, len)});
+        att.push_back({b, q0, cx + (bidirectional ? len : std::min(q0 + kAttnBlockQ, len))});
     }
   }
   std::stable_sort(att.begin(), att.end(), [](const Item& x, const Item& y) { return x.keys > y.keys; });
@@ -300,6 +302,7 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   };
   P.pos = take(size_t(T) * 4);
   P.pos3 = positions3 ? take(size_t(T) * 12) : 0;
+  P.row_seq = take(size_t(T) * 4);
   P.k_off = take(size_t(T) * 8);
   P.v_off = take(size_t(T) * 8);
   P.seq_start = take(size_t(B) * 4);
@@ -370,6 +373,7 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
       page += 1;
     }
     for (int32_t t = off[b]; t < off[b + 1]; ++t) {
+      i32(P.row_seq)[t] = b;
       const int64_t pos = cx + (t - off[b]);
       const int64_t base = pages[pos / slot_ctx], i = pos % slot_ctx;
       i32(P.pos)[t] = int32_t(pos);

@@ -79,6 +79,7 @@ struct Plan {
   // byte offsets inside image
   size_t pos = 0, k_off = 0, v_off = 0;
   size_t pos3 = 0;  // [3][T] multimodal RoPE positions (filled only when given)
+  size_t row_seq = 0;  // [T] int32: sequence of each packed row
   size_t seq_start = 0, seq_len = 0, seq_ctx = 0;
   size_t seq_page0 = 0;  // [B] int32: index of the sequence's first page in page_base
   size_t page_base = 0;  // [n_pages] int64: element offset of a page's position 0, head 0
@@ -123,6 +124,6 @@ hs_status check_block_table(const int32_t* table, int32_t pages_per_seq, int32_t
 
 hs_status build_plan(const hs_layer_cfg& c, const int32_t* seq_offsets, const int32_t* ctx_lens,
                      int32_t n_seqs, const KvPlacement& kv, Plan* out, const int32_t* positions3 = nullptr,
-                     const PlanCapacity* cap = nullptr);
+                     const PlanCapacity* cap = nullptr, bool bidirectional = false);
 
 }  // namespace hs

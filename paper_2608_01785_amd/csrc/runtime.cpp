@@ -4,6 +4,7 @@
 #include <hip/hip_ext.h>
 #include <string.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "hs_kernels.h"
@@ -933,6 +934,263 @@ hs_status hs_decode_graph_destroy(hs_decode_graph* g) {
     hipGraphExecDestroy(g->exec);
   }
   delete g;
+  return HS_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+hs_status validate_dit_cfg(const hs_dit_cfg* c) {
+  if (!c) return hs::fail(HS_ERR_INVALID_ARG, "DiT config is null");
+  if (c->hidden <= 0 || c->hidden % 256 != 0 || c->hidden > 8192)
+    return hs::fail(HS_ERR_UNSUPPORTED, "hidden %d must be a positive multiple of 256, at most 8192", c->hidden);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return hs::fail(HS_ERR_UNSUPPORTED, "head_dim %d must be 64 or 128", c->head_dim);
+  if (c->n_heads <= 0 || c->n_heads * c->head_dim != c->hidden)
+    return hs::fail(HS_ERR_INVALID_ARG, "n_heads %d * head_dim %d must equal hidden %d", c->n_heads, c->head_dim,
+                    c->hidden);
+  if (c->mlp <= 0 || c->mlp % 256 != 0)
+    return hs::fail(HS_ERR_UNSUPPORTED, "mlp %d must be a positive multiple of 256", c->mlp);
+  if (!(c->ln_eps > 0.0f)) return hs::fail(HS_ERR_INVALID_ARG, "ln_eps must be > 0");
+  return HS_OK;
+}
+
+// The decoder-layer shape the shared buffers and checks are sized by: the
+// MLP width in the FFN's place, Hq = Hkv.
+hs_layer_cfg dit_as_layer(const hs_dit_cfg& c) {
+  hs_layer_cfg l{};
+  l.hidden = c.hidden;
+  l.n_q_heads = c.n_heads;
+  l.n_kv_heads = c.n_heads;
+  l.head_dim = c.head_dim;
+  l.ffn = c.mlp;
+  l.rms_eps = c.ln_eps;
+  l.rope_base = 10000.0f;
+  return l;
+}
+
+struct DitLayout {
+  hs::WsLayout base;
+  size_t silu, mod, total;
+};
+
+DitLayout dit_layout(const hs_dit_cfg& c, int32_t T, int32_t B, int32_t max_pos) {
+  DitLayout L;
+  L.base = hs::ws_layout(dit_as_layer(c), T, B, max_pos, 0, true);
+  L.silu = hs::align_up(L.base.total, hs::kAlign);
+  L.mod = hs::align_up(L.silu + size_t(B) * c.hidden * 4, hs::kAlign);
+  L.total = hs::align_up(L.mod + size_t(B) * 6 * c.hidden * 4, hs::kAlign);
+  return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+hs_status hs_dit_workspace_size(const hs_dit_cfg* cfg, int32_t max_tokens, int32_t max_seqs, size_t* bytes) {
+  hs::clear_error();
+  hs_status st = validate_dit_cfg(cfg);
+  if (st != HS_OK) return st;
+  if (!bytes) return hs::fail(HS_ERR_INVALID_ARG, "bytes output is null");
+  if (max_tokens < 0 || max_seqs < 1) return hs::fail(HS_ERR_INVALID_ARG, "max_tokens %d, max_seqs %d", max_tokens,
+                                                      max_seqs);
+  *bytes = dit_layout(*cfg, max_tokens, max_seqs, std::max(max_tokens, 1)).total;
+  return HS_OK;
+}
+
+hs_status hs_dit_forward(hs_context* ctx, const hs_dit_cfg* cfg, const hs_dit_weights* w, int32_t n_layers,
+                         const void* x_in, void* x_out, const float* cond, const int32_t* seq_offsets,
+                         int32_t n_seqs, int32_t cu_budget, void* stream, void* workspace, size_t ws_bytes) {
+  hs::clear_error();
+  hs_status st = validate_dit_cfg(cfg);
+  if (st != HS_OK) return st;
+  if (!w || n_layers < 1) return hs::fail(HS_ERR_INVALID_ARG, "weights missing or n_layers %d < 1", n_layers);
+  for (int l = 0; l < n_layers; ++l) {
+    const hs_dit_weights& lw = w[l];
+    if (!lw.w_ada || !lw.b_ada || !lw.w_qkv || !lw.b_qkv || !lw.w_o || !lw.b_o || !lw.w_fc1 || !lw.b_fc1 ||
+        !lw.w_fc2 || !lw.b_fc2)
+      return hs::fail(HS_ERR_INVALID_ARG, "block %d has a null weight pointer", l);
+    if (lw.format != HS_WEIGHTS_BF16 && lw.format != HS_WEIGHTS_F16)
+      return hs::fail(HS_ERR_INVALID_ARG, "block %d has weight format %d", l, lw.format);
+  }
+  if (!x_in || !x_out || !cond) return hs::fail(HS_ERR_INVALID_ARG, "x_in / x_out / cond is null");
+  if (x_in == x_out) return hs::fail(HS_ERR_INVALID_ARG, "x_in and x_out must not alias");
+  int32_t T = 0, max_pos = 0;
+  st = hs::validate_batch(seq_offsets, nullptr, n_seqs, &T, &max_pos);
+  if (st != HS_OK) return st;
+  const hs_layer_cfg lcfg = dit_as_layer(*cfg);
+  st = hs::check_32bit_extents(lcfg, T, 0);
+  if (st != HS_OK) return st;
+  if (int64_t(6) * cfg->hidden * cfg->hidden * 2 >= (int64_t(1) << 32))
+    return hs::fail(HS_ERR_UNSUPPORTED, "w_ada of %d x %d exceeds 2^32 bytes", 6 * cfg->hidden, cfg->hidden);
+  if (!ctx) return hs::fail(HS_ERR_INVALID_ARG, "context is null");
+  hipStream_t s = nullptr;
+  st = resolve_stream(ctx, cu_budget, HS_ROLE_DOWN, stream, &s);
+  if (st != HS_OK) return st;
+  if (!workspace) return hs::fail(HS_ERR_WORKSPACE, "workspace is null");
+  const DitLayout DL = dit_layout(*cfg, T, n_seqs, std::max(max_pos, 1));
+  if (ws_bytes < DL.total) return hs::fail(HS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, DL.total);
+  const hs::WsLayout& lay = DL.base;
+  hs::KvPlacement place;
+  place.packed_ctx = lay.packed_ctx;
+  hs::Plan plan;
+  st = hs::build_plan(lcfg, seq_offsets, nullptr, n_seqs, place, &plan, nullptr, nullptr, true);
+  if (st != HS_OK) return st;
+  if (plan.image.size() > lay.meta_bytes) return hs::fail(HS_ERR_INTERNAL, "metadata image exceeds its region");
+
+  HIP_TRY(hipSetDevice(ctx->device));
+  (void)hipGetLastError();
+  st = stage_metadata(ctx, plan, at<void>(workspace, lay.meta), s);
+  if (st != HS_OK) return st;
+  if (T == 0) return HS_OK;
+
+  const int d = cfg->hidden, H = cfg->n_heads, dh = cfg->head_dim, mlp = cfg->mlp;
+  void* ws = workspace;
+  uint8_t* meta = at<uint8_t>(ws, lay.meta);
+  const int32_t* row_seq = reinterpret_cast<const int32_t*>(meta + plan.row_seq);
+  uint16_t* n_buf = at<uint16_t>(ws, lay.n);
+  uint16_t* q_buf = at<uint16_t>(ws, lay.q);
+  uint16_t* o_buf = at<uint16_t>(ws, lay.o);
+  float* h_buf = at<float>(ws, lay.h);
+  uint16_t* a_buf = at<uint16_t>(ws, lay.a);
+  float* xtmp = at<float>(ws, lay.xtmp);
+  float* s_buf = at<float>(ws, DL.silu);
+  float* mod = at<float>(ws, DL.mod);
+  uint16_t* kstore = at<uint16_t>(ws, lay.kpack);
+  uint16_t* vstore = at<uint16_t>(ws, lay.vpack);
+  const int grid_cap = cu_budget;
+  const float scale_log2 = 1.4426950408889634f / sqrtf(float(dh));
+
+  TIMED(HS_KERNEL_MODULATION, hs::launch_silu_rows(cond, s_buf, n_seqs * d, s));
+  const uint16_t* x_cur = static_cast<const uint16_t*>(x_in);
+  const float* x_cur_f32 = nullptr;
+  for (int l = 0; l < n_layers; ++l) {
+    const int remaining = n_layers - 1 - l;
+    float* x_next = (remaining % 2 == 0) ? static_cast<float*>(x_out) : xtmp;
+    const bool f16 = w[l].format == HS_WEIGHTS_F16;
+    TIMED(HS_KERNEL_MODULATION, hs::launch_dit_modulation(static_cast<const uint16_t*>(w[l].w_ada),
+                                                          static_cast<const uint16_t*>(w[l].b_ada), s_buf, mod,
+                                                          n_seqs, d, s));
+    TIMED(HS_KERNEL_LN_MOD, hs::launch_ln_modulate(x_cur, x_cur_f32, mod, row_seq, n_buf, T, d, cfg->ln_eps, 0, d,
+                                                   4 * cu_budget, s));
+    hs::GemmArgs g{};
+    g.A = n_buf;
+    g.W = static_cast<const uint16_t*>(w[l].w_qkv);
+    g.w_f16 = f16;
+    g.M = T;
+    g.K = d;
+    g.n_tiles_n = 3 * d / 256;
+    g.q = q_buf;
+    g.kstore = kstore;
+    g.vstore = vstore;
+    g.pos = reinterpret_cast<const int32_t*>(meta + plan.pos);
+    g.sec1 = g.sec2 = dh / 2;
+    g.k_off = reinterpret_cast<const int64_t*>(meta + plan.k_off);
+    g.v_off = reinterpret_cast<const int64_t*>(meta + plan.v_off);
+    g.kv_head_stride = plan.kv_head_stride;
+    g.rope = nullptr;  // positions enter with the token embeddings
+    g.bias = static_cast<const uint16_t*>(w[l].b_qkv);
+    g.hq = H;
+    g.hkv = H;
+    g.dh = dh;
+    g.clock = clock_slot(ctx);
+    TIMED(HS_KERNEL_QKV, hs::launch_gemm(hs::EPI_QKV, g, grid_cap, s));
+
+    hs::AttnArgs at_args{};
+    at_args.q = q_buf;
+    at_args.kstore = kstore;
+    at_args.vstore = vstore;
+    at_args.o = o_buf;
+    at_args.items = reinterpret_cast<const int32_t*>(meta + plan.att_items);
+    at_args.n_items = plan.n_att_items;
+    at_args.seq_start = reinterpret_cast<const int32_t*>(meta + plan.seq_start);
+    at_args.seq_len = reinterpret_cast<const int32_t*>(meta + plan.seq_len);
+    at_args.seq_ctx = reinterpret_cast<const int32_t*>(meta + plan.seq_ctx);
+    at_args.seq_page0 = reinterpret_cast<const int32_t*>(meta + plan.seq_page0);
+    at_args.page_base = reinterpret_cast<const int64_t*>(meta + plan.page_base);
+    at_args.page_keys = plan.page_keys;
+    at_args.kv_head_stride = plan.kv_head_stride;
+    at_args.hq = H;
+    at_args.hkv = H;
+    at_args.dh = dh;
+    at_args.scale_log2 = scale_log2;
+    at_args.bidirectional = 1;
+    at_args.clock = clock_slot(ctx);
+    if (plan.n_att_items > 0) TIMED(HS_KERNEL_ATTENTION, hs::launch_attention(at_args, s));
+    if (plan.n_dec_rows > 0) {
+      // One-row sequences: attention over the row itself.
+      hs::DecodeAttnArgs da{};
+      da.q = q_buf;
+      da.kstore = kstore;
+      da.vstore = vstore;
+      da.o = o_buf;
+      da.items = reinterpret_cast<const hs::DecItem*>(meta + plan.dec_items);
+      da.n_items = plan.n_dec_items;
+      da.part = lay.dec_part_bytes ? at<float>(ws, lay.dec_part) : nullptr;
+      da.counters = reinterpret_cast<int32_t*>(meta + plan.dec_count);
+      da.kv_head_stride = plan.kv_head_stride;
+      da.page_keys = plan.page_keys;
+      da.unit_keys = plan.unit_keys;
+      da.hq = H;
+      da.hkv = H;
+      da.dh = dh;
+      da.scale_log2 = scale_log2;
+      TIMED(HS_KERNEL_DECODE_ATTN, hs::launch_decode_attention(da, s));
+    }
+
+    hs::GemmArgs go{};
+    go.A = o_buf;
+    go.W = static_cast<const uint16_t*>(w[l].w_o);
+    go.w_f16 = f16;
+    go.M = T;
+    go.K = d;
+    go.n_tiles_n = d / 256;
+    go.out_f32 = h_buf;
+    go.ldo = d;
+    go.resid = x_cur;
+    go.resid_f32 = x_cur_f32;
+    go.bias = static_cast<const uint16_t*>(w[l].b_o);
+    go.gate = mod + 2 * d;
+    go.gate_stride = 6 * d;
+    go.row_seq = row_seq;
+    go.clock = clock_slot(ctx);
+    TIMED(HS_KERNEL_O_PROJ, hs::launch_gemm(hs::EPI_GATED, go, grid_cap, s));
+
+    TIMED(HS_KERNEL_LN_MOD, hs::launch_ln_modulate(nullptr, h_buf, mod, row_seq, n_buf, T, d, cfg->ln_eps, 3 * d,
+                                                   4 * d, 4 * cu_budget, s));
+    hs::GemmArgs g1{};
+    g1.A = n_buf;
+    g1.W = static_cast<const uint16_t*>(w[l].w_fc1);
+    g1.w_f16 = f16;
+    g1.M = T;
+    g1.K = d;
+    g1.n_tiles_n = mlp / 256;
+    g1.out = a_buf;
+    g1.ldo = mlp;
+    g1.bias = static_cast<const uint16_t*>(w[l].b_fc1);
+    g1.clock = clock_slot(ctx);
+    TIMED(HS_KERNEL_MLP_UP, hs::launch_gemm(hs::EPI_GELU, g1, grid_cap, s));
+
+    hs::GemmArgs g2{};
+    g2.A = a_buf;
+    g2.W = static_cast<const uint16_t*>(w[l].w_fc2);
+    g2.w_f16 = f16;
+    g2.M = T;
+    g2.K = mlp;
+    g2.n_tiles_n = d / 256;
+    g2.out_f32 = x_next;
+    g2.ldo = d;
+    g2.resid_f32 = h_buf;
+    g2.bias = static_cast<const uint16_t*>(w[l].b_fc2);
+    g2.gate = mod + 5 * d;
+    g2.gate_stride = 6 * d;
+    g2.row_seq = row_seq;
+    g2.clock = clock_slot(ctx);
+    TIMED(HS_KERNEL_MLP_DOWN, hs::launch_gemm(hs::EPI_GATED, g2, grid_cap, s));
+    x_cur = nullptr;
+    x_cur_f32 = x_next;
+  }
   return HS_OK;
 }
 

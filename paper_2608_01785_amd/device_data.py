@@ -146,3 +146,21 @@ class PagedCache(DeviceCache):
             vs.append(v)
             p = j * P + hi
         return np.concatenate(ks), np.concatenate(vs)
+
+
+def prepare_dit_f16(ctx, layers_dev: List[Dict[str, torch.Tensor]]) -> List[Dict[str, object]]:
+    """The DiT projections (w_qkv, w_o, w_fc1, w_fc2) as fp16 panel-major copies; the
+    modulation matrix and the biases stay bf16."""
+    from paper_2608_01785_amd import binding
+    out = []
+    for lw in layers_dev:
+        d = {k: v for k, v in lw.items() if k not in binding.DIT_MATRICES}
+        d["format"] = binding.HS_WEIGHTS_F16
+        for name in binding.DIT_MATRICES:
+            n, k = lw[name].shape
+            dst = torch.empty((k // 32, n, 32), dtype=torch.float16, device=lw[name].device)
+            binding.hs_convert_weights_f16(ctx, lw[name], dst, n, k)
+            d[name] = dst
+        out.append(d)
+    torch.cuda.synchronize()
+    return out
