@@ -82,6 +82,7 @@ def main():
     ap.add_argument("--no-tpot", action="store_true")
     ap.add_argument("--no-mixed", action="store_true")
     ap.add_argument("--no-loop", action="store_true")
+    ap.add_argument("--no-dit", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows per sequence in the CPU-reference sample (0: sized to take about 15 s)")
     ap.add_argument("--quick", action="store_true", help="headline stack only (no budget sweep, co-run, CPU leg)")
@@ -104,6 +105,7 @@ def main():
         budgets, args.no_corun, args.no_cpu_baseline, args.no_controller, args.no_tpot = [], True, True, True, True
         args.no_mixed = True
         args.no_loop = True
+        args.no_dit = True
     # One context holds every level the sections below use (each level is a
     # pair of CU-masked hardware queues).
     # The timed loops issue many short library calls from Python.  A cyclic
@@ -226,6 +228,12 @@ def main():
     if not args.no_corun:
         corun = corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flops_step)
 
+    # ---------------------------------------------------------------- second downstream workload (DiT)
+    gc.collect()
+    dit = None
+    if not args.no_dit:
+        dit = dit_corun(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flops_step)
+
     # ---------------------------------------------------------------- downstream-heavy mixed step
     gc.collect()
     mixed = None
@@ -295,6 +303,7 @@ def main():
         "budgets": per_budget,
         "corun": corun,
         "mixed_corun": mixed,
+        "dit_corun": dit,
         "decode_tpot_vs_cus": tpot,
         "controller": controller,
         "policy_model": policy,
@@ -672,6 +681,85 @@ def corun_mixed(torch, binding, W, ctx, dev, steps=4):
         f"(solo {tk_solo:.3f}, eager solo {tk_solo_eager:.3f}), {n_in} talker steps in window")
     tgraph.close()
     del wth, tl, cache, tcache
+    return res
+
+
+def dit_corun(torch, binding, W, ctx, th_shape, wdev, x, y, batch, ws, dev, flops_th, steps=6):
+    """Second downstream workload: a DiT denoising step (16 adaLN-Zero blocks, hidden 1024,
+    16 heads, MLP 4096) over 4 latents of 1024 tokens, solo on 128 CUs and co-running with the
+    thinker prefill on the other 128."""
+    from paper_2608_01785_amd.device_data import prepare_dit_f16, to_device, upload_weights
+    shape, n_blocks = W.DIT, 16
+    seeds = W.SEEDS["dit"]
+    lengths = [1024] * 4
+    off = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+    T = int(off[-1])
+    wd = prepare_dit_f16(ctx, upload_weights(W.make_dit_weights(shape, n_blocks, seeds["weights"]), dev))
+    xd = to_device(W.token_rows(seeds["tokens"], T, shape.hidden), dev)
+    yd = torch.empty((T, shape.hidden), dtype=torch.float32, device=dev)
+    cond = torch.from_numpy(W.dit_cond(seeds["cond"], len(lengths), shape.hidden)).to(dev)
+    wsd = torch.empty(binding.hs_dit_workspace_size(shape, T, len(lengths)), dtype=torch.uint8, device=dev)
+    d, m = shape.hidden, shape.mlp
+    flops = n_blocks * (2.0 * T * (4 * d * d + 2 * d * m) + 4.0 * d * float(np.sum(np.square(lengths))))
+    s_sh = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_SHARED))
+    s_dn = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_DOWN))
+
+    def dit(n):
+        ev = []
+        for _ in range(n):
+            binding.hs_dit_forward(ctx, shape, wd, xd, yd, cond, off, 128, None, wsd)
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(s_dn)
+            ev.append(e)
+        return ev
+
+    dit(1)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e0.record(s_dn)
+    ev = dit(steps)
+    torch.cuda.synchronize()
+    solo = e0.elapsed_time(ev[-1]) / steps
+    binding.hs_timing_enable(ctx, True)
+    dit(1)
+    kms = {k: binding.hs_timing_read(ctx, k) for k in binding.KERNEL_KINDS}
+    clk = {k: binding.hs_timing_read_clock(ctx, k)[0] for k in binding.KERNEL_KINDS}
+    binding.hs_timing_enable(ctx, False)
+    kms = {k: round(v[0] / v[1], 4) for k, v in kms.items() if v[1]}
+    # Co-run: DiT steps loop on the 128 DOWN CUs while the thinker stack prefills on the other 128.
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    start.record(s_sh)
+    s_dn.wait_event(start)
+    binding.hs_shared_stage_forward(ctx, th_shape, wdev, x, y, batch.seq_offsets, None, None, 128, None, ws)
+    p_end = torch.cuda.Event(enable_timing=True)
+    p_end.record(s_sh)
+    dec = []
+    while True:
+        dec += dit(1)
+        if p_end.query() or len(dec) > 200:
+            break
+        if len(dec) > 2:
+            dec[-2].synchronize()
+    torch.cuda.synchronize()
+    window = start.elapsed_time(p_end)
+    done = [start.elapsed_time(e) for e in dec]
+    n_in = sum(1 for t in done if t <= window)
+    t_last = max([t for t in done if t <= window], default=0.0)
+    co = t_last / n_in if n_in else float("nan")
+    peak128 = PEAK_BF16 * 128 / N_CUS
+    res = {"workload": f"DiT {n_blocks} blocks, hidden 1024, 16 heads, MLP 4096, 4 latents x 1024 tokens, "
+                       "on 128 CUs beside the thinker prefill on 128",
+           "flops_per_step": flops, "solo_ms_per_step": round(solo, 3),
+           "solo_mfma_frac_cu_scaled": round(flops / (solo / 1e3) / peak128, 4),
+           "corun_ms_per_step": round(co, 3) if n_in else None, "steps_in_window": n_in,
+           "corun_mfma_frac_cu_scaled": round(flops / (co / 1e3) / peak128, 4) if n_in else None,
+           "prefill_ms": round(window, 3), "prefill_tok_s": round(batch.n_tokens / (window / 1e3)),
+           "prefill_mfma_frac_cu_scaled": round(flops_th / (window / 1e3) / peak128, 4),
+           "kernel_ms": kms, "kernel_clock_mhz": {k: round(v, 1) for k, v in clk.items() if v > 0}}
+    log(f"[bench] DiT step: solo {solo:.3f} ms ({res['solo_mfma_frac_cu_scaled']:.3f} of CU-scaled MFMA) on 128 "
+        f"CUs; co-run {co:.3f} ms/step, {n_in} steps beside a {window:.2f} ms thinker prefill")
+    del wd
     return res
 
 
