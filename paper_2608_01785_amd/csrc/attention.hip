@@ -172,17 +172,30 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
       for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[st][r] = 0.0f;
+      // K fragments are read one 16-wide step ahead of the MFMAs that use
+      // them (two independent accumulator chains, one per 32-key half), so
+      // each MFMA waits for a read issued a step earlier, not for its own.
+      auto kfrag = [&](int kb, int st) {
+        const int row = 32 * st + perm32(fr);
+        return *reinterpret_cast<const u32x4*>(ks + row * KROW + kphys<DH>(row, 2 * kb + fh) * 16);
+      };
+      u32x4 kf[2][2];
+      kf[0][0] = kfrag(0, 0);
+      kf[0][1] = kfrag(0, 1);
 #pragma unroll
       for (int kb = 0; kb < DH / 16; ++kb) {
-        const int c = 2 * kb + fh;
-#pragma unroll
-        for (int st = 0; st < 2; ++st) {
-          const int row = 32 * st + perm32(fr);
-          const int phys = kphys<DH>(row, c);
-          const u32x4 kf = *reinterpret_cast<const u32x4*>(ks + row * KROW + phys * 16);
-          s[st] = mfma32(kf, qf[kb], s[st]);
+        if (kb + 1 < DH / 16) {
+          kf[(kb + 1) & 1][0] = kfrag(kb + 1, 0);
+          kf[(kb + 1) & 1][1] = kfrag(kb + 1, 1);
+        }
+        s[0] = mfma32(kf[kb & 1][0], qf[kb], s[0]);
+        s[1] = mfma32(kf[kb & 1][1], qf[kb], s[1]);
+        if (kb + 1 < DH / 16) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // the next step's two reads
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // then this step's two MFMAs
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
       // Register r of subtile st holds key kv0 + 32 st + 16 (r / 8) + 8 fh + r % 8.
       // Only tiles reaching past the wave's first query position need the
       // causal mask (every key of an earlier tile is visible to all of the
@@ -232,16 +245,29 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) pf[kb2][e] = pack2h_unit(s[st][r0 + 2 * e], s[st][r0 + 2 * e + 1]);
       }
-#pragma unroll
-      for (int i = 0; i < NDS; ++i) {
+      // V fragments likewise one 16-key step ahead; the NDS output subtiles
+      // are independent accumulator chains.
+      auto vfrag = [&](int kb2, int i) {
         const int d = 32 * i + fr;
+        return *reinterpret_cast<const u32x4*>(vs + d * 128 + vphys(d, 2 * kb2 + fh) * 16);
+      };
+      u32x4 vf[2][NDS];
 #pragma unroll
-        for (int kb2 = 0; kb2 < 4; ++kb2) {
-          const int c = 2 * kb2 + fh;
-          const u32x4 vf = *reinterpret_cast<const u32x4*>(vs + d * 128 + vphys(d, c) * 16);
-          o[i] = mfma32(vf, pf[kb2], o[i]);
+      for (int i = 0; i < NDS; ++i) vf[0][i] = vfrag(0, i);
+#pragma unroll
+      for (int kb2 = 0; kb2 < 4; ++kb2) {
+        if (kb2 + 1 < 4) {
+#pragma unroll
+          for (int i = 0; i < NDS; ++i) vf[(kb2 + 1) & 1][i] = vfrag(kb2 + 1, i);
+        }
+#pragma unroll
+        for (int i = 0; i < NDS; ++i) o[i] = mfma32(vf[kb2 & 1][i], pf[kb2], o[i]);
+        if (kb2 + 1 < 4) {
+          __builtin_amdgcn_sched_group_barrier(0x100, NDS, 0);  // the next step's reads
+          __builtin_amdgcn_sched_group_barrier(0x008, NDS, 0);  // then this step's MFMAs
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
     if (t + 1 < n_tiles) lstore((t + 1) & 1);
     __syncthreads();
