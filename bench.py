@@ -37,6 +37,7 @@ SPEC_MHZ = 2400.0        # clock of the published peak
 # source these counters were taken on.
 MEASURED_TRAFFIC = {
     "35c5cac0be380a8f": {"fetch_kib": 2241038.6, "fetch_scale": 2.0, "write_kib": 397954.7, "write_scale": 1.0},
+    "b13966ab4f6ab1ce": {"fetch_kib": 2240940.5, "fetch_scale": 2.0, "write_kib": 400059.4, "write_scale": 1.0},
 }
 
 
@@ -83,6 +84,13 @@ def main():
     ap.add_argument("--no-mixed", action="store_true")
     ap.add_argument("--no-loop", action="store_true")
     ap.add_argument("--no-dit", action="store_true")
+    # Profiling runs (under rocprofv3): one piece of work only, then exit.
+    ap.add_argument("--profile-budget", type=int, default=0,
+                    help="run only the thinker stack at this CU budget, --steps times")
+    ap.add_argument("--profile-decode", action="store_true",
+                    help="run only the talker decode step (batch 32, 16 layers) on 128 CUs, --steps times")
+    ap.add_argument("--profile-ladder", action="store_true",
+                    help="launch the topology probe once on every stream of the bench's ladder")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows per sequence in the CPU-reference sample (0: sized to take about 15 s)")
     ap.add_argument("--quick", action="store_true", help="headline stack only (no budget sweep, co-run, CPU leg)")
@@ -115,6 +123,8 @@ def main():
     gc.disable()
     ladder = sorted(set(budgets + [96, 128, 160, 224, 256] + ([] if args.no_tpot else TPOT_CAPS)
                         + ([] if args.no_corun else [N_CUS - c for c in DOWN_SWEEP])))
+    if args.profile_budget or args.profile_decode or args.profile_ladder:
+        return profile_only(args, torch, binding, W, ladder)
     ctx = binding.Context(0, budgets=ladder)
 
     # ---------------------------------------------------------------- thinker stack
@@ -313,6 +323,92 @@ def main():
     print(json.dumps(out), flush=True)
     torch.cuda.synchronize()
     ctx.close()
+
+
+def profile_only(args, torch, binding, W, ladder):
+    """A single piece of work for a profiler run: the thinker stack at one budget, the talker
+    decode step, or one probe launch on every stream of the bench's ladder (the full ladder,
+    as the default run builds it).  Prints one JSON line."""
+    from paper_2608_01785_amd.device_data import DeviceCache, prepare_f16, to_device, upload_weights
+    dev = "cuda:0"
+    full_ladder = sorted(set([64, 128, 192, 96, 160, 224, 256] + TPOT_CAPS + [N_CUS - c for c in DOWN_SWEEP]))
+    ctx = binding.Context(0, budgets=full_ladder if args.profile_ladder else
+                          sorted(set([128, 256] + ([args.profile_budget] if args.profile_budget else []))))
+    out = {}
+    try:
+        if args.profile_ladder:
+            ids = torch.zeros(1024 * 4, dtype=torch.int32, device=dev)
+            streams = []
+            for b in full_ladder:
+                for role in (binding.HS_ROLE_SHARED, binding.HS_ROLE_DOWN):
+                    if role == binding.HS_ROLE_DOWN and b == N_CUS:
+                        continue
+                    s = binding.hs_context_stream(ctx, b, role)
+                    binding.hs_probe_hw_ids(ctx, s, 1024, ids)
+                    torch.cuda.synchronize()
+                    streams.append((b, role))
+            out = {"probe_launches": len(streams), "levels": full_ladder}
+        elif args.profile_budget:
+            shape, n_layers = W.THINKER, 4
+            layers = W.make_weights(shape, n_layers, W.SEEDS["thinker"]["weights"])
+            batch = W.thinker_batch()
+            wdev = prepare_f16(ctx, upload_weights(layers, dev))
+            x = to_device(batch.x, dev)
+            y = torch.empty(x.shape, dtype=torch.float32, device=dev)
+            ws = torch.empty(binding.hs_workspace_size(shape, batch.n_tokens, batch.n_seqs, int(batch.lengths.max())),
+                             dtype=torch.uint8, device=dev)
+            b = args.profile_budget
+            s = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, b, binding.HS_ROLE_SHARED))
+            for _ in range(args.warmup):
+                binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, None, None, b, None, ws)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            for _ in range(args.steps):
+                binding.hs_shared_stage_forward(ctx, shape, wdev, x, y, batch.seq_offsets, None, None, b, None, ws)
+            e1.record(s)
+            torch.cuda.synchronize()
+            out = {"budget": b, "ms_per_step": round(e0.elapsed_time(e1) / args.steps, 3)}
+        else:
+            ts, n_layers, bt = W.TALKER, 16, 32
+            seeds = W.SEEDS["talker"]
+            kv_lens = W.talker_kv_lens(bt, seeds["cache"])
+            tl = prepare_f16(ctx, upload_weights(W.make_weights(ts, n_layers, seeds["weights"]), dev))
+            max_ctx = int(np.ceil((kv_lens.max() + 1) / 64) * 64)
+            cache = DeviceCache(n_layers, bt, max_ctx, ts.n_kv_heads, ts.head_dim, dev)
+            gen = torch.Generator(device=dev)
+            gen.manual_seed(seeds["cache"])
+            for l in range(n_layers):
+                for b in range(bt):
+                    cache.fill_random(l, b, int(kv_lens[b]), gen)
+            xt = to_device(W.talker_batch(ts, n_layers, bt, seeds, with_cache=False).x, dev)
+            yt = torch.empty(xt.shape, dtype=torch.float32, device=dev)
+            wst = torch.empty(binding.hs_workspace_size(ts, bt, bt, int(kv_lens.max()) + 1), dtype=torch.uint8,
+                              device=dev)
+            s = torch.cuda.ExternalStream(binding.hs_context_stream(ctx, 128, binding.HS_ROLE_DOWN))
+            for _ in range(args.warmup):
+                binding.hs_downstream_decode_step(ctx, ts, tl, xt, yt, cache.as_arg(), kv_lens, 128, None, wst)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            for _ in range(args.steps):
+                binding.hs_downstream_decode_step(ctx, ts, tl, xt, yt, cache.as_arg(), kv_lens, 128, None, wst)
+            e1.record(s)
+            torch.cuda.synchronize()
+            out = {"decode_ms_per_step": round(e0.elapsed_time(e1) / args.steps, 4),
+                   "bytes_per_step": talker_bytes(ts, n_layers, kv_lens)}
+        if args.calib_copy_mib:
+            n = args.calib_copy_mib * (1 << 20) // 4
+            src = torch.ones(n, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            torch.cuda.synchronize()
+            dst.copy_(src)
+            torch.cuda.synchronize()
+            out["calibration_copy_mib"] = args.calib_copy_mib
+    finally:
+        torch.cuda.synchronize()
+        ctx.close()
+    print(json.dumps(out), flush=True)
 
 
 def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flops_step):
