@@ -272,8 +272,24 @@ def main():
         if corun is not None:
             tb = corun["decode_bytes_per_step"]
             b_sat = round(max(tb / (ms_ / 1e3) / PEAK_HBM for ms_ in corun["decode_ms_vs_cus"].values()), 4)
-        loop = [serving_loop(torch, binding, W, ctx, wdev, dev, p, saturation=b_sat, short_budget=sb)
-                for p, sb in (("baseline", 0), ("joint", 0), ("joint", 1024))]
+        # Three seeded arrival streams per policy: one 48-request stream is a small sample.
+        loop = {"runs": [], "seeds": LOOP_SEEDS}
+        for p, sb in (("baseline", 0), ("joint", 0), ("joint", 1024)):
+            runs = [serving_loop(torch, binding, W, ctx, wdev, dev, p, saturation=b_sat, short_budget=sb, seed=sd)
+                    for sd in LOOP_SEEDS]
+            loop["runs"] += runs
+            agg = {"policy": p, "short_budget": runs[0]["short_budget"], "saturation": b_sat}
+            for c in ("short", "long"):
+                agg[c] = {k: round(float(np.mean([r[c][k] for r in runs if r[c][k] is not None])), 4)
+                          for k in ("slo_attainment", "p50_ms", "p95_ms")}
+            agg["mean_shared_cus"] = round(float(np.mean([r["mean_shared_cus"] for r in runs])), 1)
+            agg["makespan_ms"] = round(float(np.mean([r["makespan_ms"] for r in runs])), 2)
+            loop.setdefault("mean_over_seeds", []).append(agg)
+            log(f"[bench] serving loop mean over seeds {LOOP_SEEDS} ({p}, short budget {agg['short_budget']}): "
+                f"short SLO {agg['short']['slo_attainment']:.3f} p95 {agg['short']['p95_ms']:.1f} ms, long SLO "
+                f"{agg['long']['slo_attainment']:.3f} p95 {agg['long']['p95_ms']:.1f} ms")
+        for r in loop["runs"][1:]:      # one step trace is kept, to keep the line short
+            r.pop("trace", None)
 
     # ---------------------------------------------------------------- serving-loop model on measured times
     policy = None
@@ -490,8 +506,8 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
         torch.cuda.synchronize()
         return e0.elapsed_time(ev[-1]) / 20, host
 
-    solo_eager_ms, host_eager_ms = solo(False)
-    solo_ms, host_graph_ms = solo(True)
+    solo_ms, host_eager_ms = solo(False)
+    solo_graph_ms, host_graph_ms = solo(True)
 
     # Per-kernel averages of the solo decode step (events on the decode stream).
     binding.hs_timing_enable(ctx, True)
@@ -551,8 +567,8 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
         t_last = max([t for t in done if t <= window], default=0.0)
         return window, (t_last / n_in if n_in else float("nan")), n_in
 
-    window_e, dec_eager_ms, n_in_e = corun(False)
-    window, dec_ms, n_in = corun(True)
+    window, dec_ms, n_in = corun(False)
+    window_g, dec_graph_ms, n_in_g = corun(True)
     tgraph.close()
     T = batch.n_tokens
     res = {
@@ -564,9 +580,9 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
         "decode_ms_per_step": round(dec_ms, 4),
         "decode_tok_s": round(32 / (dec_ms / 1e3)) if n_in else None,
         "decode_hbm_frac_cu_scaled": round(step_bytes / (dec_ms / 1e3) / (PEAK_HBM * 128 / N_CUS), 4) if n_in else None,
-        "decode_path": "captured decode step replayed per step (hs_decode_graph_launch)",
-        "decode_eager_ms_per_step": round(dec_eager_ms, 4), "prefill_ms_with_eager_decode": round(window_e, 3),
-        "decode_eager_solo_ms_per_step": round(solo_eager_ms, 4),
+        "decode_path": "eager decode steps (decode_graph_*: the captured step replayed, hs_decode_graph_launch)",
+        "decode_graph_ms_per_step": round(dec_graph_ms, 4), "prefill_ms_with_graph_decode": round(window_g, 3),
+        "decode_graph_solo_ms_per_step": round(solo_graph_ms, 4),
         "decode_host_ms_per_step": {"graph": round(host_graph_ms, 4), "eager": round(host_eager_ms, 4)},
         "decode_solo_ms_per_step": round(solo_ms, 4),
         "decode_solo_tok_s": round(32 / (solo_ms / 1e3)),
@@ -577,8 +593,8 @@ def corun_measure(torch, binding, W, ctx, shape, wdev, x, y, batch, ws, dev, flo
         "talker": "16 layers, hidden 1024, 16/16 heads, dh 64, ffn 4096, batch 32, kv_len U[128,1024] (sum 17437)",
     }
     log(f"[bench] co-run: prefill {window:.2f} ms (solo {prefill_solo:.2f}), decode {dec_ms:.3f} ms/step "
-        f"(solo {solo_ms:.3f}), {n_in} steps in window; eager decode steps: {dec_eager_ms:.3f} ms/step "
-        f"(solo {solo_eager_ms:.3f}); host time per step: graph {host_graph_ms:.3f} ms, eager {host_eager_ms:.3f} ms")
+        f"(solo {solo_ms:.3f}), {n_in} steps in window; captured decode step: {dec_graph_ms:.3f} ms/step "
+        f"(solo {solo_graph_ms:.3f}); host time per step: graph {host_graph_ms:.3f} ms, eager {host_eager_ms:.3f} ms")
 
     # Talker step time against its CU count (the complement of each ladder level).
     sweep = {}
@@ -735,27 +751,32 @@ def corun_mixed(torch, binding, W, ctx, dev, steps=4):
     torch.cuda.synchronize()
     tk_solo = e0.elapsed_time(ev[-1]) / 10
 
-    # Co-run: talker steps loop on the 160 CUs while the thinker runs `steps` steps on 96.
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    start.record(s_sh)
-    s_dn.wait_event(start)
-    thinker(steps)
-    end = torch.cuda.Event(enable_timing=True)
-    end.record(s_sh)
-    dec = []
-    while True:
-        dec += talker(1)
-        if end.query() or len(dec) > 500:
-            break
-        if len(dec) > 3:
-            dec[-3].synchronize()
-    torch.cuda.synchronize()
-    window = start.elapsed_time(end)
-    done = [start.elapsed_time(e) for e in dec]
-    n_in = sum(1 for t in done if t <= window)
-    t_last = max([t for t in done if t <= window], default=0.0)
-    tk_ms = t_last / n_in if n_in else float("nan")
+    # Co-run: talker steps loop on the 160 CUs while the thinker runs `steps` steps on 96;
+    # eager talker launches, then the captured step.
+    def corun(graph):
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        start.record(s_sh)
+        s_dn.wait_event(start)
+        thinker(steps)
+        end = torch.cuda.Event(enable_timing=True)
+        end.record(s_sh)
+        dec = []
+        while True:
+            dec += talker(1, graph)
+            if end.query() or len(dec) > 500:
+                break
+            if len(dec) > 3:
+                dec[-3].synchronize()
+        torch.cuda.synchronize()
+        window = start.elapsed_time(end)
+        done = [start.elapsed_time(e) for e in dec]
+        n_in = sum(1 for t in done if t <= window)
+        t_last = max([t for t in done if t <= window], default=0.0)
+        return window, (t_last / n_in if n_in else float("nan")), n_in
+
+    window, tk_ms, n_in = corun(False)
+    window_g, tk_ms_g, n_in_g = corun(True)
     th_ms = window / steps
     res = {
         "workload": "thinker layer hidden 4096, 32/8 heads, ffn 14336: 4 x 2048-row chunks behind 0/2048/4096/6144 "
@@ -765,16 +786,19 @@ def corun_mixed(torch, binding, W, ctx, dev, steps=4):
         "thinker_tflops": round(th_flops / (th_ms / 1e3) / 1e12, 1),
         "thinker_mfma_frac_cu_scaled": round(th_flops / (th_ms / 1e3) / (PEAK_BF16 * 96 / N_CUS), 4),
         "thinker_solo_mfma_frac_cu_scaled": round(th_flops / (th_solo / 1e3) / (PEAK_BF16 * 96 / N_CUS), 4),
-        "talker_ms_per_step": round(tk_ms, 4), "talker_solo_ms_per_step": round(tk_solo, 4),
+        "talker_ms_per_step": round(tk_ms, 4), "talker_solo_ms_per_step": round(tk_solo_eager, 4),
+        "talker_graph_solo_ms_per_step": round(tk_solo, 4),
         "talker_tok_s": round(bt / (tk_ms / 1e3)) if n_in else None,
         "talker_hbm_frac_cu_scaled": round(t_bytes / (tk_ms / 1e3) / (PEAK_HBM * 160 / N_CUS), 4) if n_in else None,
-        "talker_solo_hbm_frac_cu_scaled": round(t_bytes / (tk_solo / 1e3) / (PEAK_HBM * 160 / N_CUS), 4),
+        "talker_solo_hbm_frac_cu_scaled": round(t_bytes / (tk_solo_eager / 1e3) / (PEAK_HBM * 160 / N_CUS), 4),
         "talker_steps_in_window": n_in, "thinker_flops": th_flops, "talker_bytes_per_step": int(t_bytes),
-        "talker_path": "captured decode step replayed per step",
-        "talker_eager_solo_ms_per_step": round(tk_solo_eager, 4),
+        "talker_path": "eager decode steps (talker_graph_*: the captured step replayed)",
+        "talker_graph_ms_per_step": round(tk_ms_g, 4) if n_in_g else None,
+        "talker_graph_steps_in_window": n_in_g, "thinker_ms_beside_graph": round(window_g / steps, 3),
     }
     log(f"[bench] mixed co-run: thinker {th_ms:.3f} ms/step (solo {th_solo:.3f}), talker {tk_ms:.3f} ms/step "
-        f"(solo {tk_solo:.3f}, eager solo {tk_solo_eager:.3f}), {n_in} talker steps in window")
+        f"(solo {tk_solo_eager:.3f}), {n_in} talker steps in window; captured talker step: {tk_ms_g:.3f} ms/step "
+        f"(solo {tk_solo:.3f}), {n_in_g} steps beside a {window_g / steps:.3f} ms thinker step")
     tgraph.close()
     del wth, tl, cache, tcache
     return res
@@ -860,6 +884,7 @@ def dit_corun(torch, binding, W, ctx, th_shape, wdev, x, y, batch, ws, dev, flop
 
 
 TPOT_CAPS = [16, 32, 48, 64, 96, 128, 192, 256]
+LOOP_SEEDS = (11, 12, 13)
 DOWN_SWEEP = (64, 128, 160, 192, 224, 240)   # talker CU counts of the co-run sweep
 
 
