@@ -18,54 +18,66 @@ __global__ __launch_bounds__(256) void silu_rows_kernel(const float* __restrict_
   }
 }
 
-// One wave per modulation row j: the row of W (bf16, d values) stays in
-// registers while the wave takes its dot product with every sequence's
-// silu(c).  mod[b][j] = bias[j] + sum_k s[b][k] W[j][k], fp32.
-__global__ __launch_bounds__(256) void dit_mod_kernel(const uint16_t* __restrict__ w, const uint16_t* __restrict__ bias,
-                                                      const float* __restrict__ s, float* __restrict__ mod,
-                                                      int n_seqs, int d) {
+// The modulation of up to kDitModLayers layers in one launch (it depends on
+// the conditioning only, not on the layer's input).  Each wave takes RW
+// consecutive rows j of one layer's W (bf16 [6d, d]) with every load in
+// flight at once, then takes their dot products with each sequence's
+// silu(c) (fp32, L2-resident): mod[l][b][j] = bias_l[j] + sum_k s[b][k] W_l[j][k].
+// CPL = 16-byte chunks per lane (d <= 512 CPL).
+template <int CPL, int RW>
+__global__ __launch_bounds__(256) void dit_mod_kernel(DitModArgs p, const float* __restrict__ s,
+                                                      float* __restrict__ mod, int n_seqs, int d) {
   const int lane = threadIdx.x & 63;
-  const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int rows = 6 * d;
-  if (j >= rows) return;
+  const int64_t row0 = (int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6)) * RW;
+  if (row0 >= int64_t(p.n_layers) * rows) return;
+  const int l = int(row0 / rows), j0 = int(row0 % rows);  // RW divides rows
   const int chunks = d >> 3;
-  float wv[kMaxChunksPerLane][8];
-  const uint16_t* wr = w + int64_t(j) * d;
+  const uint16_t* wl = p.w[l];
+  u32x4 wv[RW][CPL];
 #pragma unroll
-  for (int i = 0; i < kMaxChunksPerLane; ++i) {
-    const int c = lane + 64 * i;
-    if (c < chunks) {
-      const u32x4 u = *reinterpret_cast<const u32x4*>(wr + c * 8);
+  for (int r = 0; r < RW; ++r)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        wv[i][2 * e] = __uint_as_float(u[e] << 16);
-        wv[i][2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
-      }
+    for (int i = 0; i < CPL; ++i) {
+      const int c = lane + 64 * i;
+      wv[r][i] = c < chunks ? *reinterpret_cast<const u32x4*>(wl + int64_t(j0 + r) * d + c * 8) : u32x4{0, 0, 0, 0};
     }
-  }
-  const float bj = __uint_as_float(uint32_t(bias[j]) << 16);
+  float bj[RW];
+#pragma unroll
+  for (int r = 0; r < RW; ++r) bj[r] = __uint_as_float(uint32_t(p.bias[l][j0 + r]) << 16);
+  float* ml = mod + int64_t(l) * n_seqs * rows;
   for (int b = 0; b < n_seqs; ++b) {
     const float* sr = s + int64_t(b) * d;
-    float acc = 0.0f;
+    float acc[RW];
 #pragma unroll
-    for (int i = 0; i < kMaxChunksPerLane; ++i) {
+    for (int r = 0; r < RW; ++r) acc[r] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
       const int c = lane + 64 * i;
       if (c < chunks) {
         const f32x4 lo = *reinterpret_cast<const f32x4*>(sr + c * 8);
         const f32x4 hi = *reinterpret_cast<const f32x4*>(sr + c * 8 + 4);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc += wv[i][e] * lo[e] + wv[i][4 + e] * hi[e];
+        for (int r = 0; r < RW; ++r)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            acc[r] += __uint_as_float(wv[r][i][e] << 16) * (e < 2 ? lo[2 * e] : hi[2 * e - 4]) +
+                      __uint_as_float(wv[r][i][e] & 0xffff0000u) * (e < 2 ? lo[2 * e + 1] : hi[2 * e - 3]);
       }
     }
-    acc = wave_sum(acc);
-    if (lane == 0) mod[int64_t(b) * rows + j] = acc + bj;
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+      const float v = wave_sum(acc[r]);
+      if (lane == 0) ml[int64_t(b) * rows + j0 + r] = v + bj[r];
+    }
   }
 }
 
 // One wave per row: y = fp16(((x - mean) / sqrt(var + eps)) * (1 + scale) + shift)
 // with the row's sequence's scale and shift; fp32 statistics, the row kept in
-// registers between the passes.
-template <typename TIn>
+// registers between the passes and the row's shift and scale loaded with it.
+// CPL = 8-element chunks per lane (d <= 512 CPL).
+template <typename TIn, int CPL>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const TIn* __restrict__ x, const float* __restrict__ mod,
                                                      const int32_t* __restrict__ row_seq, uint16_t* __restrict__ y,
                                                      int rows, int d, float eps, int shift_off, int scale_off) {
@@ -75,10 +87,12 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const TIn* __restrict__ x, 
   const float inv_d = 1.0f / float(d);
   for (int row = blockIdx.x * 4 + wave; row < rows; row += gridDim.x * 4) {
     const TIn* xr = x + int64_t(row) * d;
-    float v[kMaxChunksPerLane][8];
+    const float* mrow = mod + int64_t(row_seq[row]) * (6 * d);
+    float v[CPL][8];
+    f32x4 sh[CPL][2], sc[CPL][2];
     float sum = 0.0f;
 #pragma unroll
-    for (int i = 0; i < kMaxChunksPerLane; ++i) {
+    for (int i = 0; i < CPL; ++i) {
       const int c = lane + 64 * i;
       if (c < chunks) {
         if constexpr (sizeof(TIn) == 2) {
@@ -97,6 +111,10 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const TIn* __restrict__ x, 
             v[i][4 + e] = hi[e];
           }
         }
+        sh[i][0] = *reinterpret_cast<const f32x4*>(mrow + shift_off + c * 8);
+        sh[i][1] = *reinterpret_cast<const f32x4*>(mrow + shift_off + c * 8 + 4);
+        sc[i][0] = *reinterpret_cast<const f32x4*>(mrow + scale_off + c * 8);
+        sc[i][1] = *reinterpret_cast<const f32x4*>(mrow + scale_off + c * 8 + 4);
 #pragma unroll
         for (int e = 0; e < 8; ++e) sum += v[i][e];
       }
@@ -104,7 +122,7 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const TIn* __restrict__ x, 
     const float mean = wave_sum(sum) * inv_d;
     float ss = 0.0f;
 #pragma unroll
-    for (int i = 0; i < kMaxChunksPerLane; ++i) {
+    for (int i = 0; i < CPL; ++i) {
       const int c = lane + 64 * i;
       if (c < chunks) {
 #pragma unroll
@@ -115,20 +133,15 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const TIn* __restrict__ x, 
       }
     }
     const float r = rsqrtf(wave_sum(ss) * inv_d + eps);
-    const float* mrow = mod + int64_t(row_seq[row]) * (6 * d);
 #pragma unroll
-    for (int i = 0; i < kMaxChunksPerLane; ++i) {
+    for (int i = 0; i < CPL; ++i) {
       const int c = lane + 64 * i;
       if (c < chunks) {
-        const float* sh = mrow + shift_off + c * 8;
-        const float* sc = mrow + scale_off + c * 8;
-        const f32x4 sh0 = *reinterpret_cast<const f32x4*>(sh), sh1 = *reinterpret_cast<const f32x4*>(sh + 4);
-        const f32x4 sc0 = *reinterpret_cast<const f32x4*>(sc), sc1 = *reinterpret_cast<const f32x4*>(sc + 4);
         float o[8];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          o[e] = v[i][e] * r * (1.0f + sc0[e]) + sh0[e];
-          o[4 + e] = v[i][4 + e] * r * (1.0f + sc1[e]) + sh1[e];
+          o[e] = v[i][e] * r * (1.0f + sc[i][0][e]) + sh[i][0][e];
+          o[4 + e] = v[i][4 + e] * r * (1.0f + sc[i][1][e]) + sh[i][1][e];
         }
         u32x4 out;
 #pragma unroll
@@ -148,13 +161,48 @@ hipError_t launch_silu_rows(const float* c, float* s, int n, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_dit_modulation(const uint16_t* w, const uint16_t* bias, const float* s, float* mod, int n_seqs,
-                                 int d, hipStream_t st) {
-  if (n_seqs <= 0) return hipSuccess;
-  if (d % 8 != 0 || d > 64 * kMaxChunksPerLane * 8) return hipErrorInvalidValue;
-  const int grid = (6 * d + 3) / 4;
-  hipLaunchKernelGGL(dit_mod_kernel, dim3(grid), dim3(256), 0, st, w, bias, s, mod, n_seqs, d);
+namespace {
+
+template <int CPL, int RW>
+hipError_t launch_mod(const DitModArgs& p, const float* s, float* mod, int n_seqs, int d, hipStream_t st) {
+  const int64_t waves = (int64_t(p.n_layers) * 6 * d + RW - 1) / RW;
+  hipLaunchKernelGGL((dit_mod_kernel<CPL, RW>), dim3(unsigned((waves + 3) / 4)), dim3(256), 0, st, p, s, mod, n_seqs,
+                     d);
   return hipGetLastError();
+}
+
+template <typename TIn, int CPL>
+hipError_t launch_ln(const TIn* x, const float* mod, const int32_t* row_seq, uint16_t* y, int rows, int d, float eps,
+                     int shift_off, int scale_off, int grid, hipStream_t st) {
+  hipLaunchKernelGGL((ln_mod_kernel<TIn, CPL>), dim3(grid), dim3(256), 0, st, x, mod, row_seq, y, rows, d, eps,
+                     shift_off, scale_off);
+  return hipGetLastError();
+}
+
+template <typename TIn>
+hipError_t launch_ln_cpl(const TIn* x, const float* mod, const int32_t* row_seq, uint16_t* y, int rows, int d,
+                         float eps, int shift_off, int scale_off, int grid, hipStream_t st) {
+  const int cpl = (d / 8 + 63) / 64;
+  if (cpl <= 1) return launch_ln<TIn, 1>(x, mod, row_seq, y, rows, d, eps, shift_off, scale_off, grid, st);
+  if (cpl <= 2) return launch_ln<TIn, 2>(x, mod, row_seq, y, rows, d, eps, shift_off, scale_off, grid, st);
+  if (cpl <= 4) return launch_ln<TIn, 4>(x, mod, row_seq, y, rows, d, eps, shift_off, scale_off, grid, st);
+  if (cpl <= 8) return launch_ln<TIn, 8>(x, mod, row_seq, y, rows, d, eps, shift_off, scale_off, grid, st);
+  return launch_ln<TIn, kMaxChunksPerLane>(x, mod, row_seq, y, rows, d, eps, shift_off, scale_off, grid, st);
+}
+
+}  // namespace
+
+hipError_t launch_dit_modulation(const DitModArgs& p, const float* s, float* mod, int n_seqs, int d, hipStream_t st) {
+  if (n_seqs <= 0 || p.n_layers <= 0) return hipSuccess;
+  if (p.n_layers > kDitModLayers || d % 8 != 0 || d > 64 * kMaxChunksPerLane * 8) return hipErrorInvalidValue;
+  const int cpl = (d / 8 + 63) / 64;
+  // Rows per wave: about 8 KB of weights in flight per wave (RW divides 6 d
+  // since d is a multiple of 8).
+  if (cpl <= 1) return launch_mod<1, 8>(p, s, mod, n_seqs, d, st);
+  if (cpl <= 2) return launch_mod<2, 4>(p, s, mod, n_seqs, d, st);
+  if (cpl <= 4) return launch_mod<4, 2>(p, s, mod, n_seqs, d, st);
+  if (cpl <= 8) return launch_mod<8, 1>(p, s, mod, n_seqs, d, st);
+  return launch_mod<kMaxChunksPerLane, 1>(p, s, mod, n_seqs, d, st);
 }
 
 hipError_t launch_ln_modulate(const uint16_t* x, const float* x_f32, const float* mod, const int32_t* row_seq,
@@ -164,13 +212,8 @@ hipError_t launch_ln_modulate(const uint16_t* x, const float* x_f32, const float
   if (d % 8 != 0 || d > 64 * kMaxChunksPerLane * 8) return hipErrorInvalidValue;
   int grid = (rows + 3) / 4;
   if (max_blocks > 0 && grid > max_blocks) grid = max_blocks;
-  if (x_f32)
-    hipLaunchKernelGGL(ln_mod_kernel<float>, dim3(grid), dim3(256), 0, st, x_f32, mod, row_seq, y, rows, d, eps,
-                       shift_off, scale_off);
-  else
-    hipLaunchKernelGGL(ln_mod_kernel<uint16_t>, dim3(grid), dim3(256), 0, st, x, mod, row_seq, y, rows, d, eps,
-                       shift_off, scale_off);
-  return hipGetLastError();
+  if (x_f32) return launch_ln_cpl<float>(x_f32, mod, row_seq, y, rows, d, eps, shift_off, scale_off, grid, st);
+  return launch_ln_cpl<uint16_t>(x, mod, row_seq, y, rows, d, eps, shift_off, scale_off, grid, st);
 }
 
 }  // namespace hs

@@ -143,11 +143,17 @@ hipError_t launch_rmsnorm(const uint16_t* x, const float* x_f32, const uint16_t*
 hipError_t launch_rope_table(float2* tab, int max_pos, int dh, float base, hipStream_t s);
 
 // Diffusion-transformer pieces (dit.hip).  s = silu(c) for B x d conditioning
-// values (fp32); mod[b][j] = bias[j] + sum_k s[b][k] W[j][k] for the 6d
-// modulation rows of one layer (W bf16 [6d, d] row-major, bias bf16 [6d]).
+// values (fp32); for each of n_layers (at most kDitModLayers) layers l,
+// mod[l][b][j] = bias_l[j] + sum_k s[b][k] W_l[j][k] over its 6d modulation
+// rows (W_l bf16 [6d, d] row-major, bias_l bf16 [6d]).
+constexpr int kDitModLayers = 8;
+struct DitModArgs {
+  const uint16_t* w[kDitModLayers];
+  const uint16_t* bias[kDitModLayers];
+  int n_layers;
+};
 hipError_t launch_silu_rows(const float* c, float* s, int n, hipStream_t st);
-hipError_t launch_dit_modulation(const uint16_t* w, const uint16_t* bias, const float* s, float* mod, int n_seqs,
-                                 int d, hipStream_t st);
+hipError_t launch_dit_modulation(const DitModArgs& p, const float* s, float* mod, int n_seqs, int d, hipStream_t st);
 // y[t] = fp16(LN(x[t]) * (1 + mod[b][scale_off + j]) + mod[b][shift_off + j]),
 // b = row_seq[t]; x bf16 (x_f32 null) or fp32; mod rows of 6d floats.
 hipError_t launch_ln_modulate(const uint16_t* x, const float* x_f32, const float* mod, const int32_t* row_seq,

@@ -980,7 +980,8 @@ DitLayout dit_layout(const hs_dit_cfg& c, int32_t T, int32_t B, int32_t max_pos)
   L.base = hs::ws_layout(dit_as_layer(c), T, B, max_pos, 0, true);
   L.silu = hs::align_up(L.base.total, hs::kAlign);
   L.mod = hs::align_up(L.silu + size_t(B) * c.hidden * 4, hs::kAlign);
-  L.total = hs::align_up(L.mod + size_t(B) * 6 * c.hidden * 4, hs::kAlign);
+  // The modulation of up to kDitModLayers layers, computed in one launch.
+  L.total = hs::align_up(L.mod + size_t(hs::kDitModLayers) * B * 6 * c.hidden * 4, hs::kAlign);
   return L;
 }
 
@@ -1056,7 +1057,7 @@ hs_status hs_dit_forward(hs_context* ctx, const hs_dit_cfg* cfg, const hs_dit_we
   uint16_t* a_buf = at<uint16_t>(ws, lay.a);
   float* xtmp = at<float>(ws, lay.xtmp);
   float* s_buf = at<float>(ws, DL.silu);
-  float* mod = at<float>(ws, DL.mod);
+  float* mod_all = at<float>(ws, DL.mod);
   uint16_t* kstore = at<uint16_t>(ws, lay.kpack);
   uint16_t* vstore = at<uint16_t>(ws, lay.vpack);
   const int grid_cap = cu_budget;
@@ -1069,9 +1070,18 @@ hs_status hs_dit_forward(hs_context* ctx, const hs_dit_cfg* cfg, const hs_dit_we
     const int remaining = n_layers - 1 - l;
     float* x_next = (remaining % 2 == 0) ? static_cast<float*>(x_out) : xtmp;
     const bool f16 = w[l].format == HS_WEIGHTS_F16;
-    TIMED(HS_KERNEL_MODULATION, hs::launch_dit_modulation(static_cast<const uint16_t*>(w[l].w_ada),
-                                                          static_cast<const uint16_t*>(w[l].b_ada), s_buf, mod,
-                                                          n_seqs, d, s));
+    if (l % hs::kDitModLayers == 0) {
+      // Every block's modulation depends on the conditioning only: up to
+      // kDitModLayers layers' at once, one slot of B x 6d floats per layer.
+      hs::DitModArgs mp{};
+      mp.n_layers = std::min(hs::kDitModLayers, n_layers - l);
+      for (int i = 0; i < mp.n_layers; ++i) {
+        mp.w[i] = static_cast<const uint16_t*>(w[l + i].w_ada);
+        mp.bias[i] = static_cast<const uint16_t*>(w[l + i].b_ada);
+      }
+      TIMED(HS_KERNEL_MODULATION, hs::launch_dit_modulation(mp, s_buf, mod_all, n_seqs, d, s));
+    }
+    float* const mod = mod_all + size_t(l % hs::kDitModLayers) * n_seqs * 6 * d;
     TIMED(HS_KERNEL_LN_MOD, hs::launch_ln_modulate(x_cur, x_cur_f32, mod, row_seq, n_buf, T, d, cfg->ln_eps, 0, d,
                                                    4 * cu_budget, s));
     hs::GemmArgs g{};
