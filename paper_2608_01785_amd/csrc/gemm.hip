@@ -413,6 +413,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
             store_h4(a.out + int64_t(m) * a.ldo + c_base + i * 32 + 8 * g, v[0], v[1], v[2], v[3]);
           }
       } else {  // EPI_QKV
+        // The row's positions (one per RoPE section) and cache offsets, loaded
+        // once per row rather than once per four pairs.
+        const bool sectioned = a.pos_stride != 0;
+        const int p0 = a.pos[m];
+        const int p1 = sectioned ? a.pos[a.pos_stride + m] : p0;
+        const int p2 = sectioned ? a.pos[2 * a.pos_stride + m] : p0;
+        const int64_t k_row = a.k_off[m], v_row = a.v_off[m];
 #pragma unroll
         for (int pr = 0; pr < 2; ++pr) {  // (lo subtile, hi subtile) pairs of the wave
           // DH 128: one head per wave, pairs (0, 2), (1, 3); d_lo = 32 pr + ...
@@ -425,7 +432,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
           for (int g = 0; g < 4; ++g) {
             const int d = dsub + 8 * g + 4 * fh;  // < DH / 2
             // Pairs d .. d + 3 share one RoPE section (sections are multiples of 4 pairs).
-            const float2* rt = a.rope ? a.rope + int64_t(rope_pos(a, m, d)) * (DH / 2) : nullptr;
+            const int pc = d >= a.sec2 ? p2 : (d >= a.sec1 ? p1 : p0);
+            const float2* rt = a.rope ? a.rope + int64_t(pc) * (DH / 2) : nullptr;
             float lo[4], hi[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -460,12 +468,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
               }
               uint16_t* dst = (head < a.hq)
                                   ? a.q + (int64_t(m) * a.hq + head) * DH
-                                  : a.kstore + a.k_off[m] + int64_t(head - a.hq) * a.kv_head_stride;
+                                  : a.kstore + k_row + int64_t(head - a.hq) * a.kv_head_stride;
               store_h4(dst + d, rl[0], rl[1], rl[2], rl[3]);
               store_h4(dst + d + DH / 2, rh[0], rh[1], rh[2], rh[3]);
             } else {
               const int gh = head - a.hq - a.hkv;
-              uint16_t* dst = a.vstore + a.v_off[m] + int64_t(gh) * a.kv_head_stride;
+              uint16_t* dst = a.vstore + v_row + int64_t(gh) * a.kv_head_stride;
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
                 dst[(d + e) * kv_tile_keys] = f2h(lo[e]);
