@@ -38,6 +38,7 @@ SPEC_MHZ = 2400.0        # clock of the published peak
 MEASURED_TRAFFIC = {
     "35c5cac0be380a8f": {"fetch_kib": 2241038.6, "fetch_scale": 2.0, "write_kib": 397954.7, "write_scale": 1.0},
     "b13966ab4f6ab1ce": {"fetch_kib": 2240940.5, "fetch_scale": 2.0, "write_kib": 400059.4, "write_scale": 1.0},
+    "03c73fb21179ef2c": {"fetch_kib": 2241088.2, "fetch_scale": 2.0, "write_kib": 399894.8, "write_scale": 1.0},
 }
 
 
