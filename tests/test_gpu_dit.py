@@ -125,3 +125,20 @@ def test_dit_token_permutation_permutes_outputs(env):
     y = run_dit(env, shape, wdev, x, cond, off).cpu().numpy().astype(np.float64)
     yp = run_dit(env, shape, wdev, x[perm], cond, off).cpu().numpy().astype(np.float64)
     assert err_ratio(yp, y[perm]) <= TOL
+
+
+def test_dit_modulation_batches_across_blocks(env):
+    """Nine blocks (the modulation runs for up to eight blocks per launch, so the
+    ninth takes a second launch and the first slot again) over eleven sequences,
+    one of them empty, at hidden 512 (two 16-byte chunks per lane)."""
+    torch, ctx = env
+    from paper_2608_01785_amd.device_data import upload_weights
+    shape = W.DitShape(512, 8, 64, 1024)
+    lengths = [5, 0, 40, 1, 17, 64, 3, 29, 8, 2, 11]
+    layers, off, x, cond = _case(shape, 9, lengths, 98)
+    log(f"[dit] hidden 512, 9 blocks, {len(lengths)} sequences")
+    got = run_dit(env, shape, upload_weights(layers), x, cond, off).cpu().numpy().astype(np.float64)
+    want = D.dit_forward(f64(x), cond.astype(np.float64), w64(layers), shape, off)
+    e = err_ratio(got, want)
+    log(f"  max err / rms = {e:.3e}")
+    assert e <= TOL
