@@ -10,7 +10,8 @@ constexpr int kMaxChunksPerLane = 16;  // hidden <= 64 lanes * 16 chunks * 8 = 8
 // One wave per row: y = x / sqrt(mean(x^2) + eps) * gamma, fp32 reduction,
 // fp16 output (the next GEMM's operand).  The input row (bf16 or fp32) stays in registers between the
 // two passes; loads are 16 bytes wide.
-template <typename TIn>
+// CPL = 8-element chunks per lane (d <= 512 CPL): registers for the row only.
+template <typename TIn, int CPL>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const TIn* __restrict__ x, const uint16_t* __restrict__ gamma,
                                                       uint16_t* __restrict__ y, int rows, int d, float eps,
                                                       int k8_rows) {
@@ -20,10 +21,10 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const TIn* __restrict__ x,
   const float inv_d = 1.0f / float(d);
   for (int row = blockIdx.x * 4 + wave; row < rows; row += gridDim.x * 4) {
     const TIn* xr = x + int64_t(row) * d;
-    float v[kMaxChunksPerLane][8];
+    float v[CPL][8];
     float ss = 0.0f;
 #pragma unroll
-    for (int i = 0; i < kMaxChunksPerLane; ++i) {
+    for (int i = 0; i < CPL; ++i) {
       const int c = lane + 64 * i;
       if (c < chunks) {
         if constexpr (sizeof(TIn) == 2) {
@@ -49,7 +50,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const TIn* __restrict__ x,
     ss = wave_sum(ss);
     const float r = rsqrtf(ss * inv_d + eps);
 #pragma unroll
-    for (int i = 0; i < kMaxChunksPerLane; ++i) {
+    for (int i = 0; i < CPL; ++i) {
       const int c = lane + 64 * i;
       if (c < chunks) {
         const u32x4 gv = *reinterpret_cast<const u32x4*>(gamma + c * 8);
@@ -126,16 +127,35 @@ hipError_t launch_convert_bf16_f16(const uint16_t* src, uint16_t* dst, int64_t r
   return hipGetLastError();
 }
 
+namespace {
+
+template <typename TIn, int CPL>
+hipError_t launch_norm(const TIn* x, const uint16_t* gamma, uint16_t* y, int rows, int d, float eps, int k8_rows,
+                       int grid, hipStream_t s) {
+  hipLaunchKernelGGL((rmsnorm_kernel<TIn, CPL>), dim3(grid), dim3(256), 0, s, x, gamma, y, rows, d, eps, k8_rows);
+  return hipGetLastError();
+}
+
+// The instance for exactly cpl chunks per lane (1 .. kMaxChunksPerLane).
+template <typename TIn, int CPL = 1>
+hipError_t launch_norm_cpl(int cpl, const TIn* x, const uint16_t* gamma, uint16_t* y, int rows, int d, float eps,
+                           int k8_rows, int grid, hipStream_t s) {
+  if constexpr (CPL < kMaxChunksPerLane) {
+    if (cpl > CPL) return launch_norm_cpl<TIn, CPL + 1>(cpl, x, gamma, y, rows, d, eps, k8_rows, grid, s);
+  }
+  return launch_norm<TIn, CPL>(x, gamma, y, rows, d, eps, k8_rows, grid, s);
+}
+
+}  // namespace
+
 hipError_t launch_rmsnorm(const uint16_t* x, const float* x_f32, const uint16_t* gamma, uint16_t* y, int rows,
                           int d, float eps, int k8_rows, int max_blocks, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   int grid = (rows + 3) / 4;
   if (grid > max_blocks) grid = max_blocks;
-  if (x_f32)
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(grid), dim3(256), 0, s, x_f32, gamma, y, rows, d, eps, k8_rows);
-  else
-    hipLaunchKernelGGL(rmsnorm_kernel<uint16_t>, dim3(grid), dim3(256), 0, s, x, gamma, y, rows, d, eps, k8_rows);
-  return hipGetLastError();
+  const int cpl = (d / 8 + 63) / 64;  // 1 .. kMaxChunksPerLane
+  if (x_f32) return launch_norm_cpl<float>(cpl, x_f32, gamma, y, rows, d, eps, k8_rows, grid, s);
+  return launch_norm_cpl<uint16_t>(cpl, x, gamma, y, rows, d, eps, k8_rows, grid, s);
 }
 
 hipError_t launch_rope_table(float2* tab, int max_pos, int dh, float base, hipStream_t s) {
