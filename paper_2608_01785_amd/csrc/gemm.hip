@@ -74,7 +74,9 @@ __device__ __forceinline__ uint32_t weight_row(int tile_n, int r, int ffn) {
 // touches each of the 64 banks once (and any 8 consecutive rows each of 32).
 __device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
 
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+// silu(z) = z / (1 + e^-z), with the hardware reciprocal (1 ulp) in place of
+// an IEEE division: the result is rounded to fp16 next.
+__device__ __forceinline__ float silu(float z) { return z * __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
 // Buffer resource over [base, base + bytes): loads past the end return zero.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
@@ -397,7 +399,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
             for (int e = 0; e < 4; ++e) {
               const float z = acc[i][j][4 * g + e] + b4[e];
               const float u = 0.7978845608028654f * (z + 0.044715f * z * z * z);
-              v[e] = z / (1.0f + __expf(-2.0f * u));
+              v[e] = z * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * u));
             }
             store_h4(orow + n, v[0], v[1], v[2], v[3]);
           }

@@ -31,7 +31,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
 }
 
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+// silu(z) = z / (1 + e^-z), with the hardware reciprocal (1 ulp) in place of
+// an IEEE division: the result is rounded to fp16 next.
+__device__ __forceinline__ float silu(float z) { return z * __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
 // Weight row held in row r of strip `tile` (NR rows per strip).
 //   SWIGLU: [gate 32 | up 32] for output columns 32 tile .. + 31.
