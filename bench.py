@@ -39,6 +39,7 @@ MEASURED_TRAFFIC = {
     "35c5cac0be380a8f": {"fetch_kib": 2241038.6, "fetch_scale": 2.0, "write_kib": 397954.7, "write_scale": 1.0},
     "b13966ab4f6ab1ce": {"fetch_kib": 2240940.5, "fetch_scale": 2.0, "write_kib": 400059.4, "write_scale": 1.0},
     "03c73fb21179ef2c": {"fetch_kib": 2241088.2, "fetch_scale": 2.0, "write_kib": 399894.8, "write_scale": 1.0},
+    "f9d19f9ce46f207e": {"fetch_kib": 2245197.3, "fetch_scale": 2.0, "write_kib": 399491.4, "write_scale": 1.0},
 }
 
 
