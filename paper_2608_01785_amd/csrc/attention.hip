@@ -39,6 +39,85 @@ __device__ __forceinline__ int kphys(int r, int c) {
 // 32, so a pass over 16 consecutive rows needs distinct chunks per parity.
 __device__ __forceinline__ int vphys(int d, int c) { return c ^ ((d >> 1) & 7); }
 
+// Buffer resource over the cache array `base` from element `off` on: the
+// 64-bit start is block-uniform, so it is moved to scalar registers; tile
+// loads then take a per-lane constant offset plus a uniform tile offset and
+// need no vector address arithmetic.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t cache_rsrc(const uint16_t* base, int64_t off) {
+  const uint64_t addr = reinterpret_cast<uint64_t>(base + off);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(addr));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(addr >> 32));
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>((uint64_t(hi) << 32) | lo), 0, 0x7ffffff0,
+                                           0x00020000);
+}
+
+// Two fp32 values -> two fp16 values (round to nearest even), one instruction.
+__device__ __forceinline__ uint32_t pack2h_rne(float lo, float hi) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2{lo, hi}), h2));
+}
+
+// The reference maximum of the online softmax moves only when a tile's
+// maximum exceeds it by more than this (log2 units): weights are then at
+// most 2^8, well inside fp16, and the output rescale is skipped on almost
+// every tile.  Any reference value gives the same softmax; only rounding
+// differs.
+constexpr float kLazyMax = 8.0f;
+
+// One online-softmax step over a 64-key tile of scores held as two 32-key
+// subtiles (register r of subtile st: key kv0 + 32 st + 16 (r / 8) + 8 fh +
+// r % 8 of the lane's query).  `lim` = qpos - kv0 - 8 fh: keys with
+// 32 st + 16 (r / 8) + r % 8 > lim are masked when `mask` is set.  The
+// weights are left in `pf` as the B operand of O^T = V^T P^T.
+template <int NDS>
+__device__ __forceinline__ void softmax_tile(f32x16 (&s)[2], f32x16 (&o)[NDS], u32x4 (&pf)[4], float& m_run,
+                                             float& l_run, float scale_log2, bool mask, int lim) {
+  if (mask) {
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (32 * st + 16 * (r >> 3) + (r & 7) > lim) s[st][r] = -INFINITY;
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[st][r]);
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * scale_log2;
+  // A row that has seen no key yet keeps -inf; its exponents are taken
+  // against 0, which gives weight 0.
+  const bool move = mx > m_run + kLazyMax;
+  const float m_new = move ? mx : m_run;
+  const float m_use = m_new == -INFINITY ? 0.0f : m_new;
+  const float alpha = exp2_raw(m_run - m_use);
+  m_run = m_new;
+  float psum = 0.0f;
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float p = exp2_raw(fmaf(s[st][r], scale_log2, -m_use));
+      s[st][r] = p;
+      psum += p;
+    }
+  l_run = l_run * alpha + psum;
+  if (__ballot(move) != 0) {
+#pragma unroll
+    for (int i = 0; i < NDS; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+  }
+  // P^T fragments: key block kb2 (16 keys) = registers 8 (kb2 % 2) .. +8 of subtile kb2 / 2.
+#pragma unroll
+  for (int kb2 = 0; kb2 < 4; ++kb2) {
+    const int st = kb2 >> 1, r0 = 8 * (kb2 & 1);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) pf[kb2][e] = pack2h_rne(s[st][r0 + 2 * e], s[st][r0 + 2 * e + 1]);
+  }
+}
+
 template <int DH>
 __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
   constexpr int KROW = DH * 2;                 // bytes per key row
@@ -77,7 +156,6 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
   const int row0 = a.seq_start[b];
   const int64_t* pages = a.page_base + a.seq_page0[b];
   const int64_t head_off = int64_t(g) * a.kv_head_stride;
-  const int kv_row_stride = DH;
 
   // Causal: row i sees keys 0 .. ctx + i.  Bidirectional: every row sees all
   // ctx + len keys, which is the causal rule applied as if every row sat at
@@ -98,38 +176,49 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
     for (int kb = 0; kb < DH / 16; ++kb) qf[kb] = *reinterpret_cast<const u32x4*>(qp + kb * 16);
   }
 
-  u32x4 rk[KLOADS], rv[VLOADS];
-  auto gload = [&](int t) {
-    const int kv0 = t * BKV;
-    // The tile's page and its first key's place in it (page_keys % BKV == 0).
-    const int pg = kv0 / a.page_keys;
-    const int in0 = kv0 - pg * a.page_keys;
-    const int64_t base = pages[pg] + head_off;
+  // Per-lane byte offsets of the tile loads inside a page; a tile adds the
+  // uniform offset of its first key.  A value tile of 64 keys is two
+  // consecutive 32-key value tiles of the cache.
+  uint32_t koff[KLOADS], voff[VLOADS];
 #pragma unroll
-    for (int j = 0; j < KLOADS; ++j) {
-      const int idx = tid + j * kThreads;
-      const int row = idx / KCH, c = idx % KCH;
-      rk[j] = *reinterpret_cast<const u32x4*>(a.kstore + base + int64_t(in0 + row) * kv_row_stride + c * 8);
-    }
+  for (int j = 0; j < KLOADS; ++j) {
+    const int idx = tid + j * kThreads;
+    koff[j] = uint32_t(((idx / KCH) * DH + (idx % KCH) * 8) * 2);
+  }
+#pragma unroll
+  for (int j = 0; j < VLOADS; ++j) {
+    const int idx = tid + j * kThreads;
+    const int d = idx >> 3, c = idx & 7;
+    voff[j] = uint32_t(((c >> 2) * kv_tile_keys * DH + d * kv_tile_keys + (c & 3) * 8) * 2);
+  }
+  u32x4 rk[KLOADS], rv[VLOADS];
+  // pg: page-table entry of the tile the next gload fetches, read one tile
+  // ahead (index clamped, so the read is unconditional and in bounds).
+  const int t_end = n_tiles - 1;
+  auto gload = [&](int t, int64_t pg) {
+    const int kv0 = t * BKV;
+    const uint32_t so = uint32_t((kv0 % a.page_keys) * DH * 2);
+    const __amdgpu_buffer_rsrc_t kres = cache_rsrc(a.kstore, pg + head_off);
+    const __amdgpu_buffer_rsrc_t vres = cache_rsrc(a.vstore, pg + head_off);
+#pragma unroll
+    for (int j = 0; j < KLOADS; ++j) rk[j] = __builtin_amdgcn_raw_buffer_load_b128(kres, koff[j], so, 0);
+#pragma unroll
+    for (int j = 0; j < VLOADS; ++j) rv[j] = __builtin_amdgcn_raw_buffer_load_b128(vres, voff[j], so, 0);
+  };
+  // Values of keys past the last visible one may be uninitialised; their
+  // weights are 0, but 0 * NaN would still poison the sum, so the last tile's
+  // are zeroed before they reach LDS.
+  auto vmask = [&](int t) {
+    if (t * BKV + BKV <= n_keys) return;
 #pragma unroll
     for (int j = 0; j < VLOADS; ++j) {
-      const int idx = tid + j * kThreads;
-      const int d = idx >> 3, c = idx & 7;
-      const int key = kv0 + c * 8, ki = in0 + c * 8;
-      // 8 keys of dimension d inside the value tile of 32 keys holding them.
-      u32x4 v = *reinterpret_cast<const u32x4*>(a.vstore + base + int64_t(ki / kv_tile_keys) * kv_tile_keys * DH +
-                                                d * kv_tile_keys + ki % kv_tile_keys);
-      if (key + 8 > n_keys) {
-        // Keys past the last visible one may hold uninitialised data; P is 0
-        // there, but 0 * NaN would still poison the sum, so zero them.
+      const int key = t * BKV + ((tid + j * kThreads) & 7) * 8;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const uint32_t lo_ok = (key + 2 * e < n_keys) ? 0x0000ffffu : 0u;
-          const uint32_t hi_ok = (key + 2 * e + 1 < n_keys) ? 0xffff0000u : 0u;
-          v[e] &= (lo_ok | hi_ok);
-        }
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t lo_ok = (key + 2 * e < n_keys) ? 0x0000ffffu : 0u;
+        const uint32_t hi_ok = (key + 2 * e + 1 < n_keys) ? 0xffff0000u : 0u;
+        rv[j][e] &= (lo_ok | hi_ok);
       }
-      rv[j] = v;
     }
   };
   auto lstore = [&](int stage) {
@@ -157,12 +246,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
     for (int r = 0; r < 16; ++r) o[i][r] = 0.0f;
   float m_run = -INFINITY, l_run = 0.0f;
 
-  gload(0);
+  gload(0, pages[0]);
+  vmask(0);
   lstore(0);
+  int64_t pg = pages[min(1, t_end) * BKV / a.page_keys];
   __syncthreads();
 
   for (int t = 0; t < n_tiles; ++t) {
-    if (t + 1 < n_tiles) gload(t + 1);
+    if (t + 1 < n_tiles) gload(t + 1, pg);
+    pg = pages[min(t + 2, t_end) * BKV / a.page_keys];
     const int kv0 = t * BKV;
     if (kv0 <= wave_last) {
       const uint8_t* ks = smem + (t & 1) * STAGE;
@@ -182,6 +274,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
       u32x4 kf[2][2];
       kf[0][0] = kfrag(0, 0);
       kf[0][1] = kfrag(0, 1);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // the first step's reads lead the pipeline
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // the first step's reads lead the pipeline
 #pragma unroll
       for (int kb = 0; kb < DH / 16; ++kb) {
         if (kb + 1 < DH / 16) {
@@ -196,55 +290,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
         }
       }
       __builtin_amdgcn_sched_barrier(0);
-      // Register r of subtile st holds key kv0 + 32 st + 16 (r / 8) + 8 fh + r % 8.
       // Only tiles reaching past the wave's first query position need the
       // causal mask (every key of an earlier tile is visible to all of the
       // wave's rows and lies inside the sequence).  The maximum is taken on
       // the raw scores (the scale is positive) and the scale is folded into
       // the exponent's FMA; masked scores are -inf and give 0.
-      if (kv0 + BKV - 1 > wave_first) {
-#pragma unroll
-        for (int st = 0; st < 2; ++st)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = kv0 + 32 * st + 16 * (r >> 3) + 8 * fh + (r & 7);
-            if (key > qpos) s[st][r] = -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int st = 0; st < 2; ++st)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[st][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2;
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = exp2_raw(m_run - m_new);
-      m_run = m_new;
-      float psum = 0.0f;
-#pragma unroll
-      for (int st = 0; st < 2; ++st)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = exp2_raw(fmaf(s[st][r], a.scale_log2, -m_new));
-          s[st][r] = p;
-          psum += p;
-        }
-      l_run = l_run * alpha + psum;
-      // Rescale the outputs only when some lane's running maximum moved.
-      if (__ballot(alpha != 1.0f) != 0) {
-#pragma unroll
-        for (int i = 0; i < NDS; ++i)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
-      }
-      // P^T fragments: key block kb2 (16 keys) = registers 8 (kb2 % 2) .. +8 of subtile kb2 / 2.
       u32x4 pf[4];
-#pragma unroll
-      for (int kb2 = 0; kb2 < 4; ++kb2) {
-        const int st = kb2 >> 1, r0 = 8 * (kb2 & 1);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) pf[kb2][e] = pack2h_unit(s[st][r0 + 2 * e], s[st][r0 + 2 * e + 1]);
-      }
+      softmax_tile<NDS>(s, o, pf, m_run, l_run, a.scale_log2, kv0 + BKV - 1 > wave_first, qpos - kv0 - 8 * fh);
       // V fragments likewise one 16-key step ahead; the NDS output subtiles
       // are independent accumulator chains.
       auto vfrag = [&](int kb2, int i) {
@@ -254,6 +306,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
       u32x4 vf[2][NDS];
 #pragma unroll
       for (int i = 0; i < NDS; ++i) vf[0][i] = vfrag(0, i);
+    __builtin_amdgcn_sched_group_barrier(0x100, NDS, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, NDS, 0);
 #pragma unroll
       for (int kb2 = 0; kb2 < 4; ++kb2) {
         if (kb2 + 1 < 4) {
@@ -269,7 +323,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (t + 1 < n_tiles) lstore((t + 1) & 1);
+    if (t + 1 < n_tiles) {
+      vmask(t + 1);
+      lstore((t + 1) & 1);
+    }
     __syncthreads();
   }
 

@@ -319,6 +319,11 @@ hs_status build_plan(const hs_layer_cfg& c, const int32_t* off, const int32_t* c
   // block table every page a sequence reaches is listed.
   const bool paged = kv.cache && kv.table;
   const int64_t slot_ctx = kv.cache ? kv.max_ctx : kv.packed_ctx;
+  // The attention kernels address one page of one head through a 2 GiB
+  // buffer window (a cache page is bounded the same way by the caller).
+  if (slot_ctx * dh * 2 > 0x7ffffff0)
+    return fail(HS_ERR_UNSUPPORTED, "a key page of %lld positions exceeds the 2 GiB the attention kernels address",
+                (long long)slot_ctx);
   P.page_keys = int32_t(slot_ctx);
   P.unit_keys = dec_unit_keys(int(dh), paged ? kv.max_ctx : 0);
   P.n_pages = 0;
