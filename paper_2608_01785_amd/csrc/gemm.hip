@@ -119,17 +119,20 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
   const int lrow0 = (wave & 3) * 64 + ld_sub;
   uint32_t off[kLoads];
   // A half unit (hm = 0 or 1) covers activation rows hm * 128 .. + 127 of
-  // its tile: LDS activation rows 0..127 hold them; waves 6 and 7 fetch the
-  // same rows again into the unused rows 128..255, so every wave still issues
-  // four loads per stage.
+  // its tile: LDS activation rows 0..127 hold them.  Waves 6 and 7 still
+  // issue their four loads per stage (the pipeline's counts stay uniform),
+  // but at an offset past the buffer's end, like rows >= M: those loads
+  // return zeros into the unused rows 128..255 and move no data.
   auto set_loads = [&](int tile_m, int tile_n, int hm) {
 #pragma unroll
     for (int l = 0; l < kLoads; ++l) {
       const int r = lrow0 + 16 * l;
       if (w_wave) {
         off[l] = weight_row<EPI>(tile_n, r, a.ffn) * (W_F16 ? uint32_t(kRowBytes) : row_bytes) + ld_chunk * 16;
+      } else if (hm >= 0 && r >= 128) {
+        off[l] = uint32_t(a.M) * row_bytes + ld_chunk * 16;
       } else {
-        const int ar = hm < 0 ? r : hm * 128 + (r & 127);
+        const int ar = hm < 0 ? r : hm * 128 + r;
         off[l] = uint32_t(tile_m * BM + ar) * row_bytes + ld_chunk * 16;  // rows >= M read zero
       }
     }
