@@ -361,51 +361,74 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
             *reinterpret_cast<f32x4*>(orow + n) = v;
           }
       } else if constexpr (EPI == EPI_GATED) {
-        // out (fp32) = resid + gate_seq(m) * (products + bias): the adaLN-Zero residual branch.
+        // out (fp32) = resid + gate_seq(m) * (products + bias): the adaLN-Zero
+        // residual branch.  Stores count against the same completion counter
+        // as loads, so each group's operands are loaded before the previous
+        // group's store: waiting for them never waits for a store.
         const int n_base = tile_n * BN + wn * 128 + 4 * fh;
-        float* orow = a.out_f32 + int64_t(m) * a.ldo;
-        const float* grow = a.gate + int64_t(a.row_seq[m]) * a.gate_stride;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int n = n_base + i * 32 + 8 * g;
-            float b4[4], r4[4];
-            load_bf16x4(a.bias + n, b4);
-            if (a.resid_f32) {
-              const f32x4 r = *reinterpret_cast<const f32x4*>(a.resid_f32 + int64_t(m) * a.ldo + n);
-              r4[0] = r[0];
-              r4[1] = r[1];
-              r4[2] = r[2];
-              r4[3] = r[3];
-            } else {
-              load_bf16x4(a.resid + int64_t(m) * a.ldo + n, r4);
-            }
-            const f32x4 gt = *reinterpret_cast<const f32x4*>(grow + n);
-            f32x4 v;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = r4[e] + gt[e] * (acc[i][j][4 * g + e] + b4[e]);
-            *reinterpret_cast<f32x4*>(orow + n) = v;
+        float* orow = a.out_f32 + int64_t(m) * a.ldo + n_base;
+        const float* grow = a.gate + int64_t(a.row_seq[m]) * a.gate_stride + n_base;
+        const float* rrow = a.resid_f32 ? a.resid_f32 + int64_t(m) * a.ldo + n_base : nullptr;
+        const uint16_t* rrow16 = a.resid + int64_t(m) * a.ldo + n_base;
+        const uint16_t* brow = a.bias + n_base;
+        struct Ops {
+          u32x2 b;
+          f32x4 r, gt;
+        };
+        auto load_ops = [&](int q) {
+          const int c = (q >> 2) * 32 + 8 * (q & 3);
+          Ops o;
+          o.b = *reinterpret_cast<const u32x2*>(brow + c);
+          if (rrow) {
+            o.r = *reinterpret_cast<const f32x4*>(rrow + c);
+          } else {
+            const u32x2 r2 = *reinterpret_cast<const u32x2*>(rrow16 + c);
+            o.r = f32x4{__uint_as_float(r2.x << 16), __uint_as_float(r2.x & 0xffff0000u), __uint_as_float(r2.y << 16),
+                        __uint_as_float(r2.y & 0xffff0000u)};
           }
+          o.gt = *reinterpret_cast<const f32x4*>(grow + c);
+          return o;
+        };
+        Ops nx = load_ops(0);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int i = q >> 2, g = q & 3;
+          const Ops cur = nx;
+          if (q + 1 < 16) nx = load_ops(q + 1);
+          const float b4[4] = {__uint_as_float(cur.b.x << 16), __uint_as_float(cur.b.x & 0xffff0000u),
+                               __uint_as_float(cur.b.y << 16), __uint_as_float(cur.b.y & 0xffff0000u)};
+          f32x4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = cur.r[e] + cur.gt[e] * (acc[i][j][4 * g + e] + b4[e]);
+          *reinterpret_cast<f32x4*>(orow + i * 32 + 8 * g) = v;
+        }
       } else if constexpr (EPI == EPI_GELU) {
-        // out (fp16) = gelu_tanh(products + bias); 0.5 z (1 + tanh(u)) = z / (1 + exp(-2u)).
+        // out (fp16) = gelu_tanh(products + bias); 0.5 z (1 + tanh(u)) = z / (1 + exp(-2u))
+        // with u = sqrt(2 / pi) (z + 0.044715 z^3), and exp(-2u) = 2^(z (k1 + k2 z^2)),
+        // k1 = -2 sqrt(2 / pi) log2(e), k2 = 0.044715 k1.  Each group's bias is
+        // loaded before the previous group's store: stores count against the
+        // same completion counter as loads, so waiting for it never waits for
+        // a store.
+        constexpr float k1 = -2.302208198144325f, k2 = -0.1029432395800235f;
         const int n_base = tile_n * BN + wn * 128 + 4 * fh;
-        uint16_t* orow = a.out + int64_t(m) * a.ldo;
+        uint16_t* orow = a.out + int64_t(m) * a.ldo + n_base;
+        const uint16_t* brow = a.bias + n_base;
+        u32x2 bnext = *reinterpret_cast<const u32x2*>(brow);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int q = 0; q < 16; ++q) {
+          const int i = q >> 2, g = q & 3;
+          const u32x2 b = bnext;
+          if (q + 1 < 16) bnext = *reinterpret_cast<const u32x2*>(brow + ((q + 1) >> 2) * 32 + 8 * ((q + 1) & 3));
+          const float b4[4] = {__uint_as_float(b.x << 16), __uint_as_float(b.x & 0xffff0000u),
+                               __uint_as_float(b.y << 16), __uint_as_float(b.y & 0xffff0000u)};
+          float v[4];
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int n = n_base + i * 32 + 8 * g;
-            float b4[4], v[4];
-            load_bf16x4(a.bias + n, b4);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float z = acc[i][j][4 * g + e] + b4[e];
-              const float u = 0.7978845608028654f * (z + 0.044715f * z * z * z);
-              v[e] = z * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * u));
-            }
-            store_h4(orow + n, v[0], v[1], v[2], v[3]);
+          for (int e = 0; e < 4; ++e) {
+            const float z = acc[i][j][4 * g + e] + b4[e];
+            v[e] = z * __builtin_amdgcn_rcpf(1.0f + exp2_raw(z * fmaf(z * z, k2, k1)));
           }
+          store_h4(orow + i * 32 + 8 * g, v[0], v[1], v[2], v[3]);
+        }
       } else if constexpr (EPI == EPI_SWIGLU) {
         const int c_base = tile_n * 128 + wn * 64 + 4 * fh;
 #pragma unroll

@@ -36,8 +36,12 @@ __device__ __forceinline__ uint16_t f2h(float f) {
   return __builtin_bit_cast(uint16_t, (_Float16)f);
 }
 
+// Two fp32 values -> two fp16 values as f2h does, with one packed conversion.
 __device__ __forceinline__ uint32_t pack2h(float lo, float hi) {
-  return uint32_t(f2h(lo)) | (uint32_t(f2h(hi)) << 16);
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  const f2 v = {fminf(fmaxf(lo, -kF16Max), kF16Max), fminf(fmaxf(hi, -kF16Max), kF16Max)};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, h2));
 }
 
 // Two values in [0, 1] (softmax probabilities) -> two fp16 values, round to
