@@ -40,6 +40,7 @@ MEASURED_TRAFFIC = {
     "b13966ab4f6ab1ce": {"fetch_kib": 2240940.5, "fetch_scale": 2.0, "write_kib": 400059.4, "write_scale": 1.0},
     "03c73fb21179ef2c": {"fetch_kib": 2241088.2, "fetch_scale": 2.0, "write_kib": 399894.8, "write_scale": 1.0},
     "f9d19f9ce46f207e": {"fetch_kib": 2245197.3, "fetch_scale": 2.0, "write_kib": 399491.4, "write_scale": 1.0},
+    "e964d3aa53b0007d": {"fetch_kib": 2224511.9, "fetch_scale": 2.0, "write_kib": 397264.2, "write_scale": 1.0},
 }
 
 
