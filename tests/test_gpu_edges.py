@@ -94,3 +94,51 @@ def test_largest_hidden_size(env, lengths):
     e = err_ratio(got, expect)
     log(f"  max err / rms = {e:.3e}")
     assert e <= TOL
+
+
+def _score_jumps(x, w, shape, lengths):
+    """Largest rise, over the rows of every sequence and query head, of the
+    running score maximum (log2 units, scale included) after the row's first
+    64 keys: the prefill attention moves its reference maximum only when a
+    tile's maximum exceeds it by more than 8."""
+    n = ref.rms_norm(x, w["ln1"], shape.rms_eps)
+    qkv = n @ w["w_qkv"].T
+    hq, hkv, dh = shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+    T = x.shape[0]
+    q = qkv[:, : hq * dh].reshape(T, hq, dh)
+    k = qkv[:, hq * dh: (hq + hkv) * dh].reshape(T, hkv, dh)
+    best, off = 0.0, 0
+    for L in lengths:
+        pos = np.arange(L)
+        qs = ref.rope(q[off:off + L], pos, shape.rope_base)
+        ks = ref.rope(k[off:off + L], pos, shape.rope_base)
+        for h in range(hq):
+            s = qs[:, h] @ ks[:, h // (hq // hkv)].T / np.sqrt(dh) * np.log2(np.e)
+            for i in range(64, L):
+                best = max(best, s[i, 64:i + 1].max() - s[i, :64].max())
+        off += L
+    return best
+
+
+@pytest.mark.parametrize("shape", [W.TINY, W.LayerShape(512, 4, 2, 128, 1024)], ids=["dh64", "dh128"])
+def test_sharp_scores_move_the_running_maximum(env, shape):
+    """Query and key projections 6x the usual scale make the scores span tens of
+    log2 units, so rows meet keys far above their first tile's maximum: the
+    reference maximum moves on later tiles (output rescale) and weights up to
+    2^8 pass through fp16.  Checked against the oracle; the premise itself is
+    checked on the oracle's scores."""
+    layers = W.make_weights(shape, 1, 131)
+    w = layers[0]["w_qkv"]
+    layers[0]["w_qkv"] = W.bf16_bits(W.bf16_to_f32(w) * np.float32(6.0))
+    lengths = [300, 130, 1]
+    batch = W.random_batch(shape.hidden, lengths, seed=132)
+    wf = weights_f64(layers)
+    jump = _score_jumps(f64(batch.x), wf[0], shape, lengths)
+    log(f"[edges] sharp scores dh={shape.head_dim}: largest rise of a row's maximum after its first tile "
+        f"{jump:.1f} (log2 units)")
+    assert jump > 8.0
+    expect, _ = ref.stack_forward(f64(batch.x), wf, shape, batch.seq_offsets)
+    got, _ = run(env, shape, layers, batch)
+    e = err_ratio(got, expect)
+    log(f"  max err / rms = {e:.3e}")
+    assert e <= TOL
