@@ -44,12 +44,6 @@ __device__ __forceinline__ uint32_t pack2h(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, h2));
 }
 
-// Two values in [0, 1] (softmax probabilities) -> two fp16 values, round to
-// nearest even; no saturation is needed in that range.
-__device__ __forceinline__ uint32_t pack2h_unit(float lo, float hi) {
-  return uint32_t(__builtin_bit_cast(uint16_t, (_Float16)lo)) | (uint32_t(__builtin_bit_cast(uint16_t, (_Float16)hi)) << 16);
-}
-
 // 2^x with the hardware instruction alone (about 1 ulp; results below the
 // normal range flush to zero, which softmax weights can afford).
 __device__ __forceinline__ float exp2_raw(float x) { return __builtin_amdgcn_exp2f(x); }
