@@ -334,12 +334,22 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(AttnArgs a) {
   const float inv = 1.0f / l_tot;
   const int qw = q0 + wave * 32 + fr;
   if (qw < len) {
+    // Groups 2p and 2p + 1 of a subtile leave as one 16-byte store per lane:
+    // eight consecutive dimensions, one k-group of the row in either layout.
 #pragma unroll
     for (int i = 0; i < NDS; ++i)
 #pragma unroll
-      for (int gq = 0; gq < 4; ++gq)
-        store_h4(a.o + act_index(row0 + qw, head * DH + 32 * i + 8 * gq + 4 * fh, a.hq * DH, a.o_k8_rows),
-                 o[i][4 * gq] * inv, o[i][4 * gq + 1] * inv, o[i][4 * gq + 2] * inv, o[i][4 * gq + 3] * inv);
+      for (int p = 0; p < 2; ++p) {
+        float lo[4], hi[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          lo[e] = o[i][8 * p + e] * inv;
+          hi[e] = o[i][8 * p + 4 + e] * inv;
+        }
+        const u32x4 v = swap_h8(lo, hi);
+        *reinterpret_cast<u32x4*>(a.o + act_index(row0 + qw, head * DH + 32 * i + 16 * p + 8 * fh, a.hq * DH,
+                                                  a.o_k8_rows)) = v;
+      }
   }
   clk.end(a.clock);
 }

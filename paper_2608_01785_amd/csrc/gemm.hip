@@ -405,40 +405,54 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
       } else if constexpr (EPI == EPI_GELU) {
         // out (fp16) = gelu_tanh(products + bias); 0.5 z (1 + tanh(u)) = z / (1 + exp(-2u))
         // with u = sqrt(2 / pi) (z + 0.044715 z^3), and exp(-2u) = 2^(z (k1 + k2 z^2)),
-        // k1 = -2 sqrt(2 / pi) log2(e), k2 = 0.044715 k1.  Each group's bias is
-        // loaded before the previous group's store: stores count against the
+        // k1 = -2 sqrt(2 / pi) log2(e), k2 = 0.044715 k1.  Groups 2p and 2p + 1
+        // are stored as one 32-byte run of the row, and each pair's bias is
+        // loaded before the previous pair's store: stores count against the
         // same completion counter as loads, so waiting for it never waits for
         // a store.
         constexpr float k1 = -2.302208198144325f, k2 = -0.1029432395800235f;
-        const int n_base = tile_n * BN + wn * 128 + 4 * fh;
+        const int n_base = tile_n * BN + wn * 128;
         uint16_t* orow = a.out + int64_t(m) * a.ldo + n_base;
-        const uint16_t* brow = a.bias + n_base;
-        u32x2 bnext = *reinterpret_cast<const u32x2*>(brow);
+        const uint16_t* brow = a.bias + n_base + 4 * fh;
+        auto load_bias = [&](int q) {  // bias of group q of this lane
+          return *reinterpret_cast<const u32x2*>(brow + (q >> 2) * 32 + 8 * (q & 3));
+        };
+        u32x2 bnext[2] = {load_bias(0), load_bias(1)};
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          const int i = q >> 2, g = q & 3;
-          const u32x2 b = bnext;
-          if (q + 1 < 16) bnext = *reinterpret_cast<const u32x2*>(brow + ((q + 1) >> 2) * 32 + 8 * ((q + 1) & 3));
-          const float b4[4] = {__uint_as_float(b.x << 16), __uint_as_float(b.x & 0xffff0000u),
-                               __uint_as_float(b.y << 16), __uint_as_float(b.y & 0xffff0000u)};
-          float v[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float z = acc[i][j][4 * g + e] + b4[e];
-            v[e] = z * __builtin_amdgcn_rcpf(1.0f + exp2_raw(z * fmaf(z * z, k2, k1)));
+        for (int qp = 0; qp < 8; ++qp) {
+          const int i = qp >> 1, p = qp & 1;
+          const u32x2 b[2] = {bnext[0], bnext[1]};
+          if (qp + 1 < 8) {
+            bnext[0] = load_bias(2 * qp + 2);
+            bnext[1] = load_bias(2 * qp + 3);
           }
-          store_h4(orow + i * 32 + 8 * g, v[0], v[1], v[2], v[3]);
+          float v[2][4];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const float b4[4] = {__uint_as_float(b[h].x << 16), __uint_as_float(b[h].x & 0xffff0000u),
+                                 __uint_as_float(b[h].y << 16), __uint_as_float(b[h].y & 0xffff0000u)};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float z = acc[i][j][8 * p + 4 * h + e] + b4[e];
+              v[h][e] = z * __builtin_amdgcn_rcpf(1.0f + exp2_raw(z * fmaf(z * z, k2, k1)));
+            }
+          }
+          store_h8_pair(orow + i * 32 + 16 * p, fh, v[0], v[1]);
         }
       } else if constexpr (EPI == EPI_SWIGLU) {
-        const int c_base = tile_n * 128 + wn * 64 + 4 * fh;
+        // Groups 2p and 2p + 1 are stored as one 32-byte run of the row.
+        uint16_t* orow = a.out + int64_t(m) * a.ldo + tile_n * 128 + wn * 64;
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            float v[4];
+          for (int p = 0; p < 2; ++p) {
+            float lo[4], hi[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = silu(acc[i][j][4 * g + e]) * acc[i + 2][j][4 * g + e];
-            store_h4(a.out + int64_t(m) * a.ldo + c_base + i * 32 + 8 * g, v[0], v[1], v[2], v[3]);
+            for (int e = 0; e < 4; ++e) {
+              lo[e] = silu(acc[i][j][8 * p + e]) * acc[i + 2][j][8 * p + e];
+              hi[e] = silu(acc[i][j][8 * p + 4 + e]) * acc[i + 2][j][8 * p + 4 + e];
+            }
+            store_h8_pair(orow + i * 32 + 16 * p, fh, lo, hi);
           }
       } else {  // EPI_QKV
         // The row's positions (one per RoPE section) and cache offsets, loaded
@@ -456,57 +470,65 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
           const int hi_i = (DH == 128) ? pr + 2 : 2 * pr + 1;
           const int head = (tile_n * BN + wn * 128) / DH + ((DH == 128) ? 0 : pr);
           const int dsub = (DH == 128) ? 32 * pr : 0;
+          // Q and K: groups 2p and 2p + 1 are stored as one 32-byte run of
+          // each half of the head.
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int d = dsub + 8 * g + 4 * fh;  // < DH / 2
-            // Pairs d .. d + 3 share one RoPE section (sections are multiples of 4 pairs).
-            const int pc = d >= a.sec2 ? p2 : (d >= a.sec1 ? p1 : p0);
-            const float2* rt = a.rope ? a.rope + int64_t(pc) * (DH / 2) : nullptr;
-            float lo[4], hi[4];
+          for (int p = 0; p < 2; ++p) {
+            float rl[2][4], rh[2][4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              lo[e] = acc[lo_i][j][4 * g + e];
-              hi[e] = acc[hi_i][j][4 * g + e];
-            }
-            if (a.bias) {
-              float bl[4], bh[4];
-              load_bf16x4(a.bias + head * DH + d, bl);
-              load_bf16x4(a.bias + head * DH + d + DH / 2, bh);
+            for (int h = 0; h < 2; ++h) {
+              const int g = 2 * p + h;
+              const int d = dsub + 8 * g + 4 * fh;  // < DH / 2
+              // Pairs d .. d + 3 share one RoPE section (sections are multiples of 4 pairs).
+              const int pc = d >= a.sec2 ? p2 : (d >= a.sec1 ? p1 : p0);
+              const float2* rt = a.rope ? a.rope + int64_t(pc) * (DH / 2) : nullptr;
+              float lo[4], hi[4];
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
-                lo[e] += bl[e];
-                hi[e] += bh[e];
+                lo[e] = acc[lo_i][j][4 * g + e];
+                hi[e] = acc[hi_i][j][4 * g + e];
+              }
+              if (a.bias) {
+                float bl[4], bh[4];
+                load_bf16x4(a.bias + head * DH + d, bl);
+                load_bf16x4(a.bias + head * DH + d + DH / 2, bh);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  lo[e] += bl[e];
+                  hi[e] += bh[e];
+                }
+              }
+              if (head < a.hq + a.hkv) {
+                if (a.rope) {
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) {
+                    const float2 cs = rt[d + e];
+                    rl[h][e] = lo[e] * cs.x - hi[e] * cs.y;
+                    rh[h][e] = hi[e] * cs.x + lo[e] * cs.y;
+                  }
+                } else {
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) {
+                    rl[h][e] = lo[e];
+                    rh[h][e] = hi[e];
+                  }
+                }
+              } else {
+                const int gh = head - a.hq - a.hkv;
+                uint16_t* dst = a.vstore + v_row + int64_t(gh) * a.kv_head_stride;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  dst[(d + e) * kv_tile_keys] = f2h(lo[e]);
+                  dst[(d + DH / 2 + e) * kv_tile_keys] = f2h(hi[e]);
+                }
               }
             }
             if (head < a.hq + a.hkv) {
-              float rl[4], rh[4];
-              if (a.rope) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                  const float2 cs = rt[d + e];
-                  rl[e] = lo[e] * cs.x - hi[e] * cs.y;
-                  rh[e] = hi[e] * cs.x + lo[e] * cs.y;
-                }
-              } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                  rl[e] = lo[e];
-                  rh[e] = hi[e];
-                }
-              }
               uint16_t* dst = (head < a.hq)
                                   ? a.q + (int64_t(m) * a.hq + head) * DH
                                   : a.kstore + k_row + int64_t(head - a.hq) * a.kv_head_stride;
-              store_h4(dst + d, rl[0], rl[1], rl[2], rl[3]);
-              store_h4(dst + d + DH / 2, rh[0], rh[1], rh[2], rh[3]);
-            } else {
-              const int gh = head - a.hq - a.hkv;
-              uint16_t* dst = a.vstore + v_row + int64_t(gh) * a.kv_head_stride;
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                dst[(d + e) * kv_tile_keys] = f2h(lo[e]);
-                dst[(d + DH / 2 + e) * kv_tile_keys] = f2h(hi[e]);
-              }
+              store_h8_pair(dst + dsub + 16 * p, fh, rl[0], rl[1]);
+              store_h8_pair(dst + dsub + 16 * p + DH / 2, fh, rh[0], rh[1]);
             }
           }
         }

@@ -76,6 +76,33 @@ __device__ __forceinline__ void store_h4(uint16_t* p, float a, float b, float c,
   *reinterpret_cast<u32x2*>(p) = v;
 }
 
+// Two groups of four fp16 outputs of one row in the 32x32 MFMA accumulator
+// layout: lane r + 32 h holds columns 4h .. 4h + 3 of group `lo` (columns
+// 0..7 of a 16-column run) and of group `hi` (columns 8..15).  One permlane32
+// swap per dword, which exchanges lanes 32..63 of its first operand with
+// lanes 0..31 of its second, leaves all eight columns of `lo` in the low lane
+// and all eight of `hi` in the high one, as eight packed fp16 values: lane
+// r + 32 h then owns columns 8h .. 8h + 7 of the run.  Both lanes of a row
+// must be active.
+__device__ __forceinline__ u32x4 swap_h8(const float (&lo)[4], const float (&hi)[4]) {
+  const uint32_t a[2] = {pack2h(lo[0], lo[1]), pack2h(lo[2], lo[3])};
+  const uint32_t b[2] = {pack2h(hi[0], hi[1]), pack2h(hi[2], hi[3])};
+  u32x4 v;
+#pragma unroll
+  for (int d = 0; d < 2; ++d) {
+    const auto s = __builtin_amdgcn_permlane32_swap(a[d], b[d], false, false);
+    v[d] = s[0];
+    v[2 + d] = s[1];
+  }
+  return v;
+}
+
+// swap_h8 stored row-major: the run starts at p, so each lane writes 16
+// contiguous bytes at p + 8h and the two lanes of a row cover 32.
+__device__ __forceinline__ void store_h8_pair(uint16_t* p, int h, const float (&lo)[4], const float (&hi)[4]) {
+  *reinterpret_cast<u32x4*>(p + 8 * h) = swap_h8(lo, hi);
+}
+
 // Element offset of activation (m, k): row-major with row stride ld, or, when
 // k8_rows > 0, k-group-major ((k / 8) * k8_rows + m) * 8 + k % 8, the layout
 // in which a 32-row MFMA operand fragment of 8 k values per lane is one
