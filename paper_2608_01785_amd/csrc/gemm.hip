@@ -35,7 +35,8 @@
 // four: the pipeline runs across tiles and the epilogue overlaps them.
 //
 // The grid is persistent (one block per CU of the budget); blocks walk the
-// tile space in grouped order, remapped so each XCD takes a contiguous range.
+// tile space in grouped order, remapped so each XCD takes a contiguous range,
+// and in alternating block order from round to round.
 #include <type_traits>
 
 #include "hs_device.h"
@@ -171,24 +172,38 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
                                                phys * 16);
   };
 
-  // Work units: full tiles, except that when the last round would leave more
-  // than half the blocks idle its tiles are split into two 128-row halves.
-  // Each output element is accumulated in the same order either way, so the
-  // result does not depend on the grid.
+  // Work units.  When the last M-tile holds at most 128 rows, its tiles are
+  // half units (rows 0..127 of the tile, hm = 0) placed after all others.
+  // The other tiles are full units, except that when their last round would
+  // leave more than half the blocks idle (counting the short tiles' halves)
+  // its tiles are split into two 128-row halves.  Each output element is
+  // accumulated in the same order either way, so the result does not depend
+  // on the grid.
+  const bool short_last = a.M - (n_m_tiles - 1) * BM <= 128;
+  const int n_m_full = short_last ? n_m_tiles - 1 : n_m_tiles;
+  const int n_full = n_m_full * a.n_tiles_n;
+  const int n_short = short_last ? a.n_tiles_n : 0;
   const int per_group = kGroupM * a.n_tiles_n;
   auto tile_coords = [&](int L, int& tile_m, int& tile_n) {
     const int group = L / per_group;
     const int first_m = group * kGroupM;
-    const int gsize = min(n_m_tiles - first_m, kGroupM);
+    const int gsize = min(n_m_full - first_m, kGroupM);
     tile_m = first_m + (L % per_group) % gsize;
     tile_n = (L % per_group) / gsize;
   };
   const int G = gridDim.x;
-  const int full_units = (n_tiles / G) * G;
-  const int tail = n_tiles - full_units;
-  const bool split_tail = tail > 0 && 2 * tail <= G;
-  const int n_units = split_tail ? full_units + 2 * tail : n_tiles;
+  const int full_units = (n_full / G) * G;
+  const int tail = n_full - full_units;
+  const bool split_tail = tail > 0 && 2 * tail + n_short <= G;
+  const int n_split = split_tail ? full_units + 2 * tail : n_full;
+  const int n_units = n_split + n_short;
   auto unit_coords = [&](int u, int& tile_m, int& tile_n, int& hm) {
+    if (u >= n_split) {
+      tile_m = n_m_tiles - 1;
+      tile_n = u - n_split;
+      hm = 0;
+      return;
+    }
     int t = u;
     hm = -1;
     if (split_tail && u >= full_units) {
@@ -198,7 +213,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     tile_coords(t, tile_m, tile_n);
   };
 
-  int L = xcd_remap(blockIdx.x, G);
+  // Round r gives block b unit r G + b, or r G + G - 1 - b in odd rounds: the
+  // blocks left without a full tile in a round take the first halves of the
+  // next.  Every round still covers a contiguous range of units, split over
+  // the XCDs in contiguous pieces.
+  const int b = xcd_remap(blockIdx.x, G);
+  auto unit_of = [&](int r) { return r * G + ((r & 1) ? G - 1 - b : b); };
+  int round = 0;
+  int L = unit_of(0);
   if (L >= n_units) return;
   int tile_m, tile_n, hm;
   unit_coords(L, tile_m, tile_n, hm);
@@ -214,7 +236,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     // Output rows of this lane: m0 + 32 j for j < nj.
     const int nj = hm < 0 ? 2 : 1;
     const int m0 = tile_m * BM + (hm < 0 ? wm * 64 : hm * 128 + wm * 32) + fr;
-    const int L_next = L + G;
+    const int L_next = unit_of(round + 1);
 
     auto mfma_half = [&](auto jt, const Frag& h) {
       constexpr int JT = decltype(jt)::value;
@@ -536,6 +558,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     }
     if (L_next >= n_units) break;
     L = L_next;
+    ++round;
     unit_coords(L, tile_m, tile_n, hm);
   }
   clk.end(a.clock);
