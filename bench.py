@@ -42,6 +42,7 @@ MEASURED_TRAFFIC = {
     "f9d19f9ce46f207e": {"fetch_kib": 2245197.3, "fetch_scale": 2.0, "write_kib": 399491.4, "write_scale": 1.0},
     "e964d3aa53b0007d": {"fetch_kib": 2224511.9, "fetch_scale": 2.0, "write_kib": 397264.2, "write_scale": 1.0},
     "d4915bf77392150d": {"fetch_kib": 2226951.2, "fetch_scale": 2.0, "write_kib": 397023.8, "write_scale": 1.0},
+    "adc65d4733f8721b": {"fetch_kib": 2315757.9, "fetch_scale": 2.0, "write_kib": 395098.1, "write_scale": 1.0},
 }
 
 
